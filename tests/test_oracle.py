@@ -1,0 +1,408 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+CPU only.  Each test names the passage it pins.  None of them re-types the
+oracle's own formula: they use hand-derived values (tests/golden), exact
+rational arithmetic, brute force on tiny inputs, an independent library
+(torch SDPA, scipy K-means, torch's bf16 cast, NumPy's stable sort) or an
+invariant that must hold for any input.
+"""
+import itertools
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as A
+from oracle import kmeans as KM
+from oracle import numerics as NUM
+from oracle import tactic as T
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _frac(s):
+    return float(Fraction(s))
+
+
+# ---------------------------------------------------------------- numerics
+
+def test_round_bf16_matches_torch_cast():
+    rng = np.random.default_rng(0)
+    x = np.concatenate([rng.standard_normal(20000) * 10.0 ** rng.integers(-6, 6, 20000),
+                        [0.0, 1.0, -1.0, 1.00390625, 1.001953125, 1.005859375]])
+    x32 = x.astype(np.float32).astype(np.float64)
+    ref = torch.tensor(x32, dtype=torch.float32).to(torch.bfloat16).double().numpy()
+    np.testing.assert_array_equal(NUM.round_bf16(x32), ref)
+
+
+# ---------------------------------------------------------------- attention (Eq. 2-6)
+
+def test_dense_attention_matches_torch_sdpa():
+    rng = np.random.default_rng(1)
+    for n in (1, 7, 300):
+        q = rng.standard_normal(128) * 2
+        K = rng.standard_normal((n, 128))
+        V = rng.standard_normal((n, 128))
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            torch.tensor(q)[None, None, None], torch.tensor(K)[None, None],
+            torch.tensor(V)[None, None])[0, 0, 0].numpy()
+        np.testing.assert_allclose(A.dense_attention(q, K, V), ref, rtol=0, atol=1e-12)
+
+
+def test_error_bound_eq6_holds_for_any_subset():
+    """Appendix A: eps(I) <= 2 (1 - p(I)) max ||v|| for every I."""
+    rng = np.random.default_rng(2)
+    for trial in range(200):
+        n = int(rng.integers(1, 40))
+        q = rng.standard_normal(128) * rng.uniform(0.1, 3)
+        K = rng.standard_normal((n, 128))
+        V = rng.standard_normal((n, 128)) * rng.uniform(0.1, 5)
+        idx = rng.choice(n, size=int(rng.integers(1, n + 1)), replace=False)
+        assert A.attention_distance(q, K, V, idx) <= A.error_bound(q, K, V, idx) + 1e-12
+
+
+def test_optimal_selection_is_minimum_cardinality_bruteforce():
+    """Sec. 1 / 3.4: the descending-score prefix is a smallest set reaching P."""
+    rng = np.random.default_rng(3)
+    for trial in range(60):
+        n = int(rng.integers(1, 11))
+        q = rng.standard_normal(128) * rng.uniform(0.2, 3)
+        K = rng.standard_normal((n, 128))
+        P = float(rng.uniform(0.05, 0.99))
+        s = A.softmax_weights(A.logits(q, K))
+        best = None
+        for size in range(1, n + 1):
+            if any(s[list(c)].sum() >= P for c in itertools.combinations(range(n), size)):
+                best = size
+                break
+        sel = A.optimal_selection(q, K, P)
+        assert len(sel) == best
+        assert s[sel].sum() >= P
+
+
+# ---------------------------------------------------------------- geometry (Sec. 4.4 reading)
+
+@pytest.mark.parametrize("n,expect", [
+    (4096, (41, 21, 400, 420, 2448, 2468, False)),
+    (131072, (1311, 656, 12779, 13434, 78315, 78970, False)),
+    (10, (1, 8, 2, 9, 2, 9, True)),
+    (1, (1, 8, 2, 1, 2, 1, True)),
+])
+def test_geometry_hand_values(n, expect):
+    g = T.geometry(n)
+    assert (g.N, g.W, g.s1, g.t1, g.s2, g.t2, g.exact) == expect
+
+
+# ---------------------------------------------------------------- Algorithm 1
+
+def _harmonic_sum(a: Fraction, b: Fraction, lo: int, hi: int) -> Fraction:
+    return sum((max(Fraction(0), a / i + b) for i in range(lo, hi + 1)), Fraction(0))
+
+
+def test_fit_recovers_exact_curve_and_cutoff_matches_rational_arithmetic():
+    """Algorithm 1 on a list whose tail follows y = a/x + b exactly.
+
+    With one-token windows the two sampled means lie on the curve, so the fit
+    must recover (a, b) and the budget must equal the one obtained with exact
+    rational arithmetic on the closed-form scores."""
+    prm = T.FitParams(exact_bp=100, win_bp=0, win_min=1)
+    a, b = Fraction(1, 2), Fraction(1, 100)
+    for n in (200, 1000, 5000):
+        g = T.geometry(n, prm)
+        assert not g.exact and g.s1 == g.t1 and g.s2 == g.t2
+        m = 5.0
+        head = [m] + [m - 1.0 - 0.01 * i for i in range(1, g.N)]
+        tail = [m + math.log(float(a) / i + float(b)) for i in range(g.N + 1, n + 1)]
+        l_pos = np.array(head + tail)
+        for P in (0.3, 0.5, 0.8, 0.9, 0.97):
+            k, info = T.estimate_budget(l_pos, P, prm)
+            assert abs(info["a"] - float(a)) < 1e-9 and abs(info["b"] - float(b)) < 1e-9
+            E = [Fraction(math.exp(x - m)) for x in head]
+            S_n = sum(E, Fraction(0)) + _harmonic_sum(a, b, g.N + 1, n)
+            target = Fraction(P) * S_n
+            acc, k_exact = Fraction(0), None
+            for i in range(1, n + 1):
+                acc += E[i - 1] if i <= g.N else a / i + b
+                if acc >= target:
+                    k_exact = i
+                    break
+            # no rational S_k lies within 1e-9 of the target for these inputs
+            assert k == k_exact, (n, P, k, k_exact)
+
+
+def test_constant_tail_budget_closed_form():
+    """a = 0: w is constant b beyond the head, so the budget is
+    N + ceil((P S_n - E_N) / b) when the target lies beyond the head."""
+    n = 3000
+    g = T.geometry(n)
+    m = 2.0
+    head = np.array([m] + [m - 0.5] * (g.N - 1))
+    lb = m + math.log(0.25)
+    l_pos = np.concatenate([head, np.full(n - g.N, lb)])
+    for P in (0.2, 0.6, 0.95):
+        k, info = T.estimate_budget(l_pos, P, T.FitParams())
+        assert abs(info["a"]) < 1e-12
+        E_N = 1.0 + (g.N - 1) * math.exp(-0.5)
+        S_n = E_N + 0.25 * (n - g.N)
+        assert k == g.N + math.ceil((P * S_n - E_N) / 0.25)
+
+
+def test_budget_invariants_random():
+    """Algorithm 1: S_k >= P S_n and S_{k-1} < P S_n (minimality); P = 1 takes all."""
+    rng = np.random.default_rng(4)
+    for trial in range(300):
+        n = int(rng.integers(1, 3000))
+        l_pos = np.sort(rng.standard_normal(n) * rng.uniform(0.1, 6))[::-1] + rng.standard_normal(n) * 0.3
+        P = float(rng.uniform(0.01, 0.999))
+        k, info = T.estimate_budget(l_pos, P)
+        S = info["S"]
+        assert 1 <= k <= n
+        assert S[k - 1] >= P * S[-1]
+        if k > 1:
+            assert S[k - 2] < P * S[-1]
+        assert np.all(info["w"] >= 0)
+        k1, _ = T.estimate_budget(l_pos, 1.0)
+        assert k1 == n
+
+
+def test_one_cluster_per_token_exact_mode_is_top_p():
+    """One cluster per token (centroid = key) ranks tokens exactly; with every
+    score exact the selection must be the textbook top-P prefix."""
+    rng = np.random.default_rng(5)
+    prm = T.FitParams(exact_bp=10000)
+    for trial in range(40):
+        n = int(rng.integers(1, 200))
+        q = rng.standard_normal(128) * rng.uniform(0.3, 3)
+        K = rng.standard_normal((n, 128))
+        V = rng.standard_normal((n, 128))
+        P = float(rng.uniform(0.05, 0.99))
+        offsets = np.arange(n + 1)
+        r = T.decode_group(q[None], K, V, K, offsets, P, prm)
+        ref = A.optimal_selection(q, K, P)
+        assert r.k[0] == len(ref)
+        assert set(r.sel[0].tolist()) == set(ref.tolist())
+        np.testing.assert_allclose(r.out[0], A.sparse_attention(q, K, V, np.sort(ref)), atol=1e-12)
+
+
+# ---------------------------------------------------------------- whole group (Sec. 4.3-4.6)
+
+def _golden_inputs(fx):
+    d = fx["d"]
+    key0 = [{"ln4": math.log(4), "ln2": math.log(2), "0": 0.0}[s] for s in fx["key0"]]
+    n = len(key0)
+    K = np.zeros((n, d))
+    K[:, 0] = key0
+    V = np.zeros((n, d))
+    V[np.arange(n), np.arange(n)] = 1.0
+    Q = np.zeros((len(fx["q_signs"]), d))
+    Q[:, 0] = np.array(fx["q_signs"]) * math.sqrt(d)
+    cent = np.zeros((2, d))
+    cent[0, 0] = 1.0
+    return Q, K, V, cent, np.array(fx["offsets"])
+
+
+def test_golden_tiny_exact_pipeline():
+    with open(os.path.join(GOLDEN, "tiny_exact.json")) as f:
+        fx = json.load(f)
+    Q, K, V, cent, off = _golden_inputs(fx)
+    for case in fx["cases"]:
+        for use_union, key in ((True, "out_union"), (False, "out_per_head")):
+            r = T.decode_group(Q, K, V, cent, off, case["P"], use_union=use_union)
+            assert r.k.tolist() == case["k"]
+            assert r.union.tolist() == case["union"]
+            exp = np.array([[_frac(x) for x in row] for row in case[key]])
+            np.testing.assert_allclose(r.out[:, :4], exp, rtol=0, atol=1e-12)
+            assert np.all(r.out[:, 4:] == 0)
+
+
+def _random_clustered_group(rng, n, C, G=4, d=128):
+    cen = rng.standard_normal((C, d))
+    lab = rng.integers(0, C, n)
+    K = cen[lab] + 0.3 * rng.standard_normal((n, d))
+    perm = np.argsort(lab, kind="stable")
+    Ks = K[perm]
+    Vs = rng.standard_normal((n, d))
+    offsets = np.zeros(C + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum(np.bincount(lab, minlength=C))
+    Q = np.stack([2.0 * (cen[rng.choice(C, min(3, C), replace=False)].sum(0) + 0.3 * rng.standard_normal(d))
+                  for _ in range(G)])
+    return Q, Ks, Vs, cen, offsets
+
+
+def test_union_invariants():
+    """Sec. 4.5: U contains every I_h, |U| <= sum k_h, and U meets every
+    cluster in a prefix of its stored rows; each I_h is a prefix of the
+    head's unpacked list."""
+    rng = np.random.default_rng(6)
+    for trial in range(20):
+        n = int(rng.integers(50, 3000))
+        C = max(1, n // 16)
+        Q, Ks, Vs, cen, off = _random_clustered_group(rng, n, C)
+        r = T.decode_group(Q, Ks, Vs, cen, off, float(rng.uniform(0.5, 0.99)))
+        U = set(r.union.tolist())
+        for h in range(len(Q)):
+            assert set(r.sel[h].tolist()) <= U
+            np.testing.assert_array_equal(r.sel[h], r.rows[h][:r.k[h]])
+        assert len(U) <= int(r.k.sum())
+        for j in range(C):
+            inside = [row for row in range(off[j], off[j + 1]) if row in U]
+            assert inside == list(range(off[j], off[j] + len(inside)))
+
+
+def test_target_one_equals_dense_attention():
+    """P = 1 selects all tokens; the output is dense attention (Eq. 2), here
+    checked against torch's SDPA."""
+    rng = np.random.default_rng(7)
+    n, C = 700, 40
+    Q, Ks, Vs, cen, off = _random_clustered_group(rng, n, C)
+    r = T.decode_group(Q, Ks, Vs, cen, off, 1.0)
+    assert r.k.tolist() == [n] * len(Q)
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.tensor(Q)[None, :, None], torch.tensor(Ks)[None, None].expand(1, len(Q), n, 128),
+        torch.tensor(Vs)[None, None].expand(1, len(Q), n, 128))[0, :, 0].numpy()
+    np.testing.assert_allclose(r.out, ref, atol=1e-12)
+
+
+def test_decode_matches_loop_reimplementation_tiny():
+    """A loop-only re-implementation (pairwise ranking, explicit position
+    walk, explicit window sums) for n <= 64 agrees with the vectorised
+    oracle on k and on the union."""
+    rng = np.random.default_rng(8)
+    for trial in range(30):
+        n = int(rng.integers(1, 65))
+        C = int(rng.integers(1, min(n, 9) + 1))
+        Q, Ks, Vs, cen, off = _random_clustered_group(rng, n, C, G=2)
+        P = float(rng.uniform(0.2, 0.98))
+        r = T.decode_group(Q, Ks, Vs, cen, off, P)
+        d = Ks.shape[1]
+        union = set()
+        for h in range(2):
+            q = Q[h]
+            sc = [float(np.dot(q, cen[j])) for j in range(C)]
+            rank = sorted(range(C), key=lambda j: (-sc[j], j))
+            pos_rows = []
+            for j in rank:
+                for row in range(off[j], off[j + 1]):
+                    pos_rows.append(row)
+            lg = [float(np.dot(q, Ks[row])) / math.sqrt(d) for row in pos_rows]
+            N = min(n, max(1, -(-n * 100 // 10000)))
+            W = max(8, -(-n * 50 // 10000))
+            c1, c2 = (n * 1000 + 5000) // 10000, (n * 6000 + 5000) // 10000
+            s1 = max(c1 - W // 2, N + 1); t1 = min(s1 + W - 1, n)
+            s2 = max(c2 - W // 2, N + 1); t2 = min(s2 + W - 1, n)
+            m = max(lg[:N])
+            if N == n or s1 > t1 or s2 > t2 or t1 >= s2:
+                w = [math.exp(x - m) for x in lg]
+            else:
+                mu1 = sum(math.exp(lg[i - 1] - m) for i in range(s1, t1 + 1)) / (t1 - s1 + 1)
+                mu2 = sum(math.exp(lg[i - 1] - m) for i in range(s2, t2 + 1)) / (t2 - s2 + 1)
+                x1, x2 = (s1 + t1) / 2, (s2 + t2) / 2
+                a = (mu1 - mu2) / (1 / x1 - 1 / x2)
+                b = mu1 - a / x1
+                w = [math.exp(lg[i - 1] - m) if i <= N else max(0.0, a / i + b) for i in range(1, n + 1)]
+            tot = 0.0
+            for x in w:
+                tot += x
+            acc, k = 0.0, n
+            for i, x in enumerate(w, start=1):
+                acc += x
+                if acc >= P * tot:
+                    k = i
+                    break
+            assert r.k[h] == k
+            union |= set(pos_rows[:k])
+        assert set(r.union.tolist()) == union
+
+
+def test_empty_sequence_yields_zeros():
+    Q = np.ones((4, 128))
+    r = T.decode_group(Q, np.zeros((0, 128)), np.zeros((0, 128)), np.ones((1, 128)),
+                       np.array([0, 0]), 0.9)
+    assert r.k.tolist() == [0, 0, 0, 0] and r.union_count == 0 and np.all(r.out == 0)
+
+
+# ---------------------------------------------------------------- K-means (Sec. 4.2)
+
+def test_kmeans_single_cluster_is_mean():
+    rng = np.random.default_rng(9)
+    K = rng.standard_normal((500, 128))
+    r = KM.kmeans(K, [17], round_storage=False)
+    assert np.all(r.assign == 0)
+    np.testing.assert_allclose(r.centroids[0], K.mean(0), atol=1e-14)
+    r2 = KM.kmeans(K, [17], round_storage=True)
+    np.testing.assert_array_equal(r2.centroids[0], NUM.round_bf16(K.mean(0)))
+
+
+def test_kmeans_one_cluster_per_token_is_identity():
+    rng = np.random.default_rng(10)
+    K = rng.standard_normal((64, 128))
+    r = KM.kmeans(K, np.arange(64))
+    np.testing.assert_array_equal(r.assign, np.arange(64))
+    assert r.iters == 2
+
+
+def test_kmeans_matches_scipy_lloyd():
+    """Without bf16 storage the iteration is Lloyd's algorithm, which
+    scipy.cluster.vq.kmeans2(minit='matrix') also runs (same empty-cluster
+    rule); data without empty clusters must give identical results."""
+    from scipy.cluster.vq import kmeans2
+    rng = np.random.default_rng(11)
+    for trial in range(5):
+        C, per = 12, 30
+        cen = rng.standard_normal((C, 16)) * 4
+        K = np.concatenate([cen[j] + rng.standard_normal((per, 16)) for j in range(C)])
+        K = K[rng.permutation(len(K))]
+        init = rng.choice(len(K), C, replace=False)
+        r = KM.kmeans(K, init, max_iters=10, round_storage=False)
+        cb, lab = kmeans2(K, K[init].copy(), iter=10, minit="matrix")
+        np.testing.assert_array_equal(r.assign, lab)
+        np.testing.assert_allclose(r.centroids, cb, atol=1e-12)
+
+
+def test_kmeans_inertia_non_increasing():
+    rng = np.random.default_rng(12)
+    K = rng.standard_normal((2000, 128))
+    r = KM.kmeans(K, rng.choice(2000, 64, replace=False), max_iters=10, round_storage=False)
+    assert all(b <= a + 1e-9 for a, b in zip(r.inertia, r.inertia[1:]))
+
+
+def test_kmeans_stored_centroids_are_rounded_means():
+    rng = np.random.default_rng(13)
+    K = NUM.round_bf16(rng.standard_normal((3000, 128)))
+    r = KM.kmeans(K, rng.choice(3000, 100, replace=False), max_iters=10)
+    np.testing.assert_array_equal(NUM.round_bf16(r.centroids), r.centroids)
+    for j in range(100):
+        mem = r.assign == j
+        if mem.any():
+            np.testing.assert_array_equal(r.centroids[j], NUM.round_bf16(K[mem].mean(0)))
+
+
+def test_sq_distances_matches_direct_form():
+    rng = np.random.default_rng(14)
+    K = rng.standard_normal((50, 128))
+    C = rng.standard_normal((7, 128))
+    direct = ((K[:, None, :] - C[None, :, :]) ** 2).sum(-1)
+    np.testing.assert_allclose(KM.sq_distances(K, C), direct, rtol=1e-12, atol=1e-10)
+
+
+def test_cluster_layout_is_stable_sort():
+    rng = np.random.default_rng(15)
+    a = rng.integers(0, 37, 5000)
+    off, perm = KM.cluster_layout(a, 40)
+    np.testing.assert_array_equal(perm, np.argsort(a, kind="stable"))
+    np.testing.assert_array_equal(np.diff(off), np.bincount(a, minlength=40))
+
+
+def test_budget_reaching_target_exactly_counts():
+    """Algorithm 1 asks for the cumulative sum to reach P times the total
+    (>=).  Equal logits give w = 1 exactly, so S_k = k and P S_n = P n: the
+    budget is exactly ceil(P n), including when P n is an integer."""
+    for n in (10, 16, 40, 64):
+        l_pos = np.full(n, 0.75)
+        for P in (0.25, 0.5, 0.75, 0.3):
+            k, _ = T.estimate_budget(l_pos, P, T.FitParams(exact_bp=10000))
+            assert k == math.ceil(P * n - 1e-12) if (P * n) != int(P * n) else k == int(P * n)
