@@ -1,0 +1,209 @@
+/*
+ * tactic.h - C ABI of the MI355X (gfx950) library for Tactic's decode-time
+ * sparse attention ("Tactic: Adaptive Sparse Attention with Clustering and
+ * Distribution Fitting for Long-Context LLMs").
+ *
+ * Problem statement (Sec. 3.3 - 3.5): given a decode query q, the cached keys
+ * K and values V of n tokens and a target fraction P, return the attention
+ * output over a small index set I whose cumulative attention score p(I)
+ * (Eq. 5) reaches P.  The set is found as in Sec. 4: keys are grouped by
+ * K-means at prefill (Sec. 4.2); at decode every query head ranks the clusters
+ * by q . centroid (Sec. 4.3), fits y = a/x + b to sampled scores to estimate
+ * its token budget (Sec. 4.4, Algorithm 1), the query heads of a GQA group
+ * take the union of their selections (Sec. 4.5), and attention runs over the
+ * selected tokens only (Sec. 4.6, Eq. 3).
+ *
+ * Conventions for every call
+ *  - All tensor arguments are DEVICE pointers unless a field says "host".
+ *  - bf16 values are passed as uint16_t bit patterns.  head_dim must be 128.
+ *  - A ragged batch of B sequences: sequence b owns tokens
+ *    [kv_indptr[b], kv_indptr[b+1]) of every per-KV-head array; K and V are
+ *    laid out [Hkv][total_tokens][128] (head-major).  Query head h uses KV
+ *    head h / (Hq / Hkv).  Sequence lengths must be below 2^31.
+ *  - Every call is asynchronous on `stream` and does not synchronise with
+ *    the host.  Argument checks that need only host data are done before any
+ *    launch; a failed check returns an error and launches nothing.  Device
+ *    arrays are trusted to match the host-side sizes given (a mismatch is
+ *    undefined behaviour).
+ *  - The library allocates no memory and keeps no global state: the caller
+ *    owns every buffer, including the workspace.  Calls that share a
+ *    workspace must be ordered on one stream.
+ */
+#ifndef TACTIC_H_
+#define TACTIC_H_
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TACTIC_OK = 0,
+  TACTIC_ERR_INVALID_ARG = 1,  /* a null pointer, a size out of range, P outside (0, 1] ... */
+  TACTIC_ERR_UNSUPPORTED = 2,  /* a valid request this build does not implement (e.g. head_dim != 128) */
+  TACTIC_ERR_WORKSPACE = 3,    /* workspace smaller than the size query returned */
+  TACTIC_ERR_HIP = 4           /* a HIP launch failed; tactic_last_error() has the message */
+} tactic_status;
+
+/* Shape of a ragged decode batch. */
+typedef struct {
+  int32_t batch;               /* B >= 1 */
+  int32_t n_q_heads;           /* Hq, a multiple of n_kv_heads; Hq / Hkv in {1, 2, 4, 8} */
+  int32_t n_kv_heads;          /* Hkv >= 1 */
+  int32_t head_dim;            /* must be 128 */
+  int64_t total_tokens;        /* host: sum of the B sequence lengths */
+  int64_t max_seq_len;         /* host: largest sequence length */
+  const int64_t* kv_indptr;    /* device [B+1], kv_indptr[0] = 0, non-decreasing */
+} tactic_kv_shape;
+
+/* Cluster description of a cluster-sorted KV cache (the output of
+ * tactic_build_clusters, or any caller-made grouping).  Sequence b has C_b
+ * clusters per KV head (C_b >= 1 when the sequence is non-empty); they are
+ * clusters [cl_indptr[b], cl_indptr[b+1]) of every per-KV-head cluster array.
+ * Cluster j of (b, g) owns the rows offsets_bg[j] .. offsets_bg[j+1]-1 of the
+ * sequence's cluster-sorted K/V, where offsets_bg = offsets + g*(total_clusters
+ * + B) + cl_indptr[b] + b holds C_b + 1 sequence-relative offsets from 0 to
+ * n_b.  Within a cluster, rows keep their original token order (Sec. 4.3
+ * unpacks clusters in that stored order). */
+typedef struct {
+  int64_t total_clusters;      /* host: sum of C_b */
+  int32_t max_clusters;        /* host: largest C_b */
+  const int64_t* cl_indptr;    /* device [B+1] */
+  const uint16_t* centroids;   /* device bf16 [Hkv][total_clusters][128] */
+  const int32_t* offsets;      /* device int32 [Hkv][total_clusters + B] */
+} tactic_cluster_meta;
+
+/* Parameters of the decode selection.  The fractions are integers in basis
+ * points (1 bp = 1e-4) so that the library and any checker derive identical
+ * integer sizes.  For a list of n tokens:
+ *   exact head  N = min(n, max(1, ceil(n * exact_bp / 1e4)))     (Sec. 4.4: 1-2%)
+ *   window      W = max(win_min, ceil(n * win_bp / 1e4))
+ *   centres     c_j = floor((n * p_j_bp + 5000) / 1e4)           (Sec. 4.4: 10%, 60%)
+ *   window j    s_j = max(c_j - floor(W/2), N + 1), t_j = min(s_j + W - 1, n)
+ * If a window is empty, the windows overlap or N = n, every score of the list
+ * is computed exactly instead of fitted. */
+typedef struct {
+  float target_frac;           /* P in (0, 1]; P = 1 selects every token (dense) */
+  int32_t exact_bp;            /* default 100  (N = 1% of the tokens) */
+  int32_t win_bp;              /* default 50   (W = 0.5% of the tokens) */
+  int32_t win_min;             /* default 8 */
+  int32_t p1_bp;               /* default 1000 */
+  int32_t p2_bp;               /* default 6000 */
+  int32_t use_union;           /* 1: every head of a GQA group attends over the union of the
+                                  group's selections (Sec. 4.5).  0 is not supported yet. */
+} tactic_decode_params;
+
+/* Host-side launch plan of a sparse decode: sizes derived from the shape,
+ * the cluster counts and the parameters (done once per shape; it costs
+ * O(max_seq_len) host time).  Plain data owned by the caller. */
+typedef struct {
+  int64_t v[64];
+} tactic_decode_plan;
+
+/* Fills `p` with the defaults listed above and target_frac = 0.9. */
+void tactic_decode_params_default(tactic_decode_params* p);
+
+/* Validates shape, cluster counts and parameters and fills `plan`.
+ * *workspace_bytes receives the workspace size tactic_sparse_decode needs.
+ * meta's device pointers are not read and may be null here.
+ * Errors: TACTIC_ERR_INVALID_ARG, TACTIC_ERR_UNSUPPORTED. */
+tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape,
+                                        const tactic_cluster_meta* meta,
+                                        const tactic_decode_params* params,
+                                        tactic_decode_plan* plan,
+                                        size_t* workspace_bytes);
+
+/* Tactic's decode for one layer (Sec. 4.3 - 4.6, Algorithm 1).
+ *   q          bf16 [B][Hq][128]
+ *   K_sorted,  bf16 [Hkv][total_tokens][128], rows in the cluster-sorted
+ *   V_sorted   order that `meta` describes
+ *   out        fp32 [B][Hq][128]: attention of each query head over the
+ *              union of its group's selected tokens (softmax renormalised over
+ *              that set, Eq. 3); zeros for an empty sequence
+ *   sel_count_q   int32 [B][Hq]: token budget k_h of each query head
+ *   sel_count_kv  int32 [B][Hkv]: size of the group union |U_g|
+ *   workspace  at least the bytes reported by tactic_sparse_decode_plan for
+ *              the same arguments; contents on entry are irrelevant.
+ * The plan must come from the same shape, meta sizes and params. */
+tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted,
+                                   const uint16_t* V_sorted, const tactic_kv_shape* shape,
+                                   const tactic_cluster_meta* meta,
+                                   const tactic_decode_params* params,
+                                   const tactic_decode_plan* plan, float* out,
+                                   int32_t* sel_count_q, int32_t* sel_count_kv,
+                                   void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream);
+
+/* Number of fp64 fields per query head in the fit record of the view below:
+ *   0 m (logit shift: max over the exact head)   1 mu_1   2 mu_2   3 a   4 b
+ *   5 S_n (estimated total)   6 T = P * S_n   7 k   8 N   9 n   10 exact mode
+ *   11 sampled rows   12 E_N (exact-head sum)   13 cutoff rank   14 cutoff length */
+#define TACTIC_FIT_FIELDS 16
+
+/* Device pointers into a workspace after tactic_sparse_decode, for
+ * inspecting the intermediate stages (cluster order, fit, union).  Valid
+ * until the workspace is reused. */
+typedef struct {
+  const float* scores;         /* [B][Hq][max_clusters]: q . centroid (fp32) */
+  const int32_t* order;        /* [B][Hq][max_clusters]: cluster ids by rank */
+  const int32_t* rank_prefix;  /* [B][Hq][max_clusters + 1]: tokens ahead of each rank */
+  const double* fit;           /* [B][Hq][TACTIC_FIT_FIELDS] */
+  const int32_t* union_len;    /* [Hkv][total_clusters]: rows of each cluster in the union
+                                  (a prefix of the cluster) */
+} tactic_decode_view;
+
+tactic_status tactic_sparse_decode_view(const tactic_decode_plan* plan, const void* workspace,
+                                        tactic_decode_view* view);
+
+/* Dense decode attention over every token (Eq. 2), the baseline.  Same
+ * layouts as tactic_sparse_decode (any row order works: attention does not
+ * depend on it).  The workspace must be zero-filled before its first use
+ * with this call; each completed call leaves its counters zero again. */
+size_t tactic_dense_decode_workspace_size(const tactic_kv_shape* shape);
+tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const uint16_t* V,
+                                  const tactic_kv_shape* shape, float* out, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream);
+
+/* Prefill clustering (Sec. 4.2): per (sequence, KV head) K-means on the keys
+ * with C_b clusters, started from the keys of the tokens init_idx names,
+ * alternating nearest-centroid assignment (squared Euclidean distance, ties to
+ * the smaller id) and centroid = mean of members (an empty cluster keeps its
+ * centroid), for at most max_iters iterations or until an assignment step
+ * changes nothing.  Centroids are stored in bf16 and each assignment measures
+ * distances to the stored values.
+ *   K, V          bf16 [Hkv][total_tokens][128], original token order
+ *   cl_indptr     device [B+1] (C_b = cl_indptr[b+1] - cl_indptr[b], 1 <= C_b <= n_b)
+ *   init_idx      device int32 [Hkv][total_clusters]: C_b distinct sequence-relative
+ *                 token ids per (b, g)
+ * Outputs: centroids bf16 [Hkv][total_clusters][128], assign int32 [Hkv][total_tokens]
+ * (cluster of each original token), offsets int32 [Hkv][total_clusters + B] and perm
+ * int32 [Hkv][total_tokens] (original token of each cluster-sorted row, ascending
+ * within a cluster), K_sorted / V_sorted (the cache rows permuted by perm; either may
+ * be null to skip it). */
+typedef struct {
+  int32_t max_iters;           /* default 10 (Sec. 4.2) */
+} tactic_kmeans_params;
+
+size_t tactic_build_clusters_workspace_size(const tactic_kv_shape* shape, int64_t total_clusters,
+                                            int32_t max_clusters);
+tactic_status tactic_build_clusters(const uint16_t* K, const uint16_t* V,
+                                    const tactic_kv_shape* shape, const int64_t* cl_indptr,
+                                    int64_t total_clusters, int32_t max_clusters,
+                                    const int32_t* init_idx, const tactic_kmeans_params* params,
+                                    uint16_t* centroids, int32_t* assign, int32_t* offsets,
+                                    int32_t* perm, uint16_t* K_sorted, uint16_t* V_sorted,
+                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Static description of a status code. */
+const char* tactic_status_string(tactic_status s);
+/* Message of the last failure on the calling thread ("" if none). */
+const char* tactic_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TACTIC_H_ */

@@ -1,0 +1,436 @@
+// Host side of the C ABI declared in include/tactic.h: validation, launch
+// plans, workspace layout and the launch sequence of each call.
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+
+#include "../../include/tactic.h"
+#include "common.hpp"
+#include "kernels.hpp"
+#include "kmeans.hpp"
+#include "plan.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+tactic_status fail(tactic_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+tactic_status fail(tactic_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+tactic_status hip_fail(hipError_t e, const char* what) {
+  return fail(TACTIC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+int64_t align_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+struct Layout {
+  int64_t cur = 0;
+  int64_t take(int64_t bytes) {
+    const int64_t o = cur;
+    cur = align_up(cur + bytes, 256);
+    return o;
+  }
+};
+
+tactic::SelParams sel_params(const tactic_decode_params* p) {
+  tactic::SelParams s;
+  s.target_frac = p->target_frac;
+  s.exact_bp = p->exact_bp;
+  s.win_bp = p->win_bp;
+  s.win_min = p->win_min;
+  s.p1_bp = p->p1_bp;
+  s.p2_bp = p->p2_bp;
+  return s;
+}
+
+tactic_status check_shape(const tactic_kv_shape* s) {
+  if (!s) return fail(TACTIC_ERR_INVALID_ARG, "shape is null");
+  if (s->batch < 1) return fail(TACTIC_ERR_INVALID_ARG, "batch must be >= 1 (got %d)", s->batch);
+  if (s->n_kv_heads < 1 || s->n_q_heads < 1)
+    return fail(TACTIC_ERR_INVALID_ARG, "head counts must be >= 1");
+  if (s->n_q_heads % s->n_kv_heads != 0)
+    return fail(TACTIC_ERR_INVALID_ARG, "n_q_heads (%d) is not a multiple of n_kv_heads (%d)",
+                s->n_q_heads, s->n_kv_heads);
+  const int G = s->n_q_heads / s->n_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(TACTIC_ERR_UNSUPPORTED, "group size %d not in {1, 2, 4, 8}", G);
+  if (s->head_dim != tactic::kHeadDim)
+    return fail(TACTIC_ERR_UNSUPPORTED, "head_dim %d != 128", s->head_dim);
+  if (s->total_tokens < 0 || s->max_seq_len < 0 || s->max_seq_len > s->total_tokens)
+    return fail(TACTIC_ERR_INVALID_ARG, "inconsistent total_tokens / max_seq_len");
+  if (s->max_seq_len >= (int64_t)1 << 31)
+    return fail(TACTIC_ERR_UNSUPPORTED, "sequence length >= 2^31");
+  if ((int64_t)s->batch * s->n_kv_heads > tactic::kMaxGroups)
+    return fail(TACTIC_ERR_UNSUPPORTED, "batch * n_kv_heads > %d", tactic::kMaxGroups);
+  if (!s->kv_indptr) return fail(TACTIC_ERR_INVALID_ARG, "kv_indptr is null");
+  return TACTIC_OK;
+}
+
+tactic_status check_params(const tactic_decode_params* p) {
+  if (!p) return fail(TACTIC_ERR_INVALID_ARG, "params is null");
+  if (!(p->target_frac > 0.f && p->target_frac <= 1.f))
+    return fail(TACTIC_ERR_INVALID_ARG, "target_frac must be in (0, 1] (got %g)", (double)p->target_frac);
+  if (p->exact_bp < 0 || p->exact_bp > 10000 || p->win_bp < 0 || p->win_bp > 10000 || p->win_min < 1 ||
+      p->p1_bp < 0 || p->p1_bp > 10000 || p->p2_bp < 0 || p->p2_bp > 10000)
+    return fail(TACTIC_ERR_INVALID_ARG, "fit parameters out of range");
+  if (p->use_union != 1) return fail(TACTIC_ERR_UNSUPPORTED, "only use_union = 1 is implemented");
+  return TACTIC_OK;
+}
+
+const tactic::DecodePlan* as_plan(const tactic_decode_plan* p) {
+  return reinterpret_cast<const tactic::DecodePlan*>(p);
+}
+
+int64_t dense_chunk_tokens(const tactic_kv_shape* s) {
+  // about 8 items per CU on 256 CUs when the batch is large enough
+  const int64_t work = s->total_tokens * s->n_kv_heads;
+  int64_t T = tactic::kMaxChunkTokens;
+  while (T > 256 && work / T < 2048) T /= 2;
+  return T;
+}
+
+}  // namespace
+
+extern "C" {
+
+void tactic_decode_params_default(tactic_decode_params* p) {
+  if (!p) return;
+  p->target_frac = 0.9f;
+  p->exact_bp = 100;
+  p->win_bp = 50;
+  p->win_min = 8;
+  p->p1_bp = 1000;
+  p->p2_bp = 6000;
+  p->use_union = 1;
+}
+
+const char* tactic_status_string(tactic_status s) {
+  switch (s) {
+    case TACTIC_OK: return "ok";
+    case TACTIC_ERR_INVALID_ARG: return "invalid argument";
+    case TACTIC_ERR_UNSUPPORTED: return "unsupported";
+    case TACTIC_ERR_WORKSPACE: return "workspace too small";
+    case TACTIC_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char* tactic_last_error(void) { return g_last_error.c_str(); }
+
+tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape, const tactic_cluster_meta* meta,
+                                        const tactic_decode_params* params, tactic_decode_plan* plan_out,
+                                        size_t* workspace_bytes) {
+  tactic_status st = check_shape(shape);
+  if (st != TACTIC_OK) return st;
+  if ((st = check_params(params)) != TACTIC_OK) return st;
+  if (!meta || !plan_out || !workspace_bytes) return fail(TACTIC_ERR_INVALID_ARG, "null argument");
+  if (meta->max_clusters < 1 || meta->total_clusters < meta->max_clusters ||
+      meta->total_clusters > (int64_t)meta->max_clusters * shape->batch)
+    return fail(TACTIC_ERR_INVALID_ARG, "inconsistent total_clusters / max_clusters");
+  if (meta->max_clusters > (1 << 24)) return fail(TACTIC_ERR_UNSUPPORTED, "more than 2^24 clusters");
+
+  tactic::DecodePlan p;
+  memset(&p, 0, sizeof(p));
+  p.magic = tactic::kPlanMagic;
+  p.B = shape->batch;
+  p.Hq = shape->n_q_heads;
+  p.Hkv = shape->n_kv_heads;
+  p.G = p.Hq / p.Hkv;
+  p.Cm = meta->max_clusters;
+  p.Ct = meta->total_clusters;
+  p.nmax = shape->max_seq_len;
+  p.total = shape->total_tokens;
+  p.exact_bp = params->exact_bp;
+  p.win_bp = params->win_bp;
+  p.win_min = params->win_min;
+  p.p1_bp = params->p1_bp;
+  p.p2_bp = params->p2_bp;
+  // sampled rows per head: the largest list any length <= nmax can need
+  const tactic::SelParams sp = sel_params(params);
+  int64_t S_cap = 1;
+  for (int64_t n = 1; n <= p.nmax; ++n) {
+    const tactic::Geometry g = tactic::make_geometry(n, sp);
+    if (g.samples > S_cap) S_cap = g.samples;
+  }
+  p.S_cap = S_cap;
+  p.chunk_tokens = 256;
+  p.max_chunks = std::max<int64_t>(1, (p.nmax + p.chunk_tokens - 1) / p.chunk_tokens);
+  p.split = std::min<int64_t>(64, std::max<int64_t>(1, (S_cap + 63) / 64));
+  p.attn_grid = 1024;
+  int64_t nb = 1;
+  while (nb < p.Cm) nb <<= 1;
+  p.sort_lds = nb <= tactic::kSortLdsBuckets ? 1 : 0;
+  p.nb_max = p.sort_lds ? tactic::kSortLdsBuckets : nb;
+
+  const int64_t BH = p.B * p.Hq, BG = p.B * p.Hkv;
+  Layout L;
+  p.off_scores = L.take(BH * p.Cm * 4);
+  p.off_order = L.take(BH * p.Cm * 4);
+  p.off_rank = L.take(BH * p.Cm * 4);
+  p.off_rprefix = L.take(BH * (p.Cm + 1) * 4);
+  p.off_headmeta = L.take(BH * 16 * 4);
+  p.off_rows = L.take(BH * p.S_cap * 4);
+  p.off_logit = L.take(BH * p.S_cap * 8);
+  p.off_fit = L.take(BH * tactic::kFitFields * 8);
+  p.off_cut = L.take(BH * 2 * 4);
+  p.off_union_len = L.take(p.Hkv * p.Ct * 4);
+  p.off_gmeta = L.take(BG * 4 * 4);
+  p.off_rstart = L.take(BG * p.Cm * 4);
+  p.off_rupos = L.take(BG * (p.Cm + 1) * 4);
+  p.off_cfr = L.take(BG * p.max_chunks * 4);
+  p.off_partials = L.take(BG * p.max_chunks * p.G * (tactic::kHeadDim + 2) * 4);
+  p.n_counters = BH + 2 * BG;
+  p.off_counters = L.take(p.n_counters * 4);
+  if (!p.sort_lds) {
+    p.off_sort_keys = L.take(BH * p.nb_max * 8);
+    p.off_sort_cnt = L.take(BH * (p.nb_max + 4) * 4);
+    p.off_sort_start = L.take(BH * (p.nb_max + 4) * 4);
+  }
+  p.ws_bytes = L.cur;
+  memcpy(plan_out, &p, sizeof(p));
+  *workspace_bytes = (size_t)p.ws_bytes;
+  return TACTIC_OK;
+}
+
+tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, const uint16_t* V_sorted,
+                                   const tactic_kv_shape* shape, const tactic_cluster_meta* meta,
+                                   const tactic_decode_params* params, const tactic_decode_plan* plan_in,
+                                   float* out, int32_t* sel_count_q, int32_t* sel_count_kv, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream) {
+  tactic_status st = check_shape(shape);
+  if (st != TACTIC_OK) return st;
+  if ((st = check_params(params)) != TACTIC_OK) return st;
+  if (!q || !K_sorted || !V_sorted || !meta || !out || !sel_count_q || !sel_count_kv || !plan_in)
+    return fail(TACTIC_ERR_INVALID_ARG, "null argument");
+  if (!meta->cl_indptr || !meta->centroids || !meta->offsets)
+    return fail(TACTIC_ERR_INVALID_ARG, "null cluster meta pointer");
+  const tactic::DecodePlan& p = *as_plan(plan_in);
+  if (p.magic != tactic::kPlanMagic || p.B != shape->batch || p.Hq != shape->n_q_heads ||
+      p.Hkv != shape->n_kv_heads || p.nmax != shape->max_seq_len || p.total != shape->total_tokens ||
+      p.Cm != meta->max_clusters || p.Ct != meta->total_clusters || p.exact_bp != params->exact_bp ||
+      p.win_bp != params->win_bp || p.win_min != params->win_min || p.p1_bp != params->p1_bp ||
+      p.p2_bp != params->p2_bp)
+    return fail(TACTIC_ERR_INVALID_ARG, "plan does not match the shape / meta / params");
+  if (!workspace || (int64_t)workspace_bytes < p.ws_bytes)
+    return fail(TACTIC_ERR_WORKSPACE, "workspace has %zu bytes, needs %lld", workspace_bytes,
+                (long long)p.ws_bytes);
+
+  char* ws = static_cast<char*>(workspace);
+  const int BH = (int)(p.B * p.Hq), BG = (int)(p.B * p.Hkv);
+  int* counters = reinterpret_cast<int*>(ws + p.off_counters);
+
+  tactic::ScoreArgs sa;
+  sa.q = q;
+  sa.centroids = meta->centroids;
+  sa.cl_indptr = meta->cl_indptr;
+  sa.B = (int)p.B;
+  sa.Hq = (int)p.Hq;
+  sa.Hkv = (int)p.Hkv;
+  sa.Cm = (int)p.Cm;
+  sa.Ct = p.Ct;
+  sa.scores = reinterpret_cast<float*>(ws + p.off_scores);
+  sa.counters = counters;
+  sa.n_counters = (int)p.n_counters;
+  hipError_t e = tactic::launch_score(sa, (int)p.G, (int)((p.Cm + 63) / 64), BG, stream);
+  if (e != hipSuccess) return hip_fail(e, "score_clusters launch");
+
+  tactic::SortArgs so;
+  so.scores = sa.scores;
+  so.offsets = meta->offsets;
+  so.kv_indptr = shape->kv_indptr;
+  so.cl_indptr = meta->cl_indptr;
+  so.B = (int)p.B;
+  so.Hq = (int)p.Hq;
+  so.Hkv = (int)p.Hkv;
+  so.G = (int)p.G;
+  so.Cm = (int)p.Cm;
+  so.nb_max = (int)p.nb_max;
+  so.Ct = p.Ct;
+  so.S_cap = p.S_cap;
+  so.prm = sel_params(params);
+  so.g_keys = p.sort_lds ? nullptr : reinterpret_cast<uint64_t*>(ws + p.off_sort_keys);
+  so.g_cnt = p.sort_lds ? nullptr : reinterpret_cast<uint32_t*>(ws + p.off_sort_cnt);
+  so.g_start = p.sort_lds ? nullptr : reinterpret_cast<uint32_t*>(ws + p.off_sort_start);
+  so.order = reinterpret_cast<int32_t*>(ws + p.off_order);
+  so.rank_of = reinterpret_cast<int32_t*>(ws + p.off_rank);
+  so.rprefix = reinterpret_cast<int32_t*>(ws + p.off_rprefix);
+  so.sample_rows = reinterpret_cast<int32_t*>(ws + p.off_rows);
+  so.head_meta = reinterpret_cast<int32_t*>(ws + p.off_headmeta);
+  e = tactic::launch_sort(so, p.sort_lds != 0, BH, stream);
+  if (e != hipSuccess) return hip_fail(e, "sort_clusters launch");
+
+  tactic::FitArgs fa;
+  fa.q = q;
+  fa.K = K_sorted;
+  fa.kv_indptr = shape->kv_indptr;
+  fa.cl_indptr = meta->cl_indptr;
+  fa.offsets = meta->offsets;
+  fa.B = (int)p.B;
+  fa.Hq = (int)p.Hq;
+  fa.Hkv = (int)p.Hkv;
+  fa.Cm = (int)p.Cm;
+  fa.BH = BH;
+  fa.split = (int)p.split;
+  fa.Ct = p.Ct;
+  fa.total = p.total;
+  fa.S_cap = p.S_cap;
+  fa.chunk_tokens = p.chunk_tokens;
+  fa.max_chunks = p.max_chunks;
+  fa.P = (double)params->target_frac;
+  fa.head_meta = so.head_meta;
+  fa.sample_rows = so.sample_rows;
+  fa.rprefix = so.rprefix;
+  fa.rank_of = so.rank_of;
+  fa.logits = reinterpret_cast<double*>(ws + p.off_logit);
+  fa.fit = reinterpret_cast<double*>(ws + p.off_fit);
+  fa.cut = reinterpret_cast<int32_t*>(ws + p.off_cut);
+  fa.sel_count_q = sel_count_q;
+  fa.sel_count_kv = sel_count_kv;
+  fa.union_len = reinterpret_cast<int32_t*>(ws + p.off_union_len);
+  fa.gmeta = reinterpret_cast<int32_t*>(ws + p.off_gmeta);
+  fa.rstart = reinterpret_cast<int32_t*>(ws + p.off_rstart);
+  fa.rupos = reinterpret_cast<int32_t*>(ws + p.off_rupos);
+  fa.cfr = reinterpret_cast<int32_t*>(ws + p.off_cfr);
+  fa.counters = counters;
+  e = tactic::launch_fit(fa, (int)p.G, (int)p.split, BH, stream);
+  if (e != hipSuccess) return hip_fail(e, "sample_fit_union launch");
+
+  tactic::AttnArgs aa;
+  aa.q = q;
+  aa.K = K_sorted;
+  aa.V = V_sorted;
+  aa.kv_indptr = shape->kv_indptr;
+  aa.B = (int)p.B;
+  aa.Hq = (int)p.Hq;
+  aa.Hkv = (int)p.Hkv;
+  aa.Cm = (int)p.Cm;
+  aa.dense = 0;
+  aa.total = p.total;
+  aa.chunk_tokens = p.chunk_tokens;
+  aa.max_chunks = p.max_chunks;
+  aa.gmeta = fa.gmeta;
+  aa.rstart = fa.rstart;
+  aa.rupos = fa.rupos;
+  aa.cfr = fa.cfr;
+  aa.partials = reinterpret_cast<float*>(ws + p.off_partials);
+  aa.done = counters + BH + BG;
+  aa.out = out;
+  e = tactic::launch_attn(aa, (int)p.G, (int)p.attn_grid, stream);
+  if (e != hipSuccess) return hip_fail(e, "attention launch");
+  return TACTIC_OK;
+}
+
+tactic_status tactic_sparse_decode_view(const tactic_decode_plan* plan_in, const void* workspace,
+                                        tactic_decode_view* view) {
+  if (!plan_in || !workspace || !view) return fail(TACTIC_ERR_INVALID_ARG, "null argument");
+  const tactic::DecodePlan& p = *as_plan(plan_in);
+  if (p.magic != tactic::kPlanMagic) return fail(TACTIC_ERR_INVALID_ARG, "not a decode plan");
+  const char* ws = static_cast<const char*>(workspace);
+  view->scores = reinterpret_cast<const float*>(ws + p.off_scores);
+  view->order = reinterpret_cast<const int32_t*>(ws + p.off_order);
+  view->rank_prefix = reinterpret_cast<const int32_t*>(ws + p.off_rprefix);
+  view->fit = reinterpret_cast<const double*>(ws + p.off_fit);
+  view->union_len = reinterpret_cast<const int32_t*>(ws + p.off_union_len);
+  return TACTIC_OK;
+}
+
+size_t tactic_dense_decode_workspace_size(const tactic_kv_shape* shape) {
+  if (check_shape(shape) != TACTIC_OK) return 0;
+  const int64_t T = dense_chunk_tokens(shape);
+  const int64_t BG = (int64_t)shape->batch * shape->n_kv_heads;
+  const int64_t G = shape->n_q_heads / shape->n_kv_heads;
+  const int64_t max_chunks = std::max<int64_t>(1, (shape->max_seq_len + T - 1) / T);
+  Layout L;
+  L.take(BG * 4);  // counters
+  L.take(BG * max_chunks * G * (tactic::kHeadDim + 2) * 4);
+  return (size_t)L.cur;
+}
+
+tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const uint16_t* V,
+                                  const tactic_kv_shape* shape, float* out, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream) {
+  tactic_status st = check_shape(shape);
+  if (st != TACTIC_OK) return st;
+  if (!q || !K || !V || !out) return fail(TACTIC_ERR_INVALID_ARG, "null argument");
+  const size_t need = tactic_dense_decode_workspace_size(shape);
+  if (!workspace || workspace_bytes < need)
+    return fail(TACTIC_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+  const int64_t T = dense_chunk_tokens(shape);
+  const int64_t BG = (int64_t)shape->batch * shape->n_kv_heads;
+  const int64_t max_chunks = std::max<int64_t>(1, (shape->max_seq_len + T - 1) / T);
+  Layout L;
+  const int64_t off_cnt = L.take(BG * 4);
+  const int64_t off_part = L.take(BG * max_chunks * (shape->n_q_heads / shape->n_kv_heads) *
+                                  (tactic::kHeadDim + 2) * 4);
+  char* ws = static_cast<char*>(workspace);
+  tactic::AttnArgs aa;
+  memset(&aa, 0, sizeof(aa));
+  aa.q = q;
+  aa.K = K;
+  aa.V = V;
+  aa.kv_indptr = shape->kv_indptr;
+  aa.B = shape->batch;
+  aa.Hq = shape->n_q_heads;
+  aa.Hkv = shape->n_kv_heads;
+  aa.dense = 1;
+  aa.total = shape->total_tokens;
+  aa.chunk_tokens = T;
+  aa.max_chunks = max_chunks;
+  aa.partials = reinterpret_cast<float*>(ws + off_part);
+  aa.done = reinterpret_cast<int*>(ws + off_cnt);
+  aa.out = out;
+  const int64_t items = BG * max_chunks;
+  const int grid = (int)std::min<int64_t>(std::max<int64_t>(items, 1), 2048);
+  hipError_t e = tactic::launch_attn(aa, shape->n_q_heads / shape->n_kv_heads, grid, stream);
+  if (e != hipSuccess) return hip_fail(e, "dense attention launch");
+  return TACTIC_OK;
+}
+
+size_t tactic_build_clusters_workspace_size(const tactic_kv_shape* shape, int64_t total_clusters,
+                                            int32_t max_clusters) {
+  if (check_shape(shape) != TACTIC_OK || max_clusters < 1 || total_clusters < max_clusters) return 0;
+  return tactic::kmeans_workspace_bytes(shape->batch, shape->n_kv_heads, shape->total_tokens,
+                                        total_clusters, max_clusters, shape->max_seq_len);
+}
+
+tactic_status tactic_build_clusters(const uint16_t* K, const uint16_t* V, const tactic_kv_shape* shape,
+                                    const int64_t* cl_indptr, int64_t total_clusters, int32_t max_clusters,
+                                    const int32_t* init_idx, const tactic_kmeans_params* params,
+                                    uint16_t* centroids, int32_t* assign, int32_t* offsets, int32_t* perm,
+                                    uint16_t* K_sorted, uint16_t* V_sorted, void* workspace,
+                                    size_t workspace_bytes, hipStream_t stream) {
+  tactic_status st = check_shape(shape);
+  if (st != TACTIC_OK) return st;
+  if (!K || !cl_indptr || !init_idx || !params || !centroids || !assign || !offsets || !perm)
+    return fail(TACTIC_ERR_INVALID_ARG, "null argument");
+  if ((K_sorted != nullptr || V_sorted != nullptr) && (V_sorted != nullptr) && !V)
+    return fail(TACTIC_ERR_INVALID_ARG, "V_sorted requested without V");
+  if (max_clusters < 1 || total_clusters < max_clusters ||
+      total_clusters > (int64_t)max_clusters * shape->batch)
+    return fail(TACTIC_ERR_INVALID_ARG, "inconsistent total_clusters / max_clusters");
+  if (params->max_iters < 1 || params->max_iters > 1000)
+    return fail(TACTIC_ERR_INVALID_ARG, "max_iters must be in [1, 1000]");
+  const size_t need = tactic_build_clusters_workspace_size(shape, total_clusters, max_clusters);
+  if (!workspace || workspace_bytes < need)
+    return fail(TACTIC_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+  hipError_t e = tactic::run_kmeans(K, V, shape->kv_indptr, cl_indptr, shape->batch, shape->n_kv_heads,
+                                    shape->total_tokens, shape->max_seq_len, total_clusters, max_clusters,
+                                    init_idx, params->max_iters, centroids, assign, offsets, perm, K_sorted,
+                                    V_sorted, workspace, stream);
+  if (e != hipSuccess) return hip_fail(e, "k-means launch");
+  return TACTIC_OK;
+}
+
+}  // extern "C"

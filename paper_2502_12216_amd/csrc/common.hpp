@@ -1,0 +1,119 @@
+// Shared device/host helpers of the Tactic HIP library (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tactic {
+
+constexpr int kHeadDim = 128;
+constexpr int kWave = 64;
+
+// ----------------------------------------------------------------------------
+// Geometry of the exact head and the two sampling windows of a token list of
+// length n (Sec. 4.4, Algorithm 1).  All fractions are integer basis points.
+// ----------------------------------------------------------------------------
+struct SelParams {
+  float target_frac;
+  int exact_bp, win_bp, win_min, p1_bp, p2_bp;
+};
+
+struct Geometry {
+  int64_t n, N, s1, t1, s2, t2, samples;
+  int exact;
+};
+
+__host__ __device__ inline int64_t ceil_div64(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+__host__ __device__ inline Geometry make_geometry(int64_t n, const SelParams& p) {
+  Geometry g;
+  g.n = n;
+  int64_t N = ceil_div64(n * p.exact_bp, 10000);
+  if (N < 1) N = 1;
+  if (N > n) N = n;
+  int64_t W = ceil_div64(n * p.win_bp, 10000);
+  if (W < p.win_min) W = p.win_min;
+  const int64_t c1 = (n * p.p1_bp + 5000) / 10000;
+  const int64_t c2 = (n * p.p2_bp + 5000) / 10000;
+  int64_t s1 = c1 - W / 2;
+  if (s1 < N + 1) s1 = N + 1;
+  int64_t t1 = s1 + W - 1;
+  if (t1 > n) t1 = n;
+  int64_t s2 = c2 - W / 2;
+  if (s2 < N + 1) s2 = N + 1;
+  int64_t t2 = s2 + W - 1;
+  if (t2 > n) t2 = n;
+  g.N = N;
+  g.s1 = s1;
+  g.t1 = t1;
+  g.s2 = s2;
+  g.t2 = t2;
+  g.exact = (N == n) || (s1 > t1) || (s2 > t2) || (t1 >= s2);
+  g.samples = g.exact ? n : N + (t1 - s1 + 1) + (t2 - s2 + 1);
+  return g;
+}
+
+// ----------------------------------------------------------------------------
+// bf16 helpers (bf16 is the upper half of an fp32)
+// ----------------------------------------------------------------------------
+__device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+typedef short short2_t __attribute__((ext_vector_type(2)));
+
+// a.x*b.x + a.y*b.y + c on bf16 pairs, fp32 accumulate (v_dot2_f32_bf16)
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(short2_t, a),
+                                         __builtin_bit_cast(short2_t, b), c, false);
+}
+
+// ----------------------------------------------------------------------------
+// Cross-lane reductions within groups of 16 lanes (xor butterflies)
+// ----------------------------------------------------------------------------
+__device__ __forceinline__ float sum16(float v) {
+  v += __shfl_xor(v, 8, 16);
+  v += __shfl_xor(v, 4, 16);
+  v += __shfl_xor(v, 2, 16);
+  v += __shfl_xor(v, 1, 16);
+  return v;
+}
+
+__device__ __forceinline__ double sum16d(double v) {
+  v += __shfl_xor(v, 8, 16);
+  v += __shfl_xor(v, 4, 16);
+  v += __shfl_xor(v, 2, 16);
+  v += __shfl_xor(v, 1, 16);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// ----------------------------------------------------------------------------
+// Device-scope completion counters ("last workgroup finishes the job").
+// Every thread that wrote results calls arrive(); the function returns true in
+// all threads of the workgroup that observed the final arrival.  The release
+// fence before the increment and the acquire fence after it make the other
+// workgroups' writes visible across XCDs.
+// ----------------------------------------------------------------------------
+__device__ __forceinline__ bool arrive_last(int* counter, int expected, int* s_flag) {
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int prev = __hip_atomic_fetch_add(counter, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    *s_flag = (prev == expected - 1) ? 1 : 0;
+  }
+  __syncthreads();
+  const bool last = *s_flag != 0;
+  if (last) __threadfence();
+  return last;
+}
+
+}  // namespace tactic

@@ -1,0 +1,603 @@
+// Token selection of Tactic's decode (Sec. 4.3 - 4.5, Algorithm 1) for gfx950.
+//
+//   score_clusters     q . centroid for every (query head, cluster)       Sec. 4.3
+//   sort_clusters      per query head: cluster order (score desc, id asc),
+//                      tokens ahead of every rank, sampled-row list        Sec. 4.3, Alg. 1 input
+//   sample_fit_union   exact logits of the sampled rows (fp64); the last
+//                      workgroup of a head fits y = a/x + b and finds the
+//                      budget k; the last head of a GQA group forms the
+//                      union and the attention work list                   Sec. 4.4, 4.5, Alg. 1
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "common.hpp"
+#include "kernels.hpp"
+#include "plan.hpp"
+
+namespace tactic {
+
+// ============================================================================
+// Block-wide helpers (any blockDim that is a multiple of 64, at most 1024)
+// ============================================================================
+
+// Exclusive scan in place of a[0..count) (LDS or global); returns the total.
+// `s_wave` must hold 17 elements of T in LDS.  Ends with a barrier.
+template <typename T>
+__device__ T block_exclusive_scan(T* a, int count, T* s_wave) {
+  const int tid = threadIdx.x, nt = blockDim.x, nw = nt / kWave;
+  const int seg = (count + nt - 1) / nt;
+  const int beg = min(count, tid * seg), end = min(count, beg + seg);
+  T local = 0;
+  for (int i = beg; i < end; ++i) local += a[i];
+  T incl = local;
+  for (int o = 1; o < kWave; o <<= 1) {
+    const T y = __shfl_up(incl, o, kWave);
+    if ((tid & (kWave - 1)) >= o) incl += y;
+  }
+  if ((tid & (kWave - 1)) == kWave - 1) s_wave[tid / kWave] = incl;
+  __syncthreads();
+  if (tid == 0) {
+    T run = 0;
+    for (int w = 0; w < nw; ++w) {
+      const T t = s_wave[w];
+      s_wave[w] = run;
+      run += t;
+    }
+    s_wave[16] = run;
+  }
+  __syncthreads();
+  T run = s_wave[tid / kWave] + incl - local;
+  for (int i = beg; i < end; ++i) {
+    const T t = a[i];
+    a[i] = run;
+    run += t;
+  }
+  const T total = s_wave[16];
+  __syncthreads();
+  return total;
+}
+
+template <typename T>
+__device__ T block_sum(T v, T* s_wave) {
+  for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  const int nw = blockDim.x / kWave;
+  if ((threadIdx.x & (kWave - 1)) == 0) s_wave[threadIdx.x / kWave] = v;
+  __syncthreads();
+  T r = 0;
+  for (int w = 0; w < nw; ++w) r += s_wave[w];
+  __syncthreads();
+  return r;
+}
+
+__device__ double block_max_d(double v, double* s_wave) {
+  for (int o = kWave / 2; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, kWave));
+  const int nw = blockDim.x / kWave;
+  if ((threadIdx.x & (kWave - 1)) == 0) s_wave[threadIdx.x / kWave] = v;
+  __syncthreads();
+  double r = s_wave[0];
+  for (int w = 1; w < nw; ++w) r = fmax(r, s_wave[w]);
+  __syncthreads();
+  return r;
+}
+
+__device__ float block_minmax(float v, bool want_max, float* s_wave) {
+  for (int o = kWave / 2; o > 0; o >>= 1) {
+    const float y = __shfl_xor(v, o, kWave);
+    v = want_max ? fmaxf(v, y) : fminf(v, y);
+  }
+  const int nw = blockDim.x / kWave;
+  if ((threadIdx.x & (kWave - 1)) == 0) s_wave[threadIdx.x / kWave] = v;
+  __syncthreads();
+  float r = s_wave[0];
+  for (int w = 1; w < nw; ++w) r = want_max ? fmaxf(r, s_wave[w]) : fminf(r, s_wave[w]);
+  __syncthreads();
+  return r;
+}
+
+// ============================================================================
+// 1. Centroid scoring: s[b][h][j] = q_h . c_{b,g,j}, fp32 accumulation.
+//    grid (ceil(Cm/64), B*Hkv), 256 threads; 16 lanes own one centroid row
+//    (16 B each), a wave scores 4 rows per step, the group's G query heads sit
+//    in registers.  Block (0,0) also clears the call's completion counters.
+// ============================================================================
+template <int G>
+__global__ __launch_bounds__(256) void score_clusters_kernel(ScoreArgs a) {
+  const int bg = blockIdx.y;
+  if (blockIdx.x == 0 && bg == 0) {
+    for (int i = threadIdx.x; i < a.n_counters; i += blockDim.x) a.counters[i] = 0;
+  }
+  const int b = bg / a.Hkv, g = bg % a.Hkv;
+  const int64_t cb = a.cl_indptr[b];
+  const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
+  const int j0 = blockIdx.x * 64;
+  if (j0 >= C) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, sl = lane & 15, grp = lane >> 4;
+
+  uint32_t qw[G][4];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    const uint4 v = *reinterpret_cast<const uint4*>(a.q + ((int64_t)b * a.Hq + g * G + h) * kHeadDim + sl * 8);
+    qw[h][0] = v.x; qw[h][1] = v.y; qw[h][2] = v.z; qw[h][3] = v.w;
+  }
+  const uint16_t* cbase = a.centroids + ((int64_t)g * a.Ct + cb) * kHeadDim;
+#pragma unroll
+  for (int it = 0; it < 4; ++it) {
+    const int j = j0 + wave * 16 + it * 4 + grp;
+    uint4 c = make_uint4(0, 0, 0, 0);
+    if (j < C) c = *reinterpret_cast<const uint4*>(cbase + (int64_t)j * kHeadDim + sl * 8);
+    const float cf[8] = {bf16lo(c.x), bf16hi(c.x), bf16lo(c.y), bf16hi(c.y),
+                         bf16lo(c.z), bf16hi(c.z), bf16lo(c.w), bf16hi(c.w)};
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      float s = 0.f;
+      const uint32_t* w = qw[h];
+      const float qf[8] = {bf16lo(w[0]), bf16hi(w[0]), bf16lo(w[1]), bf16hi(w[1]),
+                           bf16lo(w[2]), bf16hi(w[2]), bf16lo(w[3]), bf16hi(w[3])};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s = fmaf(qf[e], cf[e], s);
+      s = sum16(s);
+      if (sl == h && j < C) a.scores[((int64_t)b * a.Hq + g * G + h) * a.Cm + j] = s;
+    }
+  }
+}
+
+// ============================================================================
+// 2. Per-head cluster order by a bucket sort.  Key = (descending-orderable
+//    score bits, cluster id): ascending keys give score descending, ties by
+//    ascending id.  Buckets split [min, max] of the scores linearly; the
+//    bucket index is a monotone function of the score, so bucket order agrees
+//    with key order and every element's rank is its bucket start plus the
+//    number of smaller keys in its bucket.  Then the tokens ahead of every
+//    rank (exclusive prefix of cluster sizes in rank order) and the rows of
+//    the sampled positions: exact head 1..N and the two windows (Alg. 1).
+//    One workgroup (1024 threads) per query head.
+// ============================================================================
+__device__ __forceinline__ uint32_t desc_key_bits(float s) {
+  const uint32_t u = __float_as_uint(s + 0.0f);  // -0 -> +0
+  const uint32_t ord = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ~ord;
+}
+
+template <bool kLds>
+__global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  __shared__ uint32_t s_wave_u[17];
+  __shared__ float s_wave_f[17];
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int bh = blockIdx.x;
+  const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
+  const int64_t cb = a.cl_indptr[b];
+  const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
+  const int n = (int)(a.kv_indptr[b + 1] - a.kv_indptr[b]);
+  const int32_t* off = a.offsets + (int64_t)g * (a.Ct + a.B) + cb + b;
+  const float* sc = a.scores + (int64_t)bh * a.Cm;
+
+  uint64_t* keys;
+  uint32_t* cnt;
+  uint32_t* start;
+  if (kLds) {
+    keys = reinterpret_cast<uint64_t*>(smem_raw);
+    cnt = reinterpret_cast<uint32_t*>(keys + a.nb_max);
+    start = cnt + a.nb_max + 4;
+  } else {
+    keys = a.g_keys + (int64_t)bh * a.nb_max;
+    cnt = a.g_cnt + (int64_t)bh * (a.nb_max + 4);
+    start = a.g_start + (int64_t)bh * (a.nb_max + 4);
+  }
+  int nb = 1;
+  while (nb < C) nb <<= 1;
+
+  for (int i = tid; i < nb + 1; i += nt) cnt[i] = 0;
+  float lo = INFINITY, hi = -INFINITY;
+  for (int j = tid; j < C; j += nt) {
+    const float s = sc[j];
+    if (s == s) {
+      lo = fminf(lo, s);
+      hi = fmaxf(hi, s);
+    }
+  }
+  lo = block_minmax(lo, false, s_wave_f);
+  hi = block_minmax(hi, true, s_wave_f);
+  const float range = hi - lo;
+  const bool spread = range > 0.f;
+  auto bucket_of = [&](float s) -> int {
+    if (!(s == s)) return nb - 1;
+    if (!spread) return 0;
+    const float t = floorf((hi - s) / range * (float)nb);
+    return (int)fminf((float)(nb - 1), fmaxf(0.f, t));
+  };
+  __syncthreads();
+  for (int j = tid; j < C; j += nt) atomicAdd(&cnt[bucket_of(sc[j])], 1u);
+  __syncthreads();
+  for (int i = tid; i < nb; i += nt) start[i] = cnt[i];
+  __syncthreads();
+  block_exclusive_scan<uint32_t>(start, nb, s_wave_u);
+  for (int j = tid; j < C; j += nt) {
+    const float s = sc[j];
+    const uint64_t key = ((uint64_t)desc_key_bits(s) << 32) | (uint32_t)j;
+    const uint32_t slot = atomicAdd(&start[bucket_of(s)], 1u);
+    keys[slot] = key;
+  }
+  __syncthreads();
+  int32_t* rank_of = a.rank_of + (int64_t)bh * a.Cm;
+  int32_t* order = a.order + (int64_t)bh * a.Cm;
+  for (int j = tid; j < C; j += nt) {
+    const float s = sc[j];
+    const uint64_t key = ((uint64_t)desc_key_bits(s) << 32) | (uint32_t)j;
+    const int bk = bucket_of(s);
+    const uint32_t end = start[bk], beg = end - cnt[bk];
+    uint32_t r = 0;
+    for (uint32_t t = beg; t < end; ++t) r += keys[t] < key ? 1u : 0u;
+    const int pos = (int)(beg + r);
+    order[pos] = j;
+    rank_of[j] = pos;
+  }
+  __syncthreads();
+  // sizes by rank -> cnt, cluster id by rank -> keys (reused as int32)
+  int32_t* ord_s = reinterpret_cast<int32_t*>(keys);
+  for (int j = tid; j < C; j += nt) {
+    const int pos = rank_of[j];
+    cnt[pos] = (uint32_t)(off[j + 1] - off[j]);
+    ord_s[pos] = j;
+  }
+  __syncthreads();
+  const uint32_t ntok = block_exclusive_scan<uint32_t>(cnt, C, s_wave_u);
+  if (tid == 0) cnt[C] = ntok;
+  __syncthreads();
+  int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
+  for (int r = tid; r <= C; r += nt) rpre[r] = (int32_t)cnt[r];
+
+  const Geometry geo = make_geometry(n, a.prm);
+  int64_t S = geo.samples;
+  if (S > a.S_cap) S = a.S_cap;
+  if (tid == 0) {
+    int32_t* hm = a.head_meta + (int64_t)bh * 16;
+    hm[0] = n;
+    hm[1] = (int32_t)geo.N;
+    hm[2] = geo.exact ? 0 : (int32_t)(geo.t1 - geo.s1 + 1);
+    hm[3] = geo.exact ? 0 : (int32_t)(geo.t2 - geo.s2 + 1);
+    hm[4] = (int32_t)geo.s1;
+    hm[5] = (int32_t)geo.t1;
+    hm[6] = (int32_t)geo.s2;
+    hm[7] = (int32_t)geo.t2;
+    hm[8] = geo.exact;
+    hm[9] = (int32_t)S;
+    hm[10] = C;
+  }
+  const int64_t N = geo.exact ? n : geo.N;
+  const int64_t W1 = geo.exact ? 0 : geo.t1 - geo.s1 + 1;
+  int32_t* rows = a.sample_rows + (int64_t)bh * a.S_cap;
+  for (int64_t u = tid; u < S; u += nt) {
+    int64_t i;  // 1-based position in the unpacked list
+    if (u < N) i = u + 1;
+    else if (u < N + W1) i = geo.s1 + (u - N);
+    else i = geo.s2 + (u - N - W1);
+    int lo_r = 0, hi_r = C;  // largest r with prefix[r] < i
+    while (lo_r < hi_r) {
+      const int mid = (lo_r + hi_r + 1) >> 1;
+      if ((int64_t)cnt[mid] < i) lo_r = mid;
+      else hi_r = mid - 1;
+    }
+    if (lo_r >= C) lo_r = C - 1;  // only with offsets that disagree with kv_indptr
+    int32_t row = off[ord_s[lo_r]] + (int32_t)(i - 1 - (int64_t)cnt[lo_r]);
+    rows[u] = min(max(row, 0), n - 1);
+  }
+}
+
+// ============================================================================
+// 3. Sampled logits, fit, cutoff, union.
+// ============================================================================
+__device__ double harmonic(int64_t x) {
+  if (x <= 0) return 0.0;
+  if (x < 64) {
+    double s = 0.0;
+    for (int64_t i = 1; i <= x; ++i) s += 1.0 / (double)i;
+    return s;
+  }
+  const double X = (double)x, r = 1.0 / X, r2 = r * r;
+  // Euler-Maclaurin expansion of H(x) = psi(x + 1) + gamma
+  return log(X) + 0.57721566490153286061 + 0.5 * r -
+         r2 * (1.0 / 12.0 - r2 * (1.0 / 120.0 - r2 * (1.0 / 252.0 - r2 * (1.0 / 240.0))));
+}
+
+// sum_{i=lo}^{hi} max(0, a/i + b), lo >= 1, evaluated in closed form over the
+// interval where a/i + b is positive (a/i + b is monotone in i).
+__device__ double tail_sum(double a, double b, int64_t lo, int64_t hi) {
+  if (hi < lo) return 0.0;
+  int64_t L = lo, R = hi;
+  auto f = [&](int64_t i) { return a / (double)i + b; };
+  if (a >= 0.0 && b >= 0.0) {
+    // all terms non-negative
+  } else if (a <= 0.0 && b <= 0.0) {
+    return 0.0;
+  } else if (a > 0.0) {  // b < 0: positive for i < a / -b
+    const double z = a / -b;
+    int64_t r = z >= (double)hi ? hi : (z <= (double)lo ? lo - 1 : (int64_t)z);
+    while (r >= lo && !(f(r) > 0.0)) --r;
+    while (r + 1 <= hi && f(r + 1) > 0.0) ++r;
+    R = r;
+  } else {  // a < 0, b > 0: positive for i > -a / b
+    const double z = -a / b;
+    int64_t l = z >= (double)hi ? hi + 1 : (z < (double)lo ? lo : (int64_t)z + 1);
+    while (l <= hi && !(f(l) > 0.0)) ++l;
+    while (l - 1 >= lo && f(l - 1) > 0.0) --l;
+    L = l;
+  }
+  if (R < L) return 0.0;
+  return a * (harmonic(R) - harmonic(L - 1)) + b * (double)(R - L + 1);
+}
+
+template <int G>
+__global__ __launch_bounds__(256) void sample_fit_union_kernel(FitArgs a) {
+  __shared__ double s_wave_d[17];
+  __shared__ uint64_t s_wave_u[17];
+  __shared__ int s_flag;
+  __shared__ int s_kmin;
+  __shared__ int s_cut[G][2];
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int bh = blockIdx.y;
+  const int b = bh / a.Hq, h = bh % a.Hq, g = h / G;
+  const int bg = b * a.Hkv + g;
+  const int32_t* hm = a.head_meta + (int64_t)bh * 16;
+  const int n = hm[0];
+  const int64_t S = hm[9];
+  const int64_t kvb = a.kv_indptr[b];
+
+  // ---- exact logits of this workgroup's share of the sampled rows (fp64)
+  {
+    const int lane = tid & 63, wave = tid >> 6, sl = lane & 15, grp = lane >> 4;
+    double qd[8];
+    {
+      const uint4 v = *reinterpret_cast<const uint4*>(a.q + (int64_t)bh * kHeadDim + sl * 8);
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        qd[2 * e] = (double)bf16lo(w[e]);
+        qd[2 * e + 1] = (double)bf16hi(w[e]);
+      }
+    }
+    const uint16_t* kbase = a.K + ((int64_t)g * a.total + kvb) * kHeadDim + sl * 8;
+    const int32_t* rows = a.sample_rows + (int64_t)bh * a.S_cap;
+    double* lg = a.logits + (int64_t)bh * a.S_cap;
+    const int64_t stride = (int64_t)a.split * 16;
+    for (int64_t u0 = ((int64_t)blockIdx.x * 4 + wave) * 4; u0 < S; u0 += stride) {
+      const int64_t u = u0 + grp;
+      double acc = 0.0;
+      if (u < S) {
+        const uint4 v = *reinterpret_cast<const uint4*>(kbase + (int64_t)rows[u] * kHeadDim);
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc = fma(qd[2 * e], (double)bf16lo(w[e]), acc);
+          acc = fma(qd[2 * e + 1], (double)bf16hi(w[e]), acc);
+        }
+      }
+      acc = sum16d(acc);
+      if (u < S && sl == 0) lg[u] = acc / 11.313708498984760390;  // sqrt(128)
+    }
+  }
+  if (!arrive_last(a.counters + bh, a.split, &s_flag)) return;
+
+  // ---- fit and budget of head bh (Algorithm 1), all in fp64
+  {
+    const double* lg = a.logits + (int64_t)bh * a.S_cap;
+    const int exact = hm[8];
+    const int64_t N = exact ? S : hm[1];
+    const int64_t W1 = hm[2], W2 = hm[3];
+    double* fit = a.fit + (int64_t)bh * kFitFields;
+    int k = 0;
+    double m = 0.0, mu1 = 0.0, mu2 = 0.0, fa = 0.0, fb = 0.0, Sn = 0.0, T = 0.0, EN = 0.0;
+    if (n > 0) {
+      double mx = -INFINITY;
+      for (int64_t u = tid; u < N; u += nt) mx = fmax(mx, lg[u]);
+      m = block_max_d(mx, s_wave_d);
+      // exact head: contiguous segment per thread, block scan of segment sums
+      const int64_t seg = (N + nt - 1) / nt;
+      const int64_t beg = min(N, (int64_t)tid * seg), end = min(N, beg + seg);
+      double loc = 0.0;
+      for (int64_t u = beg; u < end; ++u) loc += exp(lg[u] - m);
+      // block exclusive scan of loc
+      double incl = loc;
+      for (int o = 1; o < kWave; o <<= 1) {
+        const double y = __shfl_up(incl, o, kWave);
+        if ((tid & (kWave - 1)) >= o) incl += y;
+      }
+      if ((tid & (kWave - 1)) == kWave - 1) s_wave_d[tid / kWave] = incl;
+      __syncthreads();
+      if (tid == 0) {
+        double run = 0.0;
+        for (int w = 0; w < nt / kWave; ++w) {
+          const double t = s_wave_d[w];
+          s_wave_d[w] = run;
+          run += t;
+        }
+        s_wave_d[16] = run;
+      }
+      __syncthreads();
+      const double base = s_wave_d[tid / kWave] + incl - loc;
+      EN = s_wave_d[16];
+      __syncthreads();
+      double w1 = 0.0, w2 = 0.0;
+      for (int64_t u = N + tid; u < N + W1; u += nt) w1 += exp(lg[u] - m);
+      for (int64_t u = N + W1 + tid; u < N + W1 + W2; u += nt) w2 += exp(lg[u] - m);
+      w1 = block_sum<double>(w1, s_wave_d);
+      w2 = block_sum<double>(w2, s_wave_d);
+      if (exact) {
+        Sn = EN;
+      } else {
+        mu1 = w1 / (double)W1;
+        mu2 = w2 / (double)W2;
+        const double x1 = (double)(hm[4] + hm[5]) / 2.0, x2 = (double)(hm[6] + hm[7]) / 2.0;
+        fa = (mu1 - mu2) / (1.0 / x1 - 1.0 / x2);
+        fb = mu1 - fa / x1;
+        Sn = EN + tail_sum(fa, fb, N + 1, n);
+      }
+      if (a.P >= 1.0) {
+        k = n;
+      } else {
+        T = a.P * Sn;
+        if (T <= EN) {
+          if (tid == 0) s_kmin = 0x7fffffff;
+          __syncthreads();
+          double run = base;
+          for (int64_t u = beg; u < end; ++u) {
+            run += exp(lg[u] - m);
+            if (run >= T) {
+              atomicMin(&s_kmin, (int)(u + 1));
+              break;
+            }
+          }
+          __syncthreads();
+          k = s_kmin;
+          if (k == 0x7fffffff) k = (int)N;  // unreachable unless rounding lost the crossing
+        } else {
+          int64_t lo = N + 1, hi = n;
+          while (lo < hi) {
+            const int64_t mid = (lo + hi) >> 1;
+            if (EN + tail_sum(fa, fb, N + 1, mid) >= T) hi = mid;
+            else lo = mid + 1;
+          }
+          k = (int)lo;
+        }
+      }
+    }
+    // cutoff cluster: largest rank r with prefix[r] < k, and its selected length
+    const int C = hm[10];
+    const int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
+    if (tid == 0) {
+      int cut_r = -1, cut_len = 0;
+      if (k > 0) {
+        int lo_r = 0, hi_r = C;
+        while (lo_r < hi_r) {
+          const int mid = (lo_r + hi_r + 1) >> 1;
+          if (rpre[mid] < k) lo_r = mid;
+          else hi_r = mid - 1;
+        }
+        cut_r = lo_r;
+        cut_len = k - rpre[lo_r];
+      }
+      a.cut[bh * 2] = cut_r;
+      a.cut[bh * 2 + 1] = cut_len;
+      a.sel_count_q[bh] = k;
+      fit[0] = m; fit[1] = mu1; fit[2] = mu2; fit[3] = fa; fit[4] = fb; fit[5] = Sn; fit[6] = T;
+      fit[7] = (double)k; fit[8] = (double)N; fit[9] = (double)n; fit[10] = (double)exact;
+      fit[11] = (double)S; fit[12] = EN; fit[13] = (double)cut_r; fit[14] = (double)cut_len;
+      fit[15] = 0.0;
+    }
+  }
+  if (!arrive_last(a.counters + a.BH + bg, G, &s_flag)) return;
+
+  // ---- union of the group's selections (Sec. 4.5) and the attention work list
+  {
+    const int64_t cb = a.cl_indptr[b];
+    const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
+    const int32_t* off = a.offsets + (int64_t)g * (a.Ct + a.B) + cb + b;
+    if (tid < G) {
+      const int bh2 = b * a.Hq + g * G + tid;
+      s_cut[tid][0] = a.cut[bh2 * 2];
+      s_cut[tid][1] = a.cut[bh2 * 2 + 1];
+    }
+    __syncthreads();
+    int32_t* ulen = a.union_len + (int64_t)g * a.Ct + cb;
+    const int seg = (C + nt - 1) / nt;
+    const int beg = min(C, tid * seg), end = min(C, beg + seg);
+    uint64_t loc = 0;  // (ranges << 32) | tokens
+    for (int j = beg; j < end; ++j) {
+      const int size = off[j + 1] - off[j];
+      int L = 0;
+#pragma unroll
+      for (int hh = 0; hh < G; ++hh) {
+        const int bh2 = b * a.Hq + g * G + hh;
+        const int r = a.rank_of[(int64_t)bh2 * a.Cm + j];
+        const int len = r < s_cut[hh][0] ? size : (r == s_cut[hh][0] ? s_cut[hh][1] : 0);
+        L = max(L, len);
+      }
+      ulen[j] = L;
+      if (L > 0) loc += (1ull << 32) | (uint64_t)L;
+    }
+    uint64_t incl = loc;
+    for (int o = 1; o < kWave; o <<= 1) {
+      const uint64_t y = __shfl_up(incl, o, kWave);
+      if ((tid & (kWave - 1)) >= o) incl += y;
+    }
+    if ((tid & (kWave - 1)) == kWave - 1) s_wave_u[tid / kWave] = incl;
+    __syncthreads();
+    if (tid == 0) {
+      uint64_t run = 0;
+      for (int w = 0; w < nt / kWave; ++w) {
+        const uint64_t t = s_wave_u[w];
+        s_wave_u[w] = run;
+        run += t;
+      }
+      s_wave_u[16] = run;
+    }
+    __syncthreads();
+    const uint64_t base = s_wave_u[tid / kWave] + incl - loc;
+    const uint64_t tot = s_wave_u[16];
+    int idx = (int)(base >> 32);
+    int64_t upos = (int64_t)(base & 0xffffffffu);
+    const int64_t T = a.chunk_tokens;
+    int32_t* rstart = a.rstart + (int64_t)bg * a.Cm;
+    int32_t* rupos = a.rupos + (int64_t)bg * (a.Cm + 1);
+    int32_t* cfr = a.cfr + (int64_t)bg * a.max_chunks;
+    for (int j = beg; j < end; ++j) {
+      const int L = ulen[j];
+      if (L <= 0) continue;
+      rstart[idx] = off[j];
+      rupos[idx] = (int32_t)upos;
+      for (int64_t c = (upos + T - 1) / T; c * T < upos + L && c < a.max_chunks; ++c) cfr[c] = idx;
+      ++idx;
+      upos += L;
+    }
+    if (tid == 0) {
+      const int R = (int)(tot >> 32);
+      const int64_t U = (int64_t)(tot & 0xffffffffu);
+      rupos[R] = (int32_t)U;
+      a.gmeta[bg * 4 + 0] = R;
+      a.gmeta[bg * 4 + 1] = (int32_t)U;
+      a.gmeta[bg * 4 + 2] = (int32_t)((U + T - 1) / T);
+      a.gmeta[bg * 4 + 3] = 0;
+      a.sel_count_kv[bg] = (int32_t)U;
+    }
+  }
+}
+
+// ============================================================================
+// Launchers
+// ============================================================================
+hipError_t launch_score(const ScoreArgs& a, int G, int grid_x, int grid_y, hipStream_t st) {
+  dim3 grid(grid_x, grid_y);
+  switch (G) {
+    case 1: hipLaunchKernelGGL(score_clusters_kernel<1>, grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL(score_clusters_kernel<2>, grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL(score_clusters_kernel<4>, grid, dim3(256), 0, st, a); break;
+    case 8: hipLaunchKernelGGL(score_clusters_kernel<8>, grid, dim3(256), 0, st, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_sort(const SortArgs& a, bool lds, int n_heads, hipStream_t st) {
+  if (lds) {
+    const size_t bytes = (size_t)a.nb_max * 8 + 2 * ((size_t)a.nb_max + 4) * 4;
+    hipLaunchKernelGGL(sort_clusters_kernel<true>, dim3(n_heads), dim3(1024), bytes, st, a);
+  } else {
+    hipLaunchKernelGGL(sort_clusters_kernel<false>, dim3(n_heads), dim3(1024), 0, st, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_fit(const FitArgs& a, int G, int split, int n_heads, hipStream_t st) {
+  dim3 grid(split, n_heads);
+  switch (G) {
+    case 1: hipLaunchKernelGGL(sample_fit_union_kernel<1>, grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL(sample_fit_union_kernel<2>, grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL(sample_fit_union_kernel<4>, grid, dim3(256), 0, st, a); break;
+    case 8: hipLaunchKernelGGL(sample_fit_union_kernel<8>, grid, dim3(256), 0, st, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace tactic

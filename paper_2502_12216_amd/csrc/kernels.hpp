@@ -1,0 +1,87 @@
+// Kernel argument blocks and launchers (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.hpp"
+
+namespace tactic {
+
+struct ScoreArgs {
+  const uint16_t* q;          // bf16 [B][Hq][128]
+  const uint16_t* centroids;  // bf16 [Hkv][Ct][128]
+  const int64_t* cl_indptr;   // [B+1]
+  int B, Hq, Hkv, Cm;
+  int64_t Ct;
+  float* scores;              // [B*Hq][Cm]
+  int* counters;
+  int n_counters;
+};
+
+struct SortArgs {
+  const float* scores;        // [B*Hq][Cm]
+  const int32_t* offsets;     // [Hkv][Ct + B]
+  const int64_t* kv_indptr;
+  const int64_t* cl_indptr;
+  int B, Hq, Hkv, G, Cm, nb_max;
+  int64_t Ct, S_cap;
+  SelParams prm;
+  uint64_t* g_keys;           // sort scratch when the sort does not fit LDS
+  uint32_t* g_cnt;
+  uint32_t* g_start;
+  int32_t* order;             // [B*Hq][Cm]
+  int32_t* rank_of;           // [B*Hq][Cm]
+  int32_t* rprefix;           // [B*Hq][Cm+1]
+  int32_t* sample_rows;       // [B*Hq][S_cap]
+  int32_t* head_meta;         // [B*Hq][16]
+};
+
+struct FitArgs {
+  const uint16_t* q;
+  const uint16_t* K;          // cluster-sorted keys [Hkv][total][128]
+  const int64_t* kv_indptr;
+  const int64_t* cl_indptr;
+  const int32_t* offsets;
+  int B, Hq, Hkv, Cm, BH, split;
+  int64_t Ct, total, S_cap, chunk_tokens, max_chunks;
+  double P;
+  const int32_t* head_meta;
+  const int32_t* sample_rows;
+  const int32_t* rprefix;
+  const int32_t* rank_of;
+  double* logits;             // [B*Hq][S_cap]
+  double* fit;                // [B*Hq][16]
+  int32_t* cut;               // [B*Hq][2]
+  int32_t* sel_count_q;       // [B*Hq]
+  int32_t* sel_count_kv;      // [B*Hkv]
+  int32_t* union_len;         // [Hkv][Ct]
+  int32_t* gmeta;             // [B*Hkv][4]: ranges, union tokens, work items, -
+  int32_t* rstart;            // [B*Hkv][Cm]
+  int32_t* rupos;             // [B*Hkv][Cm+1]
+  int32_t* cfr;               // [B*Hkv][max_chunks]
+  int* counters;              // [BH] sampling, [BG] fitted heads
+};
+
+struct AttnArgs {
+  const uint16_t* q;
+  const uint16_t* K;
+  const uint16_t* V;
+  const int64_t* kv_indptr;
+  int B, Hq, Hkv, Cm, dense;
+  int64_t total, chunk_tokens, max_chunks;
+  const int32_t* gmeta;
+  const int32_t* rstart;
+  const int32_t* rupos;
+  const int32_t* cfr;
+  float* partials;            // [B*Hkv][max_chunks][G*130]
+  int* done;                  // [B*Hkv] items finished (self-resetting)
+  float* out;                 // [B][Hq][128]
+};
+
+hipError_t launch_score(const ScoreArgs& a, int G, int grid_x, int grid_y, hipStream_t st);
+hipError_t launch_sort(const SortArgs& a, bool lds, int n_heads, hipStream_t st);
+hipError_t launch_fit(const FitArgs& a, int G, int split, int n_heads, hipStream_t st);
+hipError_t launch_attn(const AttnArgs& a, int G, int grid, hipStream_t st);
+
+}  // namespace tactic

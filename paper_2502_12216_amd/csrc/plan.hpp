@@ -1,0 +1,41 @@
+// Host/device description of one sparse-decode launch sequence: sizes and
+// workspace offsets, derived once from the shape and parameters.
+#pragma once
+
+#include <stdint.h>
+
+#include "common.hpp"
+
+namespace tactic {
+
+constexpr int64_t kPlanMagic = 0x54414354494331LL;  // "TACTIC1"
+constexpr int kTile = 64;              // tokens per attention tile
+constexpr int kMaxChunkTokens = 1024;  // tokens per attention work item (upper bound)
+constexpr int kSortLdsBuckets = 8192;  // largest cluster count sorted in LDS
+constexpr int kMaxGroups = 4096;       // B * Hkv limit of the attention work list
+constexpr int kFitFields = 16;
+
+struct DecodePlan {
+  int64_t magic;
+  int64_t B, Hq, Hkv, G, Cm, Ct, nmax, total;
+  int64_t S_cap;         // sampled rows per head (capacity)
+  int64_t chunk_tokens;  // tokens per attention work item
+  int64_t max_chunks;    // work items per (b, g) (capacity)
+  int64_t split;         // sampling workgroups per query head
+  int64_t attn_grid;     // persistent attention workgroups
+  int64_t sort_lds;      // 1: sort in LDS, 0: sort scratch in the workspace
+  int64_t nb_max;        // bucket capacity of the sort
+  // workspace byte offsets
+  int64_t off_scores, off_order, off_rank, off_rprefix, off_headmeta, off_rows, off_logit;
+  int64_t off_fit, off_cut, off_union_len, off_gmeta, off_rstart, off_rupos, off_cfr;
+  int64_t off_partials, off_counters, off_sort_keys, off_sort_cnt, off_sort_start;
+  int64_t ws_bytes;
+  int64_t n_counters;
+  int64_t exact_bp, win_bp, win_min, p1_bp, p2_bp;
+  int64_t pad[64 - 42];
+};
+static_assert(sizeof(DecodePlan) == 64 * sizeof(int64_t), "plan must fill tactic_decode_plan");
+
+// Counters (int32) at off_counters: [0, BH) sampling done per head,
+// [BH, BH+BG) heads fitted per group, [BH+BG, BH+2BG) attention items done per group.
+}  // namespace tactic

@@ -1,0 +1,236 @@
+"""Thin torch-facing wrappers over the C ABI (include/tactic.h).
+
+Torch supplies device memory and the current stream; every step of the
+decode and of the clustering runs in libtactic.so.  There is no fallback: a
+missing library or a failing call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import _capi as C
+
+
+def _stream(stream=None) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+def _check_tensor(t: torch.Tensor, name: str, dtype, shape=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+
+
+def _indptr(lengths: Sequence[int]) -> np.ndarray:
+    ip = np.zeros(len(lengths) + 1, dtype=np.int64)
+    ip[1:] = np.cumsum(np.asarray(lengths, dtype=np.int64))
+    return ip
+
+
+class RaggedBatch:
+    """A ragged decode batch: sequence lengths, head counts, device indptr."""
+
+    def __init__(self, seq_lens: Sequence[int], n_q_heads: int, n_kv_heads: int, head_dim: int = 128,
+                 device="cuda"):
+        self.seq_lens = [int(x) for x in seq_lens]
+        self.n_q_heads, self.n_kv_heads, self.head_dim = int(n_q_heads), int(n_kv_heads), int(head_dim)
+        self.kv_indptr_host = _indptr(self.seq_lens)
+        self.kv_indptr = torch.as_tensor(self.kv_indptr_host, device=device)
+        self.total = int(self.kv_indptr_host[-1])
+        self.max_len = max(self.seq_lens) if self.seq_lens else 0
+
+    @property
+    def batch(self) -> int:
+        return len(self.seq_lens)
+
+    def struct(self) -> C.KVShape:
+        return C.KVShape(self.batch, self.n_q_heads, self.n_kv_heads, self.head_dim, self.total, self.max_len,
+                         self.kv_indptr.data_ptr())
+
+
+class ClusterSet:
+    """Cluster description of a cluster-sorted cache (see tactic_cluster_meta)."""
+
+    def __init__(self, centroids: torch.Tensor, offsets: torch.Tensor, n_clusters: Sequence[int]):
+        self.n_clusters = [int(x) for x in n_clusters]
+        self.cl_indptr_host = _indptr(self.n_clusters)
+        self.cl_indptr = torch.as_tensor(self.cl_indptr_host, device=centroids.device)
+        self.total = int(self.cl_indptr_host[-1])
+        self.max = max(self.n_clusters) if self.n_clusters else 0
+        _check_tensor(centroids, "centroids", torch.bfloat16)
+        _check_tensor(offsets, "offsets", torch.int32)
+        if centroids.shape[1:] != (self.total, 128):
+            raise ValueError(f"centroids must be [Hkv][{self.total}][128], got {tuple(centroids.shape)}")
+        if offsets.shape[1:] != (self.total + len(self.n_clusters),):
+            raise ValueError("offsets must be [Hkv][total_clusters + B]")
+        self.centroids, self.offsets = centroids, offsets
+
+    def struct(self) -> C.ClusterMeta:
+        return C.ClusterMeta(self.total, self.max, self.cl_indptr.data_ptr(), self.centroids.data_ptr(),
+                             self.offsets.data_ptr())
+
+
+def decode_params(target_frac: float = 0.9, **kw) -> C.DecodeParams:
+    p = C.DecodeParams()
+    C.lib().tactic_decode_params_default(ctypes.byref(p))
+    p.target_frac = float(target_frac)
+    for k, v in kw.items():
+        setattr(p, k, int(v))
+    return p
+
+
+class SparseDecoder:
+    """Tactic's decode for one batch shape: holds the launch plan and the
+    workspace, so repeated calls (layers, decode steps) allocate nothing."""
+
+    def __init__(self, batch: RaggedBatch, n_clusters: Sequence[int], params: Optional[C.DecodeParams] = None,
+                 device="cuda"):
+        self.batch = batch
+        self.params = params if params is not None else decode_params()
+        self.n_clusters = [int(x) for x in n_clusters]
+        meta = C.ClusterMeta(int(sum(self.n_clusters)), max(self.n_clusters), None, None, None)
+        self.plan = C.DecodePlan()
+        nbytes = ctypes.c_size_t()
+        self._shape = batch.struct()
+        C.check(C.lib().tactic_sparse_decode_plan(ctypes.byref(self._shape), ctypes.byref(meta),
+                                                  ctypes.byref(self.params), ctypes.byref(self.plan),
+                                                  ctypes.byref(nbytes)), "tactic_sparse_decode_plan")
+        self.workspace = torch.empty(max(1, nbytes.value), dtype=torch.uint8, device=device)
+        B, Hq, Hkv = batch.batch, batch.n_q_heads, batch.n_kv_heads
+        self.out = torch.empty(B, Hq, 128, dtype=torch.float32, device=device)
+        self.sel_q = torch.empty(B, Hq, dtype=torch.int32, device=device)
+        self.sel_kv = torch.empty(B, Hkv, dtype=torch.int32, device=device)
+
+    def __call__(self, q: torch.Tensor, K_sorted: torch.Tensor, V_sorted: torch.Tensor, clusters: ClusterSet,
+                 target_frac: Optional[float] = None, stream=None, out=None, sel_q=None, sel_kv=None):
+        b = self.batch
+        _check_tensor(q, "q", torch.bfloat16, (b.batch, b.n_q_heads, 128))
+        _check_tensor(K_sorted, "K_sorted", torch.bfloat16, (b.n_kv_heads, b.total, 128))
+        _check_tensor(V_sorted, "V_sorted", torch.bfloat16, (b.n_kv_heads, b.total, 128))
+        if clusters.n_clusters != self.n_clusters:
+            raise ValueError("cluster counts differ from the ones the decoder was planned for")
+        out = self.out if out is None else out
+        sel_q = self.sel_q if sel_q is None else sel_q
+        sel_kv = self.sel_kv if sel_kv is None else sel_kv
+        if target_frac is not None:
+            self.params.target_frac = float(target_frac)
+        meta = clusters.struct()
+        C.check(C.lib().tactic_sparse_decode(
+            q.data_ptr(), K_sorted.data_ptr(), V_sorted.data_ptr(), ctypes.byref(self._shape),
+            ctypes.byref(meta), ctypes.byref(self.params), ctypes.byref(self.plan), out.data_ptr(),
+            sel_q.data_ptr(), sel_kv.data_ptr(), self.workspace.data_ptr(), self.workspace.numel(),
+            _stream(stream)), "tactic_sparse_decode")
+        return out, sel_q, sel_kv
+
+    def view(self) -> dict:
+        """Intermediate stages of the last call, as tensors over the workspace."""
+        v = C.DecodeView()
+        C.check(C.lib().tactic_sparse_decode_view(ctypes.byref(self.plan), self.workspace.data_ptr(),
+                                                  ctypes.byref(v)), "tactic_sparse_decode_view")
+        base = self.workspace.data_ptr()
+        b = self.batch
+        BH = b.batch * b.n_q_heads
+        Cm = max(self.n_clusters)
+        Ct = int(sum(self.n_clusters))
+
+        def sl(ptr, count, dtype, shape):
+            off = ptr - base
+            nbytes = count * torch.empty(0, dtype=dtype).element_size()
+            return self.workspace[off:off + nbytes].view(dtype).view(*shape)
+
+        return {
+            "scores": sl(v.scores, BH * Cm, torch.float32, (b.batch, b.n_q_heads, Cm)),
+            "order": sl(v.order, BH * Cm, torch.int32, (b.batch, b.n_q_heads, Cm)),
+            "rank_prefix": sl(v.rank_prefix, BH * (Cm + 1), torch.int32, (b.batch, b.n_q_heads, Cm + 1)),
+            "fit": sl(v.fit, BH * C.FIT_FIELDS, torch.float64, (b.batch, b.n_q_heads, C.FIT_FIELDS)),
+            "union_len": sl(v.union_len, b.n_kv_heads * Ct, torch.int32, (b.n_kv_heads, Ct)),
+        }
+
+
+class DenseDecoder:
+    """Dense decode attention (the baseline) over every cached token."""
+
+    def __init__(self, batch: RaggedBatch, device="cuda"):
+        self.batch = batch
+        self._shape = batch.struct()
+        n = C.lib().tactic_dense_decode_workspace_size(ctypes.byref(self._shape))
+        if n == 0:
+            C.check(1, "tactic_dense_decode_workspace_size")
+        # the completion counters must start at zero; each call leaves them zero
+        self.workspace = torch.zeros(n, dtype=torch.uint8, device=device)
+        self.out = torch.empty(batch.batch, batch.n_q_heads, 128, dtype=torch.float32, device=device)
+
+    def __call__(self, q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, stream=None, out=None):
+        b = self.batch
+        _check_tensor(q, "q", torch.bfloat16, (b.batch, b.n_q_heads, 128))
+        _check_tensor(K, "K", torch.bfloat16, (b.n_kv_heads, b.total, 128))
+        _check_tensor(V, "V", torch.bfloat16, (b.n_kv_heads, b.total, 128))
+        out = self.out if out is None else out
+        C.check(C.lib().tactic_dense_decode(q.data_ptr(), K.data_ptr(), V.data_ptr(), ctypes.byref(self._shape),
+                                            out.data_ptr(), self.workspace.data_ptr(), self.workspace.numel(),
+                                            _stream(stream)), "tactic_dense_decode")
+        return out
+
+
+@dataclass
+class ClusterBuild:
+    clusters: ClusterSet
+    assign: torch.Tensor       # int32 [Hkv][total]
+    perm: torch.Tensor         # int32 [Hkv][total]
+    K_sorted: Optional[torch.Tensor]
+    V_sorted: Optional[torch.Tensor]
+
+
+class ClusterBuilder:
+    """Prefill K-means (tactic_build_clusters) for one batch shape."""
+
+    def __init__(self, batch: RaggedBatch, n_clusters: Sequence[int], max_iters: int = 10, device="cuda"):
+        self.batch = batch
+        self.n_clusters = [int(x) for x in n_clusters]
+        self.total_c = int(sum(self.n_clusters))
+        self.max_c = max(self.n_clusters)
+        self.cl_indptr_host = _indptr(self.n_clusters)
+        self.cl_indptr = torch.as_tensor(self.cl_indptr_host, device=device)
+        self.params = C.KMeansParams(int(max_iters))
+        self._shape = batch.struct()
+        n = C.lib().tactic_build_clusters_workspace_size(ctypes.byref(self._shape), self.total_c, self.max_c)
+        if n == 0:
+            raise C.TacticError("tactic_build_clusters_workspace_size rejected the shape")
+        self.workspace = torch.empty(n, dtype=torch.uint8, device=device)
+        self.device = device
+
+    def __call__(self, K: torch.Tensor, V: Optional[torch.Tensor], init_idx: torch.Tensor, sort_kv: bool = True,
+                 stream=None) -> ClusterBuild:
+        b = self.batch
+        Hkv = b.n_kv_heads
+        _check_tensor(K, "K", torch.bfloat16, (Hkv, b.total, 128))
+        if V is not None:
+            _check_tensor(V, "V", torch.bfloat16, (Hkv, b.total, 128))
+        _check_tensor(init_idx, "init_idx", torch.int32, (Hkv, self.total_c))
+        dev = K.device
+        cent = torch.empty(Hkv, self.total_c, 128, dtype=torch.bfloat16, device=dev)
+        assign = torch.empty(Hkv, b.total, dtype=torch.int32, device=dev)
+        offsets = torch.empty(Hkv, self.total_c + b.batch, dtype=torch.int32, device=dev)
+        perm = torch.empty(Hkv, b.total, dtype=torch.int32, device=dev)
+        Ks = torch.empty_like(K) if sort_kv else None
+        Vs = torch.empty_like(V) if (sort_kv and V is not None) else None
+        C.check(C.lib().tactic_build_clusters(
+            K.data_ptr(), V.data_ptr() if V is not None else None, ctypes.byref(self._shape),
+            self.cl_indptr.data_ptr(), self.total_c, self.max_c, init_idx.data_ptr(), ctypes.byref(self.params),
+            cent.data_ptr(), assign.data_ptr(), offsets.data_ptr(), perm.data_ptr(),
+            Ks.data_ptr() if Ks is not None else None, Vs.data_ptr() if Vs is not None else None,
+            self.workspace.data_ptr(), self.workspace.numel(), _stream(stream)), "tactic_build_clusters")
+        return ClusterBuild(ClusterSet(cent, offsets, self.n_clusters), assign, perm, Ks, Vs)

@@ -1,0 +1,132 @@
+"""Host-only checks of the C ABI: the library loads, exports every function
+include/tactic.h declares, and rejects bad arguments before any device work
+(no GPU is needed: every call here fails validation, which runs first)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2502_12216_amd import _capi as C
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x1000  # never dereferenced: validation fails before any launch
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "tactic.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(tactic_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_match_header():
+    L = C.lib()
+    names = header_functions()
+    assert sorted(C.EXPORTS) == names
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def _shape(B=1, Hq=8, Hkv=2, d=128, total=4096, nmax=4096, indptr=FAKE):
+    return C.KVShape(B, Hq, Hkv, d, total, nmax, indptr)
+
+
+def _params(P=0.9):
+    p = C.DecodeParams()
+    C.lib().tactic_decode_params_default(ctypes.byref(p))
+    p.target_frac = P
+    return p
+
+
+def _plan(shape, meta, params):
+    plan = C.DecodePlan()
+    n = ctypes.c_size_t()
+    st = C.lib().tactic_sparse_decode_plan(ctypes.byref(shape), ctypes.byref(meta), ctypes.byref(params),
+                                           ctypes.byref(plan), ctypes.byref(n))
+    return st, plan, n.value
+
+
+def test_defaults():
+    p = _params()
+    assert abs(p.target_frac - 0.9) < 1e-7
+    assert (p.exact_bp, p.win_bp, p.win_min, p.p1_bp, p.p2_bp, p.use_union) == (100, 50, 8, 1000, 6000, 1)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(d=64), 2), (dict(Hq=6, Hkv=4), 1), (dict(Hq=24, Hkv=2), 2), (dict(B=0), 1),
+    (dict(indptr=None), 1), (dict(total=10, nmax=20), 1),
+])
+def test_plan_rejects_bad_shapes(kw, code):
+    meta = C.ClusterMeta(256, 256, FAKE, FAKE, FAKE)
+    st, _, _ = _plan(_shape(**kw), meta, _params())
+    assert st == code, C.lib().tactic_last_error()
+
+
+@pytest.mark.parametrize("P", [0.0, -0.1, 1.5, float("nan")])
+def test_plan_rejects_bad_target(P):
+    meta = C.ClusterMeta(256, 256, FAKE, FAKE, FAKE)
+    st, _, _ = _plan(_shape(), meta, _params(P))
+    assert st == 1
+
+
+def test_plan_rejects_inconsistent_clusters_and_no_union():
+    st, _, _ = _plan(_shape(), C.ClusterMeta(100, 256, FAKE, FAKE, FAKE), _params())
+    assert st == 1
+    p = _params()
+    p.use_union = 0
+    st, _, _ = _plan(_shape(), C.ClusterMeta(256, 256, FAKE, FAKE, FAKE), p)
+    assert st == 2
+
+
+def test_plan_workspace_grows_with_shape():
+    meta = C.ClusterMeta(256, 256, FAKE, FAKE, FAKE)
+    st, plan, n1 = _plan(_shape(), meta, _params())
+    assert st == 0 and n1 > 0
+    st, _, n2 = _plan(_shape(B=2, total=8192), C.ClusterMeta(512, 256, FAKE, FAKE, FAKE), _params())
+    assert st == 0 and n2 > n1
+
+
+def test_decode_rejects_small_workspace_and_mismatched_plan():
+    L = C.lib()
+    shape = _shape()
+    meta = C.ClusterMeta(256, 256, FAKE, FAKE, FAKE)
+    params = _params()
+    st, plan, nbytes = _plan(shape, meta, params)
+    assert st == 0
+    st = L.tactic_sparse_decode(FAKE, FAKE, FAKE, ctypes.byref(shape), ctypes.byref(meta), ctypes.byref(params),
+                                ctypes.byref(plan), FAKE, FAKE, FAKE, FAKE, nbytes - 1, None)
+    assert st == 3
+    other = _shape(B=2, total=8192)
+    st = L.tactic_sparse_decode(FAKE, FAKE, FAKE, ctypes.byref(other), ctypes.byref(meta), ctypes.byref(params),
+                                ctypes.byref(plan), FAKE, FAKE, FAKE, FAKE, nbytes, None)
+    assert st == 1
+    st = L.tactic_sparse_decode(None, FAKE, FAKE, ctypes.byref(shape), ctypes.byref(meta), ctypes.byref(params),
+                                ctypes.byref(plan), FAKE, FAKE, FAKE, FAKE, nbytes, None)
+    assert st == 1
+    assert "null" in L.tactic_last_error().decode()
+
+
+def test_dense_and_kmeans_validation():
+    L = C.lib()
+    shape = _shape()
+    n = L.tactic_dense_decode_workspace_size(ctypes.byref(shape))
+    assert n > 0
+    assert L.tactic_dense_decode(FAKE, FAKE, FAKE, ctypes.byref(shape), FAKE, FAKE, n - 1, None) == 3
+    bad = _shape(d=96)
+    assert L.tactic_dense_decode_workspace_size(ctypes.byref(bad)) == 0
+    kp = C.KMeansParams(0)
+    m = L.tactic_build_clusters_workspace_size(ctypes.byref(shape), 256, 256)
+    assert m > 0
+    st = L.tactic_build_clusters(FAKE, FAKE, ctypes.byref(shape), FAKE, 256, 256, FAKE, ctypes.byref(kp),
+                                 FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, m, None)
+    assert st == 1
+    kp.max_iters = 10
+    st = L.tactic_build_clusters(FAKE, FAKE, ctypes.byref(shape), FAKE, 100, 256, FAKE, ctypes.byref(kp),
+                                 FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, m, None)
+    assert st == 1
+
+
+def test_status_strings():
+    L = C.lib()
+    for s in range(5):
+        assert len(L.tactic_status_string(s)) > 0

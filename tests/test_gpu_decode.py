@@ -1,0 +1,241 @@
+"""GPU parity of the sparse and dense decode against the fp64 oracle.
+
+Inputs are the seeded synthetic workloads (synth), laid out by the
+generator's own mixture labels, so no input of the oracle comes from the HIP
+path.  Every call goes through the C ABI of libtactic.so.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import attention as OA
+from oracle import tactic as OT
+from tests.parity import check_group, fit_params, group_inputs, np64
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _tactic():
+    import paper_2502_12216_amd as P
+    return P
+
+
+def _p32(P: float) -> float:
+    """The library takes P as fp32; the oracle gets the same value."""
+    return float(np.float32(P))
+
+
+def run_sparse(inp, lay, P, params=None):
+    T = _tactic()
+    wl = inp.wl
+    lens = [int(inp.kv_indptr[i + 1] - inp.kv_indptr[i]) for i in range(len(inp.kv_indptr) - 1)]
+    ncl = [int(lay.cl_indptr[i + 1] - lay.cl_indptr[i]) for i in range(len(lay.cl_indptr) - 1)]
+    batch = T.RaggedBatch(lens, wl.n_q_heads, wl.n_kv_heads)
+    params = params or T.decode_params(P)
+    dec = T.SparseDecoder(batch, ncl, params)
+    cl = T.ClusterSet(lay.centroids.to(DEV).contiguous(), lay.offsets.to(DEV).contiguous(), ncl)
+    out, sq, skv = dec(inp.q.to(DEV).contiguous(), lay.K_sorted.to(DEV).contiguous(),
+                       lay.V_sorted.to(DEV).contiguous(), cl, target_frac=P)
+    torch.cuda.synchronize()
+    view = {k: v.clone().cpu() for k, v in dec.view().items()}
+    return dict(out=out.clone().cpu(), sel_q=sq.clone().cpu(), sel_kv=skv.clone().cpu(), view=view,
+                params=params, decoder=dec)
+
+
+def check_layer(inp, lay, P, res, groups=None, label=""):
+    wl = inp.wl
+    G = wl.n_q_heads // wl.n_kv_heads
+    B = len(inp.kv_indptr) - 1
+    prm = fit_params(res["params"])
+    todo = groups if groups is not None else [(b, g) for b in range(B) for g in range(wl.n_kv_heads)]
+    allstats = []
+    for b, g in todo:
+        gi = group_inputs(inp.q, lay.K_sorted, lay.V_sorted, lay.centroids, lay.offsets, lay.kv_indptr,
+                          lay.cl_indptr, b, g, G)
+        c0, c1 = int(lay.cl_indptr[b]), int(lay.cl_indptr[b + 1])
+        v = res["view"]
+        gpu = dict(scores=np64(v["scores"][b, g * G:(g + 1) * G]),
+                   order=v["order"][b, g * G:(g + 1) * G].numpy(),
+                   k=res["sel_q"][b, g * G:(g + 1) * G].numpy(),
+                   union_len=v["union_len"][g, c0:c1].numpy(),
+                   out=np64(res["out"][b, g * G:(g + 1) * G]),
+                   sel_kv=int(res["sel_kv"][b, g]))
+        allstats.append(check_group(gi, _p32(P), prm, gpu, label=f"{label} b={b} g={g}"))
+    return allstats
+
+
+def _small(base, lens, name=None):
+    return synth.small_workload(synth.WORKLOADS[base], lens, name)
+
+
+@pytest.mark.parametrize("P", [0.5, 0.8, 0.9, 0.95, 1.0])
+def test_sparse_ctx4k_full_parity(P):
+    inp = synth.make_layer(synth.WORKLOADS["ctx4k_gqa4"], 0)
+    lay = synth.label_layout(inp)
+    res = run_sparse(inp, lay, P)
+    st = check_layer(inp, lay, P, res, label=f"ctx4k P={P}")
+    print(f"ctx4k P={P}: k={[s['k'] for s in st]} union={[s['union'] for s in st]} "
+          f"err={max(s['out_err'] for s in st):.2e}")
+    if P == 1.0:
+        assert all(s["union"] == s["n"] for s in st)
+
+
+def test_sparse_ragged_small_with_empty_and_tiny_sequences():
+    # lengths straddle tiles, a 1-token and a 5-token sequence (exact mode) and an empty one
+    wl = _small("ctx32k_llama8b", [700, 0, 1, 5, 1300, 64, 3000])
+    inp = synth.make_layer(wl, 0)
+    lay = synth.label_layout(inp)
+    for P in (0.3, 0.9):
+        res = run_sparse(inp, lay, P)
+        check_layer(inp, lay, P, res, label=f"ragged P={P}")
+        B = len(inp.kv_indptr) - 1
+        G = wl.n_q_heads // wl.n_kv_heads
+        assert torch.all(res["out"][1] == 0) and torch.all(res["sel_q"][1] == 0)
+        assert torch.all(res["sel_kv"][1] == 0)
+
+
+def test_sparse_one_cluster_per_token_is_top_p():
+    """Every token its own cluster (centroid = key) and every score exact:
+    the selection of each head must be the exact top-P prefix (Sec. 3.4)."""
+    T = _tactic()
+    torch.manual_seed(0)
+    n, Hq, Hkv = 2000, 4, 1
+    K = (torch.randn(Hkv, n, 128) * 0.6).to(torch.bfloat16)
+    V = torch.randn(Hkv, n, 128).to(torch.bfloat16)
+    q = (torch.randn(1, Hq, 128) * 1.5).to(torch.bfloat16)
+    offsets = torch.arange(n + 1, dtype=torch.int32)[None].contiguous()
+    batch = T.RaggedBatch([n], Hq, Hkv)
+    for P in (0.5, 0.9, 0.99):
+        params = T.decode_params(P, exact_bp=10000)
+        dec = T.SparseDecoder(batch, [n], params)
+        cl = T.ClusterSet(K.to(DEV).contiguous(), offsets.to(DEV), [n])
+        out, sq, skv = dec(q.to(DEV), K.to(DEV), V.to(DEV), cl)
+        torch.cuda.synchronize()
+        Kd, Vd, qd = np64(K[0]), np64(V[0]), np64(q[0])
+        U = set()
+        for h in range(Hq):
+            ref = OA.optimal_selection(qd[h], Kd, _p32(P))
+            kg = int(sq[0, h])
+            if kg != len(ref):  # accept only a cutoff tie
+                s = OA.softmax_weights(OA.logits(qd[h], Kd))
+                cs = np.add.accumulate(np.sort(s)[::-1])
+                assert abs(cs[kg - 1] - _p32(P)) <= 1e-5 or abs(cs[len(ref) - 1] - _p32(P)) <= 1e-5
+            U |= set(OA.optimal_selection(qd[h], Kd, _p32(P))[:kg].tolist())
+        assert int(skv[0, 0]) == len(U)
+        for h in range(Hq):
+            ref = OA.sparse_attention(qd[h], Kd, Vd, np.array(sorted(U)))
+            assert float(np.max(np.abs(np64(out[0, h]) - ref))) <= 2e-3
+
+
+def test_sparse_single_cluster_and_target_one_is_dense():
+    T = _tactic()
+    wl = _small("ctx4k_gqa4", [1500, 333])
+    inp = synth.make_layer(wl, 0)
+    lay = synth.label_layout(inp)
+    res = run_sparse(inp, lay, 1.0)
+    G = wl.n_q_heads // wl.n_kv_heads
+    for b, n in enumerate([1500, 333]):
+        for h in range(wl.n_q_heads):
+            g = h // G
+            s0 = int(inp.kv_indptr[b])
+            ref = OA.dense_attention(np64(inp.q[b, h]), np64(inp.K[g, s0:s0 + n]), np64(inp.V[g, s0:s0 + n]))
+            assert float(np.max(np.abs(np64(res["out"][b, h]) - ref))) <= 2e-3
+            assert int(res["sel_q"][b, h]) == n
+    # one cluster holding every token
+    K1 = lay.K_sorted.clone()
+    n = 1500
+    cent = inp.K[:, :1].clone().contiguous()
+    off = torch.tensor([[0, n]] * wl.n_kv_heads, dtype=torch.int32)
+    lay1 = synth.LabelLayout(K_sorted=K1[:, :n].contiguous(), V_sorted=lay.V_sorted[:, :n].contiguous(),
+                             centroids=cent, offsets=off, perm=lay.perm[:, :n].contiguous(),
+                             kv_indptr=np.array([0, n]), cl_indptr=np.array([0, 1]))
+    inp1 = synth.make_layer(_small("ctx4k_gqa4", [n]), 0)
+    inp1.q = inp.q[:1].clone()
+    res1 = run_sparse(inp1, lay1, 0.9)
+    check_layer(inp1, lay1, 0.9, res1, label="one cluster")
+
+
+def test_sparse_is_deterministic():
+    inp = synth.make_layer(_small("ctx32k_llama8b", [5000, 2500]), 0)
+    lay = synth.label_layout(inp)
+    a = run_sparse(inp, lay, 0.9)
+    b = run_sparse(inp, lay, 0.9)
+    assert torch.equal(a["out"], b["out"]) and torch.equal(a["sel_q"], b["sel_q"])
+    assert torch.equal(a["sel_kv"], b["sel_kv"])
+
+
+@pytest.mark.parametrize("P", [0.8, 0.9, 0.95])
+def test_sparse_ctx32k_full_parity(P):
+    inp = synth.make_layer(synth.WORKLOADS["ctx32k_llama8b"], 0, device=DEV)
+    lay = synth.label_layout(inp)
+    res = run_sparse(inp, lay, P)
+    st = check_layer(inp, lay, P, res, label=f"ctx32k P={P}")
+    ks = np.array([s["k"] for s in st]).ravel()
+    us = np.array([s["union"] for s in st])
+    print(f"ctx32k P={P}: k median {np.median(ks):.0f} max {ks.max()} union median {np.median(us):.0f}"
+          f" max {us.max()} ties(order)={sum(s['order_ties'] for s in st)} ties(cut)={sum(s['cut_ties'] for s in st)}")
+
+
+def test_sparse_ctx128k_b4_layer_sampled_parity():
+    """The timed workload's shape (batch 4 x 128K, 32q/8kv, 8192 clusters per
+    head), one layer, parity on a seeded sample of (b, g) groups."""
+    wl = synth.WORKLOADS["ctx128k_b4_32layer"]
+    inp = synth.make_layer(wl, 3, device=DEV)
+    lay = synth.label_layout(inp)
+    res = run_sparse(inp, lay, 0.9)
+    rng = np.random.default_rng(5)
+    groups = [(int(b), int(g)) for b, g in zip(rng.integers(0, 4, 4), rng.integers(0, 8, 4))]
+    st = check_layer(inp, lay, 0.9, res, groups=groups, label="ctx128k")
+    print("ctx128k sampled:", [(s["k"], s["union"]) for s in st])
+
+
+@pytest.mark.slow
+def test_sparse_ctx1m_global_sort_sampled_parity():
+    """1M tokens with 32768 clusters per head: the cluster sort runs out of
+    the workspace instead of LDS."""
+    wl = synth.WORKLOADS["ctx1m"]
+    inp = synth.make_layer(wl, 0, device=DEV)
+    lay = synth.label_layout(inp)
+    res = run_sparse(inp, lay, 0.9)
+    st = check_layer(inp, lay, 0.9, res, groups=[(0, 2), (0, 5)], label="ctx1m")
+    print("ctx1m sampled:", [(s["k"], s["union"]) for s in st])
+
+
+def test_sparse_ragged16_sampled_parity():
+    wl = synth.WORKLOADS["ragged16_16k_128k"]
+    inp = synth.make_layer(wl, 0, device=DEV, seq_subset=[0, 3, 7, 11])
+    lay = synth.label_layout(inp)
+    res = run_sparse(inp, lay, 0.9)
+    st = check_layer(inp, lay, 0.9, res, groups=[(0, 1), (1, 6), (2, 0), (3, 7)], label="ragged16")
+    print("ragged16 sampled:", [(s["n"], s["k"], s["union"]) for s in st])
+
+
+# ------------------------------------------------------------------ dense
+
+@pytest.mark.parametrize("lens", [[4096], [700, 0, 1, 5, 1300], [33000, 1000]])
+def test_dense_decode_matches_oracle(lens):
+    T = _tactic()
+    wl = _small("ctx32k_llama8b", lens)
+    inp = synth.make_layer(wl, 0, device=DEV)
+    batch = T.RaggedBatch(lens, wl.n_q_heads, wl.n_kv_heads)
+    dec = T.DenseDecoder(batch)
+    out = dec(inp.q, inp.K, inp.V)
+    out2 = dec(inp.q, inp.K, inp.V).clone()  # counters reset after a call
+    torch.cuda.synchronize()
+    G = wl.n_q_heads // wl.n_kv_heads
+    err = 0.0
+    for b, n in enumerate(lens):
+        s0 = int(batch.kv_indptr_host[b])
+        for h in range(wl.n_q_heads):
+            if n == 0:
+                assert torch.all(out2[b, h] == 0)
+                continue
+            g = h // G
+            ref = OA.dense_attention(np64(inp.q[b, h]), np64(inp.K[g, s0:s0 + n]), np64(inp.V[g, s0:s0 + n]))
+            err = max(err, float(np.max(np.abs(np64(out2[b, h]) - ref))))
+    assert err <= 2e-3, err
