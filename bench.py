@@ -1,0 +1,271 @@
+"""Benchmark of Tactic's sparse decode attention on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is one full decode step of the workload: every layer runs the whole
+hot path (centroid scoring, cluster sort, sampled logits + fit + cutoff +
+union, gather split-K attention) on its own cluster-sorted cache.  The
+default workload is 32 layers of a batch of 4 sequences of 131072 tokens
+(32 query / 8 KV heads, head_dim 128, bf16, 8192 clusters per sequence and
+KV head, target fraction 0.9) on seeded synthetic Gaussian-mixture keys.
+Its clusters come from the library's own K-means (10 iterations, timed
+separately), or from the generator's mixture labels with --clusters labels.
+
+Prints one JSON line: sparse microseconds per layer (lower is better), the
+same-GPU dense decode time and speedup, the HBM rate on the bytes the
+kernels must read, a roofline record of the dominant kernel and the CPU
+oracle's time on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "sparse decode-attn µs/layer + HBM GB/s at 128K ctx; speedup vs dense"
+
+
+def log(msg: str) -> None:
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="ctx128k_b4_32layer", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--layers", type=int, default=0, help="override the layer count (0: the workload's)")
+    ap.add_argument("--target-frac", type=float, default=0.9)
+    ap.add_argument("--clusters", choices=["kmeans", "labels"], default="kmeans")
+    ap.add_argument("--cpu-groups", type=int, default=4, help="(b, g) groups the CPU oracle times")
+    ap.add_argument("--no-cpu", action="store_true")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build runs on a single MI355X and has no multi-GPU path "
+              "(the decode shards by (sequence, KV head) with no exchange; see the design notes).",
+              file=sys.stderr)
+        sys.exit(2)
+    import paper_2502_12216_amd as T
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = "cuda"
+    wl = synth.WORKLOADS[args.workload]
+    layers = args.layers or wl.layers
+    B, Hq, Hkv = wl.batch, wl.n_q_heads, wl.n_kv_heads
+    G = Hq // Hkv
+    ncl = list(wl.cluster_counts)
+    batch = T.RaggedBatch(wl.seq_lens, Hq, Hkv)
+    P = float(np.float32(args.target_frac))
+
+    # ---------------------------------------------------------------- inputs + clustering
+    qs, Ks, Vs, cls = [], [], [], []
+    kmeans_ms = 0.0
+    builder = T.ClusterBuilder(batch, ncl, max_iters=wl.kmeans_iters) if args.clusters == "kmeans" else None
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_gen = time.time()
+    for l in range(layers):
+        inp = synth.make_layer(wl, l, device=dev)
+        if builder is not None:
+            init = torch.as_tensor(synth.kmeans_init_all(wl, l), device=dev)
+            ev0.record()
+            cb = builder(inp.K, inp.V, init)
+            ev1.record()
+            torch.cuda.synchronize()
+            kmeans_ms += ev0.elapsed_time(ev1)
+            qs.append(inp.q)
+            Ks.append(cb.K_sorted)
+            Vs.append(cb.V_sorted)
+            cls.append(cb.clusters)
+            del cb
+        else:
+            lay = synth.label_layout(inp)
+            qs.append(inp.q)
+            Ks.append(lay.K_sorted)
+            Vs.append(lay.V_sorted)
+            cls.append(T.ClusterSet(lay.centroids, lay.offsets, ncl))
+            del lay
+        del inp
+        if l % 4 == 3 or l == layers - 1:
+            log(f"layer {l + 1}/{layers} ready ({time.time() - t_gen:.1f}s, k-means {kmeans_ms / 1000:.2f}s)")
+    torch.cuda.synchronize()
+
+    params = T.decode_params(P)
+    dec = T.SparseDecoder(batch, ncl, params)
+    dense = T.DenseDecoder(batch)
+
+    def sparse_step():
+        for l in range(layers):
+            dec(qs[l], Ks[l], Vs[l], cls[l])
+
+    def dense_step():
+        for l in range(layers):
+            dense(qs[l], Ks[l], Vs[l])
+
+    def timed(step, n):
+        torch.cuda.synchronize()
+        ev0.record()
+        for _ in range(n):
+            step()
+        ev1.record()
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1) / n
+
+    for _ in range(args.warmup):
+        sparse_step()
+        dense_step()
+    ms_sparse = timed(sparse_step, args.steps)
+    log(f"sparse step {ms_sparse:.3f} ms")
+    ms_dense = timed(dense_step, args.steps)
+    log(f"dense step {ms_dense:.3f} ms")
+
+    # ---------------------------------------------------------------- per-stage timing (HIP events)
+    NS = 6
+    stage_ev = [torch.cuda.Event(enable_timing=True) for _ in range(NS + 1)]
+    for e in stage_ev:
+        e.record()
+    torch.cuda.synchronize()
+    import ctypes
+    from paper_2502_12216_amd import _capi as C
+    arr = (ctypes.c_void_p * (NS + 1))(*[e.cuda_event for e in stage_ev])
+    C.check(C.lib().tactic_sparse_decode_plan_set_events(ctypes.byref(dec.plan), arr), "set_events")
+    stage_ms = np.zeros(NS)
+    nrep = 0
+    for _ in range(args.steps):
+        for l in range(layers):
+            dec(qs[l], Ks[l], Vs[l], cls[l])
+            torch.cuda.synchronize()
+            for i in range(NS):
+                stage_ms[i] += stage_ev[i].elapsed_time(stage_ev[i + 1])
+            nrep += 1
+    C.check(C.lib().tactic_sparse_decode_plan_set_events(ctypes.byref(dec.plan), None), "set_events")
+    stage_ms /= nrep
+    stage_names = ["score_clusters", "sort_clusters", "sample_logits", "fit_union", "attn_splitk", "combine"]
+
+    # ---------------------------------------------------------------- selection statistics, bytes
+    sel_q, sel_kv, samples = [], [], []
+    for l in range(layers):
+        _, sq, skv = dec(qs[l], Ks[l], Vs[l], cls[l])
+        v = dec.view()
+        sel_q.append(sq.cpu().numpy().copy())
+        sel_kv.append(skv.cpu().numpy().copy())
+        samples.append(v["fit"][..., 11].cpu().numpy().copy())
+    sel_q, sel_kv, samples = np.array(sel_q), np.array(sel_kv), np.array(samples)
+    lens = np.array(wl.seq_lens, dtype=np.float64)
+    Csum = float(sum(ncl))
+    bytes_centroids = Hkv * Csum * 256 + Hkv * (Csum + B) * 4
+    bytes_samples = samples.sum(axis=(1, 2)) * 256            # per layer
+    bytes_union = sel_kv.sum(axis=(1, 2)) * 512               # per layer
+    bytes_layer = bytes_centroids + bytes_samples + bytes_union
+    dense_bytes_layer = float(lens.sum()) * Hkv * 512
+    us_sparse = ms_sparse * 1000 / layers
+    us_dense = ms_dense * 1000 / layers
+    gbps = float(bytes_layer.mean()) / (us_sparse * 1e3)
+    stage_us = stage_ms * 1000
+    stage_bytes = [bytes_centroids, 0.0, float(bytes_samples.mean()), 0.0, float(bytes_union.mean()), 0.0]
+    dom = int(np.argmax(stage_us))
+    dom_bytes = stage_bytes[dom]
+    roof = {
+        "kernel": stage_names[dom],
+        "bound": "hbm",
+        "achieved": round(dom_bytes / (stage_us[dom] * 1e3), 1),
+        "peak": HBM_PEAK_GBPS,
+        "unit": "GB/s",
+        "frac": round(dom_bytes / (stage_us[dom] * 1e3) / HBM_PEAK_GBPS, 4),
+        "traffic": None,
+    }
+    if stage_bytes[dom] == 0.0:
+        roof["bound"] = "alu"
+    kq = sel_q.astype(np.float64) / lens[None, :, None]
+    ku = sel_kv.astype(np.float64) / lens[None, :, None]
+
+    # ---------------------------------------------------------------- CPU oracle on a bounded sample
+    cpu = None
+    if not args.no_cpu:
+        from oracle import tactic as OT
+        rng = np.random.default_rng(17)
+        groups = [(int(rng.integers(0, B)), int(rng.integers(0, Hkv))) for _ in range(args.cpu_groups)]
+        cl0 = cls[0]
+        kvp = batch.kv_indptr_host
+        clp = cl0.cl_indptr_host
+        t_or = 0.0
+        for b, g in groups:
+            s0, s1 = int(kvp[b]), int(kvp[b + 1])
+            c0, c1 = int(clp[b]), int(clp[b + 1])
+            Qg = qs[0][b, g * G:(g + 1) * G].double().cpu().numpy()
+            Kg = Ks[0][g, s0:s1].double().cpu().numpy()
+            Vg = Vs[0][g, s0:s1].double().cpu().numpy()
+            cent = cl0.centroids[g, c0:c1].double().cpu().numpy()
+            off = cl0.offsets[g, c0 + b:c1 + b + 1].cpu().numpy().astype(np.int64)
+            t0 = time.perf_counter()
+            OT.decode_group(Qg, Kg, Vg, cent, off, P)
+            t_or += time.perf_counter() - t0
+        per_group = t_or / len(groups)
+        try:
+            from threadpoolctl import threadpool_info
+            blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        except Exception:
+            blas_threads = 1
+        cpu = {"value": round(per_group * B * Hkv * 1e6, 1), "unit": "us/layer", "cores": int(blas_threads),
+               "kind": "oracle",
+               "sample": f"{len(groups)} of the {B * Hkv} (sequence, KV head) groups of layer 0, fp64 NumPy "
+                         f"oracle decode_group each ({t_or:.1f} s total), scaled to one layer; "
+                         f"host {platform.processor() or platform.machine()}, "
+                         f"{len(os.sched_getaffinity(0))} cores visible"}
+        log(f"cpu oracle {per_group:.2f} s per group")
+
+    res = {
+        "metric": METRIC,
+        "value": round(us_sparse, 2),
+        "unit": "us/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_sparse, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": B, "seq_len": int(wl.seq_lens[0]), "layers": layers,
+                   "n_q_heads": Hq, "n_kv_heads": Hkv, "head_dim": 128, "clusters_per_seq": int(ncl[0]),
+                   "target_frac": args.target_frac, "clustering": args.clusters},
+        "dense_us_per_layer": round(us_dense, 2),
+        "speedup_vs_dense": round(us_dense / us_sparse, 3),
+        "hbm_gbps": round(gbps, 1),
+        "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
+        "dense_hbm_gbps": round(dense_bytes_layer / (us_dense * 1e3), 1),
+        "bytes_per_layer": {"centroids": bytes_centroids, "samples": float(bytes_samples.mean()),
+                            "union_kv": float(bytes_union.mean()), "dense_kv": dense_bytes_layer},
+        "stages_us_per_layer": {n: round(float(t), 2) for n, t in zip(stage_names, stage_us)},
+        "selected_frac": {"head_mean": round(float(kq.mean()), 5), "head_median": round(float(np.median(kq)), 5),
+                          "head_max": round(float(kq.max()), 5), "union_mean": round(float(ku.mean()), 5),
+                          "union_max": round(float(ku.max()), 5)},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    if args.clusters == "kmeans":
+        res["kmeans"] = {"seconds_all_layers": round(kmeans_ms / 1000, 3), "layers": layers,
+                         "iters": wl.kmeans_iters}
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -137,6 +137,14 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted,
                                    void* workspace, size_t workspace_bytes,
                                    hipStream_t stream);
 
+/* Optional per-stage timing: with events set (an array of 7 created events,
+ * or NULL to clear), every tactic_sparse_decode with this plan records
+ * events[0] before its first kernel and events[1..6] after each of its six
+ * kernels (centroid scoring, cluster sort, sampled logits, fit + union,
+ * attention, combine) on the call's stream.  The events stay owned by the
+ * caller. */
+tactic_status tactic_sparse_decode_plan_set_events(tactic_decode_plan* plan, hipEvent_t* events);
+
 /* Number of fp64 fields per query head in the fit record of the view below:
  *   0 m (logit shift: max over the exact head)   1 mu_1   2 mu_2   3 a   4 b
  *   5 S_n (estimated total)   6 T = P * S_n   7 k   8 N   9 n   10 exact mode
@@ -160,8 +168,7 @@ tactic_status tactic_sparse_decode_view(const tactic_decode_plan* plan, const vo
 
 /* Dense decode attention over every token (Eq. 2), the baseline.  Same
  * layouts as tactic_sparse_decode (any row order works: attention does not
- * depend on it).  The workspace must be zero-filled before its first use
- * with this call; each completed call leaves its counters zero again. */
+ * depend on it).  Workspace contents on entry are irrelevant. */
 size_t tactic_dense_decode_workspace_size(const tactic_kv_shape* shape);
 tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const uint16_t* V,
                                   const tactic_kv_shape* shape, float* out, void* workspace,

@@ -18,6 +18,7 @@ FIT_NAMES = ("m", "mu1", "mu2", "a", "b", "S_n", "T", "k", "N", "n", "exact", "s
 # every symbol include/tactic.h declares
 EXPORTS = (
     "tactic_decode_params_default", "tactic_sparse_decode_plan", "tactic_sparse_decode",
+    "tactic_sparse_decode_plan_set_events",
     "tactic_sparse_decode_view", "tactic_dense_decode_workspace_size", "tactic_dense_decode",
     "tactic_build_clusters_workspace_size", "tactic_build_clusters", "tactic_status_string",
     "tactic_last_error",
@@ -65,6 +66,7 @@ def lib() -> ctypes.CDLL:
     global _lib
     if _lib is not None:
         return _lib
+    import torch  # noqa: F401  (load torch's HIP runtime first so both share one)
     if not os.path.exists(LIB_PATH):
         raise TacticError(f"{LIB_PATH} is missing: build it with `python -m paper_2502_12216_amd.build`")
     L = ctypes.CDLL(LIB_PATH)
@@ -77,6 +79,8 @@ def lib() -> ctypes.CDLL:
                                        POINTER(DecodeParams), POINTER(DecodePlan), c_void_p, c_void_p,
                                        c_void_p, c_void_p, c_size_t, c_void_p]
     L.tactic_sparse_decode.restype = c_int
+    L.tactic_sparse_decode_plan_set_events.argtypes = [POINTER(DecodePlan), c_void_p]
+    L.tactic_sparse_decode_plan_set_events.restype = c_int
     L.tactic_sparse_decode_view.argtypes = [POINTER(DecodePlan), c_void_p, POINTER(DecodeView)]
     L.tactic_sparse_decode_view.restype = c_int
     L.tactic_dense_decode_workspace_size.argtypes = [POINTER(KVShape)]

@@ -167,8 +167,8 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape, const tact
   p.S_cap = S_cap;
   p.chunk_tokens = 256;
   p.max_chunks = std::max<int64_t>(1, (p.nmax + p.chunk_tokens - 1) / p.chunk_tokens);
-  p.split = std::min<int64_t>(64, std::max<int64_t>(1, (S_cap + 63) / 64));
-  p.attn_grid = 1024;
+  p.split = std::min<int64_t>(256, std::max<int64_t>(1, (S_cap + 63) / 64));
+  p.attn_grid = tactic::kAttnGrid;
   int64_t nb = 1;
   while (nb < p.Cm) nb <<= 1;
   p.sort_lds = nb <= tactic::kSortLdsBuckets ? 1 : 0;
@@ -191,8 +191,6 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape, const tact
   p.off_rupos = L.take(BG * (p.Cm + 1) * 4);
   p.off_cfr = L.take(BG * p.max_chunks * 4);
   p.off_partials = L.take(BG * p.max_chunks * p.G * (tactic::kHeadDim + 2) * 4);
-  p.n_counters = BH + 2 * BG;
-  p.off_counters = L.take(p.n_counters * 4);
   if (!p.sort_lds) {
     p.off_sort_keys = L.take(BH * p.nb_max * 8);
     p.off_sort_cnt = L.take(BH * (p.nb_max + 4) * 4);
@@ -229,7 +227,12 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
 
   char* ws = static_cast<char*>(workspace);
   const int BH = (int)(p.B * p.Hq), BG = (int)(p.B * p.Hkv);
-  int* counters = reinterpret_cast<int*>(ws + p.off_counters);
+  const bool timed = p.events[0] != 0;
+  auto record = [&](int i) -> hipError_t {
+    return timed ? hipEventRecord(reinterpret_cast<hipEvent_t>(p.events[i]), stream) : hipSuccess;
+  };
+  hipError_t e = record(0);
+  if (e != hipSuccess) return hip_fail(e, "event record");
 
   tactic::ScoreArgs sa;
   sa.q = q;
@@ -241,9 +244,8 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   sa.Cm = (int)p.Cm;
   sa.Ct = p.Ct;
   sa.scores = reinterpret_cast<float*>(ws + p.off_scores);
-  sa.counters = counters;
-  sa.n_counters = (int)p.n_counters;
-  hipError_t e = tactic::launch_score(sa, (int)p.G, (int)((p.Cm + 63) / 64), BG, stream);
+  e = tactic::launch_score(sa, (int)p.G, (int)((p.Cm + tactic::kScoreRows - 1) / tactic::kScoreRows), BG, stream);
+  if (e == hipSuccess) e = record(1);
   if (e != hipSuccess) return hip_fail(e, "score_clusters launch");
 
   tactic::SortArgs so;
@@ -269,6 +271,7 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   so.sample_rows = reinterpret_cast<int32_t*>(ws + p.off_rows);
   so.head_meta = reinterpret_cast<int32_t*>(ws + p.off_headmeta);
   e = tactic::launch_sort(so, p.sort_lds != 0, BH, stream);
+  if (e == hipSuccess) e = record(2);
   if (e != hipSuccess) return hip_fail(e, "sort_clusters launch");
 
   tactic::FitArgs fa;
@@ -280,6 +283,7 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   fa.B = (int)p.B;
   fa.Hq = (int)p.Hq;
   fa.Hkv = (int)p.Hkv;
+  fa.G = (int)p.G;
   fa.Cm = (int)p.Cm;
   fa.BH = BH;
   fa.split = (int)p.split;
@@ -303,9 +307,12 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   fa.rstart = reinterpret_cast<int32_t*>(ws + p.off_rstart);
   fa.rupos = reinterpret_cast<int32_t*>(ws + p.off_rupos);
   fa.cfr = reinterpret_cast<int32_t*>(ws + p.off_cfr);
-  fa.counters = counters;
-  e = tactic::launch_fit(fa, (int)p.G, (int)p.split, BH, stream);
-  if (e != hipSuccess) return hip_fail(e, "sample_fit_union launch");
+  e = tactic::launch_sample(fa, (int)p.split, BH, stream);
+  if (e == hipSuccess) e = record(3);
+  if (e != hipSuccess) return hip_fail(e, "sample_logits launch");
+  e = tactic::launch_fit_union(fa, (int)p.G, BG, stream);
+  if (e == hipSuccess) e = record(4);
+  if (e != hipSuccess) return hip_fail(e, "fit_union launch");
 
   tactic::AttnArgs aa;
   aa.q = q;
@@ -325,10 +332,24 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   aa.rupos = fa.rupos;
   aa.cfr = fa.cfr;
   aa.partials = reinterpret_cast<float*>(ws + p.off_partials);
-  aa.done = counters + BH + BG;
   aa.out = out;
   e = tactic::launch_attn(aa, (int)p.G, (int)p.attn_grid, stream);
+  if (e == hipSuccess) e = record(5);
   if (e != hipSuccess) return hip_fail(e, "attention launch");
+  e = tactic::launch_combine(aa, (int)p.G, stream);
+  if (e == hipSuccess) e = record(6);
+  if (e != hipSuccess) return hip_fail(e, "combine launch");
+  return TACTIC_OK;
+}
+
+tactic_status tactic_sparse_decode_plan_set_events(tactic_decode_plan* plan_in, hipEvent_t* events) {
+  if (!plan_in) return fail(TACTIC_ERR_INVALID_ARG, "null plan");
+  tactic::DecodePlan* p = reinterpret_cast<tactic::DecodePlan*>(plan_in);
+  if (p->magic != tactic::kPlanMagic) return fail(TACTIC_ERR_INVALID_ARG, "not a decode plan");
+  for (int i = 0; i < tactic::kStageEvents; ++i) {
+    if (events && !events[i]) return fail(TACTIC_ERR_INVALID_ARG, "event %d is null", i);
+    p->events[i] = events ? reinterpret_cast<int64_t>(events[i]) : 0;
+  }
   return TACTIC_OK;
 }
 
@@ -353,7 +374,6 @@ size_t tactic_dense_decode_workspace_size(const tactic_kv_shape* shape) {
   const int64_t G = shape->n_q_heads / shape->n_kv_heads;
   const int64_t max_chunks = std::max<int64_t>(1, (shape->max_seq_len + T - 1) / T);
   Layout L;
-  L.take(BG * 4);  // counters
   L.take(BG * max_chunks * G * (tactic::kHeadDim + 2) * 4);
   return (size_t)L.cur;
 }
@@ -370,11 +390,6 @@ tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const ui
   const int64_t T = dense_chunk_tokens(shape);
   const int64_t BG = (int64_t)shape->batch * shape->n_kv_heads;
   const int64_t max_chunks = std::max<int64_t>(1, (shape->max_seq_len + T - 1) / T);
-  Layout L;
-  const int64_t off_cnt = L.take(BG * 4);
-  const int64_t off_part = L.take(BG * max_chunks * (shape->n_q_heads / shape->n_kv_heads) *
-                                  (tactic::kHeadDim + 2) * 4);
-  char* ws = static_cast<char*>(workspace);
   tactic::AttnArgs aa;
   memset(&aa, 0, sizeof(aa));
   aa.q = q;
@@ -388,12 +403,13 @@ tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const ui
   aa.total = shape->total_tokens;
   aa.chunk_tokens = T;
   aa.max_chunks = max_chunks;
-  aa.partials = reinterpret_cast<float*>(ws + off_part);
-  aa.done = reinterpret_cast<int*>(ws + off_cnt);
+  aa.partials = static_cast<float*>(workspace);
   aa.out = out;
+  const int G = shape->n_q_heads / shape->n_kv_heads;
   const int64_t items = BG * max_chunks;
-  const int grid = (int)std::min<int64_t>(std::max<int64_t>(items, 1), 2048);
-  hipError_t e = tactic::launch_attn(aa, shape->n_q_heads / shape->n_kv_heads, grid, stream);
+  const int grid = (int)std::min<int64_t>(std::max<int64_t>(items, 1), tactic::kAttnGrid);
+  hipError_t e = tactic::launch_attn(aa, G, grid, stream);
+  if (e == hipSuccess) e = tactic::launch_combine(aa, G, stream);
   if (e != hipSuccess) return hip_fail(e, "dense attention launch");
   return TACTIC_OK;
 }

@@ -59,7 +59,18 @@ __host__ __device__ inline Geometry make_geometry(int64_t n, const SelParams& p)
 __device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
+// 2^x with the hardware instruction (v_exp_f32; results below 2^-126 flush
+// to zero, which is harmless for softmax weights); 2^-inf = 0
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 typedef short short2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte streaming load (non-temporal hint: the data is read once)
+__device__ __forceinline__ uint4 load_stream16(const uint16_t* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 
 // a.x*b.x + a.y*b.y + c on bf16 pairs, fp32 accumulate (v_dot2_f32_bf16)
 __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
@@ -68,13 +79,22 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
 }
 
 // ----------------------------------------------------------------------------
-// Cross-lane reductions within groups of 16 lanes (xor butterflies)
+// Cross-lane reductions within groups of 16 lanes (one DPP row)
 // ----------------------------------------------------------------------------
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF,
+                                                               false));
+}
+
+// Sum over the 16 lanes of a DPP row, bitwise identical in every lane: each
+// step adds a lane and its mirror partner (row_mirror, row_half_mirror, then
+// quad swaps), so both partners compute the same commutative sum.
 __device__ __forceinline__ float sum16(float v) {
-  v += __shfl_xor(v, 8, 16);
-  v += __shfl_xor(v, 4, 16);
-  v += __shfl_xor(v, 2, 16);
-  v += __shfl_xor(v, 1, 16);
+  v += dpp<0x140>(v);  // row_mirror: lane i + lane 15-i
+  v += dpp<0x141>(v);  // row_half_mirror: lane i + lane 7-i within each half
+  v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]
   return v;
 }
 
@@ -94,26 +114,6 @@ __device__ __forceinline__ float wave_max(float v) {
 __device__ __forceinline__ float wave_sum(float v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;
-}
-
-// ----------------------------------------------------------------------------
-// Device-scope completion counters ("last workgroup finishes the job").
-// Every thread that wrote results calls arrive(); the function returns true in
-// all threads of the workgroup that observed the final arrival.  The release
-// fence before the increment and the acquire fence after it make the other
-// workgroups' writes visible across XCDs.
-// ----------------------------------------------------------------------------
-__device__ __forceinline__ bool arrive_last(int* counter, int expected, int* s_flag) {
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const int prev = __hip_atomic_fetch_add(counter, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    *s_flag = (prev == expected - 1) ? 1 : 0;
-  }
-  __syncthreads();
-  const bool last = *s_flag != 0;
-  if (last) __threadfence();
-  return last;
 }
 
 }  // namespace tactic

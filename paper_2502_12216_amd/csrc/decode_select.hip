@@ -3,10 +3,10 @@
 //   score_clusters     q . centroid for every (query head, cluster)       Sec. 4.3
 //   sort_clusters      per query head: cluster order (score desc, id asc),
 //                      tokens ahead of every rank, sampled-row list        Sec. 4.3, Alg. 1 input
-//   sample_fit_union   exact logits of the sampled rows (fp64); the last
-//                      workgroup of a head fits y = a/x + b and finds the
-//                      budget k; the last head of a GQA group forms the
-//                      union and the attention work list                   Sec. 4.4, 4.5, Alg. 1
+//   sample_logits      exact logits of the sampled rows (fp64)             Alg. 1
+//   fit_union          per GQA group: fit y = a/x + b and the budget k of
+//                      every head, then the union of the group's selections
+//                      and the attention work list                         Sec. 4.4, 4.5, Alg. 1
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -96,21 +96,19 @@ __device__ float block_minmax(float v, bool want_max, float* s_wave) {
 }
 
 // ============================================================================
-// 1. Centroid scoring: s[b][h][j] = q_h . c_{b,g,j}, fp32 accumulation.
-//    grid (ceil(Cm/64), B*Hkv), 256 threads; 16 lanes own one centroid row
-//    (16 B each), a wave scores 4 rows per step, the group's G query heads sit
-//    in registers.  Block (0,0) also clears the call's completion counters.
+// 1. Centroid scoring: s[b][h][j] = q_h . c_{b,g,j}, fp32 accumulation of
+//    bf16 products (v_dot2).  grid (ceil(Cm/kScoreRows), B*Hkv), 256 threads;
+//    16 lanes own one centroid row (16 B each), a wave scores 4 rows per step
+//    with 4 steps of loads in flight; the group's G query heads sit in
+//    registers.
 // ============================================================================
 template <int G>
 __global__ __launch_bounds__(256) void score_clusters_kernel(ScoreArgs a) {
   const int bg = blockIdx.y;
-  if (blockIdx.x == 0 && bg == 0) {
-    for (int i = threadIdx.x; i < a.n_counters; i += blockDim.x) a.counters[i] = 0;
-  }
   const int b = bg / a.Hkv, g = bg % a.Hkv;
   const int64_t cb = a.cl_indptr[b];
   const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
-  const int j0 = blockIdx.x * 64;
+  const int j0 = blockIdx.x * kScoreRows;
   if (j0 >= C) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, sl = lane & 15, grp = lane >> 4;
 
@@ -120,24 +118,29 @@ __global__ __launch_bounds__(256) void score_clusters_kernel(ScoreArgs a) {
     const uint4 v = *reinterpret_cast<const uint4*>(a.q + ((int64_t)b * a.Hq + g * G + h) * kHeadDim + sl * 8);
     qw[h][0] = v.x; qw[h][1] = v.y; qw[h][2] = v.z; qw[h][3] = v.w;
   }
-  const uint16_t* cbase = a.centroids + ((int64_t)g * a.Ct + cb) * kHeadDim;
+  const uint16_t* cbase = a.centroids + ((int64_t)g * a.Ct + cb) * kHeadDim + sl * 8;
+  float* sc = a.scores + ((int64_t)b * a.Hq + g * G) * a.Cm;
+  constexpr int kPerWave = kScoreRows / 4;  // rows per wave, 4 per step
+#pragma unroll 1
+  for (int it0 = 0; it0 < kPerWave / 4; it0 += 4) {
+    uint4 c[4];
 #pragma unroll
-  for (int it = 0; it < 4; ++it) {
-    const int j = j0 + wave * 16 + it * 4 + grp;
-    uint4 c = make_uint4(0, 0, 0, 0);
-    if (j < C) c = *reinterpret_cast<const uint4*>(cbase + (int64_t)j * kHeadDim + sl * 8);
-    const float cf[8] = {bf16lo(c.x), bf16hi(c.x), bf16lo(c.y), bf16hi(c.y),
-                         bf16lo(c.z), bf16hi(c.z), bf16lo(c.w), bf16hi(c.w)};
+    for (int k = 0; k < 4; ++k) {
+      const int j = j0 + wave * kPerWave + (it0 + k) * 4 + grp;
+      c[k] = j < C ? load_stream16(cbase + (int64_t)j * kHeadDim) : make_uint4(0, 0, 0, 0);
+    }
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      float s = 0.f;
-      const uint32_t* w = qw[h];
-      const float qf[8] = {bf16lo(w[0]), bf16hi(w[0]), bf16lo(w[1]), bf16hi(w[1]),
-                           bf16lo(w[2]), bf16hi(w[2]), bf16lo(w[3]), bf16hi(w[3])};
+    for (int k = 0; k < 4; ++k) {
+      const int j = j0 + wave * kPerWave + (it0 + k) * 4 + grp;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) s = fmaf(qf[e], cf[e], s);
-      s = sum16(s);
-      if (sl == h && j < C) a.scores[((int64_t)b * a.Hq + g * G + h) * a.Cm + j] = s;
+      for (int h = 0; h < G; ++h) {
+        float d = dot2_bf16(c[k].x, qw[h][0], 0.f);
+        d = dot2_bf16(c[k].y, qw[h][1], d);
+        d = dot2_bf16(c[k].z, qw[h][2], d);
+        d = dot2_bf16(c[k].w, qw[h][3], d);
+        d = sum16(d);
+        if (sl == h && j < C) sc[(int64_t)h * a.Cm + j] = d;
+      }
     }
   }
 }
@@ -189,59 +192,122 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
   while (nb < C) nb <<= 1;
 
   for (int i = tid; i < nb + 1; i += nt) cnt[i] = 0;
-  float lo = INFINITY, hi = -INFINITY;
-  for (int j = tid; j < C; j += nt) {
-    const float s = sc[j];
-    if (s == s) {
-      lo = fminf(lo, s);
-      hi = fmaxf(hi, s);
-    }
-  }
-  lo = block_minmax(lo, false, s_wave_f);
-  hi = block_minmax(hi, true, s_wave_f);
-  const float range = hi - lo;
-  const bool spread = range > 0.f;
-  auto bucket_of = [&](float s) -> int {
-    if (!(s == s)) return nb - 1;
-    if (!spread) return 0;
-    const float t = floorf((hi - s) / range * (float)nb);
-    return (int)fminf((float)(nb - 1), fmaxf(0.f, t));
-  };
-  __syncthreads();
-  for (int j = tid; j < C; j += nt) atomicAdd(&cnt[bucket_of(sc[j])], 1u);
-  __syncthreads();
-  for (int i = tid; i < nb; i += nt) start[i] = cnt[i];
-  __syncthreads();
-  block_exclusive_scan<uint32_t>(start, nb, s_wave_u);
-  for (int j = tid; j < C; j += nt) {
-    const float s = sc[j];
-    const uint64_t key = ((uint64_t)desc_key_bits(s) << 32) | (uint32_t)j;
-    const uint32_t slot = atomicAdd(&start[bucket_of(s)], 1u);
-    keys[slot] = key;
-  }
-  __syncthreads();
   int32_t* rank_of = a.rank_of + (int64_t)bh * a.Cm;
   int32_t* order = a.order + (int64_t)bh * a.Cm;
-  for (int j = tid; j < C; j += nt) {
-    const float s = sc[j];
-    const uint64_t key = ((uint64_t)desc_key_bits(s) << 32) | (uint32_t)j;
-    const int bk = bucket_of(s);
-    const uint32_t end = start[bk], beg = end - cnt[bk];
-    uint32_t r = 0;
-    for (uint32_t t = beg; t < end; ++t) r += keys[t] < key ? 1u : 0u;
-    const int pos = (int)(beg + r);
-    order[pos] = j;
-    rank_of[j] = pos;
+  int32_t* ord_s = reinterpret_cast<int32_t*>(keys);  // cluster id by rank, after the sort
+  if constexpr (kLds) {
+    // C <= 8192 = 8 * 1024: every thread keeps its 8 elements in registers
+    float v[8];
+    int sz[8], bk[8], pos[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int j = tid + e * 1024;
+      v[e] = j < C ? sc[j] : NAN;
+      sz[e] = j < C ? off[j + 1] - off[j] : 0;
+    }
+    float lo = INFINITY, hi = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      if (v[e] == v[e]) {
+        lo = fminf(lo, v[e]);
+        hi = fmaxf(hi, v[e]);
+      }
+    }
+    lo = block_minmax(lo, false, s_wave_f);
+    hi = block_minmax(hi, true, s_wave_f);
+    const float range = hi - lo;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float sv = v[e];
+      int b2 = nb - 1;
+      if (sv == sv) b2 = range > 0.f ? (int)fminf((float)(nb - 1), fmaxf(0.f, floorf((hi - sv) / range * (float)nb))) : 0;
+      bk[e] = b2;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (tid + e * 1024 < C) atomicAdd(&cnt[bk[e]], 1u);
+    __syncthreads();
+    for (int i = tid; i < nb; i += nt) start[i] = cnt[i];
+    __syncthreads();
+    block_exclusive_scan<uint32_t>(start, nb, s_wave_u);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int j = tid + e * 1024;
+      if (j < C) keys[atomicAdd(&start[bk[e]], 1u)] = ((uint64_t)desc_key_bits(v[e]) << 32) | (uint32_t)j;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int j = tid + e * 1024;
+      pos[e] = 0;
+      if (j < C) {
+        const uint64_t key = ((uint64_t)desc_key_bits(v[e]) << 32) | (uint32_t)j;
+        const uint32_t end = start[bk[e]], beg = end - cnt[bk[e]];
+        uint32_t r = 0;
+        for (uint32_t t = beg; t < end; ++t) r += keys[t] < key ? 1u : 0u;
+        pos[e] = (int)(beg + r);
+        order[pos[e]] = j;
+        rank_of[j] = pos[e];
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int j = tid + e * 1024;
+      if (j < C) {
+        cnt[pos[e]] = (uint32_t)sz[e];
+        ord_s[pos[e]] = j;
+      }
+    }
+    __syncthreads();
+  } else {
+    float lo = INFINITY, hi = -INFINITY;
+    for (int j = tid; j < C; j += nt) {
+      const float sv = sc[j];
+      if (sv == sv) {
+        lo = fminf(lo, sv);
+        hi = fmaxf(hi, sv);
+      }
+    }
+    lo = block_minmax(lo, false, s_wave_f);
+    hi = block_minmax(hi, true, s_wave_f);
+    const float range = hi - lo;
+    auto bucket_of = [&](float sv) -> int {
+      if (!(sv == sv)) return nb - 1;
+      if (!(range > 0.f)) return 0;
+      return (int)fminf((float)(nb - 1), fmaxf(0.f, floorf((hi - sv) / range * (float)nb)));
+    };
+    __syncthreads();
+    for (int j = tid; j < C; j += nt) atomicAdd(&cnt[bucket_of(sc[j])], 1u);
+    __syncthreads();
+    for (int i = tid; i < nb; i += nt) start[i] = cnt[i];
+    __syncthreads();
+    block_exclusive_scan<uint32_t>(start, nb, s_wave_u);
+    for (int j = tid; j < C; j += nt) {
+      const float sv = sc[j];
+      keys[atomicAdd(&start[bucket_of(sv)], 1u)] = ((uint64_t)desc_key_bits(sv) << 32) | (uint32_t)j;
+    }
+    __syncthreads();
+    for (int j = tid; j < C; j += nt) {
+      const float sv = sc[j];
+      const uint64_t key = ((uint64_t)desc_key_bits(sv) << 32) | (uint32_t)j;
+      const int b2 = bucket_of(sv);
+      const uint32_t end = start[b2], beg = end - cnt[b2];
+      uint32_t r = 0;
+      for (uint32_t t = beg; t < end; ++t) r += keys[t] < key ? 1u : 0u;
+      const int p2 = (int)(beg + r);
+      order[p2] = j;
+      rank_of[j] = p2;
+    }
+    __syncthreads();
+    for (int j = tid; j < C; j += nt) {
+      const int p2 = rank_of[j];
+      cnt[p2] = (uint32_t)(off[j + 1] - off[j]);
+      ord_s[p2] = j;
+    }
+    __syncthreads();
   }
-  __syncthreads();
-  // sizes by rank -> cnt, cluster id by rank -> keys (reused as int32)
-  int32_t* ord_s = reinterpret_cast<int32_t*>(keys);
-  for (int j = tid; j < C; j += nt) {
-    const int pos = rank_of[j];
-    cnt[pos] = (uint32_t)(off[j + 1] - off[j]);
-    ord_s[pos] = j;
-  }
-  __syncthreads();
   const uint32_t ntok = block_exclusive_scan<uint32_t>(cnt, C, s_wave_u);
   if (tid == 0) cnt[C] = ntok;
   __syncthreads();
@@ -301,265 +367,294 @@ __device__ double harmonic(int64_t x) {
          r2 * (1.0 / 12.0 - r2 * (1.0 / 120.0 - r2 * (1.0 / 252.0 - r2 * (1.0 / 240.0))));
 }
 
-// sum_{i=lo}^{hi} max(0, a/i + b), lo >= 1, evaluated in closed form over the
-// interval where a/i + b is positive (a/i + b is monotone in i).
-__device__ double tail_sum(double a, double b, int64_t lo, int64_t hi) {
-  if (hi < lo) return 0.0;
-  int64_t L = lo, R = hi;
+// Positive interval [L, R] of a/i + b over integer i in [lo, hi] (the
+// function is monotone in i, so where it is positive is an interval); returns
+// false when it is empty.
+__device__ bool positive_interval(double a, double b, int64_t lo, int64_t hi, int64_t* L, int64_t* R) {
+  if (hi < lo) return false;
+  *L = lo;
+  *R = hi;
   auto f = [&](int64_t i) { return a / (double)i + b; };
   if (a >= 0.0 && b >= 0.0) {
-    // all terms non-negative
+    // every term is non-negative
   } else if (a <= 0.0 && b <= 0.0) {
-    return 0.0;
+    return false;
   } else if (a > 0.0) {  // b < 0: positive for i < a / -b
     const double z = a / -b;
     int64_t r = z >= (double)hi ? hi : (z <= (double)lo ? lo - 1 : (int64_t)z);
     while (r >= lo && !(f(r) > 0.0)) --r;
     while (r + 1 <= hi && f(r + 1) > 0.0) ++r;
-    R = r;
+    *R = r;
   } else {  // a < 0, b > 0: positive for i > -a / b
     const double z = -a / b;
     int64_t l = z >= (double)hi ? hi + 1 : (z < (double)lo ? lo : (int64_t)z + 1);
     while (l <= hi && !(f(l) > 0.0)) ++l;
     while (l - 1 >= lo && f(l - 1) > 0.0) --l;
-    L = l;
+    *L = l;
   }
-  if (R < L) return 0.0;
+  return *L <= *R;
+}
+
+// sum_{i=lo}^{hi} max(0, a/i + b) in closed form: a (H(R) - H(L-1)) + b (R - L + 1)
+// over the positive interval [L, R].
+__device__ double tail_sum(double a, double b, int64_t lo, int64_t hi) {
+  int64_t L, R;
+  if (!positive_interval(a, b, lo, hi, &L, &R)) return 0.0;
   return a * (harmonic(R) - harmonic(L - 1)) + b * (double)(R - L + 1);
 }
 
-template <int G>
-__global__ __launch_bounds__(256) void sample_fit_union_kernel(FitArgs a) {
-  __shared__ double s_wave_d[17];
-  __shared__ uint64_t s_wave_u[17];
-  __shared__ int s_flag;
-  __shared__ int s_kmin;
-  __shared__ int s_cut[G][2];
-  const int tid = threadIdx.x, nt = blockDim.x;
+// 3a. Exact logits of the sampled rows, fp64 (products of bf16 values are
+//     exact in fp64).  grid (split, B*Hq), 256 threads; 16 lanes per row, each
+//     wave gathers 16 rows per round with all loads issued before use.
+__global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
+  const int tid = threadIdx.x;
   const int bh = blockIdx.y;
-  const int b = bh / a.Hq, h = bh % a.Hq, g = h / G;
-  const int bg = b * a.Hkv + g;
-  const int32_t* hm = a.head_meta + (int64_t)bh * 16;
-  const int n = hm[0];
-  const int64_t S = hm[9];
-  const int64_t kvb = a.kv_indptr[b];
-
-  // ---- exact logits of this workgroup's share of the sampled rows (fp64)
+  const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
+  const int64_t S = a.head_meta[(int64_t)bh * 16 + 9];
+  const int lane = tid & 63, wave = tid >> 6, sl = lane & 15, grp = lane >> 4;
+  double qd[8];
   {
-    const int lane = tid & 63, wave = tid >> 6, sl = lane & 15, grp = lane >> 4;
-    double qd[8];
-    {
-      const uint4 v = *reinterpret_cast<const uint4*>(a.q + (int64_t)bh * kHeadDim + sl * 8);
-      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    const uint4 v = *reinterpret_cast<const uint4*>(a.q + (int64_t)bh * kHeadDim + sl * 8);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      qd[2 * e] = (double)bf16lo(w[e]);
+      qd[2 * e + 1] = (double)bf16hi(w[e]);
+    }
+  }
+  const uint16_t* kbase = a.K + ((int64_t)g * a.total + a.kv_indptr[b]) * kHeadDim + sl * 8;
+  const int32_t* rows = a.sample_rows + (int64_t)bh * a.S_cap;
+  double* lg = a.logits + (int64_t)bh * a.S_cap;
+  const int64_t stride = (int64_t)a.split * 64;
+  for (int64_t base = ((int64_t)blockIdx.x * 4 + wave) * 16; base < S; base += stride) {
+    int32_t r[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int64_t u = base + k * 4 + grp;
+      r[k] = u < S ? rows[u] : -1;
+    }
+    uint4 kv[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      kv[k] = r[k] >= 0 ? load_stream16(kbase + (int64_t)r[k] * kHeadDim) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t w[4] = {kv[k].x, kv[k].y, kv[k].z, kv[k].w};
+      double acc = 0.0;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        qd[2 * e] = (double)bf16lo(w[e]);
-        qd[2 * e + 1] = (double)bf16hi(w[e]);
-      }
-    }
-    const uint16_t* kbase = a.K + ((int64_t)g * a.total + kvb) * kHeadDim + sl * 8;
-    const int32_t* rows = a.sample_rows + (int64_t)bh * a.S_cap;
-    double* lg = a.logits + (int64_t)bh * a.S_cap;
-    const int64_t stride = (int64_t)a.split * 16;
-    for (int64_t u0 = ((int64_t)blockIdx.x * 4 + wave) * 4; u0 < S; u0 += stride) {
-      const int64_t u = u0 + grp;
-      double acc = 0.0;
-      if (u < S) {
-        const uint4 v = *reinterpret_cast<const uint4*>(kbase + (int64_t)rows[u] * kHeadDim);
-        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc = fma(qd[2 * e], (double)bf16lo(w[e]), acc);
-          acc = fma(qd[2 * e + 1], (double)bf16hi(w[e]), acc);
-        }
+        acc = fma(qd[2 * e], (double)bf16lo(w[e]), acc);
+        acc = fma(qd[2 * e + 1], (double)bf16hi(w[e]), acc);
       }
       acc = sum16d(acc);
+      const int64_t u = base + k * 4 + grp;
       if (u < S && sl == 0) lg[u] = acc / 11.313708498984760390;  // sqrt(128)
     }
   }
-  if (!arrive_last(a.counters + bh, a.split, &s_flag)) return;
+}
 
-  // ---- fit and budget of head bh (Algorithm 1), all in fp64
-  {
-    const double* lg = a.logits + (int64_t)bh * a.S_cap;
-    const int exact = hm[8];
-    const int64_t N = exact ? S : hm[1];
-    const int64_t W1 = hm[2], W2 = hm[3];
-    double* fit = a.fit + (int64_t)bh * kFitFields;
-    int k = 0;
-    double m = 0.0, mu1 = 0.0, mu2 = 0.0, fa = 0.0, fb = 0.0, Sn = 0.0, T = 0.0, EN = 0.0;
-    if (n > 0) {
-      double mx = -INFINITY;
-      for (int64_t u = tid; u < N; u += nt) mx = fmax(mx, lg[u]);
-      m = block_max_d(mx, s_wave_d);
-      // exact head: contiguous segment per thread, block scan of segment sums
-      const int64_t seg = (N + nt - 1) / nt;
-      const int64_t beg = min(N, (int64_t)tid * seg), end = min(N, beg + seg);
-      double loc = 0.0;
-      for (int64_t u = beg; u < end; ++u) loc += exp(lg[u] - m);
-      // block exclusive scan of loc
-      double incl = loc;
-      for (int o = 1; o < kWave; o <<= 1) {
-        const double y = __shfl_up(incl, o, kWave);
-        if ((tid & (kWave - 1)) >= o) incl += y;
-      }
-      if ((tid & (kWave - 1)) == kWave - 1) s_wave_d[tid / kWave] = incl;
-      __syncthreads();
-      if (tid == 0) {
-        double run = 0.0;
-        for (int w = 0; w < nt / kWave; ++w) {
-          const double t = s_wave_d[w];
-          s_wave_d[w] = run;
-          run += t;
-        }
-        s_wave_d[16] = run;
-      }
-      __syncthreads();
-      const double base = s_wave_d[tid / kWave] + incl - loc;
-      EN = s_wave_d[16];
-      __syncthreads();
-      double w1 = 0.0, w2 = 0.0;
-      for (int64_t u = N + tid; u < N + W1; u += nt) w1 += exp(lg[u] - m);
-      for (int64_t u = N + W1 + tid; u < N + W1 + W2; u += nt) w2 += exp(lg[u] - m);
-      w1 = block_sum<double>(w1, s_wave_d);
-      w2 = block_sum<double>(w2, s_wave_d);
-      if (exact) {
-        Sn = EN;
-      } else {
-        mu1 = w1 / (double)W1;
-        mu2 = w2 / (double)W2;
-        const double x1 = (double)(hm[4] + hm[5]) / 2.0, x2 = (double)(hm[6] + hm[7]) / 2.0;
-        fa = (mu1 - mu2) / (1.0 / x1 - 1.0 / x2);
-        fb = mu1 - fa / x1;
-        Sn = EN + tail_sum(fa, fb, N + 1, n);
-      }
-      if (a.P >= 1.0) {
-        k = n;
-      } else {
-        T = a.P * Sn;
-        if (T <= EN) {
-          if (tid == 0) s_kmin = 0x7fffffff;
-          __syncthreads();
-          double run = base;
-          for (int64_t u = beg; u < end; ++u) {
-            run += exp(lg[u] - m);
-            if (run >= T) {
-              atomicMin(&s_kmin, (int)(u + 1));
-              break;
-            }
-          }
-          __syncthreads();
-          k = s_kmin;
-          if (k == 0x7fffffff) k = (int)N;  // unreachable unless rounding lost the crossing
-        } else {
-          int64_t lo = N + 1, hi = n;
-          while (lo < hi) {
-            const int64_t mid = (lo + hi) >> 1;
-            if (EN + tail_sum(fa, fb, N + 1, mid) >= T) hi = mid;
-            else lo = mid + 1;
-          }
-          k = (int)lo;
-        }
-      }
+__device__ __forceinline__ double wave_sum_d(double v) {
+  for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+__device__ __forceinline__ double wave_max_d(double v) {
+  for (int o = kWave / 2; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+
+// Fit and budget of one query head (Algorithm 1) by one wave, fp64.  Lane 0
+// writes the head's record and returns the cutoff (rank, length) in cut[2].
+__device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
+  const int32_t* hm = a.head_meta + (int64_t)bh * 16;
+  const int n = hm[0];
+  const int64_t S = hm[9];
+  const double* lg = a.logits + (int64_t)bh * a.S_cap;
+  const int exact = hm[8];
+  const int64_t N = exact ? S : hm[1];
+  const int64_t W1 = hm[2], W2 = hm[3];
+  int k = 0;
+  double m = 0.0, mu1 = 0.0, mu2 = 0.0, fa = 0.0, fb = 0.0, Sn = 0.0, T = 0.0, EN = 0.0;
+  if (n > 0) {
+    double mx = -INFINITY;
+#pragma unroll 4
+    for (int64_t u = lane; u < N; u += kWave) mx = fmax(mx, lg[u]);
+    m = wave_max_d(mx);
+    double loc = 0.0, w1 = 0.0, w2 = 0.0;
+#pragma unroll 4
+    for (int64_t u = lane; u < N; u += kWave) loc += exp(lg[u] - m);
+#pragma unroll 4
+    for (int64_t u = N + lane; u < N + W1; u += kWave) w1 += exp(lg[u] - m);
+#pragma unroll 4
+    for (int64_t u = N + W1 + lane; u < N + W1 + W2; u += kWave) w2 += exp(lg[u] - m);
+    EN = wave_sum_d(loc);
+    w1 = wave_sum_d(w1);
+    w2 = wave_sum_d(w2);
+    if (exact) {
+      Sn = EN;
+    } else {
+      mu1 = w1 / (double)W1;
+      mu2 = w2 / (double)W2;
+      const double x1 = (double)(hm[4] + hm[5]) / 2.0, x2 = (double)(hm[6] + hm[7]) / 2.0;
+      fa = (mu1 - mu2) / (1.0 / x1 - 1.0 / x2);
+      fb = mu1 - fa / x1;
+      Sn = EN + tail_sum(fa, fb, N + 1, n);
     }
-    // cutoff cluster: largest rank r with prefix[r] < k, and its selected length
-    const int C = hm[10];
-    const int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
-    if (tid == 0) {
-      int cut_r = -1, cut_len = 0;
-      if (k > 0) {
-        int lo_r = 0, hi_r = C;
-        while (lo_r < hi_r) {
-          const int mid = (lo_r + hi_r + 1) >> 1;
-          if (rpre[mid] < k) lo_r = mid;
-          else hi_r = mid - 1;
+    if (a.P >= 1.0) {
+      k = n;
+    } else {
+      T = a.P * Sn;
+      if (T <= EN) {
+        // the budget lies in the exact head: scan it in position order, 64 at a time
+        int cand = 0x7fffffff;
+        double run = 0.0;
+        for (int64_t u0 = 0; u0 < N && cand == 0x7fffffff; u0 += kWave) {
+          const int64_t u = u0 + lane;
+          const double e = u < N ? exp(lg[u] - m) : 0.0;
+          double incl = e;
+          for (int o = 1; o < kWave; o <<= 1) {
+            const double y = __shfl_up(incl, o, kWave);
+            if (lane >= o) incl += y;
+          }
+          int c2 = (u < N && run + incl >= T) ? (int)(u + 1) : 0x7fffffff;
+          for (int o = kWave / 2; o > 0; o >>= 1) c2 = min(c2, __shfl_xor(c2, o, kWave));
+          cand = c2;
+          run += __shfl(incl, kWave - 1, kWave);
         }
-        cut_r = lo_r;
-        cut_len = k - rpre[lo_r];
+        k = cand == 0x7fffffff ? (int)N : cand;  // N only if rounding lost the crossing
+      } else {
+        // minimal k in (N, n] with E_N + tail(N+1..k) >= T; the tail is the
+        // closed form over the positive interval [L, R] of the fitted curve
+        int64_t L, R;
+        const bool any = positive_interval(fa, fb, N + 1, n, &L, &R);
+        const double HL = any ? harmonic(L - 1) : 0.0;
+        auto tail_to = [&](int64_t kk) -> double {
+          const int64_t r = min(kk, R);
+          return (!any || r < L) ? 0.0 : fa * (harmonic(r) - HL) + fb * (double)(r - L + 1);
+        };
+        int64_t lo = N + 1, hi = n;
+        while (lo < hi) {
+          const int64_t mid = (lo + hi) >> 1;
+          if (EN + tail_to(mid) >= T) hi = mid;
+          else lo = mid + 1;
+        }
+        k = (int)lo;
       }
-      a.cut[bh * 2] = cut_r;
-      a.cut[bh * 2 + 1] = cut_len;
-      a.sel_count_q[bh] = k;
-      fit[0] = m; fit[1] = mu1; fit[2] = mu2; fit[3] = fa; fit[4] = fb; fit[5] = Sn; fit[6] = T;
-      fit[7] = (double)k; fit[8] = (double)N; fit[9] = (double)n; fit[10] = (double)exact;
-      fit[11] = (double)S; fit[12] = EN; fit[13] = (double)cut_r; fit[14] = (double)cut_len;
-      fit[15] = 0.0;
     }
   }
-  if (!arrive_last(a.counters + a.BH + bg, G, &s_flag)) return;
+  if (lane == 0) {
+    const int C = hm[10];
+    const int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
+    int cut_r = -1, cut_len = 0;
+    if (k > 0) {  // cutoff cluster: largest rank r with prefix[r] < k
+      int lo_r = 0, hi_r = C;
+      while (lo_r < hi_r) {
+        const int mid = (lo_r + hi_r + 1) >> 1;
+        if (rpre[mid] < k) lo_r = mid;
+        else hi_r = mid - 1;
+      }
+      cut_r = lo_r;
+      cut_len = k - rpre[lo_r];
+    }
+    cut[0] = cut_r;
+    cut[1] = cut_len;
+    a.sel_count_q[bh] = k;
+    double* fit = a.fit + (int64_t)bh * kFitFields;
+    fit[0] = m; fit[1] = mu1; fit[2] = mu2; fit[3] = fa; fit[4] = fb; fit[5] = Sn; fit[6] = T;
+    fit[7] = (double)k; fit[8] = (double)N; fit[9] = (double)n; fit[10] = (double)exact;
+    fit[11] = (double)S; fit[12] = EN; fit[13] = (double)cut_r; fit[14] = (double)cut_len;
+    fit[15] = 0.0;
+  }
+}
 
-  // ---- union of the group's selections (Sec. 4.5) and the attention work list
-  {
-    const int64_t cb = a.cl_indptr[b];
-    const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
-    const int32_t* off = a.offsets + (int64_t)g * (a.Ct + a.B) + cb + b;
-    if (tid < G) {
-      const int bh2 = b * a.Hq + g * G + tid;
-      s_cut[tid][0] = a.cut[bh2 * 2];
-      s_cut[tid][1] = a.cut[bh2 * 2 + 1];
-    }
-    __syncthreads();
-    int32_t* ulen = a.union_len + (int64_t)g * a.Ct + cb;
-    const int seg = (C + nt - 1) / nt;
-    const int beg = min(C, tid * seg), end = min(C, beg + seg);
-    uint64_t loc = 0;  // (ranges << 32) | tokens
-    for (int j = beg; j < end; ++j) {
-      const int size = off[j + 1] - off[j];
-      int L = 0;
+// 3b. Fit of the G heads of a group (one wave each), then the union of their
+//     selections (Sec. 4.5) and the attention work list.  grid B*Hkv, 1024
+//     threads (the first G waves fit); the per-cluster union lengths are
+//     staged in LDS when they fit.
+template <int G>
+__global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  __shared__ uint64_t s_wave_u[17];
+  __shared__ int s_cut[G][2];
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int bg = blockIdx.x;
+  const int b = bg / a.Hkv, g = bg % a.Hkv;
+  if (wave < G) fit_head_wave(a, b * a.Hq + g * G + wave, lane, s_cut[wave]);
+  __syncthreads();
+
+  const int64_t cb = a.cl_indptr[b];
+  const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
+  const int32_t* off = a.offsets + (int64_t)g * (a.Ct + a.B) + cb + b;
+  int32_t* ulen = a.union_len + (int64_t)g * a.Ct + cb;
+  int32_t* Ls = a.Cm <= kUnionLdsMax ? reinterpret_cast<int32_t*>(smem_raw) : ulen;
+  // pass 1 (coalesced): selected prefix length of every cluster = max over heads
+#pragma unroll 4
+  for (int j = tid; j < C; j += nt) {
+    const int size = off[j + 1] - off[j];
+    int L = 0;
 #pragma unroll
-      for (int hh = 0; hh < G; ++hh) {
-        const int bh2 = b * a.Hq + g * G + hh;
-        const int r = a.rank_of[(int64_t)bh2 * a.Cm + j];
-        const int len = r < s_cut[hh][0] ? size : (r == s_cut[hh][0] ? s_cut[hh][1] : 0);
-        L = max(L, len);
-      }
-      ulen[j] = L;
-      if (L > 0) loc += (1ull << 32) | (uint64_t)L;
+    for (int hh = 0; hh < G; ++hh) {
+      const int r = a.rank_of[(int64_t)(b * a.Hq + g * G + hh) * a.Cm + j];
+      const int len = r < s_cut[hh][0] ? size : (r == s_cut[hh][0] ? s_cut[hh][1] : 0);
+      L = max(L, len);
     }
-    uint64_t incl = loc;
-    for (int o = 1; o < kWave; o <<= 1) {
-      const uint64_t y = __shfl_up(incl, o, kWave);
-      if ((tid & (kWave - 1)) >= o) incl += y;
+    Ls[j] = L;
+    ulen[j] = L;
+  }
+  __syncthreads();
+  // pass 2: compact the non-empty clusters into ranges (contiguous segment per thread)
+  const int seg = (C + nt - 1) / nt;
+  const int beg = min(C, tid * seg), end = min(C, beg + seg);
+  uint64_t loc = 0;  // (ranges << 32) | tokens
+  for (int j = beg; j < end; ++j) {
+    const int L = Ls[j];
+    if (L > 0) loc += (1ull << 32) | (uint64_t)L;
+  }
+  uint64_t incl = loc;
+  for (int o = 1; o < kWave; o <<= 1) {
+    const uint64_t y = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += y;
+  }
+  if (lane == kWave - 1) s_wave_u[wave] = incl;
+  __syncthreads();
+  if (tid == 0) {
+    uint64_t run = 0;
+    for (int w = 0; w < nt / kWave; ++w) {
+      const uint64_t t = s_wave_u[w];
+      s_wave_u[w] = run;
+      run += t;
     }
-    if ((tid & (kWave - 1)) == kWave - 1) s_wave_u[tid / kWave] = incl;
-    __syncthreads();
-    if (tid == 0) {
-      uint64_t run = 0;
-      for (int w = 0; w < nt / kWave; ++w) {
-        const uint64_t t = s_wave_u[w];
-        s_wave_u[w] = run;
-        run += t;
-      }
-      s_wave_u[16] = run;
-    }
-    __syncthreads();
-    const uint64_t base = s_wave_u[tid / kWave] + incl - loc;
-    const uint64_t tot = s_wave_u[16];
-    int idx = (int)(base >> 32);
-    int64_t upos = (int64_t)(base & 0xffffffffu);
-    const int64_t T = a.chunk_tokens;
-    int32_t* rstart = a.rstart + (int64_t)bg * a.Cm;
-    int32_t* rupos = a.rupos + (int64_t)bg * (a.Cm + 1);
-    int32_t* cfr = a.cfr + (int64_t)bg * a.max_chunks;
-    for (int j = beg; j < end; ++j) {
-      const int L = ulen[j];
-      if (L <= 0) continue;
-      rstart[idx] = off[j];
-      rupos[idx] = (int32_t)upos;
-      for (int64_t c = (upos + T - 1) / T; c * T < upos + L && c < a.max_chunks; ++c) cfr[c] = idx;
-      ++idx;
-      upos += L;
-    }
-    if (tid == 0) {
-      const int R = (int)(tot >> 32);
-      const int64_t U = (int64_t)(tot & 0xffffffffu);
-      rupos[R] = (int32_t)U;
-      a.gmeta[bg * 4 + 0] = R;
-      a.gmeta[bg * 4 + 1] = (int32_t)U;
-      a.gmeta[bg * 4 + 2] = (int32_t)((U + T - 1) / T);
-      a.gmeta[bg * 4 + 3] = 0;
-      a.sel_count_kv[bg] = (int32_t)U;
-    }
+    s_wave_u[16] = run;
+  }
+  __syncthreads();
+  const uint64_t base = s_wave_u[wave] + incl - loc;
+  const uint64_t tot = s_wave_u[16];
+  const int64_t U = (int64_t)(tot & 0xffffffffu);
+  // tokens per attention work item: larger items for larger unions
+  const int64_t T = U >= 65536 ? 1024 : (U >= 16384 ? 512 : 256);
+  int idx = (int)(base >> 32);
+  int64_t upos = (int64_t)(base & 0xffffffffu);
+  int32_t* rstart = a.rstart + (int64_t)bg * a.Cm;
+  int32_t* rupos = a.rupos + (int64_t)bg * (a.Cm + 1);
+  int32_t* cfr = a.cfr + (int64_t)bg * a.max_chunks;
+  for (int j = beg; j < end; ++j) {
+    const int L = Ls[j];
+    if (L <= 0) continue;
+    rstart[idx] = off[j];
+    rupos[idx] = (int32_t)upos;
+    for (int64_t c = (upos + T - 1) / T; c * T < upos + L && c < a.max_chunks; ++c) cfr[c] = idx;
+    ++idx;
+    upos += L;
+  }
+  if (tid == 0) {
+    const int R = (int)(tot >> 32);
+    rupos[R] = (int32_t)U;
+    a.gmeta[bg * 4 + 0] = R;
+    a.gmeta[bg * 4 + 1] = (int32_t)U;
+    a.gmeta[bg * 4 + 2] = (int32_t)((U + T - 1) / T);
+    a.gmeta[bg * 4 + 3] = (int32_t)T;
+    a.sel_count_kv[bg] = (int32_t)U;
   }
 }
 
@@ -588,13 +683,18 @@ hipError_t launch_sort(const SortArgs& a, bool lds, int n_heads, hipStream_t st)
   return hipGetLastError();
 }
 
-hipError_t launch_fit(const FitArgs& a, int G, int split, int n_heads, hipStream_t st) {
-  dim3 grid(split, n_heads);
+hipError_t launch_sample(const FitArgs& a, int split, int n_heads, hipStream_t st) {
+  hipLaunchKernelGGL(sample_logits_kernel, dim3(split, n_heads), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fit_union(const FitArgs& a, int G, int n_groups, hipStream_t st) {
+  const size_t lds = a.Cm <= kUnionLdsMax ? (size_t)a.Cm * 4 : 0;
   switch (G) {
-    case 1: hipLaunchKernelGGL(sample_fit_union_kernel<1>, grid, dim3(256), 0, st, a); break;
-    case 2: hipLaunchKernelGGL(sample_fit_union_kernel<2>, grid, dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL(sample_fit_union_kernel<4>, grid, dim3(256), 0, st, a); break;
-    case 8: hipLaunchKernelGGL(sample_fit_union_kernel<8>, grid, dim3(256), 0, st, a); break;
+    case 1: hipLaunchKernelGGL(fit_union_kernel<1>, dim3(n_groups), dim3(1024), lds, st, a); break;
+    case 2: hipLaunchKernelGGL(fit_union_kernel<2>, dim3(n_groups), dim3(1024), lds, st, a); break;
+    case 4: hipLaunchKernelGGL(fit_union_kernel<4>, dim3(n_groups), dim3(1024), lds, st, a); break;
+    case 8: hipLaunchKernelGGL(fit_union_kernel<8>, dim3(n_groups), dim3(1024), lds, st, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -15,8 +15,6 @@ struct ScoreArgs {
   int B, Hq, Hkv, Cm;
   int64_t Ct;
   float* scores;              // [B*Hq][Cm]
-  int* counters;
-  int n_counters;
 };
 
 struct SortArgs {
@@ -43,7 +41,7 @@ struct FitArgs {
   const int64_t* kv_indptr;
   const int64_t* cl_indptr;
   const int32_t* offsets;
-  int B, Hq, Hkv, Cm, BH, split;
+  int B, Hq, Hkv, G, Cm, BH, split;
   int64_t Ct, total, S_cap, chunk_tokens, max_chunks;
   double P;
   const int32_t* head_meta;
@@ -56,11 +54,10 @@ struct FitArgs {
   int32_t* sel_count_q;       // [B*Hq]
   int32_t* sel_count_kv;      // [B*Hkv]
   int32_t* union_len;         // [Hkv][Ct]
-  int32_t* gmeta;             // [B*Hkv][4]: ranges, union tokens, work items, -
+  int32_t* gmeta;             // [B*Hkv][4]: ranges, union tokens, work items, tokens per item
   int32_t* rstart;            // [B*Hkv][Cm]
   int32_t* rupos;             // [B*Hkv][Cm+1]
   int32_t* cfr;               // [B*Hkv][max_chunks]
-  int* counters;              // [BH] sampling, [BG] fitted heads
 };
 
 struct AttnArgs {
@@ -75,13 +72,14 @@ struct AttnArgs {
   const int32_t* rupos;
   const int32_t* cfr;
   float* partials;            // [B*Hkv][max_chunks][G*130]
-  int* done;                  // [B*Hkv] items finished (self-resetting)
   float* out;                 // [B][Hq][128]
 };
 
 hipError_t launch_score(const ScoreArgs& a, int G, int grid_x, int grid_y, hipStream_t st);
 hipError_t launch_sort(const SortArgs& a, bool lds, int n_heads, hipStream_t st);
-hipError_t launch_fit(const FitArgs& a, int G, int split, int n_heads, hipStream_t st);
+hipError_t launch_sample(const FitArgs& a, int split, int n_heads, hipStream_t st);
+hipError_t launch_fit_union(const FitArgs& a, int G, int n_groups, hipStream_t st);
 hipError_t launch_attn(const AttnArgs& a, int G, int grid, hipStream_t st);
+hipError_t launch_combine(const AttnArgs& a, int G, hipStream_t st);
 
 }  // namespace tactic

@@ -14,6 +14,10 @@ constexpr int kMaxChunkTokens = 1024;  // tokens per attention work item (upper 
 constexpr int kSortLdsBuckets = 8192;  // largest cluster count sorted in LDS
 constexpr int kMaxGroups = 4096;       // B * Hkv limit of the attention work list
 constexpr int kFitFields = 16;
+constexpr int kStageEvents = 7;        // start + after each of the six decode kernels
+constexpr int kAttnGrid = 1024;        // persistent attention workgroups
+constexpr int kUnionLdsMax = 32768;
+constexpr int kScoreRows = 256;        // centroids per scoring workgroup    // clusters whose union lengths are staged in LDS
 
 struct DecodePlan {
   int64_t magic;
@@ -28,14 +32,12 @@ struct DecodePlan {
   // workspace byte offsets
   int64_t off_scores, off_order, off_rank, off_rprefix, off_headmeta, off_rows, off_logit;
   int64_t off_fit, off_cut, off_union_len, off_gmeta, off_rstart, off_rupos, off_cfr;
-  int64_t off_partials, off_counters, off_sort_keys, off_sort_cnt, off_sort_start;
+  int64_t off_partials, off_sort_keys, off_sort_cnt, off_sort_start;
   int64_t ws_bytes;
-  int64_t n_counters;
   int64_t exact_bp, win_bp, win_min, p1_bp, p2_bp;
-  int64_t pad[64 - 42];
+  int64_t events[kStageEvents];  // optional hipEvent_t recorded between the kernels
+  int64_t pad[64 - 47];
 };
 static_assert(sizeof(DecodePlan) == 64 * sizeof(int64_t), "plan must fill tactic_decode_plan");
 
-// Counters (int32) at off_counters: [0, BH) sampling done per head,
-// [BH, BH+BG) heads fitted per group, [BH+BG, BH+2BG) attention items done per group.
 }  // namespace tactic

@@ -169,8 +169,7 @@ class DenseDecoder:
         n = C.lib().tactic_dense_decode_workspace_size(ctypes.byref(self._shape))
         if n == 0:
             C.check(1, "tactic_dense_decode_workspace_size")
-        # the completion counters must start at zero; each call leaves them zero
-        self.workspace = torch.zeros(n, dtype=torch.uint8, device=device)
+        self.workspace = torch.empty(n, dtype=torch.uint8, device=device)
         self.out = torch.empty(batch.batch, batch.n_q_heads, 128, dtype=torch.float32, device=device)
 
     def __call__(self, q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, stream=None, out=None):
