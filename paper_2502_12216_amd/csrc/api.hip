@@ -438,6 +438,7 @@ tactic_status tactic_build_clusters(const uint16_t* K, const uint16_t* V, const 
     return fail(TACTIC_ERR_INVALID_ARG, "inconsistent total_clusters / max_clusters");
   if (params->max_iters < 1 || params->max_iters > 1000)
     return fail(TACTIC_ERR_INVALID_ARG, "max_iters must be in [1, 1000]");
+  if (max_clusters >= (1 << 21)) return fail(TACTIC_ERR_UNSUPPORTED, "more than 2^21 - 1 clusters");
   const size_t need = tactic_build_clusters_workspace_size(shape, total_clusters, max_clusters);
   if (!workspace || workspace_bytes < need)
     return fail(TACTIC_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);

@@ -1,14 +1,524 @@
-// Prefill K-means clustering (Sec. 4.2) -- placeholder until the kernels land.
+// Prefill K-means clustering of the keys (Sec. 4.2) for gfx950.
+//
+// One problem per (sequence b, KV head g): n_b keys, C_b clusters, started
+// from the keys of the sampled tokens init_idx.  Each iteration:
+//   km_assign   nearest stored centroid of every key: ||c||^2 - 2 k.c with
+//               the k.c contraction on MFMA (v_mfma_f32_32x32x16_bf16, fp32
+//               accumulation) and a fused argmin (ties to the smaller id);
+//               counts assignments that changed.
+//   km_hist     per tile of 2048 tokens: sort (cluster, token) keys in LDS,
+//               giving each token its rank among same-cluster tokens of the
+//               tile, and the tile's count of every cluster.  An iteration
+//               whose assignment step changed nothing ends the problem.
+//   km_scan*    exclusive scan of the (cluster, tile) counts: start row of
+//               every cluster and of every (cluster, tile) run.
+//   km_perm     stable counting-sort scatter: perm[row] = token.
+//   km_mean     centroid = mean of the members, summed in row order (fixed,
+//               so results are deterministic), rounded to bf16; an empty
+//               cluster keeps its centroid.
+// After the last iteration the K/V rows are permuted into cluster order.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "common.hpp"
 #include "kmeans.hpp"
 
 namespace tactic {
 
-size_t kmeans_workspace_bytes(int, int, int64_t, int64_t, int, int64_t) { return 256; }
+constexpr int kKmTile = 2048;       // tokens per counting tile
+constexpr int kKmChunk = 16384;     // table entries per scan chunk
+constexpr int kKmMaxIters = 1000;
+constexpr int kAsgTok = 256;        // tokens per assignment workgroup (4 waves x 64)
+constexpr int kAsgCen = 128;        // centroids staged in LDS per step
+constexpr int kLdsRow = kHeadDim + 8;  // padded LDS row (bf16): 272 bytes, 2-way bank conflicts
 
-hipError_t run_kmeans(const uint16_t*, const uint16_t*, const int64_t*, const int64_t*, int, int, int64_t,
-                      int64_t, int64_t, int, const int32_t*, int, uint16_t*, int32_t*, int32_t*, int32_t*,
-                      uint16_t*, uint16_t*, void*, hipStream_t) {
-  return hipErrorNotSupported;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+struct KmArgs {
+  const uint16_t* K;
+  const uint16_t* V;
+  const int64_t* kv_indptr;
+  const int64_t* cl_indptr;
+  int B, Hkv, Cm, tiles_max, chunks_max, iter, max_iters;
+  int64_t total, Ct;
+  const int32_t* init_idx;
+  uint16_t* centroids;
+  float* cnorm;
+  int32_t* assign;
+  int32_t* offsets;
+  int32_t* perm;
+  int32_t* local_rank;
+  int32_t* table;
+  int32_t* chunk_sums;
+  int32_t* changed;  // [max_iters + 1][BG]
+  int32_t* done;     // [BG]
+  uint16_t* K_sorted;
+  uint16_t* V_sorted;
+};
+
+struct Problem {
+  int b, g, n, C, tiles;
+  int64_t tok_base, cl_base, off_base;
+};
+
+__device__ __forceinline__ Problem problem(const KmArgs& a, int p) {
+  Problem q;
+  q.b = p / a.Hkv;
+  q.g = p % a.Hkv;
+  const int64_t s0 = a.kv_indptr[q.b], c0 = a.cl_indptr[q.b];
+  q.n = (int)(a.kv_indptr[q.b + 1] - s0);
+  q.C = min((int)(a.cl_indptr[q.b + 1] - c0), a.Cm);
+  q.tiles = (q.n + kKmTile - 1) / kKmTile;
+  q.tok_base = (int64_t)q.g * a.total + s0;
+  q.cl_base = (int64_t)q.g * a.Ct + c0;
+  q.off_base = (int64_t)q.g * (a.Ct + a.B) + c0 + q.b;
+  return q;
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// ---------------------------------------------------------------------------
+// init: c0 = K[init_idx], ||c0||^2, per-problem flags.  grid (ceil(Cm/4), BG)
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void km_init_kernel(KmArgs a) {
+  const int p = blockIdx.y;
+  const Problem q = problem(a, p);
+  if (blockIdx.x == 0) {
+    for (int i = threadIdx.x; i <= a.max_iters; i += blockDim.x) a.changed[(int64_t)i * a.B * a.Hkv + p] = 0;
+    if (threadIdx.x == 0) a.done[p] = 0;
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, sl = lane & 15, grp = lane >> 4;
+  const int j = blockIdx.x * 4 + wave;
+  if (j >= q.C || grp != 0 || q.n == 0) return;
+  const int t = min(max(a.init_idx[q.cl_base + j], 0), q.n - 1);
+  const uint4 v = *reinterpret_cast<const uint4*>(a.K + (q.tok_base + t) * kHeadDim + sl * 8);
+  *reinterpret_cast<uint4*>(a.centroids + (q.cl_base + j) * kHeadDim + sl * 8) = v;
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  float s = 0.f;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float x = bf16lo(w[e]), y = bf16hi(w[e]);
+    s = fmaf(x, x, s);
+    s = fmaf(y, y, s);
+  }
+  s = sum16(s);
+  if (sl == 0) a.cnorm[q.cl_base + j] = s;
+}
+
+// ---------------------------------------------------------------------------
+// assignment: grid (ceil(nmax/256), BG), 256 threads.  A wave owns 64 tokens
+// (two 32-token MFMA B operands held in registers for the whole pass);
+// centroids stream through LDS 128 at a time as the A operand.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void km_assign_kernel(KmArgs a) {
+  __shared__ __align__(16) uint16_t s_c[kAsgCen * kLdsRow];
+  __shared__ float s_cn[kAsgCen];
+  const int p = blockIdx.y;
+  if (a.done[p]) return;
+  const Problem q = problem(a, p);
+  const int i0 = blockIdx.x * kAsgTok;
+  if (i0 >= q.n) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, col = lane & 31;
+
+  bf16x8 bt[2][8];
+#pragma unroll
+  for (int bb = 0; bb < 2; ++bb) {
+    const int tok = i0 + wave * 64 + bb * 32 + col;
+    const uint16_t* src = a.K + (q.tok_base + min(tok, q.n - 1)) * kHeadDim + 64 * half;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (tok < q.n) v = *reinterpret_cast<const uint4*>(src + 8 * s);
+      bt[bb][s] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+  float best_v[2] = {INFINITY, INFINITY};
+  int best_j[2] = {0x7fffffff, 0x7fffffff};
+  const uint16_t* cbase = a.centroids + q.cl_base * kHeadDim;
+  for (int c0 = 0; c0 < q.C; c0 += kAsgCen) {
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int idx = tid + 256 * k;  // 16-byte piece: row idx / 16, piece idx % 16
+      const int row = idx >> 4, pc = idx & 15;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (c0 + row < q.C) v = *reinterpret_cast<const uint4*>(cbase + (int64_t)(c0 + row) * kHeadDim + pc * 8);
+      *reinterpret_cast<uint4*>(s_c + row * kLdsRow + pc * 8) = v;
+    }
+    if (tid < kAsgCen) s_cn[tid] = c0 + tid < q.C ? a.cnorm[q.cl_base + c0 + tid] : INFINITY;
+    __syncthreads();
+    const int nblk = min(4, (q.C - c0 + 31) / 32);
+    for (int cb = 0; cb < nblk; ++cb) {
+      f32x16 acc0 = {}, acc1 = {};
+      const uint16_t* arow = s_c + (cb * 32 + col) * kLdsRow + 64 * half;
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const bf16x8 av = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(arow + 8 * s));
+        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bt[0][s], acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bt[1][s], acc1, 0, 0, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int r = 8 * (i / 4) + 4 * half + (i % 4);  // centroid row of this accumulator
+        const float cn = s_cn[cb * 32 + r];
+        const int j = c0 + cb * 32 + r;
+        const float d0 = fmaf(-2.f, acc0[i], cn), d1 = fmaf(-2.f, acc1[i], cn);
+        if (d0 < best_v[0]) { best_v[0] = d0; best_j[0] = j; }
+        if (d1 < best_v[1]) { best_v[1] = d1; best_j[1] = j; }
+      }
+    }
+  }
+  int nchg = 0;
+#pragma unroll
+  for (int bb = 0; bb < 2; ++bb) {
+    const float ov = __shfl_xor(best_v[bb], 32, 64);
+    const int oj = __shfl_xor(best_j[bb], 32, 64);
+    if (ov < best_v[bb] || (ov == best_v[bb] && oj < best_j[bb])) {
+      best_v[bb] = ov;
+      best_j[bb] = oj;
+    }
+    const int tok = i0 + wave * 64 + bb * 32 + col;
+    if (half == 0 && tok < q.n) {
+      const int jn = min(max(best_j[bb], 0), q.C - 1);
+      int32_t* dst = a.assign + q.tok_base + tok;
+      if (a.iter > 1 && *dst != jn) ++nchg;
+      *dst = jn;
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) nchg += __shfl_xor(nchg, o, 64);
+  if (lane == 0 && nchg > 0) atomicAdd(a.changed + (int64_t)a.iter * a.B * a.Hkv + p, nchg);
+}
+
+// ---------------------------------------------------------------------------
+// counting tile: grid (tiles_max, BG), 1024 threads
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int lower_bound_u32(const uint32_t* s, int n, uint32_t key) {
+  int lo = 0, hi = n;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (s[mid] < key) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
+__global__ __launch_bounds__(1024) void km_hist_kernel(KmArgs a) {
+  __shared__ uint32_t s_key[kKmTile];
+  const int p = blockIdx.y;
+  if (a.done[p]) return;
+  if (a.iter > 1 && a.changed[(int64_t)a.iter * a.B * a.Hkv + p] == 0) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) a.done[p] = 1;  // converged: nothing changed
+    return;
+  }
+  const Problem q = problem(a, p);
+  const int t = blockIdx.x;
+  const int i0 = t * kKmTile;
+  if (i0 >= q.n) return;
+  const int m = min(kKmTile, q.n - i0);
+  const int tid = threadIdx.x;
+  for (int x = tid; x < kKmTile; x += 1024)
+    s_key[x] = x < m ? ((uint32_t)a.assign[q.tok_base + i0 + x] << 11) | (uint32_t)x : 0xffffffffu;
+  // bitonic sort of 2048 keys, one compare-exchange per thread per step
+  for (int k = 2; k <= kKmTile; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      __syncthreads();
+      const int i = 2 * tid - (tid & (j - 1));  // lower index of this thread's pair
+      const int l = i + j;
+      const uint32_t x = s_key[i], y = s_key[l];
+      const bool up = (i & k) == 0;
+      if ((x > y) == up) {
+        s_key[i] = y;
+        s_key[l] = x;
+      }
+    }
+  }
+  __syncthreads();
+  for (int s = tid; s < m; s += 1024) {
+    const uint32_t key = s_key[s];
+    const uint32_t c = key >> 11;
+    const int lb = lower_bound_u32(s_key, m, c << 11);
+    a.local_rank[q.tok_base + i0 + (key & 2047u)] = s - lb;
+  }
+  int32_t* tab = a.table + (int64_t)p * a.Cm * a.tiles_max;
+  for (int c = tid; c < q.C; c += 1024) {
+    const int lo = lower_bound_u32(s_key, m, (uint32_t)c << 11);
+    const int hi = lower_bound_u32(s_key, m, (uint32_t)(c + 1) << 11);
+    tab[(int64_t)c * q.tiles + t] = hi - lo;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// exclusive scan of the (cluster, tile) counts, cluster-major
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ bool km_active(const KmArgs& a, int p) {
+  return !a.done[p];
+}
+
+__global__ __launch_bounds__(1024) void km_scan1_kernel(KmArgs a) {
+  __shared__ int s_w[16];
+  const int p = blockIdx.y;
+  if (!km_active(a, p)) return;
+  const Problem q = problem(a, p);
+  const int64_t E = (int64_t)q.C * q.tiles;
+  const int64_t x0 = (int64_t)blockIdx.x * kKmChunk;
+  if (x0 >= E) return;
+  const int32_t* tab = a.table + (int64_t)p * a.Cm * a.tiles_max;
+  int s = 0;
+  for (int64_t x = x0 + threadIdx.x; x < min(E, x0 + kKmChunk); x += 1024) s += tab[x];
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+  if ((threadIdx.x & 63) == 0) s_w[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int t = 0;
+    for (int w = 0; w < 16; ++w) t += s_w[w];
+    a.chunk_sums[(int64_t)p * a.chunks_max + blockIdx.x] = t;
+  }
+}
+
+__global__ __launch_bounds__(64) void km_scan2_kernel(KmArgs a) {
+  const int p = blockIdx.x;
+  if (!km_active(a, p)) return;
+  const Problem q = problem(a, p);
+  const int64_t E = (int64_t)q.C * q.tiles;
+  const int nch = (int)((E + kKmChunk - 1) / kKmChunk);
+  int32_t* cs = a.chunk_sums + (int64_t)p * a.chunks_max;
+  if (threadIdx.x == 0) {
+    int run = 0;
+    for (int c = 0; c < nch; ++c) {
+      const int t = cs[c];
+      cs[c] = run;
+      run += t;
+    }
+  }
+}
+
+__global__ __launch_bounds__(1024) void km_scan3_kernel(KmArgs a) {
+  __shared__ int s_w[17];
+  const int p = blockIdx.y;
+  if (!km_active(a, p)) return;
+  const Problem q = problem(a, p);
+  const int64_t E = (int64_t)q.C * q.tiles;
+  const int64_t x0 = (int64_t)blockIdx.x * kKmChunk;
+  if (blockIdx.x == 0 && threadIdx.x == 0) a.offsets[q.off_base + q.C] = q.n;
+  if (x0 >= E) return;
+  int32_t* tab = a.table + (int64_t)p * a.Cm * a.tiles_max;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t b0 = x0 + (int64_t)tid * 16, b1 = min(E, b0 + 16);
+  int v[16];
+  int loc = 0;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    v[e] = b0 + e < b1 ? tab[b0 + e] : 0;
+    loc += v[e];
+  }
+  int incl = loc;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += y;
+  }
+  if (lane == 63) s_w[wave] = incl;
+  __syncthreads();
+  if (tid == 0) {
+    int run = a.chunk_sums[(int64_t)p * a.chunks_max + blockIdx.x];
+    for (int w = 0; w < 16; ++w) {
+      const int t = s_w[w];
+      s_w[w] = run;
+      run += t;
+    }
+  }
+  __syncthreads();
+  int run = s_w[wave] + incl - loc;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const int64_t x = b0 + e;
+    if (x < b1) {
+      tab[x] = run;
+      if (x % q.tiles == 0) a.offsets[q.off_base + x / q.tiles] = run;  // start of cluster x / tiles
+      run += v[e];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// stable scatter: perm[row] = token.  grid (tiles_max, BG), 1024 threads
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(1024) void km_perm_kernel(KmArgs a) {
+  const int p = blockIdx.y;
+  if (!km_active(a, p)) return;
+  const Problem q = problem(a, p);
+  const int t = blockIdx.x;
+  const int i0 = t * kKmTile;
+  if (i0 >= q.n) return;
+  const int32_t* tab = a.table + (int64_t)p * a.Cm * a.tiles_max;
+  for (int x = threadIdx.x; x < min(kKmTile, q.n - i0); x += 1024) {
+    const int i = i0 + x;
+    const int c = a.assign[q.tok_base + i];
+    const int row = tab[(int64_t)c * q.tiles + t] + a.local_rank[q.tok_base + i];
+    a.perm[q.tok_base + min(max(row, 0), q.n - 1)] = i;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// centroid = bf16(mean of members).  grid (ceil(Cm/4), BG), a wave per cluster
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void km_mean_kernel(KmArgs a) {
+  const int p = blockIdx.y;
+  if (!km_active(a, p)) return;
+  const Problem q = problem(a, p);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, sl = lane & 15, grp = lane >> 4;
+  const int j = blockIdx.x * 4 + wave;
+  if (j >= q.C) return;
+  const int o0 = a.offsets[q.off_base + j], o1 = a.offsets[q.off_base + j + 1];
+  if (o1 <= o0) return;  // empty cluster keeps its centroid
+  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int r = o0 + grp; r < o1; r += 4) {
+    const int tok = a.perm[q.tok_base + r];
+    const uint4 v = *reinterpret_cast<const uint4*>(a.K + (q.tok_base + tok) * kHeadDim + sl * 8);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      s[2 * e] += bf16lo(w[e]);
+      s[2 * e + 1] += bf16hi(w[e]);
+    }
+  }
+  const float inv = 1.f / (float)(o1 - o0);
+  float cn = 0.f;
+  uint32_t out[4];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    float v = s[e];
+    v += __shfl_xor(v, 16, 64);
+    v += __shfl_xor(v, 32, 64);
+    const uint16_t hb = f32_to_bf16_rne(v * inv);
+    const float r = __uint_as_float((uint32_t)hb << 16);
+    cn = fmaf(r, r, cn);
+    if (e & 1) out[e >> 1] |= (uint32_t)hb << 16;
+    else out[e >> 1] = hb;
+  }
+  cn = sum16(cn);
+  if (grp == 0) *reinterpret_cast<uint4*>(a.centroids + (q.cl_base + j) * kHeadDim + sl * 8) =
+      make_uint4(out[0], out[1], out[2], out[3]);
+  if (lane == 0) a.cnorm[q.cl_base + j] = cn;
+}
+
+// ---------------------------------------------------------------------------
+// K_sorted[row] = K[perm[row]] (and V).  grid (ceil(nmax/16), BG), 256 threads
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void km_permute_kv_kernel(KmArgs a) {
+  const int p = blockIdx.y;
+  const Problem q = problem(a, p);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, sl = lane & 15, grp = lane >> 4;
+  const int r = blockIdx.x * 16 + wave * 4 + grp;
+  if (r >= q.n) return;
+  const int tok = min(max(a.perm[q.tok_base + r], 0), q.n - 1);
+  const int64_t src = (q.tok_base + tok) * kHeadDim + sl * 8, dst = (q.tok_base + r) * kHeadDim + sl * 8;
+  if (a.K_sorted) *reinterpret_cast<uint4*>(a.K_sorted + dst) = load_stream16(a.K + src);
+  if (a.V_sorted) *reinterpret_cast<uint4*>(a.V_sorted + dst) = load_stream16(a.V + src);
+}
+
+// ---------------------------------------------------------------------------
+// host driver
+// ---------------------------------------------------------------------------
+namespace {
+
+struct KmLayout {
+  int tiles_max, chunks_max;
+  int64_t off_cnorm, off_rank, off_table, off_chunks, off_changed, off_done, bytes;
+};
+
+KmLayout km_layout(int B, int Hkv, int64_t total, int64_t Ct, int Cm, int64_t nmax) {
+  KmLayout L;
+  const int64_t BG = (int64_t)B * Hkv;
+  L.tiles_max = (int)std::max<int64_t>(1, (nmax + kKmTile - 1) / kKmTile);
+  L.chunks_max = (int)std::max<int64_t>(1, ((int64_t)Cm * L.tiles_max + kKmChunk - 1) / kKmChunk);
+  int64_t cur = 0;
+  auto take = [&](int64_t bytes) {
+    const int64_t o = cur;
+    cur = (cur + bytes + 255) / 256 * 256;
+    return o;
+  };
+  L.off_cnorm = take((int64_t)Hkv * Ct * 4);
+  L.off_rank = take((int64_t)Hkv * total * 4);
+  L.off_table = take(BG * Cm * (int64_t)L.tiles_max * 4);
+  L.off_chunks = take(BG * L.chunks_max * 4);
+  L.off_changed = take((int64_t)(kKmMaxIters + 1) * BG * 4);
+  L.off_done = take(BG * 4);
+  L.bytes = cur;
+  return L;
+}
+
+}  // namespace
+
+size_t kmeans_workspace_bytes(int B, int Hkv, int64_t total, int64_t Ct, int Cm, int64_t nmax) {
+  return (size_t)km_layout(B, Hkv, total, Ct, Cm, nmax).bytes;
+}
+
+hipError_t run_kmeans(const uint16_t* K, const uint16_t* V, const int64_t* kv_indptr,
+                      const int64_t* cl_indptr, int B, int Hkv, int64_t total, int64_t nmax,
+                      int64_t Ct, int Cm, const int32_t* init_idx, int max_iters,
+                      uint16_t* centroids, int32_t* assign, int32_t* offsets, int32_t* perm,
+                      uint16_t* K_sorted, uint16_t* V_sorted, void* workspace, hipStream_t st) {
+  if (max_iters > kKmMaxIters) return hipErrorInvalidValue;
+  const KmLayout L = km_layout(B, Hkv, total, Ct, Cm, nmax);
+  char* ws = static_cast<char*>(workspace);
+  KmArgs a;
+  a.K = K;
+  a.V = V;
+  a.kv_indptr = kv_indptr;
+  a.cl_indptr = cl_indptr;
+  a.B = B;
+  a.Hkv = Hkv;
+  a.Cm = Cm;
+  a.tiles_max = L.tiles_max;
+  a.chunks_max = L.chunks_max;
+  a.iter = 0;
+  a.max_iters = max_iters;
+  a.total = total;
+  a.Ct = Ct;
+  a.init_idx = init_idx;
+  a.centroids = centroids;
+  a.cnorm = reinterpret_cast<float*>(ws + L.off_cnorm);
+  a.assign = assign;
+  a.offsets = offsets;
+  a.perm = perm;
+  a.local_rank = reinterpret_cast<int32_t*>(ws + L.off_rank);
+  a.table = reinterpret_cast<int32_t*>(ws + L.off_table);
+  a.chunk_sums = reinterpret_cast<int32_t*>(ws + L.off_chunks);
+  a.changed = reinterpret_cast<int32_t*>(ws + L.off_changed);
+  a.done = reinterpret_cast<int32_t*>(ws + L.off_done);
+  a.K_sorted = K_sorted;
+  a.V_sorted = V_sorted;
+  const int BG = B * Hkv;
+  const dim3 g_cl((Cm + 3) / 4, BG), g_tok((unsigned)((nmax + kAsgTok - 1) / kAsgTok), BG);
+  const dim3 g_tile(L.tiles_max, BG), g_chunk(L.chunks_max, BG);
+  hipLaunchKernelGGL(km_init_kernel, g_cl, dim3(256), 0, st, a);
+  hipError_t e = hipGetLastError();
+  for (int it = 1; it <= max_iters && e == hipSuccess; ++it) {
+    a.iter = it;
+    hipLaunchKernelGGL(km_assign_kernel, g_tok, dim3(256), 0, st, a);
+    hipLaunchKernelGGL(km_hist_kernel, g_tile, dim3(1024), 0, st, a);
+    hipLaunchKernelGGL(km_scan1_kernel, g_chunk, dim3(1024), 0, st, a);
+    hipLaunchKernelGGL(km_scan2_kernel, dim3(BG), dim3(64), 0, st, a);
+    hipLaunchKernelGGL(km_scan3_kernel, g_chunk, dim3(1024), 0, st, a);
+    hipLaunchKernelGGL(km_perm_kernel, g_tile, dim3(1024), 0, st, a);
+    hipLaunchKernelGGL(km_mean_kernel, g_cl, dim3(256), 0, st, a);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess && (K_sorted || V_sorted)) {
+    if (!V) a.V_sorted = nullptr;
+    hipLaunchKernelGGL(km_permute_kv_kernel, dim3((unsigned)((nmax + 15) / 16), BG), dim3(256), 0, st, a);
+    e = hipGetLastError();
+  }
+  return e;
 }
 
 }  // namespace tactic

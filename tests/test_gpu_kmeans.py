@@ -1,0 +1,159 @@
+"""GPU parity of the prefill K-means (tactic_build_clusters) with the fp64 oracle.
+
+Procedure (the two trajectories may drift apart after a near-tie, so they are
+compared step by step from shared states, then on the final objective):
+  * one assignment from the shared starting centroids: identical except near
+    ties (|d1 - d2| <= 1e-4 (|k|^2 + |c|^2));
+  * the update from the GPU's own assignment: centroids within 1 bf16 ulp of
+    the oracle's rounded means; the layout (offsets, perm) is exactly the
+    stable counting sort of the GPU's assignment, and K_sorted = K[perm];
+  * after 10 iterations the inertia is within 0.1% of the oracle's.
+Starting tokens come from the seeded generator, never from the GPU.
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import kmeans as OK
+from oracle import numerics as ON
+from tests.parity import np64
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _tactic():
+    import paper_2502_12216_amd as P
+    return P
+
+
+def _build(inp, wl, iters):
+    T = _tactic()
+    lens = [int(inp.kv_indptr[i + 1] - inp.kv_indptr[i]) for i in range(len(inp.kv_indptr) - 1)]
+    ncl = [wl.n_clusters(n) for n in lens]
+    batch = T.RaggedBatch(lens, wl.n_q_heads, wl.n_kv_heads)
+    builder = T.ClusterBuilder(batch, ncl, max_iters=iters)
+    init = torch.as_tensor(synth.kmeans_init_all(wl, inp.layer), device=DEV)
+    res = builder(inp.K.to(DEV).contiguous(), inp.V.to(DEV).contiguous(), init)
+    torch.cuda.synchronize()
+    return res, lens, ncl, init.cpu().numpy()
+
+
+def _bf16_bits(x: np.ndarray) -> np.ndarray:
+    return torch.tensor(x, dtype=torch.float64).to(torch.bfloat16).view(torch.int16).numpy().astype(np.int64)
+
+
+def _groups(lens, Hkv):
+    return [(b, g) for b in range(len(lens)) for g in range(Hkv) if lens[b] > 0]
+
+
+def _slices(inp, res, lens, ncl, b, g):
+    kv = np.concatenate([[0], np.cumsum(lens)])
+    cl = np.concatenate([[0], np.cumsum(ncl)])
+    s0, s1, c0, c1 = int(kv[b]), int(kv[b + 1]), int(cl[b]), int(cl[b + 1])
+    K = np64(inp.K[g, s0:s1])
+    return dict(K=K, s0=s0, s1=s1, c0=c0, c1=c1,
+                assign=res.assign[g, s0:s1].cpu().numpy().astype(np.int64),
+                cent=np64(res.clusters.centroids[g, c0:c1]),
+                off=res.clusters.offsets[g, c0 + b:c1 + b + 1].cpu().numpy().astype(np.int64),
+                perm=res.perm[g, s0:s1].cpu().numpy().astype(np.int64))
+
+
+@pytest.mark.parametrize("lens", [[4096], [3000, 1500, 700]])
+def test_kmeans_one_step_parity(lens):
+    wl = synth.small_workload(synth.WORKLOADS["ctx4k_gqa4"], lens)
+    inp = synth.make_layer(wl, 0)
+    res, lens, ncl, init = _build(inp, wl, 1)
+    cl = np.concatenate([[0], np.cumsum(ncl)])
+    ties = 0
+    for b, g in _groups(lens, wl.n_kv_heads):
+        sl = _slices(inp, res, lens, ncl, b, g)
+        K = sl["K"]
+        c0 = K[init[g, int(cl[b]):int(cl[b + 1])]]
+        D = OK.sq_distances(K, c0)
+        a_or = np.argmin(D, axis=1)
+        a_gpu = sl["assign"]
+        diff = np.nonzero(a_or != a_gpu)[0]
+        if len(diff):
+            kk = np.einsum("ij,ij->i", K[diff], K[diff])
+            cc = np.einsum("ij,ij->i", c0[a_or[diff]], c0[a_or[diff]])
+            gap = np.abs(D[diff, a_gpu[diff]] - D[diff, a_or[diff]])
+            assert np.all(gap <= 1e-4 * (kk + cc)), f"b={b} g={g}: {len(diff)} assignments differ beyond ties"
+            ties += len(diff)
+        # update from the GPU's own assignment
+        c_or = OK.update_step(K, a_gpu, c0, round_storage=True)
+        bits_o, bits_g = _bf16_bits(c_or), _bf16_bits(sl["cent"])
+        assert np.max(np.abs(bits_o - bits_g)) <= 1, f"b={b} g={g}: centroid differs by more than 1 bf16 ulp"
+        # layout = stable counting sort of the GPU's assignment
+        off_or, perm_or = OK.cluster_layout(a_gpu, len(c0))
+        np.testing.assert_array_equal(sl["off"], off_or)
+        np.testing.assert_array_equal(sl["perm"], perm_or)
+        Ks = np64(res.K_sorted[g, sl["s0"]:sl["s1"]])
+        np.testing.assert_array_equal(Ks, K[perm_or])
+        Vs = np64(res.V_sorted[g, sl["s0"]:sl["s1"]])
+        np.testing.assert_array_equal(Vs, np64(inp.V[g, sl["s0"]:sl["s1"]])[perm_or])
+    print(f"kmeans one step {lens}: near-tie assignment differences {ties}")
+
+
+@pytest.mark.parametrize("base,lens", [("ctx4k_gqa4", [4096]), ("ctx32k_llama8b", [32768])])
+def test_kmeans_ten_iterations_inertia(base, lens):
+    wl = synth.small_workload(synth.WORKLOADS[base], lens)
+    inp = synth.make_layer(wl, 0, device=DEV)
+    res, lens, ncl, init = _build(inp, wl, 10)
+    cl = np.concatenate([[0], np.cumsum(ncl)])
+    groups = _groups(lens, wl.n_kv_heads)[:2]
+    for b, g in groups:
+        sl = _slices(inp, res, lens, ncl, b, g)
+        K = sl["K"]
+        r = OK.kmeans(K, init[g, int(cl[b]):int(cl[b + 1])], max_iters=10)
+        in_or = OK.inertia(K, r.assign, r.centroids)
+        in_gpu = OK.inertia(K, sl["assign"], sl["cent"])
+        assert abs(in_gpu - in_or) <= 1e-3 * in_or, f"b={b} g={g}: inertia gpu {in_gpu} oracle {in_or}"
+        # the returned layout always matches the returned assignment
+        off_or, perm_or = OK.cluster_layout(sl["assign"], len(sl["cent"]))
+        np.testing.assert_array_equal(sl["off"], off_or)
+        np.testing.assert_array_equal(sl["perm"], perm_or)
+        # every non-empty centroid is the (bf16) mean of its members
+        for j in range(0, len(sl["cent"]), max(1, len(sl["cent"]) // 64)):
+            mem = sl["assign"] == j
+            if mem.any():
+                d = np.abs(_bf16_bits(ON.round_bf16(K[mem].mean(0))) - _bf16_bits(sl["cent"][j]))
+                assert d.max() <= 1
+        print(f"kmeans 10 it {base} b={b} g={g}: inertia gpu {in_gpu:.6e} oracle {in_or:.6e} "
+              f"(oracle iters {r.iters})")
+
+
+def test_kmeans_is_deterministic():
+    wl = synth.small_workload(synth.WORKLOADS["ctx32k_llama8b"], [6000, 2500])
+    inp = synth.make_layer(wl, 0, device=DEV)
+    r1, *_ = _build(inp, wl, 10)
+    r2, *_ = _build(inp, wl, 10)
+    assert torch.equal(r1.assign, r2.assign) and torch.equal(r1.perm, r2.perm)
+    assert torch.equal(r1.clusters.centroids, r2.clusters.centroids)
+    assert torch.equal(r1.K_sorted, r2.K_sorted)
+
+
+def test_decode_on_kmeans_clusters_invariants():
+    """Decode over the library's own clusters (no oracle input comes from the
+    GPU here): properties that hold for any valid cluster layout."""
+    T = _tactic()
+    wl = synth.small_workload(synth.WORKLOADS["ctx32k_llama8b"], [9000, 4000])
+    inp = synth.make_layer(wl, 0, device=DEV)
+    res, lens, ncl, _ = _build(inp, wl, 10)
+    batch = T.RaggedBatch(lens, wl.n_q_heads, wl.n_kv_heads)
+    for P in (0.5, 0.9, 1.0):
+        dec = T.SparseDecoder(batch, ncl, T.decode_params(P))
+        out, sq, skv = dec(inp.q, res.K_sorted, res.V_sorted, res.clusters)
+        torch.cuda.synchronize()
+        G = wl.n_q_heads // wl.n_kv_heads
+        sq, skv = sq.cpu().numpy(), skv.cpu().numpy()
+        for b, n in enumerate(lens):
+            for g in range(wl.n_kv_heads):
+                k = sq[b, g * G:(g + 1) * G]
+                assert np.all(k >= 1) and np.all(k <= n)
+                assert k.max() <= skv[b, g] <= min(n, k.sum())
+                if P == 1.0:
+                    assert skv[b, g] == n
+        assert torch.isfinite(out).all()
