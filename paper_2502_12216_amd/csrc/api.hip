@@ -167,8 +167,8 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape, const tact
   p.S_cap = S_cap;
   p.chunk_tokens = 256;
   p.max_chunks = std::max<int64_t>(1, (p.nmax + p.chunk_tokens - 1) / p.chunk_tokens);
-  p.split = std::min<int64_t>(256, std::max<int64_t>(1, (S_cap + 63) / 64));
-  p.attn_grid = tactic::kAttnGrid;
+  p.split = std::max<int64_t>(1, (S_cap + tactic::kSampleChunk - 1) / tactic::kSampleChunk);
+  p.attn_grid = 0;  // sized at launch from the device's occupancy
   int64_t nb = 1;
   while (nb < p.Cm) nb <<= 1;
   p.sort_lds = nb <= tactic::kSortLdsBuckets ? 1 : 0;
@@ -184,6 +184,7 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape, const tact
   p.off_rows = L.take(BH * p.S_cap * 4);
   p.off_logit = L.take(BH * p.S_cap * 8);
   p.off_fit = L.take(BH * tactic::kFitFields * 8);
+  p.off_lse = L.take(BH * p.split * 6 * 8);
   p.off_cut = L.take(BH * 2 * 4);
   p.off_union_len = L.take(p.Hkv * p.Ct * 4);
   p.off_gmeta = L.take(BG * 4 * 4);
@@ -299,6 +300,7 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   fa.rank_of = so.rank_of;
   fa.logits = reinterpret_cast<double*>(ws + p.off_logit);
   fa.fit = reinterpret_cast<double*>(ws + p.off_fit);
+  fa.lse = reinterpret_cast<double*>(ws + p.off_lse);
   fa.cut = reinterpret_cast<int32_t*>(ws + p.off_cut);
   fa.sel_count_q = sel_count_q;
   fa.sel_count_kv = sel_count_kv;
@@ -333,7 +335,10 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   aa.cfr = fa.cfr;
   aa.partials = reinterpret_cast<float*>(ws + p.off_partials);
   aa.out = out;
-  e = tactic::launch_attn(aa, (int)p.G, (int)p.attn_grid, stream);
+  int grid = 0;
+  e = tactic::attn_resident_grid((int)p.G, &grid);
+  if (e != hipSuccess) return hip_fail(e, "attention occupancy query");
+  e = tactic::launch_attn(aa, (int)p.G, grid, stream);
   if (e == hipSuccess) e = record(5);
   if (e != hipSuccess) return hip_fail(e, "attention launch");
   e = tactic::launch_combine(aa, (int)p.G, stream);
@@ -407,8 +412,11 @@ tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const ui
   aa.out = out;
   const int G = shape->n_q_heads / shape->n_kv_heads;
   const int64_t items = BG * max_chunks;
-  const int grid = (int)std::min<int64_t>(std::max<int64_t>(items, 1), tactic::kAttnGrid);
-  hipError_t e = tactic::launch_attn(aa, G, grid, stream);
+  int resident = 0;
+  hipError_t e = tactic::attn_resident_grid(G, &resident);
+  if (e != hipSuccess) return hip_fail(e, "attention occupancy query");
+  const int grid = (int)std::min<int64_t>(std::max<int64_t>(items, 1), resident);
+  e = tactic::launch_attn(aa, G, grid, stream);
   if (e == hipSuccess) e = tactic::launch_combine(aa, G, stream);
   if (e != hipSuccess) return hip_fail(e, "dense attention launch");
   return TACTIC_OK;

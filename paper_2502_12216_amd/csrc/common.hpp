@@ -65,6 +65,7 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 
 typedef short short2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // 16-byte streaming load (non-temporal hint: the data is read once)
 __device__ __forceinline__ uint4 load_stream16(const uint16_t* p) {

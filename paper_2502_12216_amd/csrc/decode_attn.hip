@@ -38,21 +38,38 @@ __device__ __forceinline__ int item_count(const AttnArgs& a, int bg) {
   return a.gmeta[bg * 4 + 2];
 }
 
-template <int G, int TOK>
+template <int W>
+__device__ __forceinline__ void load_words(const uint16_t* p, uint32_t* w) {
+  if constexpr (W == 4) {
+    const uint4 v = load_stream16(p);
+    w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+  } else {
+    const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+    w[0] = v.x; w[1] = v.y;
+  }
+}
+
+// LPR lanes share one 256-byte row (16: 16 B per lane, 32: 8 B per lane);
+// a lane-group streams TOK rows per tile.
+template <int G, int TOK, int LPR>
 __global__ __launch_bounds__(256) void attn_splitk_kernel(AttnArgs a) {
   constexpr int kPart = G * (kHeadDim + 2);
-  constexpr int kTileTok = 16 * TOK;  // tokens per workgroup tile
+  constexpr int EPL = kHeadDim / LPR;     // bf16 elements per lane
+  constexpr int W = EPL / 2;              // 32-bit words per lane
+  constexpr int GPW = kWave / LPR;        // lane-groups per wave
+  constexpr int NG = 4 * GPW;             // lane-groups per workgroup
+  constexpr int kTileTok = NG * TOK;      // tokens per workgroup tile
   __shared__ int s_prefix[kMaxGroups + 1];
   __shared__ int s_rows[kMaxChunkTokens];
   __shared__ int s_rupos[kMaxChunkTokens + 1];
   __shared__ int s_rstart[kMaxChunkTokens + 1];
-  __shared__ float s_ml[16][2][G];
+  __shared__ float s_ml[NG][2][G];
   __shared__ float s_M[G], s_L[G];
   __shared__ float s_red[4][G][kHeadDim];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6, sl = lane & 15, grp = lane >> 4;
-  const int gid = wave * 4 + grp;  // 16 lane-groups of 16 lanes
+  const int lane = tid & 63, wave = tid >> 6, sl = lane % LPR, grp = lane / LPR;
+  const int gid = wave * GPW + grp;
   const int BG = a.B * a.Hkv;
 
   for (int i = tid; i < BG; i += 256) s_prefix[i + 1] = item_count(a, i);
@@ -80,12 +97,10 @@ __global__ __launch_bounds__(256) void attn_splitk_kernel(AttnArgs a) {
     const int64_t p0 = (int64_t)c * T;
     const int cnt = (int)min(T, U - p0);
 
-    uint32_t qw[G][4];
+    uint32_t qw[G][W];
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const uint4 v = *reinterpret_cast<const uint4*>(a.q + ((int64_t)b * a.Hq + g * G + h) * kHeadDim + sl * 8);
-      qw[h][0] = v.x; qw[h][1] = v.y; qw[h][2] = v.z; qw[h][3] = v.w;
-    }
+    for (int h = 0; h < G; ++h)
+      load_words<W>(a.q + ((int64_t)b * a.Hq + g * G + h) * kHeadDim + sl * EPL, qw[h]);
 
     // rows of this item (sequence-relative)
     if (a.dense) {
@@ -115,46 +130,53 @@ __global__ __launch_bounds__(256) void attn_splitk_kernel(AttnArgs a) {
     }
     __syncthreads();
 
-    float m[G], l[G], acc[G][8];
+    float m[G], l[G], acc[G][EPL];
 #pragma unroll
     for (int h = 0; h < G; ++h) {
       m[h] = -INFINITY;
       l[h] = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
+      for (int e = 0; e < EPL; ++e) acc[h][e] = 0.f;
     }
 
-    const uint16_t* Kb = a.K + ((int64_t)g * a.total + kvb) * kHeadDim + sl * 8;
-    const uint16_t* Vb = a.V + ((int64_t)g * a.total + kvb) * kHeadDim + sl * 8;
+    const uint16_t* Kb = a.K + ((int64_t)g * a.total + kvb) * kHeadDim + sl * EPL;
+    const uint16_t* Vb = a.V + ((int64_t)g * a.total + kvb) * kHeadDim + sl * EPL;
     const int ntile = (cnt + kTileTok - 1) / kTileTok;
-    auto load_tile = [&](int tile, uint4* kk, uint4* vv) {
+    struct Tile {
+      uint32_t k[TOK][W];
+      uint32_t v[TOK][W];
+    };
+    auto load_tile = [&](int tile) -> Tile {
+      Tile r;
 #pragma unroll
       for (int i = 0; i < TOK; ++i) {
         const int t = tile * kTileTok + gid * TOK + i;
         if (t < cnt) {
           const int64_t row = s_rows[t];
-          kk[i] = load_stream16(Kb + row * kHeadDim);
-          vv[i] = load_stream16(Vb + row * kHeadDim);
+          load_words<W>(Kb + row * kHeadDim, r.k[i]);
+          load_words<W>(Vb + row * kHeadDim, r.v[i]);
         } else {
-          kk[i] = make_uint4(0, 0, 0, 0);
-          vv[i] = make_uint4(0, 0, 0, 0);
+#pragma unroll
+          for (int w = 0; w < W; ++w) r.k[i][w] = r.v[i][w] = 0u;
         }
       }
+      return r;
     };
     // one tile of TOK tokens per lane-group: logits of the G heads, running max
     // (rescale only when some group's max grows), p * v
-    auto consume = [&](const uint4* kx, const uint4* vx, int tile) {
+    auto consume = [&](const Tile& x, int tile) {
       float s[TOK][G];
 #pragma unroll
       for (int i = 0; i < TOK; ++i) {
         const bool valid = tile * kTileTok + gid * TOK + i < cnt;
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-          float d = dot2_bf16(kx[i].x, qw[h][0], 0.f);
-          d = dot2_bf16(kx[i].y, qw[h][1], d);
-          d = dot2_bf16(kx[i].z, qw[h][2], d);
-          d = dot2_bf16(kx[i].w, qw[h][3], d);
-          s[i][h] = valid ? sum16(d) * kScaleLog2 : -INFINITY;
+          float d = 0.f;
+#pragma unroll
+          for (int w = 0; w < W; ++w) d = dot2_bf16(x.k[i][w], qw[h][w], d);
+          d = sum16(d);
+          if constexpr (LPR == 32) d += __shfl_xor(d, 16, 32);
+          s[i][h] = valid ? d * kScaleLog2 : -INFINITY;
         }
       }
       float mn[G];
@@ -174,36 +196,35 @@ __global__ __launch_bounds__(256) void attn_splitk_kernel(AttnArgs a) {
           m[h] = mn[h];
           l[h] *= corr;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) acc[h][e] *= corr;
+          for (int e = 0; e < EPL; ++e) acc[h][e] *= corr;
         }
       }
 #pragma unroll
       for (int i = 0; i < TOK; ++i) {
-        const float vf[8] = {bf16lo(vx[i].x), bf16hi(vx[i].x), bf16lo(vx[i].y), bf16hi(vx[i].y),
-                             bf16lo(vx[i].z), bf16hi(vx[i].z), bf16lo(vx[i].w), bf16hi(vx[i].w)};
+        float vf[EPL];
+#pragma unroll
+        for (int w = 0; w < W; ++w) {
+          vf[2 * w] = bf16lo(x.v[i][w]);
+          vf[2 * w + 1] = bf16hi(x.v[i][w]);
+        }
 #pragma unroll
         for (int h = 0; h < G; ++h) {
           const float p = s[i][h] == -INFINITY ? 0.f : fast_exp2(s[i][h] - m[h]);
           l[h] += p;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(p, vf[e], acc[h][e]);
+          for (int e = 0; e < EPL; ++e) acc[h][e] = fmaf(p, vf[e], acc[h][e]);
         }
       }
     };
-    uint4 kc[TOK], vc[TOK], kn[TOK], vn[TOK];
-    load_tile(0, kc, vc);
+    Tile cur = load_tile(0);
 #pragma unroll 1
     for (int tile = 0; tile < ntile; ++tile) {
-      load_tile(tile + 1, kn, vn);  // zeros past the end
-      consume(kc, vc, tile);
-#pragma unroll
-      for (int i = 0; i < TOK; ++i) {
-        kc[i] = kn[i];
-        vc[i] = vn[i];
-      }
+      const Tile nxt = load_tile(tile + 1);  // zeros past the end
+      consume(cur, tile);
+      cur = nxt;
     }
 
-    // ---- merge the 16 lane-group states: common max, rescale, sum
+    // ---- merge the lane-group states: common max, rescale, sum
     if (sl == 0) {
 #pragma unroll
       for (int h = 0; h < G; ++h) {
@@ -214,9 +235,9 @@ __global__ __launch_bounds__(256) void attn_splitk_kernel(AttnArgs a) {
     __syncthreads();
     if (tid < G) {
       float mm = -INFINITY;
-      for (int q2 = 0; q2 < 16; ++q2) mm = fmaxf(mm, s_ml[q2][0][tid]);
+      for (int q2 = 0; q2 < NG; ++q2) mm = fmaxf(mm, s_ml[q2][0][tid]);
       float ll = 0.f;
-      for (int q2 = 0; q2 < 16; ++q2) {
+      for (int q2 = 0; q2 < NG; ++q2) {
         const float mq = s_ml[q2][0][tid];
         ll += mq == -INFINITY ? 0.f : s_ml[q2][1][tid] * fast_exp2(mq - mm);
       }
@@ -228,9 +249,9 @@ __global__ __launch_bounds__(256) void attn_splitk_kernel(AttnArgs a) {
     for (int h = 0; h < G; ++h) {
       const float sc = m[h] == -INFINITY ? 0.f : fast_exp2(m[h] - s_M[h]);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
+      for (int e = 0; e < EPL; ++e) {
         float v = acc[h][e] * sc;
-        v += __shfl_xor(v, 16, 64);
+        if constexpr (LPR == 16) v += __shfl_xor(v, 16, 64);
         v += __shfl_xor(v, 32, 64);
         acc[h][e] = v;
       }
@@ -239,7 +260,7 @@ __global__ __launch_bounds__(256) void attn_splitk_kernel(AttnArgs a) {
 #pragma unroll
       for (int h = 0; h < G; ++h)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) s_red[wave][h][sl * 8 + e] = acc[h][e];
+        for (int e = 0; e < EPL; ++e) s_red[wave][h][sl * EPL + e] = acc[h][e];
     }
     __syncthreads();
     float* part = a.partials + ((int64_t)bg * a.max_chunks + c) * kPart;
@@ -255,80 +276,105 @@ __global__ __launch_bounds__(256) void attn_splitk_kernel(AttnArgs a) {
   }
 }
 
-// Combine the partials of every (b, g) in chunk order: out = sum_c acc_c 2^(m_c - M)
-// / sum_c l_c 2^(m_c - M).  Groups without tokens get zeros.  grid (B*Hkv, G),
-// 128 threads: one head per workgroup, one output dimension per thread.
+// Combine the partials of every (b, g): out = sum_c acc_c 2^(m_c - M) /
+// sum_c l_c 2^(m_c - M).  grid (B*Hkv, G), 512 threads: four slices of the
+// chunks (c = slice mod 4) x 128 output dimensions, each slice a single pass
+// with a running maximum, merged in slice order.  Groups without tokens get
+// zeros.
 template <int G>
-__global__ __launch_bounds__(128) void combine_kernel(AttnArgs a) {
+__global__ __launch_bounds__(512) void combine_kernel(AttnArgs a) {
   constexpr int kPart = G * (kHeadDim + 2);
-  constexpr int kMaxC = 1024;
-  __shared__ float s_w[kMaxC];
-  __shared__ float s_red[2];
+  __shared__ float s_m[4][kHeadDim], s_num[4][kHeadDim], s_den[4][kHeadDim];
   const int bg = blockIdx.x, h = blockIdx.y;
   const int b = bg / a.Hkv, g = bg % a.Hkv;
-  const int tid = threadIdx.x;
+  const int d = threadIdx.x & (kHeadDim - 1), slice = threadIdx.x >> 7;
   const int nchunks = item_count(a, bg);
   float* out = a.out + ((int64_t)b * a.Hq + g * G + h) * kHeadDim;
   if (nchunks == 0) {
-    out[tid] = 0.f;
+    if (slice == 0) out[d] = 0.f;
     return;
   }
   const float* pb = a.partials + (int64_t)bg * a.max_chunks * kPart;
-  float M = -INFINITY;
-  for (int c = tid; c < nchunks; c += 128) M = fmaxf(M, pb[(int64_t)c * kPart + G * kHeadDim + h]);
-  for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, 64));
-  if ((tid & 63) == 0) s_red[tid >> 6] = M;
-  __syncthreads();
-  M = fmaxf(s_red[0], s_red[1]);
-  __syncthreads();
-  float den = 0.f;
-  for (int c0 = 0; c0 < nchunks; c0 += kMaxC) {
-    const int nc = min(kMaxC, nchunks - c0);
-    for (int c = tid; c < nc; c += 128) {
-      const float* pc = pb + (int64_t)(c0 + c) * kPart;
-      const float w = fast_exp2(pc[G * kHeadDim + h] - M);
-      s_w[c] = w;
-      den = fmaf(pc[G * kHeadDim + G + h], w, den);
+  float M = -INFINITY, num = 0.f, den = 0.f;
+#pragma unroll 4
+  for (int c = slice; c < nchunks; c += 4) {
+    const float* pc = pb + (int64_t)c * kPart;
+    const float mc = pc[G * kHeadDim + h], lc = pc[G * kHeadDim + G + h], ac = pc[h * kHeadDim + d];
+    if (mc > M) {
+      const float sc = fast_exp2(M - mc);
+      num *= sc;
+      den *= sc;
+      M = mc;
     }
-    __syncthreads();
-    float num = 0.f;
-    const float* pa = pb + (int64_t)c0 * kPart + h * kHeadDim + tid;
-#pragma unroll 8
-    for (int c = 0; c < nc; ++c) num = fmaf(pa[(int64_t)c * kPart], s_w[c], num);
-    if (c0 == 0) out[tid] = num;
-    else out[tid] += num;
-    __syncthreads();
+    const float w = fast_exp2(mc - M);
+    num = fmaf(ac, w, num);
+    den = fmaf(lc, w, den);
   }
-  for (int o = 32; o > 0; o >>= 1) den += __shfl_xor(den, o, 64);
-  if ((tid & 63) == 0) s_red[tid >> 6] = den;
+  s_m[slice][d] = M;
+  s_num[slice][d] = num;
+  s_den[slice][d] = den;
   __syncthreads();
-  den = s_red[0] + s_red[1];
-  out[tid] = out[tid] / den;
+  if (slice == 0) {
+    float mm = -INFINITY;
+    for (int q = 0; q < 4; ++q) mm = fmaxf(mm, s_m[q][d]);
+    float nn = 0.f, dd = 0.f;
+    for (int q = 0; q < 4; ++q) {
+      const float w = s_m[q][d] == -INFINITY ? 0.f : fast_exp2(s_m[q][d] - mm);
+      nn = fmaf(s_num[q][d], w, nn);
+      dd = fmaf(s_den[q][d], w, dd);
+    }
+    out[d] = nn / dd;
+  }
 }
 
 #ifndef TACTIC_ATTN_TOK
 #define TACTIC_ATTN_TOK 2
 #endif
+#ifndef TACTIC_ATTN_LPR
+#define TACTIC_ATTN_LPR 16
+#endif
 
 hipError_t launch_attn(const AttnArgs& a, int G, int grid, hipStream_t st) {
   constexpr int TOK = TACTIC_ATTN_TOK;
+  constexpr int LPR = TACTIC_ATTN_LPR;
   switch (G) {
-    case 1: hipLaunchKernelGGL((attn_splitk_kernel<1, TOK>), dim3(grid), dim3(256), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((attn_splitk_kernel<2, TOK>), dim3(grid), dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((attn_splitk_kernel<4, TOK>), dim3(grid), dim3(256), 0, st, a); break;
-    case 8: hipLaunchKernelGGL((attn_splitk_kernel<8, TOK>), dim3(grid), dim3(256), 0, st, a); break;
+    case 1: hipLaunchKernelGGL((attn_splitk_kernel<1, TOK, LPR>), dim3(grid), dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((attn_splitk_kernel<2, TOK, LPR>), dim3(grid), dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((attn_splitk_kernel<4, TOK, LPR>), dim3(grid), dim3(256), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((attn_splitk_kernel<8, TOK, LPR>), dim3(grid), dim3(256), 0, st, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
+// Workgroups of the attention kernel that fit on the device at once: the
+// persistent grid is sized to exactly this, so the round-robin item
+// assignment never leaves late-starting workgroups on the critical path.
+hipError_t attn_resident_grid(int G, int* grid) {
+  constexpr int TOK = TACTIC_ATTN_TOK;
+  constexpr int LPR = TACTIC_ATTN_LPR;
+  int dev = 0, cus = 0, per = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  switch (G) {
+    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<1, TOK, LPR>, 256, 0); break;
+    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<2, TOK, LPR>, 256, 0); break;
+    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<4, TOK, LPR>, 256, 0); break;
+    case 8: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<8, TOK, LPR>, 256, 0); break;
+    default: return hipErrorInvalidValue;
+  }
+  *grid = (per > 0 ? per : 1) * (cus > 0 ? cus : 1);
+  return e;
+}
+
 hipError_t launch_combine(const AttnArgs& a, int G, hipStream_t st) {
   const dim3 grid(a.B * a.Hkv, G);
   switch (G) {
-    case 1: hipLaunchKernelGGL(combine_kernel<1>, grid, dim3(128), 0, st, a); break;
-    case 2: hipLaunchKernelGGL(combine_kernel<2>, grid, dim3(128), 0, st, a); break;
-    case 4: hipLaunchKernelGGL(combine_kernel<4>, grid, dim3(128), 0, st, a); break;
-    case 8: hipLaunchKernelGGL(combine_kernel<8>, grid, dim3(128), 0, st, a); break;
+    case 1: hipLaunchKernelGGL(combine_kernel<1>, grid, dim3(512), 0, st, a); break;
+    case 2: hipLaunchKernelGGL(combine_kernel<2>, grid, dim3(512), 0, st, a); break;
+    case 4: hipLaunchKernelGGL(combine_kernel<4>, grid, dim3(512), 0, st, a); break;
+    case 8: hipLaunchKernelGGL(combine_kernel<8>, grid, dim3(512), 0, st, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

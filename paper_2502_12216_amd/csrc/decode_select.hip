@@ -148,13 +148,16 @@ __global__ __launch_bounds__(256) void score_clusters_kernel(ScoreArgs a) {
 // ============================================================================
 // 2. Per-head cluster order by a bucket sort.  Key = (descending-orderable
 //    score bits, cluster id): ascending keys give score descending, ties by
-//    ascending id.  Buckets split [min, max] of the scores linearly; the
-//    bucket index is a monotone function of the score, so bucket order agrees
-//    with key order and every element's rank is its bucket start plus the
-//    number of smaller keys in its bucket.  Then the tokens ahead of every
-//    rank (exclusive prefix of cluster sizes in rank order) and the rows of
-//    the sampled positions: exact head 1..N and the two windows (Alg. 1).
-//    One workgroup (1024 threads) per query head.
+//    ascending id.  The bucket of a score is a monotone function of it, so
+//    bucket order agrees with key order and every element's rank is its
+//    bucket start plus the number of smaller keys in its bucket.  The map
+//    squashes the standardised score z = (s - mean) / sd through
+//    z / (1 + |z|), which spreads a bell-shaped score distribution with far
+//    outliers evenly over the buckets (about one element per bucket), where a
+//    linear map over [min, max] would crowd the bulk into a few buckets.  Then
+//    the tokens ahead of every rank (exclusive prefix of cluster sizes in rank
+//    order) and the rows of the sampled positions: exact head 1..N and the
+//    two windows (Alg. 1).  One workgroup (1024 threads) per query head.
 // ============================================================================
 __device__ __forceinline__ uint32_t desc_key_bits(float s) {
   const uint32_t u = __float_as_uint(s + 0.0f);  // -0 -> +0
@@ -162,11 +165,66 @@ __device__ __forceinline__ uint32_t desc_key_bits(float s) {
   return ~ord;
 }
 
+// Monotone non-increasing in s (NaN last): every step below is a correctly
+// rounded operation that is monotone in its input (fp32 subtract and scale by
+// a positive constant, fp64 add, divide and subtract, truncation, clamp).
+__device__ __forceinline__ int squash_bucket(float s, float mu, float inv_sd, int nb) {
+  if (!(s == s)) return nb - 1;
+  const double z = (double)((s - mu) * inv_sd);
+  const double t = 1.0 - 1.0 / (1.0 + fabs(z));  // [0, 1), non-decreasing in |z|
+  const double u = z >= 0.0 ? 0.5 + 0.5 * t : 0.5 - 0.5 * t;  // non-decreasing in z
+  const int bk = (int)((1.0 - u) * (double)nb);
+  return min(max(bk, 0), nb - 1);
+}
+
+// Exclusive scan in place of a[0..8192) in LDS by 1024 threads, 8 consecutive
+// entries each (two 16-byte LDS accesses); returns the total.  Ends with a barrier.
+__device__ uint32_t scan8k_lds(uint32_t* a, uint32_t* s_wave) {
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  uint4* a4 = reinterpret_cast<uint4*>(a) + tid * 2;
+  const uint4 x = a4[0], y = a4[1];
+  const uint32_t v[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
+  uint32_t local = 0;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) local += v[e];
+  uint32_t incl = local;
+  for (int o = 1; o < kWave; o <<= 1) {
+    const uint32_t t = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += t;
+  }
+  if (lane == kWave - 1) s_wave[wave] = incl;
+  __syncthreads();
+  if (wave == 0) {
+    const uint32_t w = lane < 16 ? s_wave[lane] : 0u;
+    uint32_t wi = w;
+    for (int o = 1; o < 16; o <<= 1) {
+      const uint32_t t = __shfl_up(wi, o, kWave);
+      if (lane >= o) wi += t;
+    }
+    if (lane < 16) s_wave[lane] = wi - w;
+    if (lane == 15) s_wave[16] = wi;
+  }
+  __syncthreads();
+  uint32_t run = s_wave[wave] + incl - local;
+  uint32_t o[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    o[e] = run;
+    run += v[e];
+  }
+  a4[0] = make_uint4(o[0], o[1], o[2], o[3]);
+  a4[1] = make_uint4(o[4], o[5], o[6], o[7]);
+  const uint32_t total = s_wave[16];
+  __syncthreads();
+  return total;
+}
+
 template <bool kLds>
 __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   __shared__ uint32_t s_wave_u[17];
   __shared__ float s_wave_f[17];
+  __shared__ float s_red[16][4];
   const int tid = threadIdx.x, nt = blockDim.x;
   const int bh = blockIdx.x;
   const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
@@ -175,93 +233,149 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
   const int n = (int)(a.kv_indptr[b + 1] - a.kv_indptr[b]);
   const int32_t* off = a.offsets + (int64_t)g * (a.Ct + a.B) + cb + b;
   const float* sc = a.scores + (int64_t)bh * a.Cm;
-
-  uint64_t* keys;
-  uint32_t* cnt;
-  uint32_t* start;
-  if (kLds) {
-    keys = reinterpret_cast<uint64_t*>(smem_raw);
-    cnt = reinterpret_cast<uint32_t*>(keys + a.nb_max);
-    start = cnt + a.nb_max + 4;
-  } else {
-    keys = a.g_keys + (int64_t)bh * a.nb_max;
-    cnt = a.g_cnt + (int64_t)bh * (a.nb_max + 4);
-    start = a.g_start + (int64_t)bh * (a.nb_max + 4);
-  }
-  int nb = 1;
-  while (nb < C) nb <<= 1;
-
-  for (int i = tid; i < nb + 1; i += nt) cnt[i] = 0;
   int32_t* rank_of = a.rank_of + (int64_t)bh * a.Cm;
   int32_t* order = a.order + (int64_t)bh * a.Cm;
-  int32_t* ord_s = reinterpret_cast<int32_t*>(keys);  // cluster id by rank, after the sort
+
+  uint32_t* cnt;      // per rank: cluster size, then the exclusive prefix
+  int32_t* ostart;    // per rank: first row of the cluster
+  uint32_t total = 0; // tokens of the sequence (prefix at rank C)
   if constexpr (kLds) {
-    // C <= 8192 = 8 * 1024: every thread keeps its 8 elements in registers
+    // LDS: keys u64[8192] (after ranking: ostart i32[8192], ord_s i32[8192]),
+    // cnt u32[8192], start u32[8192]
+    uint64_t* keys = reinterpret_cast<uint64_t*>(smem_raw);
+    cnt = reinterpret_cast<uint32_t*>(keys + kSortLdsBuckets);
+    uint32_t* start = cnt + kSortLdsBuckets;
+    ostart = reinterpret_cast<int32_t*>(keys);
+    int32_t* ord_s = ostart + kSortLdsBuckets;
+    constexpr int nb = kSortLdsBuckets;
+    // every thread keeps its 8 elements in registers (C <= 8192 = 8 * 1024)
     float v[8];
-    int sz[8], bk[8], pos[8];
+    int sz[8], o0[8], bk[8], pos[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int j = tid + e * 1024;
       v[e] = j < C ? sc[j] : NAN;
-      sz[e] = j < C ? off[j + 1] - off[j] : 0;
+      o0[e] = j < C ? off[j] : 0;
+      sz[e] = j < C ? off[j + 1] - o0[e] : 0;
     }
-    float lo = INFINITY, hi = -INFINITY;
+    {
+      uint4* c4 = reinterpret_cast<uint4*>(cnt) + tid * 2;
+      c4[0] = make_uint4(0, 0, 0, 0);
+      c4[1] = make_uint4(0, 0, 0, 0);
+    }
+    // moments and range of the finite scores (one barrier)
+    float sm = 0.f, sq = 0.f, lo = INFINITY, hi = -INFINITY, nf = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       if (v[e] == v[e]) {
+        sm += v[e];
+        sq += v[e] * v[e];
         lo = fminf(lo, v[e]);
         hi = fmaxf(hi, v[e]);
+        nf += 1.f;
       }
     }
-    lo = block_minmax(lo, false, s_wave_f);
-    hi = block_minmax(hi, true, s_wave_f);
-    const float range = hi - lo;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float sv = v[e];
-      int b2 = nb - 1;
-      if (sv == sv) b2 = range > 0.f ? (int)fminf((float)(nb - 1), fmaxf(0.f, floorf((hi - sv) / range * (float)nb))) : 0;
-      bk[e] = b2;
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+      sm += __shfl_xor(sm, o, kWave);
+      sq += __shfl_xor(sq, o, kWave);
+      nf += __shfl_xor(nf, o, kWave);
+      lo = fminf(lo, __shfl_xor(lo, o, kWave));
+      hi = fmaxf(hi, __shfl_xor(hi, o, kWave));
+    }
+    if ((tid & (kWave - 1)) == 0) {
+      s_red[tid / kWave][0] = sm;
+      s_red[tid / kWave][1] = sq;
+      s_red[tid / kWave][2] = lo;
+      s_red[tid / kWave][3] = hi;
+      s_wave_f[tid / kWave] = nf;
     }
     __syncthreads();
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      if (tid + e * 1024 < C) atomicAdd(&cnt[bk[e]], 1u);
-    __syncthreads();
-    for (int i = tid; i < nb; i += nt) start[i] = cnt[i];
-    __syncthreads();
-    block_exclusive_scan<uint32_t>(start, nb, s_wave_u);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int j = tid + e * 1024;
-      if (j < C) keys[atomicAdd(&start[bk[e]], 1u)] = ((uint64_t)desc_key_bits(v[e]) << 32) | (uint32_t)j;
+    sm = 0.f, sq = 0.f, lo = INFINITY, hi = -INFINITY, nf = 0.f;
+    for (int w = 0; w < 16; ++w) {
+      sm += s_red[w][0];
+      sq += s_red[w][1];
+      lo = fminf(lo, s_red[w][2]);
+      hi = fmaxf(hi, s_red[w][3]);
+      nf += s_wave_f[w];
     }
-    __syncthreads();
+    if (lo == hi && nf == (float)C) {
+      // all scores equal: the order is the cluster id
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int j = tid + e * 1024;
-      pos[e] = 0;
-      if (j < C) {
-        const uint64_t key = ((uint64_t)desc_key_bits(v[e]) << 32) | (uint32_t)j;
-        const uint32_t end = start[bk[e]], beg = end - cnt[bk[e]];
-        uint32_t r = 0;
-        for (uint32_t t = beg; t < end; ++t) r += keys[t] < key ? 1u : 0u;
-        pos[e] = (int)(beg + r);
-        order[pos[e]] = j;
-        rank_of[j] = pos[e];
+      for (int e = 0; e < 8; ++e) pos[e] = tid + e * 1024;
+    } else {
+      const float mu = nf > 0.f ? sm / nf : 0.f;
+      const float var = nf > 0.f ? fmaxf(sq / nf - mu * mu, 0.f) : 0.f;
+      const float sd = sqrtf(var);
+      const float inv_sd = sd > 0.f ? 1.f / sd : (hi > lo ? 1.f / (hi - lo) : 1.f);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        bk[e] = squash_bucket(v[e], mu, inv_sd, nb);
+        if (tid + e * 1024 < C) atomicAdd(&cnt[bk[e]], 1u);
       }
+      __syncthreads();
+      {
+        const uint4* c4 = reinterpret_cast<const uint4*>(cnt) + tid * 2;
+        uint4* s4 = reinterpret_cast<uint4*>(start) + tid * 2;
+        s4[0] = c4[0];
+        s4[1] = c4[1];
+      }
+      scan8k_lds(start, s_wave_u);  // (each thread copied the entries it scans)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int j = tid + e * 1024;
+        if (j < C) keys[atomicAdd(&start[bk[e]], 1u)] = ((uint64_t)desc_key_bits(v[e]) << 32) | (uint32_t)j;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int j = tid + e * 1024;
+        pos[e] = 0;
+        if (j < C) {
+          const uint64_t key = ((uint64_t)desc_key_bits(v[e]) << 32) | (uint32_t)j;
+          const uint32_t end = start[bk[e]], beg = end - cnt[bk[e]];
+          uint32_t r = 0;
+          for (uint32_t t = beg; t < end; ++t) r += keys[t] < key ? 1u : 0u;
+          pos[e] = (int)(beg + r);
+        }
+      }
+      __syncthreads();
+    }
+    // sizes, starts and ids by rank; ranks >= C hold size 0
+    {
+      uint4* c4 = reinterpret_cast<uint4*>(cnt) + tid * 2;
+      c4[0] = make_uint4(0, 0, 0, 0);
+      c4[1] = make_uint4(0, 0, 0, 0);
     }
     __syncthreads();
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const int j = tid + e * 1024;
-      if (j < C) {
+      if (tid + e * 1024 < C) {
         cnt[pos[e]] = (uint32_t)sz[e];
-        ord_s[pos[e]] = j;
+        ostart[pos[e]] = o0[e];
+        ord_s[pos[e]] = tid + e * 1024;
       }
     }
     __syncthreads();
+    total = scan8k_lds(cnt, s_wave_u);  // cnt has no entry C when C == 8192
+    // global results after the last barrier (no barrier waits on these stores)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int j = tid + e * 1024;
+      if (j < C) {
+        rank_of[j] = pos[e];
+        order[j] = ord_s[j];
+      }
+    }
+    int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
+    for (int r = tid; r <= C; r += nt) rpre[r] = (int32_t)(r < C ? cnt[r] : total);
   } else {
+    uint64_t* keys = a.g_keys + (int64_t)bh * a.nb_max;
+    cnt = a.g_cnt + (int64_t)bh * (a.nb_max + 4);
+    uint32_t* start = a.g_start + (int64_t)bh * (a.nb_max + 4);
+    ostart = reinterpret_cast<int32_t*>(keys);
+    int nb = 1;
+    while (nb < C) nb <<= 1;
+    for (int i = tid; i < nb + 1; i += nt) cnt[i] = 0;
     float lo = INFINITY, hi = -INFINITY;
     for (int j = tid; j < C; j += nt) {
       const float sv = sc[j];
@@ -304,15 +418,13 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     for (int j = tid; j < C; j += nt) {
       const int p2 = rank_of[j];
       cnt[p2] = (uint32_t)(off[j + 1] - off[j]);
-      ord_s[p2] = j;
+      ostart[p2] = off[j];
     }
     __syncthreads();
+    total = block_exclusive_scan<uint32_t>(cnt, C, s_wave_u);
+    int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
+    for (int r = tid; r <= C; r += nt) rpre[r] = (int32_t)(r < C ? cnt[r] : total);
   }
-  const uint32_t ntok = block_exclusive_scan<uint32_t>(cnt, C, s_wave_u);
-  if (tid == 0) cnt[C] = ntok;
-  __syncthreads();
-  int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
-  for (int r = tid; r <= C; r += nt) rpre[r] = (int32_t)cnt[r];
 
   const Geometry geo = make_geometry(n, a.prm);
   int64_t S = geo.samples;
@@ -331,23 +443,45 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     hm[9] = (int32_t)S;
     hm[10] = C;
   }
+  if (C <= 0) return;
   const int64_t N = geo.exact ? n : geo.N;
   const int64_t W1 = geo.exact ? 0 : geo.t1 - geo.s1 + 1;
   int32_t* rows = a.sample_rows + (int64_t)bh * a.S_cap;
-  for (int64_t u = tid; u < S; u += nt) {
-    int64_t i;  // 1-based position in the unpacked list
-    if (u < N) i = u + 1;
-    else if (u < N + W1) i = geo.s1 + (u - N);
-    else i = geo.s2 + (u - N - W1);
-    int lo_r = 0, hi_r = C;  // largest r with prefix[r] < i
-    while (lo_r < hi_r) {
-      const int mid = (lo_r + hi_r + 1) >> 1;
-      if ((int64_t)cnt[mid] < i) lo_r = mid;
-      else hi_r = mid - 1;
+  auto prefix_at = [&](int r) -> uint32_t { return r < C ? cnt[r] : total; };  // r in [0, C]
+  int top = 1;
+  while (top * 2 <= C) top <<= 1;
+  constexpr int kU = 4;  // independent searches in flight per thread
+  for (int64_t u0 = tid; u0 < S; u0 += (int64_t)kU * nt) {
+    int64_t iv[kU];  // 1-based position in the unpacked list
+    int lr[kU];
+#pragma unroll
+    for (int k = 0; k < kU; ++k) {
+      const int64_t u = u0 + (int64_t)k * nt;
+      iv[k] = u < N ? u + 1 : (u < N + W1 ? geo.s1 + (u - N) : geo.s2 + (u - N - W1));
+      lr[k] = 0;
     }
-    if (lo_r >= C) lo_r = C - 1;  // only with offsets that disagree with kv_indptr
-    int32_t row = off[ord_s[lo_r]] + (int32_t)(i - 1 - (int64_t)cnt[lo_r]);
-    rows[u] = min(max(row, 0), n - 1);
+    // largest r in [0, C] with prefix[r] < i (prefix[0] = 0 < i); branch-free
+    // so that the kU lookups of a step are in flight together
+    for (int step = top; step > 0; step >>= 1) {
+      uint32_t pv[kU];
+#pragma unroll
+      for (int k = 0; k < kU; ++k) pv[k] = cnt[min(lr[k] + step, C - 1)];
+#pragma unroll
+      for (int k = 0; k < kU; ++k) {
+        const int t = lr[k] + step;
+        const int64_t p = t < C ? (int64_t)pv[k] : (t == C ? (int64_t)total : INT64_MAX);
+        lr[k] = p < iv[k] ? t : lr[k];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kU; ++k) {
+      const int64_t u = u0 + (int64_t)k * nt;
+      if (u < S) {
+        const int r = min(lr[k], C - 1);  // C only with offsets that disagree with kv_indptr
+        const int32_t row = ostart[r] + (int32_t)(iv[k] - 1 - (int64_t)prefix_at(r));
+        rows[u] = min(max(row, 0), n - 1);
+      }
+    }
   }
 }
 
@@ -404,13 +538,34 @@ __device__ double tail_sum(double a, double b, int64_t lo, int64_t hi) {
 }
 
 // 3a. Exact logits of the sampled rows, fp64 (products of bf16 values are
-//     exact in fp64).  grid (split, B*Hq), 256 threads; 16 lanes per row, each
-//     wave gathers 16 rows per round with all loads issued before use.
+//     exact in fp64).  grid (ceil(S_cap/128), B*Hq), 256 threads: workgroup c
+//     owns samples [128c, 128c + 128); 16 lanes per row, each wave gathers 32
+//     rows with all loads in flight together.  The workgroup also reduces its
+//     logits per region (exact head, window 1, window 2) to (max, sum of
+//     exp(l - max)), so the fit needs one exponential per chunk instead of one
+//     per sample.
+__device__ __forceinline__ double wave_sum_d(double v) {
+  for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+__device__ __forceinline__ double wave_max_d(double v) {
+  for (int o = kWave / 2; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+
 __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
+  __shared__ double s_lg[kSampleChunk];
+  constexpr int kRW = kSampleChunk / kWave;  // waves that reduce the chunk, one sample per lane
+  static_assert(kSampleChunk % kWave == 0 && kRW <= 4, "chunk must fit the workgroup's waves");
+  __shared__ double s_part[kRW][3][2];
   const int tid = threadIdx.x;
   const int bh = blockIdx.y;
   const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
-  const int64_t S = a.head_meta[(int64_t)bh * 16 + 9];
+  const int32_t* hm = a.head_meta + (int64_t)bh * 16;
+  const int64_t S = hm[9];
+  const int64_t u0 = (int64_t)blockIdx.x * kSampleChunk;
+  if (u0 >= S) return;
   const int lane = tid & 63, wave = tid >> 6, sl = lane & 15, grp = lane >> 4;
   double qd[8];
   {
@@ -425,76 +580,122 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
   const uint16_t* kbase = a.K + ((int64_t)g * a.total + a.kv_indptr[b]) * kHeadDim + sl * 8;
   const int32_t* rows = a.sample_rows + (int64_t)bh * a.S_cap;
   double* lg = a.logits + (int64_t)bh * a.S_cap;
-  const int64_t stride = (int64_t)a.split * 64;
-  for (int64_t base = ((int64_t)blockIdx.x * 4 + wave) * 16; base < S; base += stride) {
-    int32_t r[4];
+  constexpr int kR = kSampleChunk / 16;  // rows per lane-group
+  int32_t r[kR];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int64_t u = base + k * 4 + grp;
-      r[k] = u < S ? rows[u] : -1;
+  for (int k = 0; k < kR; ++k) {
+    const int64_t u = u0 + wave * (kSampleChunk / 4) + k * 4 + grp;
+    r[k] = u < S ? rows[u] : -1;
+  }
+  uint4 kv[kR];
+#pragma unroll
+  for (int k = 0; k < kR; ++k)
+    kv[k] = r[k] >= 0 ? load_stream16(kbase + (int64_t)r[k] * kHeadDim) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+  for (int k = 0; k < kR; ++k) {
+    const uint32_t w[4] = {kv[k].x, kv[k].y, kv[k].z, kv[k].w};
+    double acc = 0.0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc = fma(qd[2 * e], (double)bf16lo(w[e]), acc);
+      acc = fma(qd[2 * e + 1], (double)bf16hi(w[e]), acc);
     }
-    uint4 kv[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-      kv[k] = r[k] >= 0 ? load_stream16(kbase + (int64_t)r[k] * kHeadDim) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const uint32_t w[4] = {kv[k].x, kv[k].y, kv[k].z, kv[k].w};
-      double acc = 0.0;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        acc = fma(qd[2 * e], (double)bf16lo(w[e]), acc);
-        acc = fma(qd[2 * e + 1], (double)bf16hi(w[e]), acc);
-      }
-      acc = sum16d(acc);
-      const int64_t u = base + k * 4 + grp;
-      if (u < S && sl == 0) lg[u] = acc / 11.313708498984760390;  // sqrt(128)
+    acc = sum16d(acc) / 11.313708498984760390;  // sqrt(128)
+    const int t = wave * (kSampleChunk / 4) + k * 4 + grp;
+    if (sl == 0) {
+      s_lg[t] = acc;
+      if (u0 + t < S) lg[u0 + t] = acc;
     }
   }
-}
-
-__device__ __forceinline__ double wave_sum_d(double v) {
-  for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
-}
-
-__device__ __forceinline__ double wave_max_d(double v) {
-  for (int o = kWave / 2; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, kWave));
-  return v;
+  __syncthreads();
+  // per-region (max, sum exp(l - max)) of this chunk: waves 0 and 1 hold 64 samples each
+  const int64_t N = hm[8] ? S : hm[1];
+  const int64_t N1 = N + hm[2];
+  auto region = [&](int64_t u) { return u < N ? 0 : (u < N1 ? 1 : (u < S ? 2 : 3)); };
+  const int rg_lo = region(u0), rg_hi = region(min(S, u0 + kSampleChunk) - 1);  // regions present
+  if (wave < kRW) {
+    const int t = wave * kWave + lane;
+    const int reg = region(u0 + t);
+    const double l = s_lg[t];
+    for (int rg = rg_lo; rg <= rg_hi; ++rg) {
+      const double mx = wave_max_d(reg == rg ? l : -INFINITY);
+      const double sm = wave_sum_d(reg == rg ? exp(l - mx) : 0.0);
+      if (lane == 0) {
+        s_part[wave][rg][0] = mx;
+        s_part[wave][rg][1] = mx == -INFINITY ? 0.0 : sm;
+      }
+    }
+  }
+  __syncthreads();
+  if (tid < 3) {
+    double M = -INFINITY, Ssum = 0.0;
+    if (tid >= rg_lo && tid <= rg_hi) {
+#pragma unroll
+      for (int w = 0; w < kRW; ++w) M = fmax(M, s_part[w][tid][0]);
+      if (M != -INFINITY)
+#pragma unroll
+        for (int w = 0; w < kRW; ++w) {
+          const double mw = s_part[w][tid][0];
+          if (mw != -INFINITY) Ssum += s_part[w][tid][1] * exp(mw - M);
+        }
+    }
+    double* out = a.lse + (((int64_t)bh * a.split + blockIdx.x) * 3 + tid) * 2;
+    out[0] = M;
+    out[1] = Ssum;
+  }
 }
 
 // Fit and budget of one query head (Algorithm 1) by one wave, fp64.  Lane 0
 // writes the head's record and returns the cutoff (rank, length) in cut[2].
+// Region sums come from the per-chunk (max, sum) partials of the sampling
+// kernel: with M the maximum over the exact head (the shift m), a region's sum
+// of exp(l - m) is sum_c exp(M_c - m) S_c.
 __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
   const int32_t* hm = a.head_meta + (int64_t)bh * 16;
+  const double* lg = a.logits + (int64_t)bh * a.S_cap;
+  const double* lse = a.lse + (int64_t)bh * a.split * 6;
+  // the partials of the first 64 chunks load together with the head's metadata
+  double pre[6];
+#pragma unroll
+  for (int i = 0; i < 6; ++i) pre[i] = lane < a.split ? lse[lane * 6 + i] : 0.0;
   const int n = hm[0];
   const int64_t S = hm[9];
-  const double* lg = a.logits + (int64_t)bh * a.S_cap;
   const int exact = hm[8];
   const int64_t N = exact ? S : hm[1];
   const int64_t W1 = hm[2], W2 = hm[3];
+  const int nch = (int)((S + kSampleChunk - 1) / kSampleChunk);
   int k = 0;
   double m = 0.0, mu1 = 0.0, mu2 = 0.0, fa = 0.0, fb = 0.0, Sn = 0.0, T = 0.0, EN = 0.0;
   if (n > 0) {
-    double mx = -INFINITY;
-#pragma unroll 4
-    for (int64_t u = lane; u < N; u += kWave) mx = fmax(mx, lg[u]);
-    m = wave_max_d(mx);
-    double loc = 0.0, w1 = 0.0, w2 = 0.0;
-#pragma unroll 4
-    for (int64_t u = lane; u < N; u += kWave) loc += exp(lg[u] - m);
-#pragma unroll 4
-    for (int64_t u = N + lane; u < N + W1; u += kWave) w1 += exp(lg[u] - m);
-#pragma unroll 4
-    for (int64_t u = N + W1 + lane; u < N + W1 + W2; u += kWave) w2 += exp(lg[u] - m);
-    EN = wave_sum_d(loc);
-    w1 = wave_sum_d(w1);
-    w2 = wave_sum_d(w2);
+    double M[3] = {-INFINITY, -INFINITY, -INFINITY};
+    if (lane < nch)
+#pragma unroll
+      for (int rg = 0; rg < 3; ++rg) M[rg] = pre[rg * 2];
+    for (int c = lane + kWave; c < nch; c += kWave)
+#pragma unroll
+      for (int rg = 0; rg < 3; ++rg) M[rg] = fmax(M[rg], lse[(c * 3 + rg) * 2]);
+#pragma unroll
+    for (int rg = 0; rg < 3; ++rg) M[rg] = wave_max_d(M[rg]);
+    m = M[0];
+    double R[3] = {0.0, 0.0, 0.0};
+    if (lane < nch)
+#pragma unroll
+      for (int rg = 0; rg < 3; ++rg)
+        if (pre[rg * 2] != -INFINITY) R[rg] = pre[rg * 2 + 1] * exp(pre[rg * 2] - m);
+    for (int c = lane + kWave; c < nch; c += kWave)
+#pragma unroll
+      for (int rg = 0; rg < 3; ++rg) {
+        const double mc = lse[(c * 3 + rg) * 2];
+        if (mc != -INFINITY) R[rg] += lse[(c * 3 + rg) * 2 + 1] * exp(mc - m);
+      }
+#pragma unroll
+    for (int rg = 0; rg < 3; ++rg) R[rg] = wave_sum_d(R[rg]);
+    EN = R[0];
     if (exact) {
       Sn = EN;
     } else {
-      mu1 = w1 / (double)W1;
-      mu2 = w2 / (double)W2;
+      mu1 = R[1] / (double)W1;
+      mu2 = R[2] / (double)W2;
       const double x1 = (double)(hm[4] + hm[5]) / 2.0, x2 = (double)(hm[6] + hm[7]) / 2.0;
       fa = (mu1 - mu2) / (1.0 / x1 - 1.0 / x2);
       fb = mu1 - fa / x1;
@@ -505,38 +706,69 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
     } else {
       T = a.P * Sn;
       if (T <= EN) {
-        // the budget lies in the exact head: scan it in position order, 64 at a time
+        // the budget lies in the exact head: find the chunk whose head part
+        // crosses T, then scan that chunk in position order
+        const int nhc = (int)((N + kSampleChunk - 1) / kSampleChunk);
+        double base = 0.0;
+        int cstar = nhc - 1;
+        for (int c0 = 0; c0 < nhc; c0 += kWave) {
+          const int c = c0 + lane;
+          const double mc = c < nhc ? lse[(c * 3) * 2] : -INFINITY;
+          const double v = (c < nhc && mc != -INFINITY) ? lse[(c * 3) * 2 + 1] * exp(mc - m) : 0.0;
+          double incl = v;
+          for (int o = 1; o < kWave; o <<= 1) {
+            const double y = __shfl_up(incl, o, kWave);
+            if (lane >= o) incl += y;
+          }
+          int hit = (c < nhc && base + incl >= T) ? c : 0x7fffffff;
+          for (int o = kWave / 2; o > 0; o >>= 1) hit = min(hit, __shfl_xor(hit, o, kWave));
+          if (hit != 0x7fffffff) {
+            cstar = hit;
+            base += __shfl(incl - v, hit - c0, kWave);
+            break;
+          }
+          base += __shfl(incl, kWave - 1, kWave);
+        }
+        const int64_t ub = (int64_t)cstar * kSampleChunk, ue = min(N, ub + kSampleChunk);
         int cand = 0x7fffffff;
-        double run = 0.0;
-        for (int64_t u0 = 0; u0 < N && cand == 0x7fffffff; u0 += kWave) {
-          const int64_t u = u0 + lane;
-          const double e = u < N ? exp(lg[u] - m) : 0.0;
+        double run = base;
+        for (int64_t v0 = ub; v0 < ue && cand == 0x7fffffff; v0 += kWave) {
+          const int64_t u = v0 + lane;
+          const double e = u < ue ? exp(lg[u] - m) : 0.0;
           double incl = e;
           for (int o = 1; o < kWave; o <<= 1) {
             const double y = __shfl_up(incl, o, kWave);
             if (lane >= o) incl += y;
           }
-          int c2 = (u < N && run + incl >= T) ? (int)(u + 1) : 0x7fffffff;
+          int c2 = (u < ue && run + incl >= T) ? (int)(u + 1) : 0x7fffffff;
           for (int o = kWave / 2; o > 0; o >>= 1) c2 = min(c2, __shfl_xor(c2, o, kWave));
           cand = c2;
           run += __shfl(incl, kWave - 1, kWave);
         }
-        k = cand == 0x7fffffff ? (int)N : cand;  // N only if rounding lost the crossing
+        k = cand == 0x7fffffff ? (int)ue : cand;  // ue only if rounding lost the crossing
       } else {
-        // minimal k in (N, n] with E_N + tail(N+1..k) >= T; the tail is the
-        // closed form over the positive interval [L, R] of the fitted curve
-        int64_t L, R;
-        const bool any = positive_interval(fa, fb, N + 1, n, &L, &R);
+        // minimal k in (N, n] with E_N + tail(N+1..k) >= T: 64-way parallel
+        // search on the closed form over the positive interval [L, R]
+        int64_t L, Rr;
+        const bool any = positive_interval(fa, fb, N + 1, n, &L, &Rr);
         const double HL = any ? harmonic(L - 1) : 0.0;
-        auto tail_to = [&](int64_t kk) -> double {
-          const int64_t r = min(kk, R);
-          return (!any || r < L) ? 0.0 : fa * (harmonic(r) - HL) + fb * (double)(r - L + 1);
+        auto reached = [&](int64_t kk) -> bool {
+          const int64_t r = min(kk, Rr);
+          const double t = (!any || r < L) ? 0.0 : fa * (harmonic(r) - HL) + fb * (double)(r - L + 1);
+          return EN + t >= T;
         };
-        int64_t lo = N + 1, hi = n;
+        int64_t lo = N + 1, hi = n;  // the answer lies in [lo, hi]
         while (lo < hi) {
-          const int64_t mid = (lo + hi) >> 1;
-          if (EN + tail_to(mid) >= T) hi = mid;
-          else lo = mid + 1;
+          const int64_t step = (hi - lo + kWave) / kWave;
+          const int64_t cand = min(hi, lo + (int64_t)lane * step);
+          int first = reached(cand) ? lane : kWave;
+          for (int o = kWave / 2; o > 0; o >>= 1) first = min(first, __shfl_xor(first, o, kWave));
+          const int64_t chi = first < kWave ? min(hi, lo + (int64_t)first * step) : hi;
+          // a reached candidate bounds the answer above; if rounding left none
+          // reached, the clamp ends the search at hi
+          const int64_t clo = first > 0 ? min(hi, min(hi, lo + (int64_t)(first - 1) * step) + 1) : lo;
+          lo = clo;
+          hi = chi;
         }
         k = (int)lo;
       }
@@ -675,7 +907,7 @@ hipError_t launch_score(const ScoreArgs& a, int G, int grid_x, int grid_y, hipSt
 
 hipError_t launch_sort(const SortArgs& a, bool lds, int n_heads, hipStream_t st) {
   if (lds) {
-    const size_t bytes = (size_t)a.nb_max * 8 + 2 * ((size_t)a.nb_max + 4) * 4;
+    const size_t bytes = (size_t)kSortLdsBuckets * 16;  // keys u64, cnt u32, start u32
     hipLaunchKernelGGL(sort_clusters_kernel<true>, dim3(n_heads), dim3(1024), bytes, st, a);
   } else {
     hipLaunchKernelGGL(sort_clusters_kernel<false>, dim3(n_heads), dim3(1024), 0, st, a);

@@ -49,6 +49,7 @@ struct FitArgs {
   const int32_t* rprefix;
   const int32_t* rank_of;
   double* logits;             // [B*Hq][S_cap]
+  double* lse;                // [B*Hq][split][3 regions][max, sum exp(l - max)]
   double* fit;                // [B*Hq][16]
   int32_t* cut;               // [B*Hq][2]
   int32_t* sel_count_q;       // [B*Hq]
@@ -81,5 +82,6 @@ hipError_t launch_sample(const FitArgs& a, int split, int n_heads, hipStream_t s
 hipError_t launch_fit_union(const FitArgs& a, int G, int n_groups, hipStream_t st);
 hipError_t launch_attn(const AttnArgs& a, int G, int grid, hipStream_t st);
 hipError_t launch_combine(const AttnArgs& a, int G, hipStream_t st);
+hipError_t attn_resident_grid(int G, int* grid);
 
 }  // namespace tactic

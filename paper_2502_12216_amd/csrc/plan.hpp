@@ -15,9 +15,9 @@ constexpr int kSortLdsBuckets = 8192;  // largest cluster count sorted in LDS
 constexpr int kMaxGroups = 4096;       // B * Hkv limit of the attention work list
 constexpr int kFitFields = 16;
 constexpr int kStageEvents = 7;        // start + after each of the six decode kernels
-constexpr int kAttnGrid = 1024;        // persistent attention workgroups
-constexpr int kUnionLdsMax = 32768;
-constexpr int kScoreRows = 256;        // centroids per scoring workgroup    // clusters whose union lengths are staged in LDS
+constexpr int kUnionLdsMax = 32768;     // clusters whose union lengths are staged in LDS
+constexpr int kScoreRows = 128;        // centroids per scoring workgroup
+constexpr int kSampleChunk = 128;      // sampled rows per sampling workgroup
 
 struct DecodePlan {
   int64_t magic;
@@ -26,17 +26,17 @@ struct DecodePlan {
   int64_t chunk_tokens;  // tokens per attention work item
   int64_t max_chunks;    // work items per (b, g) (capacity)
   int64_t split;         // sampling workgroups per query head
-  int64_t attn_grid;     // persistent attention workgroups
+  int64_t attn_grid;     // unused (the attention grid is sized from the device's occupancy)
   int64_t sort_lds;      // 1: sort in LDS, 0: sort scratch in the workspace
   int64_t nb_max;        // bucket capacity of the sort
   // workspace byte offsets
   int64_t off_scores, off_order, off_rank, off_rprefix, off_headmeta, off_rows, off_logit;
-  int64_t off_fit, off_cut, off_union_len, off_gmeta, off_rstart, off_rupos, off_cfr;
+  int64_t off_fit, off_cut, off_union_len, off_gmeta, off_rstart, off_rupos, off_cfr, off_lse;
   int64_t off_partials, off_sort_keys, off_sort_cnt, off_sort_start;
   int64_t ws_bytes;
   int64_t exact_bp, win_bp, win_min, p1_bp, p2_bp;
   int64_t events[kStageEvents];  // optional hipEvent_t recorded between the kernels
-  int64_t pad[64 - 47];
+  int64_t pad[64 - 48];
 };
 static_assert(sizeof(DecodePlan) == 64 * sizeof(int64_t), "plan must fill tactic_decode_plan");
 
