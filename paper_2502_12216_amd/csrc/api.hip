@@ -93,11 +93,14 @@ const tactic::DecodePlan* as_plan(const tactic_decode_plan* p) {
   return reinterpret_cast<const tactic::DecodePlan*>(p);
 }
 
+constexpr int64_t kDenseMinChunk = 256;
+
+// Tokens per dense work item: 1024 (fewest item prologues) unless the batch is
+// too small to give the device about 2048 items; the workspace is sized for 256.
 int64_t dense_chunk_tokens(const tactic_kv_shape* s) {
-  // about 8 items per CU on 256 CUs when the batch is large enough
   const int64_t work = s->total_tokens * s->n_kv_heads;
   int64_t T = tactic::kMaxChunkTokens;
-  while (T > 256 && work / T < 2048) T /= 2;
+  while (T > kDenseMinChunk && work / T < 2048) T /= 2;
   return T;
 }
 
@@ -336,7 +339,7 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   aa.partials = reinterpret_cast<float*>(ws + p.off_partials);
   aa.out = out;
   int grid = 0;
-  e = tactic::attn_resident_grid((int)p.G, &grid);
+  e = tactic::attn_resident_grid((int)p.G, (int)(p.B * p.Hkv), &grid);
   if (e != hipSuccess) return hip_fail(e, "attention occupancy query");
   e = tactic::launch_attn(aa, (int)p.G, grid, stream);
   if (e == hipSuccess) e = record(5);
@@ -374,7 +377,7 @@ tactic_status tactic_sparse_decode_view(const tactic_decode_plan* plan_in, const
 
 size_t tactic_dense_decode_workspace_size(const tactic_kv_shape* shape) {
   if (check_shape(shape) != TACTIC_OK) return 0;
-  const int64_t T = dense_chunk_tokens(shape);
+  const int64_t T = kDenseMinChunk;  // the most work items any launch uses
   const int64_t BG = (int64_t)shape->batch * shape->n_kv_heads;
   const int64_t G = shape->n_q_heads / shape->n_kv_heads;
   const int64_t max_chunks = std::max<int64_t>(1, (shape->max_seq_len + T - 1) / T);
@@ -392,8 +395,12 @@ tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const ui
   const size_t need = tactic_dense_decode_workspace_size(shape);
   if (!workspace || workspace_bytes < need)
     return fail(TACTIC_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
-  const int64_t T = dense_chunk_tokens(shape);
   const int64_t BG = (int64_t)shape->batch * shape->n_kv_heads;
+  const int G = shape->n_q_heads / shape->n_kv_heads;
+  int resident = 0;
+  hipError_t e = tactic::attn_resident_grid(G, (int)BG, &resident);
+  if (e != hipSuccess) return hip_fail(e, "attention occupancy query");
+  const int64_t T = dense_chunk_tokens(shape);
   const int64_t max_chunks = std::max<int64_t>(1, (shape->max_seq_len + T - 1) / T);
   tactic::AttnArgs aa;
   memset(&aa, 0, sizeof(aa));
@@ -410,11 +417,7 @@ tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const ui
   aa.max_chunks = max_chunks;
   aa.partials = static_cast<float*>(workspace);
   aa.out = out;
-  const int G = shape->n_q_heads / shape->n_kv_heads;
   const int64_t items = BG * max_chunks;
-  int resident = 0;
-  hipError_t e = tactic::attn_resident_grid(G, &resident);
-  if (e != hipSuccess) return hip_fail(e, "attention occupancy query");
   const int grid = (int)std::min<int64_t>(std::max<int64_t>(items, 1), resident);
   e = tactic::launch_attn(aa, G, grid, stream);
   if (e == hipSuccess) e = tactic::launch_combine(aa, G, stream);

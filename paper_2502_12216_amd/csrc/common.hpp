@@ -99,11 +99,21 @@ __device__ __forceinline__ float sum16(float v) {
   return v;
 }
 
+template <int CTRL>
+__device__ __forceinline__ double dpp(double v) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, CTRL, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), CTRL, 0xF, 0xF, false);
+  return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+// fp64 sum over the 16 lanes of a DPP row, bitwise identical in every lane
+// (the same mirror-partner steps as sum16)
 __device__ __forceinline__ double sum16d(double v) {
-  v += __shfl_xor(v, 8, 16);
-  v += __shfl_xor(v, 4, 16);
-  v += __shfl_xor(v, 2, 16);
-  v += __shfl_xor(v, 1, 16);
+  v += dpp<0x140>(v);
+  v += dpp<0x141>(v);
+  v += dpp<0x4E>(v);
+  v += dpp<0xB1>(v);
   return v;
 }
 

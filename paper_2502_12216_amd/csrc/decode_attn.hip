@@ -51,21 +51,46 @@ __device__ __forceinline__ void load_words(const uint16_t* p, uint32_t* w) {
 
 // LPR lanes share one 256-byte row (16: 16 B per lane, 32: 8 B per lane);
 // a lane-group streams TOK rows per tile.
+#ifndef TACTIC_ATTN_TOK
+#define TACTIC_ATTN_TOK 2
+#endif
+#ifndef TACTIC_ATTN_LPR
+#define TACTIC_ATTN_LPR 16
+#endif
+#ifndef TACTIC_ATTN_DEPTH
+#define TACTIC_ATTN_DEPTH 2  // tiles in flight while one is consumed
+#endif
+#ifndef TACTIC_ATTN_WPE
+#define TACTIC_ATTN_WPE 3  // resident waves per SIMD the register budget must allow
+#endif
+
 template <int G, int TOK, int LPR>
-__global__ __launch_bounds__(256) void attn_splitk_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(G >= 8 ? 2 : TACTIC_ATTN_WPE)))
+void attn_splitk_kernel(AttnArgs a) {
   constexpr int kPart = G * (kHeadDim + 2);
   constexpr int EPL = kHeadDim / LPR;     // bf16 elements per lane
   constexpr int W = EPL / 2;              // 32-bit words per lane
   constexpr int GPW = kWave / LPR;        // lane-groups per wave
   constexpr int NG = 4 * GPW;             // lane-groups per workgroup
   constexpr int kTileTok = NG * TOK;      // tokens per workgroup tile
-  __shared__ int s_prefix[kMaxGroups + 1];
-  __shared__ int s_rows[kMaxChunkTokens];
-  __shared__ int s_rupos[kMaxChunkTokens + 1];
-  __shared__ int s_rstart[kMaxChunkTokens + 1];
+  extern __shared__ int s_prefix[];  // [B * Hkv + 1] work items before each group
+  // the row table of an item is dead once the merge starts, so the merge's
+  // partial sums reuse its storage
+  union ItemShared {
+    struct {
+      int rows[kMaxChunkTokens];
+      int rupos[kMaxChunkTokens + 1];
+      int rstart[kMaxChunkTokens + 1];
+    } r;
+    float red[4][G][kHeadDim];
+  };
+  __shared__ ItemShared sh;
+  int* s_rows = sh.r.rows;
+  int* s_rupos = sh.r.rupos;
+  int* s_rstart = sh.r.rstart;
+  auto s_red = sh.red;
   __shared__ float s_ml[NG][2][G];
   __shared__ float s_M[G], s_L[G];
-  __shared__ float s_red[4][G][kHeadDim];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, sl = lane % LPR, grp = lane / LPR;
@@ -216,6 +241,37 @@ __global__ __launch_bounds__(256) void attn_splitk_kernel(AttnArgs a) {
         }
       }
     };
+#if TACTIC_ATTN_DEPTH == 2
+    // two tiles in flight while one is consumed (rotation unrolled by three)
+    Tile t0 = load_tile(0), t1 = load_tile(1);
+#pragma unroll 1
+    for (int tile = 0; tile < ntile; tile += 3) {
+      Tile t2 = load_tile(tile + 2);
+      consume(t0, tile);
+      if (tile + 1 >= ntile) break;
+      t0 = load_tile(tile + 3);
+      consume(t1, tile + 1);
+      if (tile + 2 >= ntile) break;
+      t1 = load_tile(tile + 4);
+      consume(t2, tile + 2);
+    }
+#elif TACTIC_ATTN_DEPTH == 3
+    Tile t0 = load_tile(0), t1 = load_tile(1), t2 = load_tile(2);
+#pragma unroll 1
+    for (int tile = 0; tile < ntile; tile += 4) {
+      Tile t3 = load_tile(tile + 3);
+      consume(t0, tile);
+      if (tile + 1 >= ntile) break;
+      t0 = load_tile(tile + 4);
+      consume(t1, tile + 1);
+      if (tile + 2 >= ntile) break;
+      t1 = load_tile(tile + 5);
+      consume(t2, tile + 2);
+      if (tile + 3 >= ntile) break;
+      t2 = load_tile(tile + 6);
+      consume(t3, tile + 3);
+    }
+#else
     Tile cur = load_tile(0);
 #pragma unroll 1
     for (int tile = 0; tile < ntile; ++tile) {
@@ -223,6 +279,7 @@ __global__ __launch_bounds__(256) void attn_splitk_kernel(AttnArgs a) {
       consume(cur, tile);
       cur = nxt;
     }
+#endif
 
     // ---- merge the lane-group states: common max, rescale, sum
     if (sl == 0) {
@@ -327,21 +384,17 @@ __global__ __launch_bounds__(512) void combine_kernel(AttnArgs a) {
   }
 }
 
-#ifndef TACTIC_ATTN_TOK
-#define TACTIC_ATTN_TOK 2
-#endif
-#ifndef TACTIC_ATTN_LPR
-#define TACTIC_ATTN_LPR 16
-#endif
+static size_t attn_dyn_lds(const AttnArgs& a) { return ((size_t)a.B * a.Hkv + 1) * sizeof(int); }
 
 hipError_t launch_attn(const AttnArgs& a, int G, int grid, hipStream_t st) {
   constexpr int TOK = TACTIC_ATTN_TOK;
   constexpr int LPR = TACTIC_ATTN_LPR;
+  const size_t lds = attn_dyn_lds(a);
   switch (G) {
-    case 1: hipLaunchKernelGGL((attn_splitk_kernel<1, TOK, LPR>), dim3(grid), dim3(256), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((attn_splitk_kernel<2, TOK, LPR>), dim3(grid), dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((attn_splitk_kernel<4, TOK, LPR>), dim3(grid), dim3(256), 0, st, a); break;
-    case 8: hipLaunchKernelGGL((attn_splitk_kernel<8, TOK, LPR>), dim3(grid), dim3(256), 0, st, a); break;
+    case 1: hipLaunchKernelGGL((attn_splitk_kernel<1, TOK, LPR>), dim3(grid), dim3(256), lds, st, a); break;
+    case 2: hipLaunchKernelGGL((attn_splitk_kernel<2, TOK, LPR>), dim3(grid), dim3(256), lds, st, a); break;
+    case 4: hipLaunchKernelGGL((attn_splitk_kernel<4, TOK, LPR>), dim3(grid), dim3(256), lds, st, a); break;
+    case 8: hipLaunchKernelGGL((attn_splitk_kernel<8, TOK, LPR>), dim3(grid), dim3(256), lds, st, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -350,18 +403,19 @@ hipError_t launch_attn(const AttnArgs& a, int G, int grid, hipStream_t st) {
 // Workgroups of the attention kernel that fit on the device at once: the
 // persistent grid is sized to exactly this, so the round-robin item
 // assignment never leaves late-starting workgroups on the critical path.
-hipError_t attn_resident_grid(int G, int* grid) {
+hipError_t attn_resident_grid(int G, int n_groups, int* grid) {
   constexpr int TOK = TACTIC_ATTN_TOK;
   constexpr int LPR = TACTIC_ATTN_LPR;
   int dev = 0, cus = 0, per = 0;
+  const size_t lds = ((size_t)n_groups + 1) * sizeof(int);
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return e;
   switch (G) {
-    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<1, TOK, LPR>, 256, 0); break;
-    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<2, TOK, LPR>, 256, 0); break;
-    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<4, TOK, LPR>, 256, 0); break;
-    case 8: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<8, TOK, LPR>, 256, 0); break;
+    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<1, TOK, LPR>, 256, lds); break;
+    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<2, TOK, LPR>, 256, lds); break;
+    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<4, TOK, LPR>, 256, lds); break;
+    case 8: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<8, TOK, LPR>, 256, lds); break;
     default: return hipErrorInvalidValue;
   }
   *grid = (per > 0 ? per : 1) * (cus > 0 ? cus : 1);

@@ -501,32 +501,66 @@ __device__ double harmonic(int64_t x) {
          r2 * (1.0 / 12.0 - r2 * (1.0 / 120.0 - r2 * (1.0 / 252.0 - r2 * (1.0 / 240.0))));
 }
 
-// Positive interval [L, R] of a/i + b over integer i in [lo, hi] (the
-// function is monotone in i, so where it is positive is an interval); returns
-// false when it is empty.
+// Positive interval [L, R] of a/i + b over integer i in [lo, hi]; false when
+// it is empty.  a/i + b evaluated in fp64 is monotone in i (non-increasing for
+// a >= 0, non-decreasing for a < 0: correctly rounded division and addition
+// are monotone), so the positive set is a prefix or a suffix of [lo, hi] and
+// a binary search finds its end in O(log n) steps for any a and b (NaN
+// coefficients give an empty interval).
 __device__ bool positive_interval(double a, double b, int64_t lo, int64_t hi, int64_t* L, int64_t* R) {
-  if (hi < lo) return false;
-  *L = lo;
-  *R = hi;
-  auto f = [&](int64_t i) { return a / (double)i + b; };
-  if (a >= 0.0 && b >= 0.0) {
-    // every term is non-negative
-  } else if (a <= 0.0 && b <= 0.0) {
-    return false;
-  } else if (a > 0.0) {  // b < 0: positive for i < a / -b
+  if (hi < lo || !(a == a) || !(b == b)) return false;
+  auto pos = [&](int64_t i) { return a / (double)i + b > 0.0; };
+  if (a >= 0.0) {  // prefix [lo, R]
+    if (!pos(lo)) return false;
+    if (pos(hi)) {
+      *L = lo;
+      *R = hi;
+      return true;
+    }
+    // the real root -a/b (b < 0 here) usually lands on the answer
     const double z = a / -b;
-    int64_t r = z >= (double)hi ? hi : (z <= (double)lo ? lo - 1 : (int64_t)z);
-    while (r >= lo && !(f(r) > 0.0)) --r;
-    while (r + 1 <= hi && f(r + 1) > 0.0) ++r;
-    *R = r;
-  } else {  // a < 0, b > 0: positive for i > -a / b
-    const double z = -a / b;
-    int64_t l = z >= (double)hi ? hi + 1 : (z < (double)lo ? lo : (int64_t)z + 1);
-    while (l <= hi && !(f(l) > 0.0)) ++l;
-    while (l - 1 >= lo && f(l - 1) > 0.0) --l;
+    if (z >= (double)lo && z < (double)hi) {
+      const int64_t r = (int64_t)z;
+      if (pos(r) && !pos(r + 1)) {
+        *L = lo;
+        *R = r;
+        return true;
+      }
+    }
+    int64_t l = lo, h = hi;  // pos(l) holds; last positive index
+    while (l < h) {
+      const int64_t m = l + (h - l + 1) / 2;
+      if (pos(m)) l = m;
+      else h = m - 1;
+    }
+    *L = lo;
+    *R = l;
+  } else {  // suffix [L, hi]
+    if (!pos(hi)) return false;
+    if (pos(lo)) {
+      *L = lo;
+      *R = hi;
+      return true;
+    }
+    const double z = -a / b;  // b > 0 here
+    if (z >= (double)lo && z < (double)hi) {
+      const int64_t l0 = (int64_t)z + 1;
+      if (pos(l0) && !pos(l0 - 1)) {
+        *L = l0;
+        *R = hi;
+        return true;
+      }
+    }
+    int64_t l = lo, h = hi;  // pos(h) holds; first positive index
+    while (l < h) {
+      const int64_t m = l + (h - l) / 2;
+      if (pos(m)) h = m;
+      else l = m + 1;
+    }
     *L = l;
+    *R = hi;
   }
-  return *L <= *R;
+  return true;
 }
 
 // sum_{i=lo}^{hi} max(0, a/i + b) in closed form: a (H(R) - H(L-1)) + b (R - L + 1)
@@ -544,13 +578,22 @@ __device__ double tail_sum(double a, double b, int64_t lo, int64_t hi) {
 //     logits per region (exact head, window 1, window 2) to (max, sum of
 //     exp(l - max)), so the fit needs one exponential per chunk instead of one
 //     per sample.
+// wave-wide fp64 sum / max, identical in every lane: DPP within rows of 16
+// lanes, then two cross-row exchanges
 __device__ __forceinline__ double wave_sum_d(double v) {
-  for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  v = sum16d(v);
+  v += __shfl_xor(v, 16, kWave);
+  v += __shfl_xor(v, 32, kWave);
   return v;
 }
 
 __device__ __forceinline__ double wave_max_d(double v) {
-  for (int o = kWave / 2; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, kWave));
+  v = fmax(v, dpp<0x140>(v));
+  v = fmax(v, dpp<0x141>(v));
+  v = fmax(v, dpp<0x4E>(v));
+  v = fmax(v, dpp<0xB1>(v));
+  v = fmax(v, __shfl_xor(v, 16, kWave));
+  v = fmax(v, __shfl_xor(v, 32, kWave));
   return v;
 }
 
@@ -563,30 +606,35 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
   const int bh = blockIdx.y;
   const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
   const int32_t* hm = a.head_meta + (int64_t)bh * 16;
-  const int64_t S = hm[9];
   const int64_t u0 = (int64_t)blockIdx.x * kSampleChunk;
-  if (u0 >= S) return;
   const int lane = tid & 63, wave = tid >> 6, sl = lane & 15, grp = lane >> 4;
-  double qd[8];
-  {
-    const uint4 v = *reinterpret_cast<const uint4*>(a.q + (int64_t)bh * kHeadDim + sl * 8);
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      qd[2 * e] = (double)bf16lo(w[e]);
-      qd[2 * e + 1] = (double)bf16hi(w[e]);
-    }
-  }
-  const uint16_t* kbase = a.K + ((int64_t)g * a.total + a.kv_indptr[b]) * kHeadDim + sl * 8;
+  // the row indices load together with the head's metadata: entries past the
+  // head's sample count (but inside its S_cap) are read and then ignored
   const int32_t* rows = a.sample_rows + (int64_t)bh * a.S_cap;
-  double* lg = a.logits + (int64_t)bh * a.S_cap;
   constexpr int kR = kSampleChunk / 16;  // rows per lane-group
   int32_t r[kR];
 #pragma unroll
   for (int k = 0; k < kR; ++k) {
     const int64_t u = u0 + wave * (kSampleChunk / 4) + k * 4 + grp;
-    r[k] = u < S ? rows[u] : -1;
+    r[k] = u < a.S_cap ? rows[u] : -1;
   }
+  const int64_t S = hm[9];
+  if (u0 >= S) return;
+#pragma unroll
+  for (int k = 0; k < kR; ++k)
+    if (u0 + wave * (kSampleChunk / 4) + k * 4 + grp >= S) r[k] = -1;
+  float qf[8];
+  {
+    const uint4 v = *reinterpret_cast<const uint4*>(a.q + (int64_t)bh * kHeadDim + sl * 8);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      qf[2 * e] = bf16lo(w[e]);
+      qf[2 * e + 1] = bf16hi(w[e]);
+    }
+  }
+  const uint16_t* kbase = a.K + ((int64_t)g * a.total + a.kv_indptr[b]) * kHeadDim + sl * 8;
+  double* lg = a.logits + (int64_t)bh * a.S_cap;
   uint4 kv[kR];
 #pragma unroll
   for (int k = 0; k < kR; ++k)
@@ -594,13 +642,15 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
 #pragma unroll
   for (int k = 0; k < kR; ++k) {
     const uint32_t w[4] = {kv[k].x, kv[k].y, kv[k].z, kv[k].w};
+    // a product of two bf16 values has at most 16 significant bits, so it is
+    // exact in fp32 (short of fp32 underflow); the sum runs in fp64
     double acc = 0.0;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      acc = fma(qd[2 * e], (double)bf16lo(w[e]), acc);
-      acc = fma(qd[2 * e + 1], (double)bf16hi(w[e]), acc);
+      acc += (double)(qf[2 * e] * bf16lo(w[e]));
+      acc += (double)(qf[2 * e + 1] * bf16hi(w[e]));
     }
-    acc = sum16d(acc) / 11.313708498984760390;  // sqrt(128)
+    acc = sum16d(acc) * 0.088388347648318440550;  // 1 / sqrt(128), within 1 ulp of the quotient
     const int t = wave * (kSampleChunk / 4) + k * 4 + grp;
     if (sl == 0) {
       s_lg[t] = acc;
@@ -774,20 +824,28 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
       }
     }
   }
-  if (lane == 0) {
+  // cutoff cluster: largest rank r in [0, C] with prefix[r] < k, by a 64-way
+  // search of the whole wave over the prefix (prefix[0] = 0 < k keeps lane 0's
+  // candidate true, and the prefix is non-decreasing)
+  int cut_r = -1, cut_len = 0;
+  if (k > 0) {
     const int C = hm[10];
     const int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
-    int cut_r = -1, cut_len = 0;
-    if (k > 0) {  // cutoff cluster: largest rank r with prefix[r] < k
-      int lo_r = 0, hi_r = C;
-      while (lo_r < hi_r) {
-        const int mid = (lo_r + hi_r + 1) >> 1;
-        if (rpre[mid] < k) lo_r = mid;
-        else hi_r = mid - 1;
-      }
-      cut_r = lo_r;
-      cut_len = k - rpre[lo_r];
+    int lo = 0, hi = C, vlo = 0;
+    while (lo < hi) {
+      const int step = (hi - lo + kWave) / kWave;
+      const int cand = lo + lane * step;
+      const int v = cand <= hi ? rpre[cand] : 0x7fffffff;
+      const uint64_t ok = __ballot(v < k);
+      const int j = 63 - __clzll((long long)ok);
+      vlo = __shfl(v, j, kWave);
+      hi = min(hi, lo + (j + 1) * step - 1);
+      lo = lo + j * step;
     }
+    cut_r = lo;
+    cut_len = k - vlo;
+  }
+  if (lane == 0) {
     cut[0] = cut_r;
     cut[1] = cut_len;
     a.sel_count_q[bh] = k;

@@ -82,6 +82,6 @@ hipError_t launch_sample(const FitArgs& a, int split, int n_heads, hipStream_t s
 hipError_t launch_fit_union(const FitArgs& a, int G, int n_groups, hipStream_t st);
 hipError_t launch_attn(const AttnArgs& a, int G, int grid, hipStream_t st);
 hipError_t launch_combine(const AttnArgs& a, int G, hipStream_t st);
-hipError_t attn_resident_grid(int G, int* grid);
+hipError_t attn_resident_grid(int G, int n_groups, int* grid);
 
 }  // namespace tactic
