@@ -77,6 +77,7 @@ def parse():
     ap.add_argument("--clusters", choices=["kmeans", "labels"], default="kmeans")
     ap.add_argument("--cpu-groups", type=int, default=4, help="(b, g) groups the CPU oracle times")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-ablation", action="store_true", help="skip the per-head (no-union) comparison")
     ap.add_argument("--calibrate", action="store_true",
                     help="also run a plain 1 GiB device copy (reference dispatch for HBM counters)")
     return ap.parse_args()
@@ -180,19 +181,51 @@ def main():
     import ctypes
     from paper_2502_12216_amd import _capi as C
     arr = (ctypes.c_void_p * (NS + 1))(*[e.cuda_event for e in stage_ev])
-    C.check(C.lib().tactic_sparse_decode_plan_set_events(ctypes.byref(dec.plan), arr), "set_events")
-    stage_ms = np.zeros(NS)
-    nrep = 0
-    for _ in range(args.steps):
-        for l in range(layers):
-            dec(qs[l], Ks[l], Vs[l], cls[l])
-            torch.cuda.synchronize()
-            for i in range(NS):
-                stage_ms[i] += stage_ev[i].elapsed_time(stage_ev[i + 1])
-            nrep += 1
-    C.check(C.lib().tactic_sparse_decode_plan_set_events(ctypes.byref(dec.plan), None), "set_events")
-    stage_ms /= nrep
+
+    def stage_times(decoder):
+        """Mean per-kernel milliseconds over args.steps passes of every layer, from
+        events the library records between its launches on the decode stream."""
+        C.check(C.lib().tactic_sparse_decode_plan_set_events(ctypes.byref(decoder.plan), arr), "set_events")
+        acc = np.zeros(NS)
+        nrep = 0
+        for _ in range(args.steps):
+            for l in range(layers):
+                decoder(qs[l], Ks[l], Vs[l], cls[l])
+                torch.cuda.synchronize()
+                for i in range(NS):
+                    acc[i] += stage_ev[i].elapsed_time(stage_ev[i + 1])
+                nrep += 1
+        C.check(C.lib().tactic_sparse_decode_plan_set_events(ctypes.byref(decoder.plan), None), "set_events")
+        return acc / nrep
+
+    stage_ms = stage_times(dec)
     stage_names = ["score_clusters", "sort_clusters", "sample_logits", "fit_union", "attn_splitk", "combine"]
+
+    # ---------------------------------------------------------------- GQA-union ablation (Sec. 4.5)
+    ablation = None
+    if not args.no_ablation:
+        dec_ph = T.SparseDecoder(batch, ncl, T.decode_params(P, use_union=0))
+
+        def per_head_step():
+            for l in range(layers):
+                dec_ph(qs[l], Ks[l], Vs[l], cls[l])
+
+        per_head_step()
+        ms_ph = timed(per_head_step, args.steps)
+        st_ph = stage_times(dec_ph)
+        rows_ph = rows_un = 0
+        for l in range(layers):
+            _, _, skv_ph = dec_ph(qs[l], Ks[l], Vs[l], cls[l])
+            _, _, skv_un = dec(qs[l], Ks[l], Vs[l], cls[l])
+            rows_ph += int(skv_ph.sum())
+            rows_un += int(skv_un.sum())
+        ablation = {"per_head_us_per_layer": round(ms_ph * 1000 / layers, 2),
+                    "per_head_attn_us": round(float(st_ph[4] + st_ph[5]) * 1000, 2),
+                    "union_attn_us": round(float(stage_ms[4] + stage_ms[5]) * 1000, 2),
+                    "attn_speedup_from_union": round(float((st_ph[4] + st_ph[5]) / (stage_ms[4] + stage_ms[5])), 3),
+                    "kv_rows_per_head_over_union": round(rows_ph / max(1, rows_un), 3)}
+        del dec_ph
+        log(f"per-head step {ms_ph:.3f} ms")
 
     # ---------------------------------------------------------------- selection statistics, bytes
     sel_q, sel_kv, samples = [], [], []
@@ -296,6 +329,7 @@ def main():
                           "union_max": round(float(ku.max()), 5)},
         "roofline": roof,
         "cpu_baseline": cpu,
+        "union_ablation": ablation,
     }
     if args.clusters == "kmeans":
         res["kmeans"] = {"seconds_all_layers": round(kmeans_ms / 1000, 3), "layers": layers,

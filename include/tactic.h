@@ -92,8 +92,12 @@ typedef struct {
   int32_t win_min;             /* default 8 */
   int32_t p1_bp;               /* default 1000 */
   int32_t p2_bp;               /* default 6000 */
-  int32_t use_union;           /* 1: every head of a GQA group attends over the union of the
-                                  group's selections (Sec. 4.5).  0 is not supported yet. */
+  int32_t use_union;           /* 1 (default): every head of a GQA group attends over the union
+                                  of the group's selections, loaded once (Sec. 4.5).  0: every
+                                  query head attends over its own selection only (the ablation
+                                  partner of the union, Sec. 5.3); sel_count_kv then counts the
+                                  K/V rows loaded for the KV head, i.e. the sum of the group's
+                                  per-head counts.  Other values: TACTIC_ERR_INVALID_ARG. */
 } tactic_decode_params;
 
 /* Host-side launch plan of a sparse decode: sizes derived from the shape,
@@ -121,10 +125,12 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape,
  *   K_sorted,  bf16 [Hkv][total_tokens][128], rows in the cluster-sorted
  *   V_sorted   order that `meta` describes
  *   out        fp32 [B][Hq][128]: attention of each query head over the
- *              union of its group's selected tokens (softmax renormalised over
- *              that set, Eq. 3); zeros for an empty sequence
+ *              union of its group's selected tokens (use_union = 1) or over
+ *              its own selection (use_union = 0), softmax renormalised over
+ *              that set (Eq. 3); zeros for an empty sequence
  *   sel_count_q   int32 [B][Hq]: token budget k_h of each query head
- *   sel_count_kv  int32 [B][Hkv]: size of the group union |U_g|
+ *   sel_count_kv  int32 [B][Hkv]: size of the group union |U_g| (use_union = 1),
+ *              or the sum of the group's k_h (use_union = 0): K/V rows loaded
  *   workspace  at least the bytes reported by tactic_sparse_decode_plan for
  *              the same arguments; contents on entry are irrelevant.
  * The plan must come from the same shape, meta sizes and params. */
@@ -159,8 +165,10 @@ typedef struct {
   const int32_t* order;        /* [B][Hq][max_clusters]: cluster ids by rank */
   const int32_t* rank_prefix;  /* [B][Hq][max_clusters + 1]: tokens ahead of each rank */
   const double* fit;           /* [B][Hq][TACTIC_FIT_FIELDS] */
-  const int32_t* union_len;    /* [Hkv][total_clusters]: rows of each cluster in the union
-                                  (a prefix of the cluster) */
+  const int32_t* union_len;    /* [Hkv][total_clusters] (use_union = 1) or
+                                  [Hq][total_clusters] (use_union = 0): rows of each cluster
+                                  in the group's union or the head's selection (a prefix of
+                                  the cluster) */
 } tactic_decode_view;
 
 tactic_status tactic_sparse_decode_view(const tactic_decode_plan* plan, const void* workspace,

@@ -85,7 +85,7 @@ tactic_status check_params(const tactic_decode_params* p) {
   if (p->exact_bp < 0 || p->exact_bp > 10000 || p->win_bp < 0 || p->win_bp > 10000 || p->win_min < 1 ||
       p->p1_bp < 0 || p->p1_bp > 10000 || p->p2_bp < 0 || p->p2_bp > 10000)
     return fail(TACTIC_ERR_INVALID_ARG, "fit parameters out of range");
-  if (p->use_union != 1) return fail(TACTIC_ERR_UNSUPPORTED, "only use_union = 1 is implemented");
+  if (p->use_union != 0 && p->use_union != 1) return fail(TACTIC_ERR_INVALID_ARG, "use_union must be 0 or 1");
   return TACTIC_OK;
 }
 
@@ -160,6 +160,9 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape, const tact
   p.win_min = params->win_min;
   p.p1_bp = params->p1_bp;
   p.p2_bp = params->p2_bp;
+  p.use_union = params->use_union;
+  p.NV = p.use_union ? p.Hkv : p.Hq;
+  p.GV = p.use_union ? p.G : 1;
   // sampled rows per head: the largest list any length <= nmax can need
   const tactic::SelParams sp = sel_params(params);
   int64_t S_cap = 1;
@@ -177,7 +180,7 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape, const tact
   p.sort_lds = nb <= tactic::kSortLdsBuckets ? 1 : 0;
   p.nb_max = p.sort_lds ? tactic::kSortLdsBuckets : nb;
 
-  const int64_t BH = p.B * p.Hq, BG = p.B * p.Hkv;
+  const int64_t BH = p.B * p.Hq, BG = p.B * p.NV;  // BG: selection groups
   Layout L;
   p.off_scores = L.take(BH * p.Cm * 4);
   p.off_order = L.take(BH * p.Cm * 4);
@@ -189,12 +192,12 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape, const tact
   p.off_fit = L.take(BH * tactic::kFitFields * 8);
   p.off_lse = L.take(BH * p.split * 6 * 8);
   p.off_cut = L.take(BH * 2 * 4);
-  p.off_union_len = L.take(p.Hkv * p.Ct * 4);
+  p.off_union_len = L.take(p.NV * p.Ct * 4);
   p.off_gmeta = L.take(BG * 4 * 4);
   p.off_rstart = L.take(BG * p.Cm * 4);
   p.off_rupos = L.take(BG * (p.Cm + 1) * 4);
   p.off_cfr = L.take(BG * p.max_chunks * 4);
-  p.off_partials = L.take(BG * p.max_chunks * p.G * (tactic::kHeadDim + 2) * 4);
+  p.off_partials = L.take(BG * p.max_chunks * p.GV * (tactic::kHeadDim + 2) * 4);
   if (!p.sort_lds) {
     p.off_sort_keys = L.take(BH * p.nb_max * 8);
     p.off_sort_cnt = L.take(BH * (p.nb_max + 4) * 4);
@@ -223,14 +226,14 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
       p.Hkv != shape->n_kv_heads || p.nmax != shape->max_seq_len || p.total != shape->total_tokens ||
       p.Cm != meta->max_clusters || p.Ct != meta->total_clusters || p.exact_bp != params->exact_bp ||
       p.win_bp != params->win_bp || p.win_min != params->win_min || p.p1_bp != params->p1_bp ||
-      p.p2_bp != params->p2_bp)
+      p.p2_bp != params->p2_bp || p.use_union != params->use_union)
     return fail(TACTIC_ERR_INVALID_ARG, "plan does not match the shape / meta / params");
   if (!workspace || (int64_t)workspace_bytes < p.ws_bytes)
     return fail(TACTIC_ERR_WORKSPACE, "workspace has %zu bytes, needs %lld", workspace_bytes,
                 (long long)p.ws_bytes);
 
   char* ws = static_cast<char*>(workspace);
-  const int BH = (int)(p.B * p.Hq), BG = (int)(p.B * p.Hkv);
+  const int BH = (int)(p.B * p.Hq), BG = (int)(p.B * p.Hkv), BV = (int)(p.B * p.NV);
   const bool timed = p.events[0] != 0;
   auto record = [&](int i) -> hipError_t {
     return timed ? hipEventRecord(reinterpret_cast<hipEvent_t>(p.events[i]), stream) : hipSuccess;
@@ -274,6 +277,8 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   so.rprefix = reinterpret_cast<int32_t*>(ws + p.off_rprefix);
   so.sample_rows = reinterpret_cast<int32_t*>(ws + p.off_rows);
   so.head_meta = reinterpret_cast<int32_t*>(ws + p.off_headmeta);
+  so.per_head = p.use_union ? 0 : 1;
+  so.sel_count_kv = sel_count_kv;
   e = tactic::launch_sort(so, p.sort_lds != 0, BH, stream);
   if (e == hipSuccess) e = record(2);
   if (e != hipSuccess) return hip_fail(e, "sort_clusters launch");
@@ -291,6 +296,9 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   fa.Cm = (int)p.Cm;
   fa.BH = BH;
   fa.split = (int)p.split;
+  fa.NV = (int)p.NV;
+  fa.kv_div = p.use_union ? 1 : (int)p.G;
+  fa.per_head = p.use_union ? 0 : 1;
   fa.Ct = p.Ct;
   fa.total = p.total;
   fa.S_cap = p.S_cap;
@@ -315,7 +323,7 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   e = tactic::launch_sample(fa, (int)p.split, BH, stream);
   if (e == hipSuccess) e = record(3);
   if (e != hipSuccess) return hip_fail(e, "sample_logits launch");
-  e = tactic::launch_fit_union(fa, (int)p.G, BG, stream);
+  e = tactic::launch_fit_union(fa, (int)p.GV, BV, stream);
   if (e == hipSuccess) e = record(4);
   if (e != hipSuccess) return hip_fail(e, "fit_union launch");
 
@@ -329,6 +337,8 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   aa.Hkv = (int)p.Hkv;
   aa.Cm = (int)p.Cm;
   aa.dense = 0;
+  aa.NV = fa.NV;
+  aa.kv_div = fa.kv_div;
   aa.total = p.total;
   aa.chunk_tokens = p.chunk_tokens;
   aa.max_chunks = p.max_chunks;
@@ -339,12 +349,12 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   aa.partials = reinterpret_cast<float*>(ws + p.off_partials);
   aa.out = out;
   int grid = 0;
-  e = tactic::attn_resident_grid((int)p.G, (int)(p.B * p.Hkv), &grid);
+  e = tactic::attn_resident_grid((int)p.GV, BV, &grid);
   if (e != hipSuccess) return hip_fail(e, "attention occupancy query");
-  e = tactic::launch_attn(aa, (int)p.G, grid, stream);
+  e = tactic::launch_attn(aa, (int)p.GV, grid, stream);
   if (e == hipSuccess) e = record(5);
   if (e != hipSuccess) return hip_fail(e, "attention launch");
-  e = tactic::launch_combine(aa, (int)p.G, stream);
+  e = tactic::launch_combine(aa, (int)p.GV, stream);
   if (e == hipSuccess) e = record(6);
   if (e != hipSuccess) return hip_fail(e, "combine launch");
   return TACTIC_OK;
@@ -412,6 +422,8 @@ tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const ui
   aa.Hq = shape->n_q_heads;
   aa.Hkv = shape->n_kv_heads;
   aa.dense = 1;
+  aa.NV = shape->n_kv_heads;
+  aa.kv_div = 1;
   aa.total = shape->total_tokens;
   aa.chunk_tokens = T;
   aa.max_chunks = max_chunks;

@@ -31,31 +31,93 @@ __device__ __forceinline__ int64_t item_tokens(const AttnArgs& a, int bg) {
 
 __device__ __forceinline__ int item_count(const AttnArgs& a, int bg) {
   if (a.dense) {
-    const int b = bg / a.Hkv;
+    const int b = bg / a.NV;
     const int64_t n = a.kv_indptr[b + 1] - a.kv_indptr[b];
     return (int)((n + a.chunk_tokens - 1) / a.chunk_tokens);
   }
   return a.gmeta[bg * 4 + 2];
 }
 
-template <int W>
 __device__ __forceinline__ void load_words(const uint16_t* p, uint32_t* w) {
-  if constexpr (W == 4) {
-    const uint4 v = load_stream16(p);
-    w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+  const uint4 v = load_stream16(p);
+  w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+}
+
+// Sum over the 16 lanes of a DPP row of G per-lane values (one per query
+// head), returning in every lane the total of head sl / (16 / G).  Each
+// butterfly step pairs lanes across one lane bit with a mirror or quad DPP
+// move; while more than one head is left, the lower lane of a pair keeps the
+// lower half of the heads and receives its partner's copy of them, so the G
+// sums take log2(16) steps of G/2, G/4, ... adds instead of 4 steps of G.
+// Lanes that end on the same head hold bitwise identical sums (each step adds
+// the same two operands in both partners).
+template <int G>
+__device__ __forceinline__ float reduce_heads(const float (&v)[G], int sl) {
+  static_assert(G == 1 || G == 2 || G == 4 || G == 8, "heads per group: 1, 2, 4 or 8");
+  if constexpr (G == 1) {
+    return sum16(v[0]);
   } else {
-    const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
-    w[0] = v.x; w[1] = v.y;
+    constexpr int G1 = G / 2;
+    float a[G1];
+    const bool up1 = sl & 8;  // row_mirror pairs lane i with 15 - i
+#pragma unroll
+    for (int i = 0; i < G1; ++i) {
+      const float keep = up1 ? v[G1 + i] : v[i], send = up1 ? v[i] : v[G1 + i];
+      a[i] = keep + dpp<0x140>(send);
+    }
+    if constexpr (G1 == 1) {
+      float x = a[0];
+      x += dpp<0x141>(x);
+      x += dpp<0x4E>(x);
+      x += dpp<0xB1>(x);
+      return x;
+    } else {
+      constexpr int G2 = G1 / 2;
+      float c[G2];
+      const bool up2 = sl & 4;  // row_half_mirror pairs lane i with 7 - i in each half
+#pragma unroll
+      for (int i = 0; i < G2; ++i) {
+        const float keep = up2 ? a[G2 + i] : a[i], send = up2 ? a[i] : a[G2 + i];
+        c[i] = keep + dpp<0x141>(send);
+      }
+      if constexpr (G2 == 1) {
+        float x = c[0];
+        x += dpp<0x4E>(x);
+        x += dpp<0xB1>(x);
+        return x;
+      } else {
+        const bool up3 = sl & 2;  // quad_perm [2,3,0,1]
+        const float keep = up3 ? c[1] : c[0], send = up3 ? c[0] : c[1];
+        float x = keep + dpp<0x4E>(send);
+        x += dpp<0xB1>(x);
+        return x;
+      }
+    }
   }
 }
 
-// LPR lanes share one 256-byte row (16: 16 B per lane, 32: 8 B per lane);
-// a lane-group streams TOK rows per tile.
+// Value of head h (h < G, a constant after unrolling) from a lane that holds
+// it: DPP row_newbcast of the first lane of head h's lanes (lane h * 16 / G of
+// the row) to the whole row.
+template <int G>
+__device__ __forceinline__ float head_value(float x, int h) {
+  constexpr int S = 16 / G;
+  switch (h) {
+    case 0: return G == 1 ? x : dpp<0x150>(x);
+    case 1: return dpp<0x150 + 1 * S>(x);
+    case 2: return dpp<0x150 + (2 * S & 15)>(x);
+    case 3: return dpp<0x150 + (3 * S & 15)>(x);
+    case 4: return dpp<0x150 + (4 * S & 15)>(x);
+    case 5: return dpp<0x150 + (5 * S & 15)>(x);
+    case 6: return dpp<0x150 + (6 * S & 15)>(x);
+    default: return dpp<0x150 + (7 * S & 15)>(x);
+  }
+}
+
+// 16 lanes share one 256-byte row (16 B per lane); a lane-group streams TOK
+// rows per tile.
 #ifndef TACTIC_ATTN_TOK
 #define TACTIC_ATTN_TOK 2
-#endif
-#ifndef TACTIC_ATTN_LPR
-#define TACTIC_ATTN_LPR 16
 #endif
 #ifndef TACTIC_ATTN_DEPTH
 #define TACTIC_ATTN_DEPTH 2  // tiles in flight while one is consumed
@@ -64,16 +126,17 @@ __device__ __forceinline__ void load_words(const uint16_t* p, uint32_t* w) {
 #define TACTIC_ATTN_WPE 3  // resident waves per SIMD the register budget must allow
 #endif
 
-template <int G, int TOK, int LPR>
+template <int G, int TOK>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(G >= 8 ? 2 : TACTIC_ATTN_WPE)))
 void attn_splitk_kernel(AttnArgs a) {
+  constexpr int LPR = 16;                 // lanes per 256-byte row
   constexpr int kPart = G * (kHeadDim + 2);
   constexpr int EPL = kHeadDim / LPR;     // bf16 elements per lane
   constexpr int W = EPL / 2;              // 32-bit words per lane
   constexpr int GPW = kWave / LPR;        // lane-groups per wave
   constexpr int NG = 4 * GPW;             // lane-groups per workgroup
   constexpr int kTileTok = NG * TOK;      // tokens per workgroup tile
-  extern __shared__ int s_prefix[];  // [B * Hkv + 1] work items before each group
+  extern __shared__ int s_prefix[];  // [B * NV + 1] work items before each selection group
   // the row table of an item is dead once the merge starts, so the merge's
   // partial sums reuse its storage
   union ItemShared {
@@ -95,7 +158,7 @@ void attn_splitk_kernel(AttnArgs a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, sl = lane % LPR, grp = lane / LPR;
   const int gid = wave * GPW + grp;
-  const int BG = a.B * a.Hkv;
+  const int BG = a.B * a.NV;
 
   for (int i = tid; i < BG; i += 256) s_prefix[i + 1] = item_count(a, i);
   if (tid == 0) s_prefix[0] = 0;
@@ -114,7 +177,7 @@ void attn_splitk_kernel(AttnArgs a) {
       else hi = mid - 1;
     }
     const int bg = lo, c = item - s_prefix[bg];
-    const int b = bg / a.Hkv, g = bg % a.Hkv;
+    const int b = bg / a.NV, jg = bg % a.NV, kvh = jg / a.kv_div;
     const int64_t kvb = a.kv_indptr[b];
     const int nseq = (int)(a.kv_indptr[b + 1] - kvb);
     const int64_t T = item_tokens(a, bg);
@@ -125,7 +188,7 @@ void attn_splitk_kernel(AttnArgs a) {
     uint32_t qw[G][W];
 #pragma unroll
     for (int h = 0; h < G; ++h)
-      load_words<W>(a.q + ((int64_t)b * a.Hq + g * G + h) * kHeadDim + sl * EPL, qw[h]);
+      load_words(a.q + ((int64_t)b * a.Hq + jg * G + h) * kHeadDim + sl * EPL, qw[h]);
 
     // rows of this item (sequence-relative)
     if (a.dense) {
@@ -155,17 +218,17 @@ void attn_splitk_kernel(AttnArgs a) {
     }
     __syncthreads();
 
-    float m[G], l[G], acc[G][EPL];
+    // online-softmax state: the running max and sum of this lane's head hl
+    // (identical in the 16 / G lanes of that head), the accumulators of every head
+    const int hl = sl / (16 / G);
+    float m = -INFINITY, l = 0.f, acc[G][EPL];
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      m[h] = -INFINITY;
-      l[h] = 0.f;
+    for (int h = 0; h < G; ++h)
 #pragma unroll
       for (int e = 0; e < EPL; ++e) acc[h][e] = 0.f;
-    }
 
-    const uint16_t* Kb = a.K + ((int64_t)g * a.total + kvb) * kHeadDim + sl * EPL;
-    const uint16_t* Vb = a.V + ((int64_t)g * a.total + kvb) * kHeadDim + sl * EPL;
+    const uint16_t* Kb = a.K + ((int64_t)kvh * a.total + kvb) * kHeadDim + sl * EPL;
+    const uint16_t* Vb = a.V + ((int64_t)kvh * a.total + kvb) * kHeadDim + sl * EPL;
     const int ntile = (cnt + kTileTok - 1) / kTileTok;
     struct Tile {
       uint32_t k[TOK][W];
@@ -178,8 +241,8 @@ void attn_splitk_kernel(AttnArgs a) {
         const int t = tile * kTileTok + gid * TOK + i;
         if (t < cnt) {
           const int64_t row = s_rows[t];
-          load_words<W>(Kb + row * kHeadDim, r.k[i]);
-          load_words<W>(Vb + row * kHeadDim, r.v[i]);
+          load_words(Kb + row * kHeadDim, r.k[i]);
+          load_words(Vb + row * kHeadDim, r.v[i]);
         } else {
 #pragma unroll
           for (int w = 0; w < W; ++w) r.k[i][w] = r.v[i][w] = 0u;
@@ -187,45 +250,42 @@ void attn_splitk_kernel(AttnArgs a) {
       }
       return r;
     };
-    // one tile of TOK tokens per lane-group: logits of the G heads, running max
-    // (rescale only when some group's max grows), p * v
+    // one tile of TOK tokens per lane-group: logits of the G heads (each lane
+    // ends with its own head's), running max (rescale only when some group's
+    // max grows), p * v with each head's weight broadcast from its lanes
     auto consume = [&](const Tile& x, int tile) {
-      float s[TOK][G];
+      float s[TOK];
 #pragma unroll
       for (int i = 0; i < TOK; ++i) {
         const bool valid = tile * kTileTok + gid * TOK + i < cnt;
+        float d[G];
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-          float d = 0.f;
+          d[h] = 0.f;
 #pragma unroll
-          for (int w = 0; w < W; ++w) d = dot2_bf16(x.k[i][w], qw[h][w], d);
-          d = sum16(d);
-          if constexpr (LPR == 32) d += __shfl_xor(d, 16, 32);
-          s[i][h] = valid ? d * kScaleLog2 : -INFINITY;
+          for (int w = 0; w < W; ++w) d[h] = dot2_bf16(x.k[i][w], qw[h][w], d[h]);
         }
+        const float r = reduce_heads<G>(d, sl);
+        s[i] = valid ? r * kScaleLog2 : -INFINITY;
       }
-      float mn[G];
-      bool grow = false;
+      float mn = m;
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
-        float mt = s[0][h];
-#pragma unroll
-        for (int i = 1; i < TOK; ++i) mt = fmaxf(mt, s[i][h]);
-        mn[h] = fmaxf(m[h], mt);
-        grow |= mn[h] > m[h];
-      }
-      if (__any(grow)) {
+      for (int i = 0; i < TOK; ++i) mn = fmaxf(mn, s[i]);
+      if (__any(mn > m)) {
+        const float corr = mn > m ? fast_exp2(m - mn) : 1.f;
+        m = mn;
+        l *= corr;
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-          const float corr = mn[h] > m[h] ? fast_exp2(m[h] - mn[h]) : 1.f;
-          m[h] = mn[h];
-          l[h] *= corr;
+          const float c = head_value<G>(corr, h);
 #pragma unroll
-          for (int e = 0; e < EPL; ++e) acc[h][e] *= corr;
+          for (int e = 0; e < EPL; ++e) acc[h][e] *= c;
         }
       }
 #pragma unroll
       for (int i = 0; i < TOK; ++i) {
+        const float p = s[i] == -INFINITY ? 0.f : fast_exp2(s[i] - m);
+        l += p;
         float vf[EPL];
 #pragma unroll
         for (int w = 0; w < W; ++w) {
@@ -234,10 +294,9 @@ void attn_splitk_kernel(AttnArgs a) {
         }
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-          const float p = s[i][h] == -INFINITY ? 0.f : fast_exp2(s[i][h] - m[h]);
-          l[h] += p;
+          const float ph = head_value<G>(p, h);
 #pragma unroll
-          for (int e = 0; e < EPL; ++e) acc[h][e] = fmaf(p, vf[e], acc[h][e]);
+          for (int e = 0; e < EPL; ++e) acc[h][e] = fmaf(ph, vf[e], acc[h][e]);
         }
       }
     };
@@ -282,12 +341,9 @@ void attn_splitk_kernel(AttnArgs a) {
 #endif
 
     // ---- merge the lane-group states: common max, rescale, sum
-    if (sl == 0) {
-#pragma unroll
-      for (int h = 0; h < G; ++h) {
-        s_ml[gid][0][h] = m[h];
-        s_ml[gid][1][h] = l[h];
-      }
+    if (sl == hl * (16 / G)) {
+      s_ml[gid][0][hl] = m;
+      s_ml[gid][1][hl] = l;
     }
     __syncthreads();
     if (tid < G) {
@@ -302,13 +358,14 @@ void attn_splitk_kernel(AttnArgs a) {
       s_L[tid] = ll;
     }
     __syncthreads();
+    const float sc_own = m == -INFINITY ? 0.f : fast_exp2(m - s_M[hl]);
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      const float sc = m[h] == -INFINITY ? 0.f : fast_exp2(m[h] - s_M[h]);
+      const float sc = head_value<G>(sc_own, h);
 #pragma unroll
       for (int e = 0; e < EPL; ++e) {
         float v = acc[h][e] * sc;
-        if constexpr (LPR == 16) v += __shfl_xor(v, 16, 64);
+        v += __shfl_xor(v, 16, 64);
         v += __shfl_xor(v, 32, 64);
         acc[h][e] = v;
       }
@@ -334,7 +391,7 @@ void attn_splitk_kernel(AttnArgs a) {
 }
 
 // Combine the partials of every (b, g): out = sum_c acc_c 2^(m_c - M) /
-// sum_c l_c 2^(m_c - M).  grid (B*Hkv, G), 512 threads: four slices of the
+// sum_c l_c 2^(m_c - M).  grid (B*NV, G), 512 threads: four slices of the
 // chunks (c = slice mod 4) x 128 output dimensions, each slice a single pass
 // with a running maximum, merged in slice order.  Groups without tokens get
 // zeros.
@@ -343,10 +400,10 @@ __global__ __launch_bounds__(512) void combine_kernel(AttnArgs a) {
   constexpr int kPart = G * (kHeadDim + 2);
   __shared__ float s_m[4][kHeadDim], s_num[4][kHeadDim], s_den[4][kHeadDim];
   const int bg = blockIdx.x, h = blockIdx.y;
-  const int b = bg / a.Hkv, g = bg % a.Hkv;
+  const int b = bg / a.NV, jg = bg % a.NV;
   const int d = threadIdx.x & (kHeadDim - 1), slice = threadIdx.x >> 7;
   const int nchunks = item_count(a, bg);
-  float* out = a.out + ((int64_t)b * a.Hq + g * G + h) * kHeadDim;
+  float* out = a.out + ((int64_t)b * a.Hq + jg * G + h) * kHeadDim;
   if (nchunks == 0) {
     if (slice == 0) out[d] = 0.f;
     return;
@@ -384,17 +441,16 @@ __global__ __launch_bounds__(512) void combine_kernel(AttnArgs a) {
   }
 }
 
-static size_t attn_dyn_lds(const AttnArgs& a) { return ((size_t)a.B * a.Hkv + 1) * sizeof(int); }
+static size_t attn_dyn_lds(const AttnArgs& a) { return ((size_t)a.B * a.NV + 1) * sizeof(int); }
 
 hipError_t launch_attn(const AttnArgs& a, int G, int grid, hipStream_t st) {
   constexpr int TOK = TACTIC_ATTN_TOK;
-  constexpr int LPR = TACTIC_ATTN_LPR;
   const size_t lds = attn_dyn_lds(a);
   switch (G) {
-    case 1: hipLaunchKernelGGL((attn_splitk_kernel<1, TOK, LPR>), dim3(grid), dim3(256), lds, st, a); break;
-    case 2: hipLaunchKernelGGL((attn_splitk_kernel<2, TOK, LPR>), dim3(grid), dim3(256), lds, st, a); break;
-    case 4: hipLaunchKernelGGL((attn_splitk_kernel<4, TOK, LPR>), dim3(grid), dim3(256), lds, st, a); break;
-    case 8: hipLaunchKernelGGL((attn_splitk_kernel<8, TOK, LPR>), dim3(grid), dim3(256), lds, st, a); break;
+    case 1: hipLaunchKernelGGL((attn_splitk_kernel<1, TOK>), dim3(grid), dim3(256), lds, st, a); break;
+    case 2: hipLaunchKernelGGL((attn_splitk_kernel<2, TOK>), dim3(grid), dim3(256), lds, st, a); break;
+    case 4: hipLaunchKernelGGL((attn_splitk_kernel<4, TOK>), dim3(grid), dim3(256), lds, st, a); break;
+    case 8: hipLaunchKernelGGL((attn_splitk_kernel<8, TOK>), dim3(grid), dim3(256), lds, st, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -405,17 +461,16 @@ hipError_t launch_attn(const AttnArgs& a, int G, int grid, hipStream_t st) {
 // assignment never leaves late-starting workgroups on the critical path.
 hipError_t attn_resident_grid(int G, int n_groups, int* grid) {
   constexpr int TOK = TACTIC_ATTN_TOK;
-  constexpr int LPR = TACTIC_ATTN_LPR;
   int dev = 0, cus = 0, per = 0;
   const size_t lds = ((size_t)n_groups + 1) * sizeof(int);
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return e;
   switch (G) {
-    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<1, TOK, LPR>, 256, lds); break;
-    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<2, TOK, LPR>, 256, lds); break;
-    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<4, TOK, LPR>, 256, lds); break;
-    case 8: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<8, TOK, LPR>, 256, lds); break;
+    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<1, TOK>, 256, lds); break;
+    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<2, TOK>, 256, lds); break;
+    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<4, TOK>, 256, lds); break;
+    case 8: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<8, TOK>, 256, lds); break;
     default: return hipErrorInvalidValue;
   }
   *grid = (per > 0 ? per : 1) * (cus > 0 ? cus : 1);
@@ -423,7 +478,7 @@ hipError_t attn_resident_grid(int G, int n_groups, int* grid) {
 }
 
 hipError_t launch_combine(const AttnArgs& a, int G, hipStream_t st) {
-  const dim3 grid(a.B * a.Hkv, G);
+  const dim3 grid(a.B * a.NV, G);
   switch (G) {
     case 1: hipLaunchKernelGGL(combine_kernel<1>, grid, dim3(512), 0, st, a); break;
     case 2: hipLaunchKernelGGL(combine_kernel<2>, grid, dim3(512), 0, st, a); break;

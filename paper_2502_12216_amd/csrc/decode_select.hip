@@ -442,6 +442,7 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     hm[8] = geo.exact;
     hm[9] = (int32_t)S;
     hm[10] = C;
+    if (a.per_head && h % a.G == 0) a.sel_count_kv[b * a.Hkv + g] = 0;  // summed by fit_union
   }
   if (C <= 0) return;
   const int64_t N = geo.exact ? n : geo.N;
@@ -868,15 +869,16 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
   __shared__ int s_cut[G][2];
   const int tid = threadIdx.x, nt = blockDim.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int bg = blockIdx.x;
-  const int b = bg / a.Hkv, g = bg % a.Hkv;
-  if (wave < G) fit_head_wave(a, b * a.Hq + g * G + wave, lane, s_cut[wave]);
+  const int bg = blockIdx.x;  // selection group: G query heads reading KV head kvh
+  const int b = bg / a.NV, jg = bg % a.NV, kvh = jg / a.kv_div;
+  const int h0 = b * a.Hq + jg * G;  // first query head of the group
+  if (wave < G) fit_head_wave(a, h0 + wave, lane, s_cut[wave]);
   __syncthreads();
 
   const int64_t cb = a.cl_indptr[b];
   const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
-  const int32_t* off = a.offsets + (int64_t)g * (a.Ct + a.B) + cb + b;
-  int32_t* ulen = a.union_len + (int64_t)g * a.Ct + cb;
+  const int32_t* off = a.offsets + (int64_t)kvh * (a.Ct + a.B) + cb + b;
+  int32_t* ulen = a.union_len + (int64_t)jg * a.Ct + cb;
   int32_t* Ls = a.Cm <= kUnionLdsMax ? reinterpret_cast<int32_t*>(smem_raw) : ulen;
   // pass 1 (coalesced): selected prefix length of every cluster = max over heads
 #pragma unroll 4
@@ -885,7 +887,7 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
     int L = 0;
 #pragma unroll
     for (int hh = 0; hh < G; ++hh) {
-      const int r = a.rank_of[(int64_t)(b * a.Hq + g * G + hh) * a.Cm + j];
+      const int r = a.rank_of[(int64_t)(h0 + hh) * a.Cm + j];
       const int len = r < s_cut[hh][0] ? size : (r == s_cut[hh][0] ? s_cut[hh][1] : 0);
       L = max(L, len);
     }
@@ -944,7 +946,8 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
     a.gmeta[bg * 4 + 1] = (int32_t)U;
     a.gmeta[bg * 4 + 2] = (int32_t)((U + T - 1) / T);
     a.gmeta[bg * 4 + 3] = (int32_t)T;
-    a.sel_count_kv[bg] = (int32_t)U;
+    if (a.per_head) atomicAdd(&a.sel_count_kv[b * a.Hkv + kvh], (int32_t)U);  // rows loaded per KV head
+    else a.sel_count_kv[bg] = (int32_t)U;
   }
 }
 

@@ -33,6 +33,8 @@ struct SortArgs {
   int32_t* rprefix;           // [B*Hq][Cm+1]
   int32_t* sample_rows;       // [B*Hq][S_cap]
   int32_t* head_meta;         // [B*Hq][16]
+  int per_head;               // 1: per-head selections (no union); sel_count_kv is then a sum
+  int32_t* sel_count_kv;      // [B*Hkv], zeroed here in per-head mode
 };
 
 struct FitArgs {
@@ -42,6 +44,9 @@ struct FitArgs {
   const int64_t* cl_indptr;
   const int32_t* offsets;
   int B, Hq, Hkv, G, Cm, BH, split;
+  // selection groups: NV per sequence of GV query heads each; group j reads KV
+  // head j / kv_div (union: NV = Hkv, GV = G, kv_div = 1; per head: NV = Hq, GV = 1, kv_div = G)
+  int NV, kv_div, per_head;
   int64_t Ct, total, S_cap, chunk_tokens, max_chunks;
   double P;
   const int32_t* head_meta;
@@ -54,11 +59,11 @@ struct FitArgs {
   int32_t* cut;               // [B*Hq][2]
   int32_t* sel_count_q;       // [B*Hq]
   int32_t* sel_count_kv;      // [B*Hkv]
-  int32_t* union_len;         // [Hkv][Ct]
-  int32_t* gmeta;             // [B*Hkv][4]: ranges, union tokens, work items, tokens per item
-  int32_t* rstart;            // [B*Hkv][Cm]
-  int32_t* rupos;             // [B*Hkv][Cm+1]
-  int32_t* cfr;               // [B*Hkv][max_chunks]
+  int32_t* union_len;         // [NV][Ct]
+  int32_t* gmeta;             // [B*NV][4]: ranges, union tokens, work items, tokens per item
+  int32_t* rstart;            // [B*NV][Cm]
+  int32_t* rupos;             // [B*NV][Cm+1]
+  int32_t* cfr;               // [B*NV][max_chunks]
 };
 
 struct AttnArgs {
@@ -67,12 +72,13 @@ struct AttnArgs {
   const uint16_t* V;
   const int64_t* kv_indptr;
   int B, Hq, Hkv, Cm, dense;
+  int NV, kv_div;             // selection groups per sequence and KV head divisor (as in FitArgs)
   int64_t total, chunk_tokens, max_chunks;
   const int32_t* gmeta;
   const int32_t* rstart;
   const int32_t* rupos;
   const int32_t* cfr;
-  float* partials;            // [B*Hkv][max_chunks][G*130]
+  float* partials;            // [B*NV][max_chunks][GV*130]
   float* out;                 // [B][Hq][128]
 };
 

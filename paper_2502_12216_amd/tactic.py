@@ -145,6 +145,7 @@ class SparseDecoder:
         BH = b.batch * b.n_q_heads
         Cm = max(self.n_clusters)
         Ct = int(sum(self.n_clusters))
+        nv = b.n_kv_heads if self.params.use_union else b.n_q_heads  # selection groups per sequence
 
         def sl(ptr, count, dtype, shape):
             off = ptr - base
@@ -156,7 +157,7 @@ class SparseDecoder:
             "order": sl(v.order, BH * Cm, torch.int32, (b.batch, b.n_q_heads, Cm)),
             "rank_prefix": sl(v.rank_prefix, BH * (Cm + 1), torch.int32, (b.batch, b.n_q_heads, Cm + 1)),
             "fit": sl(v.fit, BH * C.FIT_FIELDS, torch.float64, (b.batch, b.n_q_heads, C.FIT_FIELDS)),
-            "union_len": sl(v.union_len, b.n_kv_heads * Ct, torch.int32, (b.n_kv_heads, Ct)),
+            "union_len": sl(v.union_len, nv * Ct, torch.int32, (nv, Ct)),
         }
 
 

@@ -9,9 +9,11 @@ ones, so a tie resolved differently upstream cannot fail a later stage):
      or the oracle's cumulative sum at the GPU's k is within 1e-5 (relative)
      of the target on both sides of the cutoff;
   4. union: per-cluster selected prefix lengths identical to the oracle's
-     union of the GPU's per-head selections;
+     union of the GPU's per-head selections (per-head mode: each head's own
+     selection, and the loaded count is the sum of the k_h);
   5. output: max |out_gpu - o~(U_gpu)| <= 2e-3 with o~ the oracle's fp64
-     attention over the GPU's union (Eq. 3).
+     attention over the GPU's union (Eq. 3), or over each head's own
+     selection in per-head mode.
 """
 from __future__ import annotations
 
@@ -47,8 +49,18 @@ def group_inputs(q, Ks, Vs, cent, offsets, kv_indptr, cl_indptr, b, g, G):
     )
 
 
-def check_group(inp: dict, P: float, prm: OT.FitParams, gpu: dict, label: str = "") -> dict:
-    """gpu: scores (G, C), order (G, C), k (G,), union_len (C,), out (G, d), sel_kv (int)."""
+def _cluster_lengths(rows: np.ndarray, off: np.ndarray, C: int) -> np.ndarray:
+    """Selected rows per cluster of a set of rows of the cluster-sorted cache."""
+    if len(rows) == 0:
+        return np.zeros(C, np.int64)
+    clus = np.searchsorted(off, rows, side="right") - 1
+    return np.bincount(clus, minlength=C)[:C]
+
+
+def check_group(inp: dict, P: float, prm: OT.FitParams, gpu: dict, label: str = "",
+                use_union: bool = True) -> dict:
+    """gpu: scores (G, C), order (G, C), k (G,), union_len (C,) or per head (G, C)
+    when not use_union, out (G, d), sel_kv (int)."""
     Q, Ks, Vs, cent, off = inp["Q"], inp["Ks"], inp["Vs"], inp["cent"], inp["off"]
     G = Q.shape[0]
     C = cent.shape[0]
@@ -89,6 +101,20 @@ def check_group(inp: dict, P: float, prm: OT.FitParams, gpu: dict, label: str = 
         stats["cut_ties"] += 1
     # union of the GPU's per-head selections, as per-cluster prefix lengths
     sel_rows = [r.rows[h][:int(k_gpu[h])] for h in range(G)]
+    if not use_union:
+        loaded = 0
+        err = 0.0
+        for h in range(G):
+            I = np.sort(sel_rows[h])
+            ug = np.asarray(gpu["union_len"][h][:C], dtype=np.int64)
+            assert np.array_equal(_cluster_lengths(I, off, C), ug), f"{label} head {h}: selection differs"
+            loaded += len(I)
+            ref = OA.sparse_attention(Q[h], Ks, Vs, I) if len(I) else np.zeros(Q.shape[1])
+            err = max(err, float(np.max(np.abs(gpu["out"][h] - ref))))
+        assert int(gpu["sel_kv"]) == loaded, f"{label}: loaded gpu {int(gpu['sel_kv'])} oracle {loaded}"
+        assert err <= OUT_ATOL, f"{label}: output max-abs error {err} > {OUT_ATOL}"
+        stats.update(out_err=err, k=k_gpu.tolist(), union=loaded, n=n)
+        return stats
     U = np.unique(np.concatenate(sel_rows)) if G else np.zeros(0, np.int64)
     clus = np.searchsorted(off, U, side="right") - 1 if len(U) else np.zeros(0, np.int64)
     ulen = np.bincount(clus, minlength=C)[:C] if len(U) else np.zeros(C, np.int64)

@@ -69,13 +69,26 @@ def test_plan_rejects_bad_target(P):
     assert st == 1
 
 
-def test_plan_rejects_inconsistent_clusters_and_no_union():
+def test_plan_rejects_inconsistent_clusters_and_bad_union_flag():
     st, _, _ = _plan(_shape(), C.ClusterMeta(100, 256, FAKE, FAKE, FAKE), _params())
     assert st == 1
     p = _params()
-    p.use_union = 0
+    p.use_union = 2
     st, _, _ = _plan(_shape(), C.ClusterMeta(256, 256, FAKE, FAKE, FAKE), p)
-    assert st == 2
+    assert st == 1
+
+
+def test_per_head_plan_sizes_selection_groups_per_query_head():
+    """use_union = 0 plans one selection group per query head: the range
+    tables and partials grow with Hq instead of Hkv, the per-head tables not."""
+    meta = C.ClusterMeta(256, 256, FAKE, FAKE, FAKE)
+    pu = _params()
+    ph = _params()
+    ph.use_union = 0
+    st1, plan_u, n_u = _plan(_shape(), meta, pu)
+    st2, plan_h, n_h = _plan(_shape(), meta, ph)
+    assert st1 == 0 and st2 == 0
+    assert n_h > n_u
 
 
 def test_plan_workspace_grows_with_shape():

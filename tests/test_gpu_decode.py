@@ -50,6 +50,7 @@ def run_sparse(inp, lay, P, params=None):
 def check_layer(inp, lay, P, res, groups=None, label=""):
     wl = inp.wl
     G = wl.n_q_heads // wl.n_kv_heads
+    union = bool(res["params"].use_union)
     B = len(inp.kv_indptr) - 1
     prm = fit_params(res["params"])
     todo = groups if groups is not None else [(b, g) for b in range(B) for g in range(wl.n_kv_heads)]
@@ -62,10 +63,11 @@ def check_layer(inp, lay, P, res, groups=None, label=""):
         gpu = dict(scores=np64(v["scores"][b, g * G:(g + 1) * G]),
                    order=v["order"][b, g * G:(g + 1) * G].numpy(),
                    k=res["sel_q"][b, g * G:(g + 1) * G].numpy(),
-                   union_len=v["union_len"][g, c0:c1].numpy(),
+                   union_len=(v["union_len"][g, c0:c1].numpy() if union
+                              else v["union_len"][g * G:(g + 1) * G, c0:c1].numpy()),
                    out=np64(res["out"][b, g * G:(g + 1) * G]),
                    sel_kv=int(res["sel_kv"][b, g]))
-        allstats.append(check_group(gi, _p32(P), prm, gpu, label=f"{label} b={b} g={g}"))
+        allstats.append(check_group(gi, _p32(P), prm, gpu, label=f"{label} b={b} g={g}", use_union=union))
     return allstats
 
 
@@ -83,6 +85,24 @@ def test_sparse_ctx4k_full_parity(P):
           f"err={max(s['out_err'] for s in st):.2e}")
     if P == 1.0:
         assert all(s["union"] == s["n"] for s in st)
+
+
+@pytest.mark.parametrize("P", [0.5, 0.9])
+def test_sparse_per_head_parity_and_union_saving(P):
+    """use_union = 0: every head attends over its own selection (the ablation
+    partner of the GQA union).  Same budgets as the union path; the union
+    never loads more rows than the per-head sum."""
+    T = _tactic()
+    wl = _small("ctx32k_llama8b", [4096, 2500, 0, 3])
+    inp = synth.make_layer(wl, 0)
+    lay = synth.label_layout(inp)
+    ph = run_sparse(inp, lay, P, T.decode_params(P, use_union=0))
+    check_layer(inp, lay, P, ph, label=f"per-head P={P}")
+    un = run_sparse(inp, lay, P)
+    assert torch.equal(ph["sel_q"], un["sel_q"])
+    assert torch.all(un["sel_kv"] <= ph["sel_kv"])
+    G = wl.n_q_heads // wl.n_kv_heads
+    assert torch.equal(ph["sel_kv"], ph["sel_q"].view(len(wl.seq_lens), wl.n_kv_heads, G).sum(-1))
 
 
 def test_sparse_ragged_small_with_empty_and_tiny_sequences():
