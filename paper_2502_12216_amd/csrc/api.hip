@@ -93,15 +93,15 @@ const tactic::DecodePlan* as_plan(const tactic_decode_plan* p) {
   return reinterpret_cast<const tactic::DecodePlan*>(p);
 }
 
-constexpr int64_t kDenseMinChunk = 256;
-
-// Tokens per dense work item: 1024 (fewest item prologues) unless the batch is
-// too small to give the device about 2048 items; the workspace is sized for 256.
-int64_t dense_chunk_tokens(const tactic_kv_shape* s) {
-  const int64_t work = s->total_tokens * s->n_kv_heads;
-  int64_t T = tactic::kMaxChunkTokens;
-  while (T > kDenseMinChunk && work / T < 2048) T /= 2;
-  return T;
+// Workspace of a dense launch on `grid` attention workgroups: a partial slot
+// per (KV group, workgroup) pair that can meet, and the split's offsets.
+size_t dense_workspace_bytes(const tactic_kv_shape* s, int64_t grid) {
+  const int64_t BG = (int64_t)s->batch * s->n_kv_heads;
+  const int64_t G = s->n_q_heads / s->n_kv_heads;
+  Layout L;
+  L.take((BG + grid) * G * (tactic::kHeadDim + 2) * 4);
+  L.take((BG + 2) * 8);
+  return (size_t)L.cur;
 }
 
 }  // namespace
@@ -171,10 +171,13 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape, const tact
     if (g.samples > S_cap) S_cap = g.samples;
   }
   p.S_cap = S_cap;
-  p.chunk_tokens = 256;
+  p.chunk_tokens = tactic::kCfrTokens;
   p.max_chunks = std::max<int64_t>(1, (p.nmax + p.chunk_tokens - 1) / p.chunk_tokens);
   p.split = std::max<int64_t>(1, (S_cap + tactic::kSampleChunk - 1) / tactic::kSampleChunk);
-  p.attn_grid = 0;  // sized at launch from the device's occupancy
+  // the partials hold one slot per (selection group, attention workgroup) pair
+  // that can meet: at most groups + workgroups; the grid (the device's resident
+  // capacity) is capped so that the plan does not depend on the device
+  p.attn_grid = tactic::kMaxAttnGrid;
   int64_t nb = 1;
   while (nb < p.Cm) nb <<= 1;
   p.sort_lds = nb <= tactic::kSortLdsBuckets ? 1 : 0;
@@ -197,7 +200,8 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape, const tact
   p.off_rstart = L.take(BG * p.Cm * 4);
   p.off_rupos = L.take(BG * (p.Cm + 1) * 4);
   p.off_cfr = L.take(BG * p.max_chunks * 4);
-  p.off_partials = L.take(BG * p.max_chunks * p.GV * (tactic::kHeadDim + 2) * 4);
+  p.off_partials = L.take((BG + p.attn_grid) * p.GV * (tactic::kHeadDim + 2) * 4);
+  p.off_ameta = L.take((BG + 2) * 8);
   if (!p.sort_lds) {
     p.off_sort_keys = L.take(BH * p.nb_max * 8);
     p.off_sort_cnt = L.take(BH * (p.nb_max + 4) * 4);
@@ -347,10 +351,12 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   aa.rupos = fa.rupos;
   aa.cfr = fa.cfr;
   aa.partials = reinterpret_cast<float*>(ws + p.off_partials);
+  aa.ameta = reinterpret_cast<int64_t*>(ws + p.off_ameta);
   aa.out = out;
   int grid = 0;
   e = tactic::attn_resident_grid((int)p.GV, BV, &grid);
   if (e != hipSuccess) return hip_fail(e, "attention occupancy query");
+  grid = (int)std::min<int64_t>(grid, p.attn_grid);  // the partials are sized for attn_grid
   e = tactic::launch_attn(aa, (int)p.GV, grid, stream);
   if (e == hipSuccess) e = record(5);
   if (e != hipSuccess) return hip_fail(e, "attention launch");
@@ -387,13 +393,7 @@ tactic_status tactic_sparse_decode_view(const tactic_decode_plan* plan_in, const
 
 size_t tactic_dense_decode_workspace_size(const tactic_kv_shape* shape) {
   if (check_shape(shape) != TACTIC_OK) return 0;
-  const int64_t T = kDenseMinChunk;  // the most work items any launch uses
-  const int64_t BG = (int64_t)shape->batch * shape->n_kv_heads;
-  const int64_t G = shape->n_q_heads / shape->n_kv_heads;
-  const int64_t max_chunks = std::max<int64_t>(1, (shape->max_seq_len + T - 1) / T);
-  Layout L;
-  L.take(BG * max_chunks * G * (tactic::kHeadDim + 2) * 4);
-  return (size_t)L.cur;
+  return dense_workspace_bytes(shape, tactic::kMaxAttnGrid);
 }
 
 tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const uint16_t* V,
@@ -402,16 +402,15 @@ tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const ui
   tactic_status st = check_shape(shape);
   if (st != TACTIC_OK) return st;
   if (!q || !K || !V || !out) return fail(TACTIC_ERR_INVALID_ARG, "null argument");
-  const size_t need = tactic_dense_decode_workspace_size(shape);
-  if (!workspace || workspace_bytes < need)
-    return fail(TACTIC_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
   const int64_t BG = (int64_t)shape->batch * shape->n_kv_heads;
   const int G = shape->n_q_heads / shape->n_kv_heads;
+  const size_t need = dense_workspace_bytes(shape, tactic::kMaxAttnGrid);
+  if (!workspace || workspace_bytes < need)
+    return fail(TACTIC_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
   int resident = 0;
   hipError_t e = tactic::attn_resident_grid(G, (int)BG, &resident);
   if (e != hipSuccess) return hip_fail(e, "attention occupancy query");
-  const int64_t T = dense_chunk_tokens(shape);
-  const int64_t max_chunks = std::max<int64_t>(1, (shape->max_seq_len + T - 1) / T);
+  resident = std::min(resident, tactic::kMaxAttnGrid);
   tactic::AttnArgs aa;
   memset(&aa, 0, sizeof(aa));
   aa.q = q;
@@ -425,13 +424,14 @@ tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const ui
   aa.NV = shape->n_kv_heads;
   aa.kv_div = 1;
   aa.total = shape->total_tokens;
-  aa.chunk_tokens = T;
-  aa.max_chunks = max_chunks;
   aa.partials = static_cast<float*>(workspace);
+  {
+    Layout L;  // same layout as dense_workspace_bytes
+    L.take((BG + tactic::kMaxAttnGrid) * G * (tactic::kHeadDim + 2) * 4);
+    aa.ameta = reinterpret_cast<int64_t*>(static_cast<char*>(workspace) + L.take((BG + 2) * 8));
+  }
   aa.out = out;
-  const int64_t items = BG * max_chunks;
-  const int grid = (int)std::min<int64_t>(std::max<int64_t>(items, 1), resident);
-  e = tactic::launch_attn(aa, G, grid, stream);
+  e = tactic::launch_attn(aa, G, resident, stream);
   if (e == hipSuccess) e = tactic::launch_combine(aa, G, stream);
   if (e != hipSuccess) return hip_fail(e, "dense attention launch");
   return TACTIC_OK;

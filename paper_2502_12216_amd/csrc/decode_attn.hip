@@ -25,17 +25,13 @@ namespace tactic {
 // log2(e) / sqrt(128): logits are kept in base-2 units for exp2
 constexpr float kScaleLog2 = 0.12751743074880046f;
 
-__device__ __forceinline__ int64_t item_tokens(const AttnArgs& a, int bg) {
-  return a.dense ? a.chunk_tokens : (int64_t)a.gmeta[bg * 4 + 3];
-}
-
-__device__ __forceinline__ int item_count(const AttnArgs& a, int bg) {
+// Tokens of selection group bg: its union (sparse) or its sequence (dense).
+__device__ __forceinline__ int64_t group_tokens(const AttnArgs& a, int bg) {
   if (a.dense) {
     const int b = bg / a.NV;
-    const int64_t n = a.kv_indptr[b + 1] - a.kv_indptr[b];
-    return (int)((n + a.chunk_tokens - 1) / a.chunk_tokens);
+    return a.kv_indptr[b + 1] - a.kv_indptr[b];
   }
-  return a.gmeta[bg * 4 + 2];
+  return (int64_t)a.gmeta[bg * 4 + 1];
 }
 
 __device__ __forceinline__ void load_words(const uint16_t* p, uint32_t* w) {
@@ -136,9 +132,9 @@ void attn_splitk_kernel(AttnArgs a) {
   constexpr int GPW = kWave / LPR;        // lane-groups per wave
   constexpr int NG = 4 * GPW;             // lane-groups per workgroup
   constexpr int kTileTok = NG * TOK;      // tokens per workgroup tile
-  extern __shared__ int s_prefix[];  // [B * NV + 1] work items before each selection group
-  // the row table of an item is dead once the merge starts, so the merge's
-  // partial sums reuse its storage
+  extern __shared__ int64_t s_prefix[];  // [B * NV + 1] tokens before each selection group
+  // the row table of a sub-range is dead once the merge starts, so the
+  // merge's partial sums reuse its storage
   union ItemShared {
     struct {
       int rows[kMaxChunkTokens];
@@ -154,69 +150,62 @@ void attn_splitk_kernel(AttnArgs a) {
   auto s_red = sh.red;
   __shared__ float s_ml[NG][2][G];
   __shared__ float s_M[G], s_L[G];
+  __shared__ int64_t s_wsum[4];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, sl = lane % LPR, grp = lane / LPR;
   const int gid = wave * GPW + grp;
   const int BG = a.B * a.NV;
 
-  for (int i = tid; i < BG; i += 256) s_prefix[i + 1] = item_count(a, i);
-  if (tid == 0) s_prefix[0] = 0;
-  __syncthreads();
-  if (tid == 0) {
-    for (int i = 0; i < BG; ++i) s_prefix[i + 1] += s_prefix[i];
-  }
-  __syncthreads();
-  const int total_items = s_prefix[BG];
-
-  for (int item = blockIdx.x; item < total_items; item += gridDim.x) {
-    int lo = 0, hi = BG - 1;  // largest bg with s_prefix[bg] <= item
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (s_prefix[mid] <= item) lo = mid;
-      else hi = mid - 1;
+  // exclusive prefix of the groups' token counts: every thread sums a
+  // contiguous run of groups, then a wave scan and the four wave totals
+  {
+    const int per = (BG + 255) / 256, g0 = min(BG, tid * per), g1 = min(BG, g0 + per);
+    int64_t loc = 0;
+    for (int bg = g0; bg < g1; ++bg) loc += group_tokens(a, bg);
+    int64_t incl = loc;
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int64_t y = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += y;
     }
-    const int bg = lo, c = item - s_prefix[bg];
+    if (lane == kWave - 1) s_wsum[wave] = incl;
+    __syncthreads();
+    int64_t run = incl - loc;
+    for (int w = 0; w < wave; ++w) run += s_wsum[w];
+    for (int bg = g0; bg < g1; ++bg) {
+      s_prefix[bg] = run;
+      run += group_tokens(a, bg);
+    }
+    if (tid == 255) s_prefix[BG] = run;
+    __syncthreads();
+  }
+  const int64_t total = s_prefix[BG];
+  const int64_t share = (total + gridDim.x - 1) / gridDim.x;
+  if (blockIdx.x == 0) {  // for the combine: the split and the group offsets
+    if (tid == 0) a.ameta[0] = share;
+    for (int bg = tid; bg <= BG; bg += 256) a.ameta[1 + bg] = s_prefix[bg];
+  }
+  const int64_t t0 = (int64_t)blockIdx.x * share, t1 = min(total, t0 + share);
+  if (t0 >= t1) return;
+  int bg0 = 0, bgh = BG - 1;  // largest group with s_prefix <= t0 (it holds t0)
+  while (bg0 < bgh) {
+    const int mid = (bg0 + bgh + 1) >> 1;
+    if (s_prefix[mid] <= t0) bg0 = mid;
+    else bgh = mid - 1;
+  }
+
+  for (int bg = bg0; bg < BG && s_prefix[bg] < t1; ++bg) {
+    const int64_t seg_lo = max(t0, s_prefix[bg]) - s_prefix[bg];
+    const int64_t seg_hi = min(t1, s_prefix[bg + 1]) - s_prefix[bg];
+    if (seg_lo >= seg_hi) continue;  // empty group
     const int b = bg / a.NV, jg = bg % a.NV, kvh = jg / a.kv_div;
     const int64_t kvb = a.kv_indptr[b];
     const int nseq = (int)(a.kv_indptr[b + 1] - kvb);
-    const int64_t T = item_tokens(a, bg);
-    const int64_t U = a.dense ? (int64_t)nseq : (int64_t)a.gmeta[bg * 4 + 1];
-    const int64_t p0 = (int64_t)c * T;
-    const int cnt = (int)min(T, U - p0);
 
     uint32_t qw[G][W];
 #pragma unroll
     for (int h = 0; h < G; ++h)
       load_words(a.q + ((int64_t)b * a.Hq + jg * G + h) * kHeadDim + sl * EPL, qw[h]);
-
-    // rows of this item (sequence-relative)
-    if (a.dense) {
-      for (int t = tid; t < cnt; t += 256) s_rows[t] = (int)(p0 + t);
-    } else {
-      const int R = a.gmeta[bg * 4 + 0];
-      const int r0 = a.cfr[(int64_t)bg * a.max_chunks + c];
-      const int nr = max(1, min(R - r0, (int)T));  // ranges that can touch this item
-      const int32_t* rup = a.rupos + (int64_t)bg * (a.Cm + 1) + r0;
-      const int32_t* rst = a.rstart + (int64_t)bg * a.Cm + r0;
-      for (int i = tid; i <= nr; i += 256) {
-        s_rupos[i] = rup[i];
-        if (i < nr) s_rstart[i] = rst[i];
-      }
-      __syncthreads();
-      for (int t = tid; t < cnt; t += 256) {
-        const int pos = (int)(p0 + t);
-        int l2 = 0, h2 = nr - 1;  // largest i with s_rupos[i] <= pos
-        while (l2 < h2) {
-          const int mid = (l2 + h2 + 1) >> 1;
-          if (s_rupos[mid] <= pos) l2 = mid;
-          else h2 = mid - 1;
-        }
-        const int row = s_rstart[l2] + (pos - s_rupos[l2]);
-        s_rows[t] = min(max(row, 0), nseq - 1);  // in range unless the cluster meta is inconsistent
-      }
-    }
-    __syncthreads();
 
     // online-softmax state: the running max and sum of this lane's head hl
     // (identical in the 16 / G lanes of that head), the accumulators of every head
@@ -229,7 +218,8 @@ void attn_splitk_kernel(AttnArgs a) {
 
     const uint16_t* Kb = a.K + ((int64_t)kvh * a.total + kvb) * kHeadDim + sl * EPL;
     const uint16_t* Vb = a.V + ((int64_t)kvh * a.total + kvb) * kHeadDim + sl * EPL;
-    const int ntile = (cnt + kTileTok - 1) / kTileTok;
+    int cnt = 0;      // tokens of the current sub-range
+    int64_t p0 = 0;   // its first position in the group's token list
     struct Tile {
       uint32_t k[TOK][W];
       uint32_t v[TOK][W];
@@ -240,7 +230,7 @@ void attn_splitk_kernel(AttnArgs a) {
       for (int i = 0; i < TOK; ++i) {
         const int t = tile * kTileTok + gid * TOK + i;
         if (t < cnt) {
-          const int64_t row = s_rows[t];
+          const int64_t row = a.dense ? p0 + t : (int64_t)s_rows[t];
           load_words(Kb + row * kHeadDim, r.k[i]);
           load_words(Vb + row * kHeadDim, r.v[i]);
         } else {
@@ -300,45 +290,81 @@ void attn_splitk_kernel(AttnArgs a) {
         }
       }
     };
+    // the group's part of this workgroup's range, in sub-ranges whose row
+    // table fits LDS (dense rows are positions: one sub-range)
+    for (int64_t p = seg_lo; p < seg_hi; p += cnt) {
+      p0 = p;
+      if (a.dense) {
+        cnt = (int)(seg_hi - p);
+      } else {
+        const int64_t c = p / kCfrTokens, in = p - c * kCfrTokens;
+        cnt = (int)min(seg_hi - p, (int64_t)kMaxChunkTokens - in);
+        // ranges that can touch [p, p + cnt): from the one holding position c * kCfrTokens
+        const int R = a.gmeta[bg * 4 + 0];
+        const int r0 = a.cfr[(int64_t)bg * a.max_chunks + c];
+        const int nr = max(1, min(R - r0, (int)(in + cnt)));
+        const int32_t* rup = a.rupos + (int64_t)bg * (a.Cm + 1) + r0;
+        const int32_t* rst = a.rstart + (int64_t)bg * a.Cm + r0;
+        for (int i = tid; i <= nr; i += 256) {
+          s_rupos[i] = rup[i];
+          if (i < nr) s_rstart[i] = rst[i];
+        }
+        __syncthreads();
+        for (int t = tid; t < cnt; t += 256) {
+          const int pos = (int)(p + t);
+          int l2 = 0, h2 = nr - 1;  // largest i with s_rupos[i] <= pos
+          while (l2 < h2) {
+            const int mid = (l2 + h2 + 1) >> 1;
+            if (s_rupos[mid] <= pos) l2 = mid;
+            else h2 = mid - 1;
+          }
+          const int row = s_rstart[l2] + (pos - s_rupos[l2]);
+          s_rows[t] = min(max(row, 0), nseq - 1);  // in range unless the cluster meta is inconsistent
+        }
+        __syncthreads();
+      }
+      const int ntile = (cnt + kTileTok - 1) / kTileTok;
 #if TACTIC_ATTN_DEPTH == 2
-    // two tiles in flight while one is consumed (rotation unrolled by three)
-    Tile t0 = load_tile(0), t1 = load_tile(1);
+      // two tiles in flight while one is consumed (rotation unrolled by three)
+      Tile t0 = load_tile(0), t1 = load_tile(1);
 #pragma unroll 1
-    for (int tile = 0; tile < ntile; tile += 3) {
-      Tile t2 = load_tile(tile + 2);
-      consume(t0, tile);
-      if (tile + 1 >= ntile) break;
-      t0 = load_tile(tile + 3);
-      consume(t1, tile + 1);
-      if (tile + 2 >= ntile) break;
-      t1 = load_tile(tile + 4);
-      consume(t2, tile + 2);
-    }
+      for (int tile = 0; tile < ntile; tile += 3) {
+        Tile t2 = load_tile(tile + 2);
+        consume(t0, tile);
+        if (tile + 1 >= ntile) break;
+        t0 = load_tile(tile + 3);
+        consume(t1, tile + 1);
+        if (tile + 2 >= ntile) break;
+        t1 = load_tile(tile + 4);
+        consume(t2, tile + 2);
+      }
 #elif TACTIC_ATTN_DEPTH == 3
-    Tile t0 = load_tile(0), t1 = load_tile(1), t2 = load_tile(2);
+      Tile t0 = load_tile(0), t1 = load_tile(1), t2 = load_tile(2);
 #pragma unroll 1
-    for (int tile = 0; tile < ntile; tile += 4) {
-      Tile t3 = load_tile(tile + 3);
-      consume(t0, tile);
-      if (tile + 1 >= ntile) break;
-      t0 = load_tile(tile + 4);
-      consume(t1, tile + 1);
-      if (tile + 2 >= ntile) break;
-      t1 = load_tile(tile + 5);
-      consume(t2, tile + 2);
-      if (tile + 3 >= ntile) break;
-      t2 = load_tile(tile + 6);
-      consume(t3, tile + 3);
-    }
+      for (int tile = 0; tile < ntile; tile += 4) {
+        Tile t3 = load_tile(tile + 3);
+        consume(t0, tile);
+        if (tile + 1 >= ntile) break;
+        t0 = load_tile(tile + 4);
+        consume(t1, tile + 1);
+        if (tile + 2 >= ntile) break;
+        t1 = load_tile(tile + 5);
+        consume(t2, tile + 2);
+        if (tile + 3 >= ntile) break;
+        t2 = load_tile(tile + 6);
+        consume(t3, tile + 3);
+      }
 #else
-    Tile cur = load_tile(0);
+      Tile cur = load_tile(0);
 #pragma unroll 1
-    for (int tile = 0; tile < ntile; ++tile) {
-      const Tile nxt = load_tile(tile + 1);  // zeros past the end
-      consume(cur, tile);
-      cur = nxt;
-    }
+      for (int tile = 0; tile < ntile; ++tile) {
+        const Tile nxt = load_tile(tile + 1);  // zeros past the end
+        consume(cur, tile);
+        cur = nxt;
+      }
 #endif
+      if (!a.dense) __syncthreads();  // the next sub-range rewrites the row table
+    }
 
     // ---- merge the lane-group states: common max, rescale, sum
     if (sl == hl * (16 / G)) {
@@ -377,7 +403,7 @@ void attn_splitk_kernel(AttnArgs a) {
         for (int e = 0; e < EPL; ++e) s_red[wave][h][sl * EPL + e] = acc[h][e];
     }
     __syncthreads();
-    float* part = a.partials + ((int64_t)bg * a.max_chunks + c) * kPart;
+    float* part = a.partials + ((int64_t)bg + blockIdx.x) * kPart;  // slot bg + w is unique
     for (int i = tid; i < G * kHeadDim; i += 256) {
       const int h = i / kHeadDim, d = i % kHeadDim;
       part[i] = s_red[0][h][d] + s_red[1][h][d] + s_red[2][h][d] + s_red[3][h][d];
@@ -402,13 +428,16 @@ __global__ __launch_bounds__(512) void combine_kernel(AttnArgs a) {
   const int bg = blockIdx.x, h = blockIdx.y;
   const int b = bg / a.NV, jg = bg % a.NV;
   const int d = threadIdx.x & (kHeadDim - 1), slice = threadIdx.x >> 7;
-  const int nchunks = item_count(a, bg);
   float* out = a.out + ((int64_t)b * a.Hq + jg * G + h) * kHeadDim;
-  if (nchunks == 0) {
+  // workgroups w0..w1 covered this group's tokens; their partials sit in slots bg + w
+  const int64_t share = a.ameta[0], P0 = a.ameta[1 + bg], P1 = a.ameta[2 + bg];
+  if (P1 <= P0 || share <= 0) {
     if (slice == 0) out[d] = 0.f;
     return;
   }
-  const float* pb = a.partials + (int64_t)bg * a.max_chunks * kPart;
+  const int64_t w0 = P0 / share, w1 = (P1 - 1) / share;
+  const int nchunks = (int)(w1 - w0 + 1);
+  const float* pb = a.partials + (bg + w0) * kPart;
   float M = -INFINITY, num = 0.f, den = 0.f;
 #pragma unroll 4
   for (int c = slice; c < nchunks; c += 4) {
@@ -441,7 +470,7 @@ __global__ __launch_bounds__(512) void combine_kernel(AttnArgs a) {
   }
 }
 
-static size_t attn_dyn_lds(const AttnArgs& a) { return ((size_t)a.B * a.NV + 1) * sizeof(int); }
+static size_t attn_dyn_lds(const AttnArgs& a) { return ((size_t)a.B * a.NV + 1) * sizeof(int64_t); }
 
 hipError_t launch_attn(const AttnArgs& a, int G, int grid, hipStream_t st) {
   constexpr int TOK = TACTIC_ATTN_TOK;
@@ -462,7 +491,7 @@ hipError_t launch_attn(const AttnArgs& a, int G, int grid, hipStream_t st) {
 hipError_t attn_resident_grid(int G, int n_groups, int* grid) {
   constexpr int TOK = TACTIC_ATTN_TOK;
   int dev = 0, cus = 0, per = 0;
-  const size_t lds = ((size_t)n_groups + 1) * sizeof(int);
+  const size_t lds = ((size_t)n_groups + 1) * sizeof(int64_t);
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return e;

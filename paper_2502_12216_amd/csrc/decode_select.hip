@@ -923,8 +923,8 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
   const uint64_t base = s_wave_u[wave] + incl - loc;
   const uint64_t tot = s_wave_u[16];
   const int64_t U = (int64_t)(tot & 0xffffffffu);
-  // tokens per attention work item: larger items for larger unions
-  const int64_t T = U >= 65536 ? 1024 : (U >= 16384 ? 512 : 256);
+  // position -> range index of the union, one entry per kCfrTokens positions
+  const int64_t T = kCfrTokens;
   int idx = (int)(base >> 32);
   int64_t upos = (int64_t)(base & 0xffffffffu);
   int32_t* rstart = a.rstart + (int64_t)bg * a.Cm;

@@ -78,7 +78,8 @@ struct AttnArgs {
   const int32_t* rstart;
   const int32_t* rupos;
   const int32_t* cfr;
-  float* partials;            // [B*NV][max_chunks][GV*130]
+  float* partials;            // [B*NV + grid][GV*130]: one slot per (group, workgroup) pair
+  int64_t* ameta;             // [B*NV + 2]: tokens per workgroup, then the groups' token offsets
   float* out;                 // [B][Hq][128]
 };
 

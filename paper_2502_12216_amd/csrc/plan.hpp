@@ -10,7 +10,9 @@ namespace tactic {
 
 constexpr int64_t kPlanMagic = 0x54414354494331LL;  // "TACTIC1"
 constexpr int kTile = 64;              // tokens per attention tile
-constexpr int kMaxChunkTokens = 1024;  // tokens per attention work item (upper bound)
+constexpr int kMaxChunkTokens = 2048;  // tokens whose rows the attention stages in LDS at once
+constexpr int kCfrTokens = 256;        // granularity of the union's position -> range index
+constexpr int kMaxAttnGrid = 4096;     // attention workgroups the partials are sized for (cap)
 constexpr int kSortLdsBuckets = 8192;  // largest cluster count sorted in LDS
 constexpr int kMaxGroups = 4096;       // B * Hkv limit of the attention work list
 constexpr int kFitFields = 16;
@@ -23,22 +25,22 @@ struct DecodePlan {
   int64_t magic;
   int64_t B, Hq, Hkv, G, Cm, Ct, nmax, total;
   int64_t S_cap;         // sampled rows per head (capacity)
-  int64_t chunk_tokens;  // tokens per attention work item
-  int64_t max_chunks;    // work items per (b, g) (capacity)
+  int64_t chunk_tokens;  // kCfrTokens: positions per entry of the position -> range index
+  int64_t max_chunks;    // entries of that index per selection group (capacity)
   int64_t split;         // sampling workgroups per query head
-  int64_t attn_grid;     // unused (the attention grid is sized from the device's occupancy)
+  int64_t attn_grid;     // attention workgroups the partials are sized for (resident capacity)
   int64_t sort_lds;      // 1: sort in LDS, 0: sort scratch in the workspace
   int64_t nb_max;        // bucket capacity of the sort
   // workspace byte offsets
   int64_t off_scores, off_order, off_rank, off_rprefix, off_headmeta, off_rows, off_logit;
   int64_t off_fit, off_cut, off_union_len, off_gmeta, off_rstart, off_rupos, off_cfr, off_lse;
-  int64_t off_partials, off_sort_keys, off_sort_cnt, off_sort_start;
+  int64_t off_partials, off_sort_keys, off_sort_cnt, off_sort_start, off_ameta;
   int64_t ws_bytes;
   int64_t exact_bp, win_bp, win_min, p1_bp, p2_bp;
   int64_t events[kStageEvents];  // optional hipEvent_t recorded between the kernels
   int64_t use_union;     // 1: GQA union (Sec. 4.5); 0: every query head over its own selection
   int64_t NV, GV;        // selection groups per sequence, query heads per selection group
-  int64_t pad[64 - 51];
+  int64_t pad[64 - 52];
 };
 static_assert(sizeof(DecodePlan) == 64 * sizeof(int64_t), "plan must fill tactic_decode_plan");
 
