@@ -8,7 +8,10 @@ used; each is a parameter or a rule, never a tuning.
 Layout of one (sequence, KV head): the cache rows are stored cluster by
 cluster (cluster j owns rows offsets[j] .. offsets[j+1]-1, its tokens in
 ascending original token order), so a token is named by its row in that
-cluster-sorted cache.
+cluster-sorted cache.  Rows past the last cluster (offsets[-1] .. n-1) are
+the recent tokens generated since the clustering: they are not clustered and
+every head attends to all of them (Sec. 1: full attention on newly generated
+tokens until the next re-clustering).
 """
 from __future__ import annotations
 
@@ -95,12 +98,20 @@ def unpack(order: np.ndarray, offsets: np.ndarray) -> np.ndarray:
     return np.concatenate(parts)
 
 
-def estimate_budget(l_pos: np.ndarray, P: float, prm: FitParams = FitParams()):
+def estimate_budget(l_pos: np.ndarray, P: float, prm: FitParams = FitParams(),
+                    l_tail: Optional[np.ndarray] = None):
     """Algorithm 1: the token budget k for one query head.
 
     l_pos are the logits x_i . Q / sqrt(d) of the unpacked list, in position
-    order.  Scores are handled relative to m = max of the exact head; every
-    quantity below scales by exp(-m), which leaves k unchanged.
+    order.  Scores are handled relative to m = max of the exact head (and of
+    the recent tokens, when there are any); every quantity below scales by
+    exp(-m), which leaves k unchanged.
+
+    l_tail, if given, are the logits of the recent unclustered tokens.  They
+    are always selected, so their exact mass E_t counts toward the target:
+    the total is E_t + S_n and k is the minimal k >= 0 with
+    E_t + S_k >= P * (E_t + S_n) (reading: the paper attends to these tokens
+    in full but does not say how they enter the budget).
 
     1. Means mu_1, mu_2 of exp(l - m) over the two windows, at x-coordinates
        x_j = (s_j + t_j) / 2; solve y = a/x + b through (x_1, mu_1), (x_2, mu_2).
@@ -113,11 +124,17 @@ def estimate_budget(l_pos: np.ndarray, P: float, prm: FitParams = FitParams()):
     geo = geometry(n, prm)
     info = dict(n=n, N=geo.N, W=geo.W, s1=geo.s1, t1=geo.t1, s2=geo.s2, t2=geo.t2,
                 exact=geo.exact)
+    has_tail = l_tail is not None and len(l_tail) > 0
     if n == 0:
         info["k"] = 0
+        info["E_t"] = 0.0
         return 0, info
     m = float(np.max(l_pos[:geo.N]))
+    if has_tail:
+        m = max(m, float(np.max(l_tail)))
+    E_t = float(np.sum(np.exp(l_tail - m))) if has_tail else 0.0
     info["m"] = m
+    info["E_t"] = E_t
     if geo.exact:
         w = np.exp(l_pos - m)
     else:
@@ -132,13 +149,15 @@ def estimate_budget(l_pos: np.ndarray, P: float, prm: FitParams = FitParams()):
         w = np.concatenate([e, np.maximum(0.0, a / i + b)])
         info.update(mu1=mu1, mu2=mu2, x1=x1, x2=x2, a=a, b=b)
     S = np.add.accumulate(w)
+    if has_tail:
+        S = E_t + S  # cumulative mass of the recent tokens plus the first k listed ones
     info["S_n"] = float(S[-1])
     if P >= 1.0:
         k = n
     else:
         T = P * S[-1]
         info["T"] = float(T)
-        k = int(np.argmax(S >= T)) + 1
+        k = 0 if (has_tail and E_t >= T) else int(np.argmax(S >= T)) + 1
     info["k"] = k
     info["w"] = w
     info["S"] = S
@@ -173,10 +192,14 @@ def decode_group(Q: np.ndarray, Ks: np.ndarray, Vs: np.ndarray, centroids: np.nd
     Each head ranks the clusters, unpacks them, estimates its budget k_h and
     selects the first k_h tokens I_h.  With the union (Sec. 4.5) every head of
     the group attends over U = union of the I_h, loaded once; without it each
-    head attends over its own I_h.  An empty sequence yields zeros."""
+    head attends over its own I_h.  Rows of Ks past offsets[-1] are the recent
+    tokens: every I_h contains them and they enter the budget with their exact
+    mass (estimate_budget).  An empty sequence yields zeros."""
     G, d = Q.shape
     n = int(offsets[-1])
-    if n == 0:
+    n_all = int(Ks.shape[0])
+    tail = np.arange(n, n_all, dtype=np.int64)
+    if n_all == 0:
         z = np.zeros(0, dtype=np.int64)
         return GroupResult(out=np.zeros((G, d)), k=np.zeros(G, dtype=np.int64), sel=[z] * G,
                            union=z, orders=[np.zeros(0, dtype=np.int64)] * G, rows=[z] * G)
@@ -189,9 +212,11 @@ def decode_group(Q: np.ndarray, Ks: np.ndarray, Vs: np.ndarray, centroids: np.nd
             order = np.asarray(orders[h], dtype=np.int64)
         rows = unpack(order, offsets)
         l_pos = _logits(q, Ks[rows])
-        k, info = estimate_budget(l_pos, P, prm)
+        k, info = estimate_budget(l_pos, P, prm, _logits(q, Ks[tail]) if len(tail) else None)
+        if n == 0:  # nothing is clustered: the recent tokens are the whole selection
+            k = 0
         ks.append(k)
-        sels.append(rows[:k])
+        sels.append(np.concatenate([rows[:k], tail]))
         ords.append(order)
         rowss.append(rows)
         infos.append(info)

@@ -406,3 +406,73 @@ def test_budget_reaching_target_exactly_counts():
         for P in (0.25, 0.5, 0.75, 0.3):
             k, _ = T.estimate_budget(l_pos, P, T.FitParams(exact_bp=10000))
             assert k == math.ceil(P * n - 1e-12) if (P * n) != int(P * n) else k == int(P * n)
+
+
+# ---------------------------------------------------------------- recent-token tail (Sec. 1)
+
+def test_tail_only_is_dense_attention():
+    """Nothing clustered yet: the recent tokens are the whole selection."""
+    rng = np.random.default_rng(31)
+    n, G = 50, 4
+    Q = rng.standard_normal((G, 128))
+    K = rng.standard_normal((n, 128))
+    V = rng.standard_normal((n, 128))
+    r = T.decode_group(Q, K, V, np.zeros((1, 128)), np.array([0, 0]), 0.5)
+    assert list(r.k) == [0] * G and r.union_count == n
+    for h in range(G):
+        np.testing.assert_allclose(r.out[h], A.dense_attention(Q[h], K, V), atol=1e-12)
+
+
+def test_tail_with_target_one_is_dense_attention():
+    rng = np.random.default_rng(32)
+    Q, K, V, cent, off = _random_clustered_group(rng, 400, 24)
+    tail = rng.standard_normal((37, 128))
+    K2, V2 = np.vstack([K, tail]), np.vstack([V, rng.standard_normal((37, 128))])
+    r = T.decode_group(Q, K2, V2, cent, off, 1.0)
+    assert r.union_count == len(K2)
+    for h in range(len(Q)):
+        np.testing.assert_allclose(r.out[h], A.dense_attention(Q[h], K2, V2), atol=1e-12)
+
+
+def test_tail_budget_is_top_p_given_the_recent_mass():
+    """One cluster per token and every score exact: head h selects every recent
+    token plus the fewest clustered tokens, taken by descending score (ties by
+    id), whose mass with the recent tokens' reaches P of the total (brute force)."""
+    rng = np.random.default_rng(33)
+    prm = T.FitParams(exact_bp=10000)
+    for trial in range(30):
+        n, t = int(rng.integers(1, 120)), int(rng.integers(1, 40))
+        q = rng.standard_normal(128) * rng.uniform(0.3, 3)
+        K = rng.standard_normal((n + t, 128))
+        V = rng.standard_normal((n + t, 128))
+        P = float(rng.uniform(0.05, 0.99))
+        off = np.arange(n + 1)
+        r = T.decode_group(q[None], K, V, K[:n], off, P, prm)
+        w = A.softmax_weights(A.logits(q, K))
+        order = np.lexsort((np.arange(n), -A.logits(q, K[:n])))
+        mass, k = float(w[n:].sum()), 0
+        while mass < P * (1 - 1e-12) and k < n:
+            mass += w[order[k]]
+            k += 1
+        assert r.k[0] == k, (trial, r.k[0], k)
+        assert set(r.sel[0].tolist()) == set(order[:k].tolist()) | set(range(n, n + t))
+
+
+def test_tail_holding_the_mass_selects_no_cluster():
+    """A recent token that carries more than P of the mass leaves k = 0."""
+    rng = np.random.default_rng(34)
+    Q, K, V, cent, off = _random_clustered_group(rng, 300, 20, G=1)
+    hot = Q[0] / np.linalg.norm(Q[0]) * 40.0  # logit ~ 40 * |q| / sqrt(d)
+    K2 = np.vstack([K, hot[None]])
+    V2 = np.vstack([V, rng.standard_normal((1, 128))])
+    r = T.decode_group(Q, K2, V2, cent, off, 0.9)
+    assert r.k[0] == 0 and list(r.sel[0]) == [len(K)]
+
+
+def test_tail_of_length_zero_changes_nothing():
+    rng = np.random.default_rng(35)
+    Q, K, V, cent, off = _random_clustered_group(rng, 500, 30)
+    _, info_a = T.estimate_budget(A.logits(Q[0], K[T.unpack(T.rank_clusters(Q[0], cent)[1], off)]), 0.8)
+    _, info_b = T.estimate_budget(A.logits(Q[0], K[T.unpack(T.rank_clusters(Q[0], cent)[1], off)]), 0.8,
+                                  l_tail=np.zeros(0))
+    assert info_a["k"] == info_b["k"] and info_a["S_n"] == info_b["S_n"]
