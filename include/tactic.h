@@ -66,8 +66,12 @@ typedef struct {
  * Cluster j of (b, g) owns the rows offsets_bg[j] .. offsets_bg[j+1]-1 of the
  * sequence's cluster-sorted K/V, where offsets_bg = offsets + g*(total_clusters
  * + B) + cl_indptr[b] + b holds C_b + 1 sequence-relative offsets from 0 to
- * n_b.  Within a cluster, rows keep their original token order (Sec. 4.3
- * unpacks clusters in that stored order). */
+ * c_b <= n_b.  Within a cluster, rows keep their original token order (Sec.
+ * 4.3 unpacks clusters in that stored order).  Rows c_b .. n_b-1 are the
+ * recent tokens generated since the clustering (the same count for every KV
+ * head of the sequence): every head attends to all of them and their exact
+ * attention mass counts toward the target (Sec. 1: full attention on newly
+ * generated tokens until the next re-clustering). */
 typedef struct {
   int64_t total_clusters;      /* host: sum of C_b */
   int32_t max_clusters;        /* host: largest C_b */
@@ -98,6 +102,10 @@ typedef struct {
                                   partner of the union, Sec. 5.3); sel_count_kv then counts the
                                   K/V rows loaded for the KV head, i.e. the sum of the group's
                                   per-head counts.  Other values: TACTIC_ERR_INVALID_ARG. */
+  int32_t max_tail;            /* default 0: the most recent (unclustered) tokens any sequence
+                                  may have, n_b - c_b.  Sizes the workspace; a longer tail is
+                                  cut to its first max_tail tokens (memory-safe, but then the
+                                  result leaves the rest out).  Negative: INVALID_ARG. */
 } tactic_decode_params;
 
 /* Host-side launch plan of a sparse decode: sizes derived from the shape,
@@ -128,7 +136,8 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape,
  *              union of its group's selected tokens (use_union = 1) or over
  *              its own selection (use_union = 0), softmax renormalised over
  *              that set (Eq. 3); zeros for an empty sequence
- *   sel_count_q   int32 [B][Hq]: token budget k_h of each query head
+ *   sel_count_q   int32 [B][Hq]: tokens head h attends to of its own selection:
+ *              the budget k_h of Algorithm 1 plus the recent tokens
  *   sel_count_kv  int32 [B][Hkv]: size of the group union |U_g| (use_union = 1),
  *              or the sum of the group's k_h (use_union = 0): K/V rows loaded
  *   workspace  at least the bytes reported by tactic_sparse_decode_plan for
@@ -154,7 +163,8 @@ tactic_status tactic_sparse_decode_plan_set_events(tactic_decode_plan* plan, hip
 /* Number of fp64 fields per query head in the fit record of the view below:
  *   0 m (logit shift: max over the exact head)   1 mu_1   2 mu_2   3 a   4 b
  *   5 S_n (estimated total)   6 T = P * S_n   7 k   8 N   9 n   10 exact mode
- *   11 sampled rows   12 E_N (exact-head sum)   13 cutoff rank   14 cutoff length */
+ *   11 sampled rows   12 E_N (exact-head sum)   13 cutoff rank   14 cutoff length
+ *   15 E_t (exact mass of the recent tokens; S_n and T include it) */
 #define TACTIC_FIT_FIELDS 16
 
 /* Device pointers into a workspace after tactic_sparse_decode, for

@@ -38,7 +38,8 @@ class ClusterMeta(ctypes.Structure):
 
 class DecodeParams(ctypes.Structure):
     _fields_ = [("target_frac", c_float), ("exact_bp", c_int32), ("win_bp", c_int32),
-                ("win_min", c_int32), ("p1_bp", c_int32), ("p2_bp", c_int32), ("use_union", c_int32)]
+                ("win_min", c_int32), ("p1_bp", c_int32), ("p2_bp", c_int32), ("use_union", c_int32),
+                ("max_tail", c_int32)]
 
 
 class DecodePlan(ctypes.Structure):

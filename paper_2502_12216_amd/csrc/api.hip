@@ -86,6 +86,7 @@ tactic_status check_params(const tactic_decode_params* p) {
       p->p1_bp < 0 || p->p1_bp > 10000 || p->p2_bp < 0 || p->p2_bp > 10000)
     return fail(TACTIC_ERR_INVALID_ARG, "fit parameters out of range");
   if (p->use_union != 0 && p->use_union != 1) return fail(TACTIC_ERR_INVALID_ARG, "use_union must be 0 or 1");
+  if (p->max_tail < 0) return fail(TACTIC_ERR_INVALID_ARG, "max_tail must be >= 0");
   return TACTIC_OK;
 }
 
@@ -117,6 +118,7 @@ void tactic_decode_params_default(tactic_decode_params* p) {
   p->p1_bp = 1000;
   p->p2_bp = 6000;
   p->use_union = 1;
+  p->max_tail = 0;
 }
 
 const char* tactic_status_string(tactic_status s) {
@@ -161,6 +163,7 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape, const tact
   p.p1_bp = params->p1_bp;
   p.p2_bp = params->p2_bp;
   p.use_union = params->use_union;
+  p.max_tail = params->max_tail;
   p.NV = p.use_union ? p.Hkv : p.Hq;
   p.GV = p.use_union ? p.G : 1;
   // sampled rows per head: the largest list any length <= nmax can need
@@ -170,10 +173,10 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape, const tact
     const tactic::Geometry g = tactic::make_geometry(n, sp);
     if (g.samples > S_cap) S_cap = g.samples;
   }
-  p.S_cap = S_cap;
+  p.S_cap = S_cap + p.max_tail;  // the recent tokens follow the sampled rows
   p.chunk_tokens = tactic::kCfrTokens;
   p.max_chunks = std::max<int64_t>(1, (p.nmax + p.chunk_tokens - 1) / p.chunk_tokens);
-  p.split = std::max<int64_t>(1, (S_cap + tactic::kSampleChunk - 1) / tactic::kSampleChunk);
+  p.split = std::max<int64_t>(1, (p.S_cap + tactic::kSampleChunk - 1) / tactic::kSampleChunk);
   // the partials hold one slot per (selection group, attention workgroup) pair
   // that can meet: at most groups + workgroups; the grid (the device's resident
   // capacity) is capped so that the plan does not depend on the device
@@ -193,12 +196,12 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape, const tact
   p.off_rows = L.take(BH * p.S_cap * 4);
   p.off_logit = L.take(BH * p.S_cap * 8);
   p.off_fit = L.take(BH * tactic::kFitFields * 8);
-  p.off_lse = L.take(BH * p.split * 6 * 8);
+  p.off_lse = L.take(BH * p.split * 8 * 8);
   p.off_cut = L.take(BH * 2 * 4);
   p.off_union_len = L.take(p.NV * p.Ct * 4);
   p.off_gmeta = L.take(BG * 4 * 4);
-  p.off_rstart = L.take(BG * p.Cm * 4);
-  p.off_rupos = L.take(BG * (p.Cm + 1) * 4);
+  p.off_rstart = L.take(BG * (p.Cm + 2) * 4);  // ranges: clusters, then the recent tokens
+  p.off_rupos = L.take(BG * (p.Cm + 2) * 4);
   p.off_cfr = L.take(BG * p.max_chunks * 4);
   p.off_partials = L.take((BG + p.attn_grid) * p.GV * (tactic::kHeadDim + 2) * 4);
   p.off_ameta = L.take((BG + 2) * 8);
@@ -230,7 +233,7 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
       p.Hkv != shape->n_kv_heads || p.nmax != shape->max_seq_len || p.total != shape->total_tokens ||
       p.Cm != meta->max_clusters || p.Ct != meta->total_clusters || p.exact_bp != params->exact_bp ||
       p.win_bp != params->win_bp || p.win_min != params->win_min || p.p1_bp != params->p1_bp ||
-      p.p2_bp != params->p2_bp || p.use_union != params->use_union)
+      p.p2_bp != params->p2_bp || p.use_union != params->use_union || p.max_tail != params->max_tail)
     return fail(TACTIC_ERR_INVALID_ARG, "plan does not match the shape / meta / params");
   if (!workspace || (int64_t)workspace_bytes < p.ws_bytes)
     return fail(TACTIC_ERR_WORKSPACE, "workspace has %zu bytes, needs %lld", workspace_bytes,
@@ -272,6 +275,7 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   so.nb_max = (int)p.nb_max;
   so.Ct = p.Ct;
   so.S_cap = p.S_cap;
+  so.max_tail = (int)p.max_tail;
   so.prm = sel_params(params);
   so.g_keys = p.sort_lds ? nullptr : reinterpret_cast<uint64_t*>(ws + p.off_sort_keys);
   so.g_cnt = p.sort_lds ? nullptr : reinterpret_cast<uint32_t*>(ws + p.off_sort_cnt);

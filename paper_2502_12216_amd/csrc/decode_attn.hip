@@ -303,8 +303,8 @@ void attn_splitk_kernel(AttnArgs a) {
         const int R = a.gmeta[bg * 4 + 0];
         const int r0 = a.cfr[(int64_t)bg * a.max_chunks + c];
         const int nr = max(1, min(R - r0, (int)(in + cnt)));
-        const int32_t* rup = a.rupos + (int64_t)bg * (a.Cm + 1) + r0;
-        const int32_t* rst = a.rstart + (int64_t)bg * a.Cm + r0;
+        const int32_t* rup = a.rupos + (int64_t)bg * (a.Cm + 2) + r0;
+        const int32_t* rst = a.rstart + (int64_t)bg * (a.Cm + 2) + r0;
         for (int i = tid; i <= nr; i += 256) {
           s_rupos[i] = rup[i];
           if (i < nr) s_rstart[i] = rst[i];

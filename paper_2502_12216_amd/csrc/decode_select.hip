@@ -426,12 +426,16 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     for (int r = tid; r <= C; r += nt) rpre[r] = (int32_t)(r < C ? cnt[r] : total);
   }
 
-  const Geometry geo = make_geometry(n, a.prm);
-  int64_t S = geo.samples;
-  if (S > a.S_cap) S = a.S_cap;
+  // the clusters hold the first n_c rows; the rest are recent tokens, sampled
+  // (all of them) after the exact head and the windows of the clustered list
+  const int n_c = (int)min((int64_t)total, (int64_t)n);
+  const int tail = min(max(n - n_c, 0), a.max_tail);
+  const Geometry geo = make_geometry(n_c, a.prm);
+  const int64_t S_main = min(geo.samples, a.S_cap);
+  const int64_t S = min(S_main + tail, a.S_cap);
   if (tid == 0) {
     int32_t* hm = a.head_meta + (int64_t)bh * 16;
-    hm[0] = n;
+    hm[0] = n_c;
     hm[1] = (int32_t)geo.N;
     hm[2] = geo.exact ? 0 : (int32_t)(geo.t1 - geo.s1 + 1);
     hm[3] = geo.exact ? 0 : (int32_t)(geo.t2 - geo.s2 + 1);
@@ -442,17 +446,20 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     hm[8] = geo.exact;
     hm[9] = (int32_t)S;
     hm[10] = C;
+    hm[11] = tail;
+    hm[12] = (int32_t)S_main;
     if (a.per_head && h % a.G == 0) a.sel_count_kv[b * a.Hkv + g] = 0;  // summed by fit_union
   }
-  if (C <= 0) return;
-  const int64_t N = geo.exact ? n : geo.N;
-  const int64_t W1 = geo.exact ? 0 : geo.t1 - geo.s1 + 1;
   int32_t* rows = a.sample_rows + (int64_t)bh * a.S_cap;
+  for (int64_t u = S_main + tid; u < S; u += nt) rows[u] = n_c + (int32_t)(u - S_main);
+  if (C <= 0) return;
+  const int64_t N = geo.exact ? n_c : geo.N;
+  const int64_t W1 = geo.exact ? 0 : geo.t1 - geo.s1 + 1;
   auto prefix_at = [&](int r) -> uint32_t { return r < C ? cnt[r] : total; };  // r in [0, C]
   int top = 1;
   while (top * 2 <= C) top <<= 1;
   constexpr int kU = 4;  // independent searches in flight per thread
-  for (int64_t u0 = tid; u0 < S; u0 += (int64_t)kU * nt) {
+  for (int64_t u0 = tid; u0 < S_main; u0 += (int64_t)kU * nt) {
     int64_t iv[kU];  // 1-based position in the unpacked list
     int lr[kU];
 #pragma unroll
@@ -477,7 +484,7 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
 #pragma unroll
     for (int k = 0; k < kU; ++k) {
       const int64_t u = u0 + (int64_t)k * nt;
-      if (u < S) {
+      if (u < S_main) {
         const int r = min(lr[k], C - 1);  // C only with offsets that disagree with kv_indptr
         const int32_t row = ostart[r] + (int32_t)(iv[k] - 1 - (int64_t)prefix_at(r));
         rows[u] = min(max(row, 0), n - 1);
@@ -602,7 +609,7 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
   __shared__ double s_lg[kSampleChunk];
   constexpr int kRW = kSampleChunk / kWave;  // waves that reduce the chunk, one sample per lane
   static_assert(kSampleChunk % kWave == 0 && kRW <= 4, "chunk must fit the workgroup's waves");
-  __shared__ double s_part[kRW][3][2];
+  __shared__ double s_part[kRW][4][2];
   const int tid = threadIdx.x;
   const int bh = blockIdx.y;
   const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
@@ -659,10 +666,14 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
     }
   }
   __syncthreads();
-  // per-region (max, sum exp(l - max)) of this chunk: waves 0 and 1 hold 64 samples each
-  const int64_t N = hm[8] ? S : hm[1];
+  // per-region (max, sum exp(l - max)) of this chunk, one sample per lane of
+  // the first waves; regions: exact head, window 1, window 2, recent tokens
+  const int64_t S_main = hm[12];
+  const int64_t N = hm[8] ? S_main : hm[1];
   const int64_t N1 = N + hm[2];
-  auto region = [&](int64_t u) { return u < N ? 0 : (u < N1 ? 1 : (u < S ? 2 : 3)); };
+  auto region = [&](int64_t u) {
+    return u < N ? 0 : (u < N1 ? 1 : (u < S_main ? 2 : (u < S ? 3 : 4)));
+  };
   const int rg_lo = region(u0), rg_hi = region(min(S, u0 + kSampleChunk) - 1);  // regions present
   if (wave < kRW) {
     const int t = wave * kWave + lane;
@@ -678,7 +689,7 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
     }
   }
   __syncthreads();
-  if (tid < 3) {
+  if (tid < 4) {
     double M = -INFINITY, Ssum = 0.0;
     if (tid >= rg_lo && tid <= rg_hi) {
 #pragma unroll
@@ -690,7 +701,7 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
           if (mw != -INFINITY) Ssum += s_part[w][tid][1] * exp(mw - M);
         }
     }
-    double* out = a.lse + (((int64_t)bh * a.split + blockIdx.x) * 3 + tid) * 2;
+    double* out = a.lse + (((int64_t)bh * a.split + blockIdx.x) * 4 + tid) * 2;
     out[0] = M;
     out[1] = Ssum;
   }
@@ -702,76 +713,91 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
 // kernel: with M the maximum over the exact head (the shift m), a region's sum
 // of exp(l - m) is sum_c exp(M_c - m) S_c.
 __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
+  constexpr int kRg = 4;  // regions: exact head, window 1, window 2, recent tokens
   const int32_t* hm = a.head_meta + (int64_t)bh * 16;
   const double* lg = a.logits + (int64_t)bh * a.S_cap;
-  const double* lse = a.lse + (int64_t)bh * a.split * 6;
+  const double* lse = a.lse + (int64_t)bh * a.split * (2 * kRg);
   // the partials of the first 64 chunks load together with the head's metadata
-  double pre[6];
+  double pre[2 * kRg];
 #pragma unroll
-  for (int i = 0; i < 6; ++i) pre[i] = lane < a.split ? lse[lane * 6 + i] : 0.0;
-  const int n = hm[0];
-  const int64_t S = hm[9];
+  for (int i = 0; i < 2 * kRg; ++i) pre[i] = lane < a.split ? lse[lane * 2 * kRg + i] : 0.0;
+  const int n = hm[0];          // clustered tokens (the list of Algorithm 1)
+  const int64_t S = hm[9];      // sampled rows, the recent tokens included
+  const int tail = hm[11];      // recent tokens, all selected
   const int exact = hm[8];
-  const int64_t N = exact ? S : hm[1];
+  const int64_t N = exact ? (int64_t)hm[12] : (int64_t)hm[1];
   const int64_t W1 = hm[2], W2 = hm[3];
-  const int nch = (int)((S + kSampleChunk - 1) / kSampleChunk);
+  const int nch = min((int)((S + kSampleChunk - 1) / kSampleChunk), a.split);  // S <= S_cap
   int k = 0;
-  double m = 0.0, mu1 = 0.0, mu2 = 0.0, fa = 0.0, fb = 0.0, Sn = 0.0, T = 0.0, EN = 0.0;
-  if (n > 0) {
-    double M[3] = {-INFINITY, -INFINITY, -INFINITY};
-    if (lane < nch)
+  double m = 0.0, mu1 = 0.0, mu2 = 0.0, fa = 0.0, fb = 0.0, Sn = 0.0, T = 0.0, EN = 0.0, Et = 0.0;
+  if (S > 0) {
+    double M[kRg];
 #pragma unroll
-      for (int rg = 0; rg < 3; ++rg) M[rg] = pre[rg * 2];
+    for (int rg = 0; rg < kRg; ++rg) M[rg] = lane < nch ? pre[rg * 2] : -INFINITY;
     for (int c = lane + kWave; c < nch; c += kWave)
 #pragma unroll
-      for (int rg = 0; rg < 3; ++rg) M[rg] = fmax(M[rg], lse[(c * 3 + rg) * 2]);
+      for (int rg = 0; rg < kRg; ++rg) M[rg] = fmax(M[rg], lse[(c * kRg + rg) * 2]);
 #pragma unroll
-    for (int rg = 0; rg < 3; ++rg) M[rg] = wave_max_d(M[rg]);
-    m = M[0];
-    double R[3] = {0.0, 0.0, 0.0};
-    if (lane < nch)
+    for (int rg = 0; rg < kRg; ++rg) M[rg] = wave_max_d(M[rg]);
+    m = fmax(M[0], M[3]);  // shift: largest exact score (head and recent tokens)
+    double R[kRg];
 #pragma unroll
-      for (int rg = 0; rg < 3; ++rg)
-        if (pre[rg * 2] != -INFINITY) R[rg] = pre[rg * 2 + 1] * exp(pre[rg * 2] - m);
+    for (int rg = 0; rg < kRg; ++rg)
+      R[rg] = (lane < nch && pre[rg * 2] != -INFINITY) ? pre[rg * 2 + 1] * exp(pre[rg * 2] - m) : 0.0;
     for (int c = lane + kWave; c < nch; c += kWave)
 #pragma unroll
-      for (int rg = 0; rg < 3; ++rg) {
-        const double mc = lse[(c * 3 + rg) * 2];
-        if (mc != -INFINITY) R[rg] += lse[(c * 3 + rg) * 2 + 1] * exp(mc - m);
+      for (int rg = 0; rg < kRg; ++rg) {
+        const double mc = lse[(c * kRg + rg) * 2];
+        if (mc != -INFINITY) R[rg] += lse[(c * kRg + rg) * 2 + 1] * exp(mc - m);
       }
 #pragma unroll
-    for (int rg = 0; rg < 3; ++rg) R[rg] = wave_sum_d(R[rg]);
+    for (int rg = 0; rg < kRg; ++rg) R[rg] = wave_sum_d(R[rg]);
     EN = R[0];
+    Et = R[3];
+    mu1 = R[1];
+    mu2 = R[2];
+  }
+  double Tc = 0.0;  // the part of the target the clustered list must supply
+  if (n > 0) {
     if (exact) {
       Sn = EN;
+      mu1 = mu2 = 0.0;
     } else {
-      mu1 = R[1] / (double)W1;
-      mu2 = R[2] / (double)W2;
+      mu1 /= (double)W1;
+      mu2 /= (double)W2;
       const double x1 = (double)(hm[4] + hm[5]) / 2.0, x2 = (double)(hm[6] + hm[7]) / 2.0;
       fa = (mu1 - mu2) / (1.0 / x1 - 1.0 / x2);
       fb = mu1 - fa / x1;
       Sn = EN + tail_sum(fa, fb, N + 1, n);
     }
+  } else {
+    mu1 = mu2 = 0.0;
+  }
+  Sn += Et;
+  if (n > 0) {
     if (a.P >= 1.0) {
       k = n;
     } else {
       T = a.P * Sn;
-      if (T <= EN) {
+      Tc = T - Et;
+      if (tail > 0 && Tc <= 0.0) {
+        k = 0;  // the recent tokens alone reach the target
+      } else if (Tc <= EN) {
         // the budget lies in the exact head: find the chunk whose head part
-        // crosses T, then scan that chunk in position order
+        // crosses Tc, then scan that chunk in position order
         const int nhc = (int)((N + kSampleChunk - 1) / kSampleChunk);
         double base = 0.0;
         int cstar = nhc - 1;
         for (int c0 = 0; c0 < nhc; c0 += kWave) {
           const int c = c0 + lane;
-          const double mc = c < nhc ? lse[(c * 3) * 2] : -INFINITY;
-          const double v = (c < nhc && mc != -INFINITY) ? lse[(c * 3) * 2 + 1] * exp(mc - m) : 0.0;
+          const double mc = c < nhc ? lse[(c * kRg) * 2] : -INFINITY;
+          const double v = (c < nhc && mc != -INFINITY) ? lse[(c * kRg) * 2 + 1] * exp(mc - m) : 0.0;
           double incl = v;
           for (int o = 1; o < kWave; o <<= 1) {
             const double y = __shfl_up(incl, o, kWave);
             if (lane >= o) incl += y;
           }
-          int hit = (c < nhc && base + incl >= T) ? c : 0x7fffffff;
+          int hit = (c < nhc && base + incl >= Tc) ? c : 0x7fffffff;
           for (int o = kWave / 2; o > 0; o >>= 1) hit = min(hit, __shfl_xor(hit, o, kWave));
           if (hit != 0x7fffffff) {
             cstar = hit;
@@ -791,14 +817,14 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
             const double y = __shfl_up(incl, o, kWave);
             if (lane >= o) incl += y;
           }
-          int c2 = (u < ue && run + incl >= T) ? (int)(u + 1) : 0x7fffffff;
+          int c2 = (u < ue && run + incl >= Tc) ? (int)(u + 1) : 0x7fffffff;
           for (int o = kWave / 2; o > 0; o >>= 1) c2 = min(c2, __shfl_xor(c2, o, kWave));
           cand = c2;
           run += __shfl(incl, kWave - 1, kWave);
         }
         k = cand == 0x7fffffff ? (int)ue : cand;  // ue only if rounding lost the crossing
       } else {
-        // minimal k in (N, n] with E_N + tail(N+1..k) >= T: 64-way parallel
+        // minimal k in (N, n] with E_N + tail(N+1..k) >= Tc: 64-way parallel
         // search on the closed form over the positive interval [L, R]
         int64_t L, Rr;
         const bool any = positive_interval(fa, fb, N + 1, n, &L, &Rr);
@@ -806,7 +832,7 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
         auto reached = [&](int64_t kk) -> bool {
           const int64_t r = min(kk, Rr);
           const double t = (!any || r < L) ? 0.0 : fa * (harmonic(r) - HL) + fb * (double)(r - L + 1);
-          return EN + t >= T;
+          return EN + t >= Tc;
         };
         int64_t lo = N + 1, hi = n;  // the answer lies in [lo, hi]
         while (lo < hi) {
@@ -849,12 +875,12 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
   if (lane == 0) {
     cut[0] = cut_r;
     cut[1] = cut_len;
-    a.sel_count_q[bh] = k;
+    a.sel_count_q[bh] = k + tail;  // tokens the head attends to
     double* fit = a.fit + (int64_t)bh * kFitFields;
     fit[0] = m; fit[1] = mu1; fit[2] = mu2; fit[3] = fa; fit[4] = fb; fit[5] = Sn; fit[6] = T;
     fit[7] = (double)k; fit[8] = (double)N; fit[9] = (double)n; fit[10] = (double)exact;
     fit[11] = (double)S; fit[12] = EN; fit[13] = (double)cut_r; fit[14] = (double)cut_len;
-    fit[15] = 0.0;
+    fit[15] = Et;
   }
 }
 
@@ -927,8 +953,8 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
   const int64_t T = kCfrTokens;
   int idx = (int)(base >> 32);
   int64_t upos = (int64_t)(base & 0xffffffffu);
-  int32_t* rstart = a.rstart + (int64_t)bg * a.Cm;
-  int32_t* rupos = a.rupos + (int64_t)bg * (a.Cm + 1);
+  int32_t* rstart = a.rstart + (int64_t)bg * (a.Cm + 2);
+  int32_t* rupos = a.rupos + (int64_t)bg * (a.Cm + 2);
   int32_t* cfr = a.cfr + (int64_t)bg * a.max_chunks;
   for (int j = beg; j < end; ++j) {
     const int L = Ls[j];
@@ -940,14 +966,26 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
     upos += L;
   }
   if (tid == 0) {
-    const int R = (int)(tot >> 32);
-    rupos[R] = (int32_t)U;
+    int R = (int)(tot >> 32);
+    int64_t Ut = U;
+    // the recent tokens (rows n_c .. n_c + tail - 1, the same for every head of
+    // the group) close the list as one more range
+    const int32_t* hm0 = a.head_meta + (int64_t)h0 * 16;
+    const int tail = hm0[11];
+    if (tail > 0) {
+      rstart[R] = hm0[0];
+      rupos[R] = (int32_t)U;
+      for (int64_t c = (U + T - 1) / T; c * T < U + tail && c < a.max_chunks; ++c) cfr[c] = R;
+      ++R;
+      Ut += tail;
+    }
+    rupos[R] = (int32_t)Ut;
     a.gmeta[bg * 4 + 0] = R;
-    a.gmeta[bg * 4 + 1] = (int32_t)U;
-    a.gmeta[bg * 4 + 2] = (int32_t)((U + T - 1) / T);
+    a.gmeta[bg * 4 + 1] = (int32_t)Ut;
+    a.gmeta[bg * 4 + 2] = (int32_t)((Ut + T - 1) / T);
     a.gmeta[bg * 4 + 3] = (int32_t)T;
-    if (a.per_head) atomicAdd(&a.sel_count_kv[b * a.Hkv + kvh], (int32_t)U);  // rows loaded per KV head
-    else a.sel_count_kv[bg] = (int32_t)U;
+    if (a.per_head) atomicAdd(&a.sel_count_kv[b * a.Hkv + kvh], (int32_t)Ut);  // rows loaded per KV head
+    else a.sel_count_kv[bg] = (int32_t)Ut;
   }
 }
 

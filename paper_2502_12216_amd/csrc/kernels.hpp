@@ -24,6 +24,7 @@ struct SortArgs {
   const int64_t* cl_indptr;
   int B, Hq, Hkv, G, Cm, nb_max;
   int64_t Ct, S_cap;
+  int max_tail;               // recent tokens per sequence beyond the clusters (capacity)
   SelParams prm;
   uint64_t* g_keys;           // sort scratch when the sort does not fit LDS
   uint32_t* g_cnt;
@@ -54,15 +55,15 @@ struct FitArgs {
   const int32_t* rprefix;
   const int32_t* rank_of;
   double* logits;             // [B*Hq][S_cap]
-  double* lse;                // [B*Hq][split][3 regions][max, sum exp(l - max)]
+  double* lse;                // [B*Hq][split][4 regions][max, sum exp(l - max)]
   double* fit;                // [B*Hq][16]
   int32_t* cut;               // [B*Hq][2]
   int32_t* sel_count_q;       // [B*Hq]
   int32_t* sel_count_kv;      // [B*Hkv]
   int32_t* union_len;         // [NV][Ct]
   int32_t* gmeta;             // [B*NV][4]: ranges, union tokens, work items, tokens per item
-  int32_t* rstart;            // [B*NV][Cm]
-  int32_t* rupos;             // [B*NV][Cm+1]
+  int32_t* rstart;            // [B*NV][Cm+2]: first row of each selected range
+  int32_t* rupos;             // [B*NV][Cm+2]: its first position in the group's token list
   int32_t* cfr;               // [B*NV][max_chunks]
 };
 

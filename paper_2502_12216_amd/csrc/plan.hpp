@@ -40,7 +40,8 @@ struct DecodePlan {
   int64_t events[kStageEvents];  // optional hipEvent_t recorded between the kernels
   int64_t use_union;     // 1: GQA union (Sec. 4.5); 0: every query head over its own selection
   int64_t NV, GV;        // selection groups per sequence, query heads per selection group
-  int64_t pad[64 - 52];
+  int64_t max_tail;      // capacity for recent (unclustered) tokens per sequence
+  int64_t pad[64 - 53];
 };
 static_assert(sizeof(DecodePlan) == 64 * sizeof(int64_t), "plan must fill tactic_decode_plan");
 

@@ -218,7 +218,12 @@ class LabelLayout:
     cl_indptr: np.ndarray
 
 
-def label_layout(inp: LayerInputs) -> LabelLayout:
+def label_layout(inp: LayerInputs, tail: Optional[Sequence[int]] = None) -> LabelLayout:
+    """Cluster-sorted layout by the generator's own mixture labels.
+
+    `tail[b]` (default 0) leaves the last tail[b] tokens of sequence b
+    unclustered: they follow the clustered rows in their original order
+    (recent tokens since the clustering) and the offsets end before them."""
     Hkv = inp.K.shape[0]
     B = len(inp.kv_indptr) - 1
     dev = inp.K.device
@@ -231,9 +236,12 @@ def label_layout(inp: LayerInputs) -> LabelLayout:
         s0, s1 = int(inp.kv_indptr[b]), int(inp.kv_indptr[b + 1])
         c0, c1 = int(inp.comp_indptr[b]), int(inp.comp_indptr[b + 1])
         M = c1 - c0
+        t = int(tail[b]) if tail is not None else 0
+        t = min(max(t, 0), s1 - s0)
         for g in range(Hkv):
-            lab = inp.labels[g, s0:s1]
-            p = torch.argsort(lab, stable=True)
+            lab = inp.labels[g, s0:s1 - t]
+            p = torch.cat([torch.argsort(lab, stable=True),
+                           torch.arange(s1 - s0 - t, s1 - s0, device=dev, dtype=torch.int64)])
             cnt = torch.bincount(lab, minlength=M)
             off = torch.zeros(M + 1, dtype=torch.int64, device=dev)
             off[1:] = torch.cumsum(cnt, 0)

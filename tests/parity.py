@@ -14,6 +14,8 @@ ones, so a tie resolved differently upstream cannot fail a later stage):
   5. output: max |out_gpu - o~(U_gpu)| <= 2e-3 with o~ the oracle's fp64
      attention over the GPU's union (Eq. 3), or over each head's own
      selection in per-head mode.
+Rows of the cache past the last cluster are recent tokens: every head's
+selection holds all of them and the GPU's per-head count includes them.
 """
 from __future__ import annotations
 
@@ -65,6 +67,7 @@ def check_group(inp: dict, P: float, prm: OT.FitParams, gpu: dict, label: str = 
     G = Q.shape[0]
     C = cent.shape[0]
     n = int(off[-1])
+    tail_rows = np.arange(n, len(Ks), dtype=np.int64)
     stats = dict(order_ties=0, cut_ties=0, order_equal=0)
     cmax = float(np.max(np.linalg.norm(cent, axis=1))) if C else 0.0
     orders = []
@@ -88,19 +91,23 @@ def check_group(inp: dict, P: float, prm: OT.FitParams, gpu: dict, label: str = 
             stats["order_ties"] += 1
         orders.append(og)
     r = OT.decode_group(Q, Ks, Vs, cent, off, P, prm, orders=orders)
-    k_gpu = np.asarray(gpu["k"], dtype=np.int64)
+    k_gpu = np.asarray(gpu["k"], dtype=np.int64) - len(tail_rows)  # the GPU counts the recent tokens
     for h in range(G):
         kg, ko = int(k_gpu[h]), int(r.k[h])
         if kg == ko:
             continue
         info = r.infos[h]
         S, T = info["S"], info.get("T", None)
-        assert T is not None and 1 <= kg <= n, f"{label} head {h}: k gpu {kg} oracle {ko}"
-        ok = S[kg - 1] >= T * (1 - CUT_TIE_REL) and (kg == 1 or S[kg - 2] < T * (1 + CUT_TIE_REL))
+        assert T is not None and 0 <= kg <= n, f"{label} head {h}: k gpu {kg} oracle {ko}"
+        E_t = info.get("E_t", 0.0)
+
+        def reach(k):  # mass of the recent tokens and the first k listed ones
+            return S[k - 1] if k >= 1 else E_t
+        ok = reach(kg) >= T * (1 - CUT_TIE_REL) and (kg == 0 or reach(kg - 1) < T * (1 + CUT_TIE_REL))
         assert ok, f"{label} head {h}: k gpu {kg} oracle {ko} (S_kg={S[kg-1]}, T={T})"
         stats["cut_ties"] += 1
     # union of the GPU's per-head selections, as per-cluster prefix lengths
-    sel_rows = [r.rows[h][:int(k_gpu[h])] for h in range(G)]
+    sel_rows = [np.concatenate([r.rows[h][:int(k_gpu[h])], tail_rows]) for h in range(G)]
     if not use_union:
         loaded = 0
         err = 0.0

@@ -105,6 +105,26 @@ def test_sparse_per_head_parity_and_union_saving(P):
     assert torch.equal(ph["sel_kv"], ph["sel_q"].view(len(wl.seq_lens), wl.n_kv_heads, G).sum(-1))
 
 
+@pytest.mark.parametrize("P", [0.3, 0.9, 1.0])
+def test_sparse_recent_tail_parity(P):
+    """Recent unclustered tokens at the end of each sequence (Sec. 1): always
+    selected, exact mass counted toward the target.  Tails of 0, 1, a few
+    hundred, one longer than its clustered part, and a whole sequence."""
+    T = _tactic()
+    wl = _small("ctx32k_llama8b", [3000, 700, 1500, 257, 900])
+    inp = synth.make_layer(wl, 0)
+    tail = [0, 1, 300, 200, 900]
+    lay = synth.label_layout(inp, tail=tail)
+    for union in (1, 0):
+        res = run_sparse(inp, lay, P, T.decode_params(P, max_tail=1024, use_union=union))
+        st = check_layer(inp, lay, P, res, label=f"tail P={P} union={union}")
+        G = wl.n_q_heads // wl.n_kv_heads
+        for b, t in enumerate(tail):
+            assert torch.all(res["sel_q"][b] >= t)
+        if P == 1.0:
+            assert all(s["union"] >= s["n"] for s in st)
+
+
 def test_sparse_ragged_small_with_empty_and_tiny_sequences():
     # lengths straddle tiles, a 1-token and a 5-token sequence (exact mode) and an empty one
     wl = _small("ctx32k_llama8b", [700, 0, 1, 5, 1300, 64, 3000])
