@@ -54,9 +54,14 @@ typedef struct {
   int32_t n_q_heads;           /* Hq, a multiple of n_kv_heads; Hq / Hkv in {1, 2, 4, 8} */
   int32_t n_kv_heads;          /* Hkv >= 1 */
   int32_t head_dim;            /* must be 128 */
-  int64_t total_tokens;        /* host: sum of the B sequence lengths */
-  int64_t max_seq_len;         /* host: largest sequence length */
-  const int64_t* kv_indptr;    /* device [B+1], kv_indptr[0] = 0, non-decreasing */
+  int64_t total_tokens;        /* host: kv_indptr[B], the row count of every per-KV-head array */
+  int64_t max_seq_len;         /* host: largest kv_indptr[b+1] - kv_indptr[b] */
+  const int64_t* kv_indptr;    /* device [B+1], kv_indptr[0] = 0, non-decreasing: sequence b's
+                                  rows start at kv_indptr[b] */
+  const int64_t* seq_len;      /* device [B] or NULL: sequence b holds rows kv_indptr[b] ..
+                                  kv_indptr[b] + seq_len[b] - 1 (clamped to kv_indptr[b+1]); the
+                                  rest of its span is spare room for new tokens.  NULL: the
+                                  whole span kv_indptr[b] .. kv_indptr[b+1] - 1. */
 } tactic_kv_shape;
 
 /* Cluster description of a cluster-sorted KV cache (the output of

@@ -28,7 +28,7 @@ EXPORTS = (
 class KVShape(ctypes.Structure):
     _fields_ = [("batch", c_int32), ("n_q_heads", c_int32), ("n_kv_heads", c_int32),
                 ("head_dim", c_int32), ("total_tokens", c_int64), ("max_seq_len", c_int64),
-                ("kv_indptr", c_void_p)]
+                ("kv_indptr", c_void_p), ("seq_len", c_void_p)]
 
 
 class ClusterMeta(ctypes.Structure):

@@ -266,6 +266,7 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   so.scores = sa.scores;
   so.offsets = meta->offsets;
   so.kv_indptr = shape->kv_indptr;
+  so.seq_len = shape->seq_len;
   so.cl_indptr = meta->cl_indptr;
   so.B = (int)p.B;
   so.Hq = (int)p.Hq;
@@ -340,6 +341,7 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   aa.K = K_sorted;
   aa.V = V_sorted;
   aa.kv_indptr = shape->kv_indptr;
+  aa.seq_len = shape->seq_len;
   aa.B = (int)p.B;
   aa.Hq = (int)p.Hq;
   aa.Hkv = (int)p.Hkv;
@@ -421,6 +423,7 @@ tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const ui
   aa.K = K;
   aa.V = V;
   aa.kv_indptr = shape->kv_indptr;
+  aa.seq_len = shape->seq_len;
   aa.B = shape->batch;
   aa.Hq = shape->n_q_heads;
   aa.Hkv = shape->n_kv_heads;
@@ -469,7 +472,7 @@ tactic_status tactic_build_clusters(const uint16_t* K, const uint16_t* V, const 
   const size_t need = tactic_build_clusters_workspace_size(shape, total_clusters, max_clusters);
   if (!workspace || workspace_bytes < need)
     return fail(TACTIC_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
-  hipError_t e = tactic::run_kmeans(K, V, shape->kv_indptr, cl_indptr, shape->batch, shape->n_kv_heads,
+  hipError_t e = tactic::run_kmeans(K, V, shape->kv_indptr, shape->seq_len, cl_indptr, shape->batch, shape->n_kv_heads,
                                     shape->total_tokens, shape->max_seq_len, total_clusters, max_clusters,
                                     init_idx, params->max_iters, centroids, assign, offsets, perm, K_sorted,
                                     V_sorted, workspace, stream);

@@ -28,8 +28,7 @@ constexpr float kScaleLog2 = 0.12751743074880046f;
 // Tokens of selection group bg: its union (sparse) or its sequence (dense).
 __device__ __forceinline__ int64_t group_tokens(const AttnArgs& a, int bg) {
   if (a.dense) {
-    const int b = bg / a.NV;
-    return a.kv_indptr[b + 1] - a.kv_indptr[b];
+    return seq_tokens(a.kv_indptr, a.seq_len, bg / a.NV);
   }
   return (int64_t)a.gmeta[bg * 4 + 1];
 }
@@ -200,7 +199,7 @@ void attn_splitk_kernel(AttnArgs a) {
     if (seg_lo >= seg_hi) continue;  // empty group
     const int b = bg / a.NV, jg = bg % a.NV, kvh = jg / a.kv_div;
     const int64_t kvb = a.kv_indptr[b];
-    const int nseq = (int)(a.kv_indptr[b + 1] - kvb);
+    const int nseq = (int)seq_tokens(a.kv_indptr, a.seq_len, b);
 
     uint32_t qw[G][W];
 #pragma unroll

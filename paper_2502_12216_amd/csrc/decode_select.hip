@@ -230,7 +230,7 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
   const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
   const int64_t cb = a.cl_indptr[b];
   const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
-  const int n = (int)(a.kv_indptr[b + 1] - a.kv_indptr[b]);
+  const int n = (int)seq_tokens(a.kv_indptr, a.seq_len, b);
   const int32_t* off = a.offsets + (int64_t)g * (a.Ct + a.B) + cb + b;
   const float* sc = a.scores + (int64_t)bh * a.Cm;
   int32_t* rank_of = a.rank_of + (int64_t)bh * a.Cm;

@@ -21,6 +21,7 @@ struct SortArgs {
   const float* scores;        // [B*Hq][Cm]
   const int32_t* offsets;     // [Hkv][Ct + B]
   const int64_t* kv_indptr;
+  const int64_t* seq_len;     // [B] or null (see tactic_kv_shape)
   const int64_t* cl_indptr;
   int B, Hq, Hkv, G, Cm, nb_max;
   int64_t Ct, S_cap;
@@ -72,6 +73,7 @@ struct AttnArgs {
   const uint16_t* K;
   const uint16_t* V;
   const int64_t* kv_indptr;
+  const int64_t* seq_len;     // [B] or null
   int B, Hq, Hkv, Cm, dense;
   int NV, kv_div;             // selection groups per sequence and KV head divisor (as in FitArgs)
   int64_t total, chunk_tokens, max_chunks;

@@ -42,6 +42,7 @@ struct KmArgs {
   const uint16_t* K;
   const uint16_t* V;
   const int64_t* kv_indptr;
+  const int64_t* seq_len;     // [B] or null (see tactic_kv_shape)
   const int64_t* cl_indptr;
   int B, Hkv, Cm, tiles_max, chunks_max, iter, max_iters;
   int64_t total, Ct;
@@ -70,7 +71,7 @@ __device__ __forceinline__ Problem problem(const KmArgs& a, int p) {
   q.b = p / a.Hkv;
   q.g = p % a.Hkv;
   const int64_t s0 = a.kv_indptr[q.b], c0 = a.cl_indptr[q.b];
-  q.n = (int)(a.kv_indptr[q.b + 1] - s0);
+  q.n = (int)seq_tokens(a.kv_indptr, a.seq_len, q.b);
   q.C = min((int)(a.cl_indptr[q.b + 1] - c0), a.Cm);
   q.tiles = (q.n + kKmTile - 1) / kKmTile;
   q.tok_base = (int64_t)q.g * a.total + s0;
@@ -462,7 +463,7 @@ size_t kmeans_workspace_bytes(int B, int Hkv, int64_t total, int64_t Ct, int Cm,
   return (size_t)km_layout(B, Hkv, total, Ct, Cm, nmax).bytes;
 }
 
-hipError_t run_kmeans(const uint16_t* K, const uint16_t* V, const int64_t* kv_indptr,
+hipError_t run_kmeans(const uint16_t* K, const uint16_t* V, const int64_t* kv_indptr, const int64_t* seq_len,
                       const int64_t* cl_indptr, int B, int Hkv, int64_t total, int64_t nmax,
                       int64_t Ct, int Cm, const int32_t* init_idx, int max_iters,
                       uint16_t* centroids, int32_t* assign, int32_t* offsets, int32_t* perm,
@@ -474,6 +475,7 @@ hipError_t run_kmeans(const uint16_t* K, const uint16_t* V, const int64_t* kv_in
   a.K = K;
   a.V = V;
   a.kv_indptr = kv_indptr;
+  a.seq_len = seq_len;
   a.cl_indptr = cl_indptr;
   a.B = B;
   a.Hkv = Hkv;

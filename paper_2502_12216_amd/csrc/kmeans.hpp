@@ -9,7 +9,7 @@ namespace tactic {
 
 size_t kmeans_workspace_bytes(int B, int Hkv, int64_t total, int64_t Ct, int Cm, int64_t nmax);
 
-hipError_t run_kmeans(const uint16_t* K, const uint16_t* V, const int64_t* kv_indptr,
+hipError_t run_kmeans(const uint16_t* K, const uint16_t* V, const int64_t* kv_indptr, const int64_t* seq_len,
                       const int64_t* cl_indptr, int B, int Hkv, int64_t total, int64_t nmax,
                       int64_t Ct, int Cm, const int32_t* init_idx, int max_iters,
                       uint16_t* centroids, int32_t* assign, int32_t* offsets, int32_t* perm,

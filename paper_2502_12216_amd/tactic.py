@@ -41,16 +41,26 @@ def _indptr(lengths: Sequence[int]) -> np.ndarray:
 
 
 class RaggedBatch:
-    """A ragged decode batch: sequence lengths, head counts, device indptr."""
+    """A ragged decode batch: sequence lengths, head counts, device indptr.
+
+    With `capacities`, sequence b owns a span of capacities[b] rows of the
+    per-KV-head arrays and holds its first seq_lens[b] of them (room for new
+    tokens); the lengths live in a device array the caller may update in
+    place (`seq_len`)."""
 
     def __init__(self, seq_lens: Sequence[int], n_q_heads: int, n_kv_heads: int, head_dim: int = 128,
-                 device="cuda"):
+                 device="cuda", capacities: Optional[Sequence[int]] = None):
         self.seq_lens = [int(x) for x in seq_lens]
         self.n_q_heads, self.n_kv_heads, self.head_dim = int(n_q_heads), int(n_kv_heads), int(head_dim)
-        self.kv_indptr_host = _indptr(self.seq_lens)
+        spans = self.seq_lens if capacities is None else [int(x) for x in capacities]
+        if capacities is not None and any(n > c for n, c in zip(self.seq_lens, spans)):
+            raise ValueError("a sequence is longer than its capacity")
+        self.kv_indptr_host = _indptr(spans)
         self.kv_indptr = torch.as_tensor(self.kv_indptr_host, device=device)
+        self.seq_len = (None if capacities is None
+                        else torch.as_tensor(np.asarray(self.seq_lens, dtype=np.int64), device=device))
         self.total = int(self.kv_indptr_host[-1])
-        self.max_len = max(self.seq_lens) if self.seq_lens else 0
+        self.max_len = max(spans) if spans else 0
 
     @property
     def batch(self) -> int:
@@ -58,7 +68,7 @@ class RaggedBatch:
 
     def struct(self) -> C.KVShape:
         return C.KVShape(self.batch, self.n_q_heads, self.n_kv_heads, self.head_dim, self.total, self.max_len,
-                         self.kv_indptr.data_ptr())
+                         self.kv_indptr.data_ptr(), None if self.seq_len is None else self.seq_len.data_ptr())
 
 
 class ClusterSet:

@@ -279,3 +279,40 @@ def test_dense_decode_matches_oracle(lens):
             ref = OA.dense_attention(np64(inp.q[b, h]), np64(inp.K[g, s0:s0 + n]), np64(inp.V[g, s0:s0 + n]))
             err = max(err, float(np.max(np.abs(np64(out2[b, h]) - ref))))
     assert err <= 2e-3, err
+
+
+def test_spare_room_layout_matches_packed_layout():
+    """Sequences with spare rows after their tokens (seq_len < span): every
+    kernel reads only the first seq_len rows, so results equal the packed
+    layout's bit for bit even when the spare rows hold huge values."""
+    T = _tactic()
+    wl = _small("ctx32k_llama8b", [1800, 0, 700, 2500])
+    inp = synth.make_layer(wl, 0)
+    lay = synth.label_layout(inp, tail=[100, 0, 0, 40])
+    lens = list(wl.seq_lens)
+    caps = [n + extra for n, extra in zip(lens, [300, 5, 0, 77])]
+    ncl = [int(lay.cl_indptr[i + 1] - lay.cl_indptr[i]) for i in range(len(lens))]
+    Hkv = wl.n_kv_heads
+    packed = T.RaggedBatch(lens, wl.n_q_heads, Hkv)
+    spaced = T.RaggedBatch(lens, wl.n_q_heads, Hkv, capacities=caps)
+
+    def spread(X):
+        Y = torch.full((Hkv, spaced.total, 128), 3e4, dtype=torch.bfloat16)
+        for b, n in enumerate(lens):
+            s0, d0 = packed.kv_indptr_host[b], spaced.kv_indptr_host[b]
+            Y[:, d0:d0 + n] = X[:, s0:s0 + n]
+        return Y.to(DEV)
+
+    q = inp.q.to(DEV)
+    cl = T.ClusterSet(lay.centroids.to(DEV), lay.offsets.to(DEV), ncl)
+    for P in (0.6, 1.0):
+        params = T.decode_params(P, max_tail=256)
+        o1, q1, k1 = T.SparseDecoder(packed, ncl, params)(q, lay.K_sorted.to(DEV), lay.V_sorted.to(DEV), cl)
+        o2, q2, k2 = T.SparseDecoder(spaced, ncl, params)(q, spread(lay.K_sorted), spread(lay.V_sorted), cl)
+        torch.cuda.synchronize()
+        assert torch.equal(q1, q2) and torch.equal(k1, k2)
+        assert torch.equal(o1, o2)
+    d1 = T.DenseDecoder(packed)(q, inp.K.to(DEV), inp.V.to(DEV))
+    d2 = T.DenseDecoder(spaced)(q, spread(inp.K), spread(inp.V))
+    torch.cuda.synchronize()
+    assert torch.allclose(d1, d2, atol=1e-5, rtol=0)

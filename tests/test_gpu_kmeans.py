@@ -157,3 +157,35 @@ def test_decode_on_kmeans_clusters_invariants():
                 if P == 1.0:
                     assert skv[b, g] == n
         assert torch.isfinite(out).all()
+
+
+def test_kmeans_spare_room_layout_matches_packed():
+    """K-means over sequences with spare rows (seq_len < span) touches only
+    the sequences' tokens: same clusters and cluster-sorted rows as packed."""
+    T = _tactic()
+    wl = synth.small_workload(synth.WORKLOADS["ctx32k_llama8b"], [3000, 1200])
+    inp = synth.make_layer(wl, 0)
+    lens = list(wl.seq_lens)
+    caps = [lens[0] + 333, lens[1] + 64]
+    ncl = [wl.n_clusters(n) for n in lens]
+    Hkv = wl.n_kv_heads
+    packed = T.RaggedBatch(lens, wl.n_q_heads, Hkv)
+    spaced = T.RaggedBatch(lens, wl.n_q_heads, Hkv, capacities=caps)
+
+    def spread(X):
+        Y = torch.full((Hkv, spaced.total, 128), -7.0, dtype=torch.bfloat16)
+        for b, n in enumerate(lens):
+            s0, d0 = packed.kv_indptr_host[b], spaced.kv_indptr_host[b]
+            Y[:, d0:d0 + n] = X[:, s0:s0 + n]
+        return Y.to(DEV)
+
+    init = torch.as_tensor(synth.kmeans_init_all(wl, 0), device=DEV)
+    r1 = T.ClusterBuilder(packed, ncl, max_iters=5)(inp.K.to(DEV), inp.V.to(DEV), init)
+    r2 = T.ClusterBuilder(spaced, ncl, max_iters=5)(spread(inp.K), spread(inp.V), init)
+    torch.cuda.synchronize()
+    assert torch.equal(r1.clusters.centroids, r2.clusters.centroids)
+    assert torch.equal(r1.clusters.offsets, r2.clusters.offsets)
+    for b, n in enumerate(lens):
+        s0, d0 = packed.kv_indptr_host[b], spaced.kv_indptr_host[b]
+        assert torch.equal(r1.assign[:, s0:s0 + n], r2.assign[:, d0:d0 + n])
+        assert torch.equal(r1.K_sorted[:, s0:s0 + n], r2.K_sorted[:, d0:d0 + n])
