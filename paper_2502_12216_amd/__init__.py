@@ -6,3 +6,4 @@ include/tactic.h); this package only marshals torch tensors into those calls.
 from ._capi import TacticError, lib, LIB_PATH, EXPORTS  # noqa: F401
 from .tactic import (ClusterBuild, ClusterBuilder, ClusterSet, DenseDecoder, RaggedBatch,  # noqa: F401
                      SparseDecoder, decode_params)
+from .cache import RecentTailCache  # noqa: F401
