@@ -197,6 +197,46 @@ tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const ui
                                   const tactic_kv_shape* shape, float* out, void* workspace,
                                   size_t workspace_bytes, hipStream_t stream);
 
+/* A paged K/V cache (Sec. 4.6 reads the selected tokens from a paged cache
+ * through sub-requests): instead of a cluster-sorted copy, the keys and
+ * values stay in pages in token order and the cluster order reaches them
+ * through `perm`.  Page p holds page_size consecutive tokens of one sequence
+ * for every KV head; tokens [i*page_size, (i+1)*page_size) of sequence b are
+ * in page page_table[b*max_pages + i].  Out-of-range table entries are
+ * clamped (reads stay inside the arrays; the result is then meaningless). */
+typedef struct {
+  const uint16_t* K_pages;     /* device bf16 [num_pages][Hkv][page_size][128] */
+  const uint16_t* V_pages;     /* device bf16, same layout */
+  const int32_t* page_table;   /* device int32 [B][max_pages] */
+  const int32_t* perm;         /* device int32 [Hkv][total_tokens]: sequence-relative token at each
+                                  cluster-sorted row (the perm output of tactic_build_clusters),
+                                  for the first c_b rows; rows from c_b on (recent tokens) are
+                                  their own tokens.  NULL: the pages hold the tokens in cluster
+                                  order already. */
+  int32_t page_size;           /* tokens per page, >= 1 */
+  int32_t max_pages;           /* page-table entries per sequence; max_pages * page_size >=
+                                  max_seq_len and < 2^31 */
+  int64_t num_pages;           /* host: pages in K_pages / V_pages; num_pages * Hkv * page_size < 2^31 */
+} tactic_paged_kv;
+
+/* tactic_sparse_decode over a paged cache: same selection, outputs, plan and
+ * workspace; `shape` gives the sequence lengths (kv_indptr / seq_len) and the
+ * row stride of `perm`. */
+tactic_status tactic_sparse_decode_paged(const uint16_t* q, const tactic_paged_kv* kv,
+                                         const tactic_kv_shape* shape,
+                                         const tactic_cluster_meta* meta,
+                                         const tactic_decode_params* params,
+                                         const tactic_decode_plan* plan, float* out,
+                                         int32_t* sel_count_q, int32_t* sel_count_kv,
+                                         void* workspace, size_t workspace_bytes,
+                                         hipStream_t stream);
+
+/* tactic_dense_decode over a paged cache (perm is ignored: dense attention
+ * reads every token); workspace as tactic_dense_decode_workspace_size. */
+tactic_status tactic_dense_decode_paged(const uint16_t* q, const tactic_paged_kv* kv,
+                                        const tactic_kv_shape* shape, float* out, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream);
+
 /* Prefill clustering (Sec. 4.2): per (sequence, KV head) K-means on the keys
  * with C_b clusters, started from the keys of the tokens init_idx names,
  * alternating nearest-centroid assignment (squared Euclidean distance, ties to

@@ -4,6 +4,6 @@ The computation lives in libtactic.so (HIP kernels behind the C ABI of
 include/tactic.h); this package only marshals torch tensors into those calls.
 """
 from ._capi import TacticError, lib, LIB_PATH, EXPORTS  # noqa: F401
-from .tactic import (ClusterBuild, ClusterBuilder, ClusterSet, DenseDecoder, RaggedBatch,  # noqa: F401
+from .tactic import (ClusterBuild, ClusterBuilder, ClusterSet, DenseDecoder, PagedCache, RaggedBatch,  # noqa: F401
                      SparseDecoder, decode_params)
 from .cache import RecentTailCache  # noqa: F401

@@ -20,6 +20,7 @@ EXPORTS = (
     "tactic_decode_params_default", "tactic_sparse_decode_plan", "tactic_sparse_decode",
     "tactic_sparse_decode_plan_set_events",
     "tactic_sparse_decode_view", "tactic_dense_decode_workspace_size", "tactic_dense_decode",
+    "tactic_sparse_decode_paged", "tactic_dense_decode_paged",
     "tactic_build_clusters_workspace_size", "tactic_build_clusters", "tactic_status_string",
     "tactic_last_error",
 )
@@ -51,6 +52,11 @@ class DecodeView(ctypes.Structure):
                 ("fit", c_void_p), ("union_len", c_void_p)]
 
 
+class PagedKV(ctypes.Structure):
+    _fields_ = [("K_pages", c_void_p), ("V_pages", c_void_p), ("page_table", c_void_p), ("perm", c_void_p),
+                ("page_size", c_int32), ("max_pages", c_int32), ("num_pages", c_int64)]
+
+
 class KMeansParams(ctypes.Structure):
     _fields_ = [("max_iters", c_int32)]
 
@@ -80,6 +86,10 @@ def lib() -> ctypes.CDLL:
                                        POINTER(DecodeParams), POINTER(DecodePlan), c_void_p, c_void_p,
                                        c_void_p, c_void_p, c_size_t, c_void_p]
     L.tactic_sparse_decode.restype = c_int
+    L.tactic_sparse_decode_paged.argtypes = [c_void_p, POINTER(PagedKV), POINTER(KVShape), POINTER(ClusterMeta),
+                                             POINTER(DecodeParams), POINTER(DecodePlan), c_void_p, c_void_p,
+                                             c_void_p, c_void_p, c_size_t, c_void_p]
+    L.tactic_sparse_decode_paged.restype = c_int
     L.tactic_sparse_decode_plan_set_events.argtypes = [POINTER(DecodePlan), c_void_p]
     L.tactic_sparse_decode_plan_set_events.restype = c_int
     L.tactic_sparse_decode_view.argtypes = [POINTER(DecodePlan), c_void_p, POINTER(DecodeView)]
@@ -89,6 +99,9 @@ def lib() -> ctypes.CDLL:
     L.tactic_dense_decode.argtypes = [c_void_p, c_void_p, c_void_p, POINTER(KVShape), c_void_p, c_void_p,
                                       c_size_t, c_void_p]
     L.tactic_dense_decode.restype = c_int
+    L.tactic_dense_decode_paged.argtypes = [c_void_p, POINTER(PagedKV), POINTER(KVShape), c_void_p, c_void_p,
+                                            c_size_t, c_void_p]
+    L.tactic_dense_decode_paged.restype = c_int
     L.tactic_build_clusters_workspace_size.argtypes = [POINTER(KVShape), c_int64, c_int32]
     L.tactic_build_clusters_workspace_size.restype = c_size_t
     L.tactic_build_clusters.argtypes = [c_void_p, c_void_p, POINTER(KVShape), c_void_p, c_int64, c_int32,
@@ -110,5 +123,5 @@ def check(status: int, what: str) -> None:
                           f"{L.tactic_last_error().decode()} (status {status})")
 
 
-__all__ = ["KVShape", "ClusterMeta", "DecodeParams", "DecodePlan", "DecodeView", "KMeansParams",
+__all__ = ["KVShape", "ClusterMeta", "DecodeParams", "DecodePlan", "DecodeView", "KMeansParams", "PagedKV",
            "TacticError", "lib", "check", "EXPORTS", "LIB_PATH", "FIT_FIELDS", "FIT_NAMES", "c_double"]

@@ -90,6 +90,24 @@ tactic_status check_params(const tactic_decode_params* p) {
   return TACTIC_OK;
 }
 
+tactic_status paged_args(const tactic_paged_kv* kv, const tactic_kv_shape* s, tactic::PagedKV* pk) {
+  if (!kv || !kv->K_pages || !kv->V_pages || !kv->page_table) return fail(TACTIC_ERR_INVALID_ARG, "null paged-KV pointer");
+  if (kv->page_size < 1 || kv->max_pages < 1 || kv->num_pages < 1)
+    return fail(TACTIC_ERR_INVALID_ARG, "page_size, max_pages and num_pages must be >= 1");
+  if ((int64_t)kv->page_size * kv->max_pages < s->max_seq_len)
+    return fail(TACTIC_ERR_INVALID_ARG, "max_pages * page_size < max_seq_len");
+  if ((int64_t)kv->page_size * kv->max_pages >= ((int64_t)1 << 31))
+    return fail(TACTIC_ERR_UNSUPPORTED, "max_pages * page_size >= 2^31");
+  if (kv->num_pages * s->n_kv_heads * kv->page_size >= ((int64_t)1 << 31))
+    return fail(TACTIC_ERR_UNSUPPORTED, "num_pages * n_kv_heads * page_size >= 2^31 rows");
+  pk->page_table = kv->page_table;
+  pk->perm = kv->perm;
+  pk->page_size = kv->page_size;
+  pk->max_pages = kv->max_pages;
+  pk->num_pages = kv->num_pages;
+  return TACTIC_OK;
+}
+
 const tactic::DecodePlan* as_plan(const tactic_decode_plan* p) {
   return reinterpret_cast<const tactic::DecodePlan*>(p);
 }
@@ -216,7 +234,9 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape, const tact
   return TACTIC_OK;
 }
 
-tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, const uint16_t* V_sorted,
+// The sparse decode launch sequence; pk non-null reads K/V through a page table.
+static tactic_status sparse_decode_impl(const uint16_t* q, const uint16_t* K_sorted, const uint16_t* V_sorted,
+                                   const tactic::PagedKV* pk,
                                    const tactic_kv_shape* shape, const tactic_cluster_meta* meta,
                                    const tactic_decode_params* params, const tactic_decode_plan* plan_in,
                                    float* out, int32_t* sel_count_q, int32_t* sel_count_kv, void* workspace,
@@ -248,7 +268,7 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   hipError_t e = record(0);
   if (e != hipSuccess) return hip_fail(e, "event record");
 
-  tactic::ScoreArgs sa;
+  tactic::ScoreArgs sa{};
   sa.q = q;
   sa.centroids = meta->centroids;
   sa.cl_indptr = meta->cl_indptr;
@@ -262,7 +282,7 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   if (e == hipSuccess) e = record(1);
   if (e != hipSuccess) return hip_fail(e, "score_clusters launch");
 
-  tactic::SortArgs so;
+  tactic::SortArgs so{};
   so.scores = sa.scores;
   so.offsets = meta->offsets;
   so.kv_indptr = shape->kv_indptr;
@@ -292,7 +312,7 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   if (e == hipSuccess) e = record(2);
   if (e != hipSuccess) return hip_fail(e, "sort_clusters launch");
 
-  tactic::FitArgs fa;
+  tactic::FitArgs fa{};
   fa.q = q;
   fa.K = K_sorted;
   fa.kv_indptr = shape->kv_indptr;
@@ -329,14 +349,15 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   fa.rstart = reinterpret_cast<int32_t*>(ws + p.off_rstart);
   fa.rupos = reinterpret_cast<int32_t*>(ws + p.off_rupos);
   fa.cfr = reinterpret_cast<int32_t*>(ws + p.off_cfr);
-  e = tactic::launch_sample(fa, (int)p.split, BH, stream);
+  if (pk) fa.pk = *pk;
+  e = tactic::launch_sample(fa, (int)p.split, BH, pk != nullptr, stream);
   if (e == hipSuccess) e = record(3);
   if (e != hipSuccess) return hip_fail(e, "sample_logits launch");
   e = tactic::launch_fit_union(fa, (int)p.GV, BV, stream);
   if (e == hipSuccess) e = record(4);
   if (e != hipSuccess) return hip_fail(e, "fit_union launch");
 
-  tactic::AttnArgs aa;
+  tactic::AttnArgs aa{};
   aa.q = q;
   aa.K = K_sorted;
   aa.V = V_sorted;
@@ -358,18 +379,42 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
   aa.cfr = fa.cfr;
   aa.partials = reinterpret_cast<float*>(ws + p.off_partials);
   aa.ameta = reinterpret_cast<int64_t*>(ws + p.off_ameta);
+  aa.head_meta = so.head_meta;
+  if (pk) aa.pk = *pk;
   aa.out = out;
   int grid = 0;
-  e = tactic::attn_resident_grid((int)p.GV, BV, &grid);
+  e = tactic::attn_resident_grid((int)p.GV, BV, pk != nullptr, &grid);
   if (e != hipSuccess) return hip_fail(e, "attention occupancy query");
   grid = (int)std::min<int64_t>(grid, p.attn_grid);  // the partials are sized for attn_grid
-  e = tactic::launch_attn(aa, (int)p.GV, grid, stream);
+  e = tactic::launch_attn(aa, (int)p.GV, grid, pk != nullptr, stream);
   if (e == hipSuccess) e = record(5);
   if (e != hipSuccess) return hip_fail(e, "attention launch");
   e = tactic::launch_combine(aa, (int)p.GV, stream);
   if (e == hipSuccess) e = record(6);
   if (e != hipSuccess) return hip_fail(e, "combine launch");
   return TACTIC_OK;
+}
+
+tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, const uint16_t* V_sorted,
+                                   const tactic_kv_shape* shape, const tactic_cluster_meta* meta,
+                                   const tactic_decode_params* params, const tactic_decode_plan* plan_in,
+                                   float* out, int32_t* sel_count_q, int32_t* sel_count_kv, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream) {
+  return sparse_decode_impl(q, K_sorted, V_sorted, nullptr, shape, meta, params, plan_in, out, sel_count_q,
+                            sel_count_kv, workspace, workspace_bytes, stream);
+}
+
+tactic_status tactic_sparse_decode_paged(const uint16_t* q, const tactic_paged_kv* kv,
+                                         const tactic_kv_shape* shape, const tactic_cluster_meta* meta,
+                                         const tactic_decode_params* params, const tactic_decode_plan* plan_in,
+                                         float* out, int32_t* sel_count_q, int32_t* sel_count_kv,
+                                         void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  tactic_status st = check_shape(shape);
+  if (st != TACTIC_OK) return st;
+  tactic::PagedKV pk;
+  if ((st = paged_args(kv, shape, &pk)) != TACTIC_OK) return st;
+  return sparse_decode_impl(q, kv->K_pages, kv->V_pages, &pk, shape, meta, params, plan_in, out, sel_count_q,
+                            sel_count_kv, workspace, workspace_bytes, stream);
 }
 
 tactic_status tactic_sparse_decode_plan_set_events(tactic_decode_plan* plan_in, hipEvent_t* events) {
@@ -402,9 +447,9 @@ size_t tactic_dense_decode_workspace_size(const tactic_kv_shape* shape) {
   return dense_workspace_bytes(shape, tactic::kMaxAttnGrid);
 }
 
-tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const uint16_t* V,
-                                  const tactic_kv_shape* shape, float* out, void* workspace,
-                                  size_t workspace_bytes, hipStream_t stream) {
+static tactic_status dense_decode_impl(const uint16_t* q, const uint16_t* K, const uint16_t* V,
+                                       const tactic::PagedKV* pk, const tactic_kv_shape* shape, float* out,
+                                       void* workspace, size_t workspace_bytes, hipStream_t stream) {
   tactic_status st = check_shape(shape);
   if (st != TACTIC_OK) return st;
   if (!q || !K || !V || !out) return fail(TACTIC_ERR_INVALID_ARG, "null argument");
@@ -414,10 +459,10 @@ tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const ui
   if (!workspace || workspace_bytes < need)
     return fail(TACTIC_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
   int resident = 0;
-  hipError_t e = tactic::attn_resident_grid(G, (int)BG, &resident);
+  hipError_t e = tactic::attn_resident_grid(G, (int)BG, pk != nullptr, &resident);
   if (e != hipSuccess) return hip_fail(e, "attention occupancy query");
   resident = std::min(resident, tactic::kMaxAttnGrid);
-  tactic::AttnArgs aa;
+  tactic::AttnArgs aa{};
   memset(&aa, 0, sizeof(aa));
   aa.q = q;
   aa.K = K;
@@ -437,11 +482,29 @@ tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const ui
     L.take((BG + tactic::kMaxAttnGrid) * G * (tactic::kHeadDim + 2) * 4);
     aa.ameta = reinterpret_cast<int64_t*>(static_cast<char*>(workspace) + L.take((BG + 2) * 8));
   }
+  if (pk) aa.pk = *pk;
   aa.out = out;
-  e = tactic::launch_attn(aa, G, resident, stream);
+  e = tactic::launch_attn(aa, G, resident, pk != nullptr, stream);
   if (e == hipSuccess) e = tactic::launch_combine(aa, G, stream);
   if (e != hipSuccess) return hip_fail(e, "dense attention launch");
   return TACTIC_OK;
+}
+
+tactic_status tactic_dense_decode(const uint16_t* q, const uint16_t* K, const uint16_t* V,
+                                  const tactic_kv_shape* shape, float* out, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream) {
+  return dense_decode_impl(q, K, V, nullptr, shape, out, workspace, workspace_bytes, stream);
+}
+
+tactic_status tactic_dense_decode_paged(const uint16_t* q, const tactic_paged_kv* kv,
+                                        const tactic_kv_shape* shape, float* out, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream) {
+  tactic_status st = check_shape(shape);
+  if (st != TACTIC_OK) return st;
+  tactic::PagedKV pk;
+  if ((st = paged_args(kv, shape, &pk)) != TACTIC_OK) return st;
+  pk.perm = nullptr;  // dense decode reads positions: no cluster order
+  return dense_decode_impl(q, kv->K_pages, kv->V_pages, &pk, shape, out, workspace, workspace_bytes, stream);
 }
 
 size_t tactic_build_clusters_workspace_size(const tactic_kv_shape* shape, int64_t total_clusters,

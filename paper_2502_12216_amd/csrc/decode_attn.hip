@@ -121,7 +121,7 @@ __device__ __forceinline__ float head_value(float x, int h) {
 #define TACTIC_ATTN_WPE 3  // resident waves per SIMD the register budget must allow
 #endif
 
-template <int G, int TOK>
+template <int G, int TOK, bool kPaged>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(G >= 8 ? 2 : TACTIC_ATTN_WPE)))
 void attn_splitk_kernel(AttnArgs a) {
   constexpr int LPR = 16;                 // lanes per 256-byte row
@@ -215,8 +215,12 @@ void attn_splitk_kernel(AttnArgs a) {
 #pragma unroll
       for (int e = 0; e < EPL; ++e) acc[h][e] = 0.f;
 
-    const uint16_t* Kb = a.K + ((int64_t)kvh * a.total + kvb) * kHeadDim + sl * EPL;
-    const uint16_t* Vb = a.V + ((int64_t)kvh * a.total + kvb) * kHeadDim + sl * EPL;
+    // contiguous: rows of this (sequence, KV head); paged: row indices into the page array
+    const int64_t rbase = kPaged ? 0 : (int64_t)kvh * a.total + kvb;
+    const uint16_t* Kb = a.K + rbase * kHeadDim + sl * EPL;
+    const uint16_t* Vb = a.V + rbase * kHeadDim + sl * EPL;
+    // clustered rows of the group (paged: rows from there on are their own tokens)
+    const int n_c = (kPaged && !a.dense) ? a.head_meta[(int64_t)(b * a.Hq + jg * G) * 16] : nseq;
     int cnt = 0;      // tokens of the current sub-range
     int64_t p0 = 0;   // its first position in the group's token list
     struct Tile {
@@ -229,7 +233,7 @@ void attn_splitk_kernel(AttnArgs a) {
       for (int i = 0; i < TOK; ++i) {
         const int t = tile * kTileTok + gid * TOK + i;
         if (t < cnt) {
-          const int64_t row = a.dense ? p0 + t : (int64_t)s_rows[t];
+          const int64_t row = (a.dense && !kPaged) ? p0 + t : (int64_t)s_rows[t];
           load_words(Kb + row * kHeadDim, r.k[i]);
           load_words(Vb + row * kHeadDim, r.v[i]);
         } else {
@@ -293,8 +297,14 @@ void attn_splitk_kernel(AttnArgs a) {
     // table fits LDS (dense rows are positions: one sub-range)
     for (int64_t p = seg_lo; p < seg_hi; p += cnt) {
       p0 = p;
-      if (a.dense) {
+      if (a.dense && !kPaged) {
         cnt = (int)(seg_hi - p);
+      } else if (a.dense) {
+        // paged dense: the row table holds each position's page row
+        cnt = (int)min(seg_hi - p, (int64_t)kMaxChunkTokens);
+        for (int t = tid; t < cnt; t += 256)
+          s_rows[t] = (int)paged_row(a.pk, a.Hkv, a.total, kvb, b, kvh, (int)(p + t), 0);
+        __syncthreads();
       } else {
         const int64_t c = p / kCfrTokens, in = p - c * kCfrTokens;
         cnt = (int)min(seg_hi - p, (int64_t)kMaxChunkTokens - in);
@@ -317,8 +327,8 @@ void attn_splitk_kernel(AttnArgs a) {
             if (s_rupos[mid] <= pos) l2 = mid;
             else h2 = mid - 1;
           }
-          const int row = s_rstart[l2] + (pos - s_rupos[l2]);
-          s_rows[t] = min(max(row, 0), nseq - 1);  // in range unless the cluster meta is inconsistent
+          const int row = min(max(s_rstart[l2] + (pos - s_rupos[l2]), 0), nseq - 1);  // clamp: bad meta only
+          s_rows[t] = kPaged ? (int)paged_row(a.pk, a.Hkv, a.total, kvb, b, kvh, row, n_c) : row;
         }
         __syncthreads();
       }
@@ -362,7 +372,7 @@ void attn_splitk_kernel(AttnArgs a) {
         cur = nxt;
       }
 #endif
-      if (!a.dense) __syncthreads();  // the next sub-range rewrites the row table
+      if (!a.dense || kPaged) __syncthreads();  // the next sub-range rewrites the row table
     }
 
     // ---- merge the lane-group states: common max, rescale, sum
@@ -471,36 +481,46 @@ __global__ __launch_bounds__(512) void combine_kernel(AttnArgs a) {
 
 static size_t attn_dyn_lds(const AttnArgs& a) { return ((size_t)a.B * a.NV + 1) * sizeof(int64_t); }
 
-hipError_t launch_attn(const AttnArgs& a, int G, int grid, hipStream_t st) {
+template <bool kPaged>
+static hipError_t launch_attn_t(const AttnArgs& a, int G, int grid, hipStream_t st) {
   constexpr int TOK = TACTIC_ATTN_TOK;
   const size_t lds = attn_dyn_lds(a);
   switch (G) {
-    case 1: hipLaunchKernelGGL((attn_splitk_kernel<1, TOK>), dim3(grid), dim3(256), lds, st, a); break;
-    case 2: hipLaunchKernelGGL((attn_splitk_kernel<2, TOK>), dim3(grid), dim3(256), lds, st, a); break;
-    case 4: hipLaunchKernelGGL((attn_splitk_kernel<4, TOK>), dim3(grid), dim3(256), lds, st, a); break;
-    case 8: hipLaunchKernelGGL((attn_splitk_kernel<8, TOK>), dim3(grid), dim3(256), lds, st, a); break;
+    case 1: hipLaunchKernelGGL((attn_splitk_kernel<1, TOK, kPaged>), dim3(grid), dim3(256), lds, st, a); break;
+    case 2: hipLaunchKernelGGL((attn_splitk_kernel<2, TOK, kPaged>), dim3(grid), dim3(256), lds, st, a); break;
+    case 4: hipLaunchKernelGGL((attn_splitk_kernel<4, TOK, kPaged>), dim3(grid), dim3(256), lds, st, a); break;
+    case 8: hipLaunchKernelGGL((attn_splitk_kernel<8, TOK, kPaged>), dim3(grid), dim3(256), lds, st, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
+hipError_t launch_attn(const AttnArgs& a, int G, int grid, bool paged, hipStream_t st) {
+  return paged ? launch_attn_t<true>(a, G, grid, st) : launch_attn_t<false>(a, G, grid, st);
+}
+
 // Workgroups of the attention kernel that fit on the device at once: the
-// persistent grid is sized to exactly this, so the round-robin item
-// assignment never leaves late-starting workgroups on the critical path.
-hipError_t attn_resident_grid(int G, int n_groups, int* grid) {
+// persistent grid is sized to exactly this, so every workgroup streams its
+// share of the tokens from the start.
+template <bool kPaged>
+static hipError_t resident_t(int G, size_t lds, int* per) {
   constexpr int TOK = TACTIC_ATTN_TOK;
+  switch (G) {
+    case 1: return hipOccupancyMaxActiveBlocksPerMultiprocessor(per, attn_splitk_kernel<1, TOK, kPaged>, 256, lds);
+    case 2: return hipOccupancyMaxActiveBlocksPerMultiprocessor(per, attn_splitk_kernel<2, TOK, kPaged>, 256, lds);
+    case 4: return hipOccupancyMaxActiveBlocksPerMultiprocessor(per, attn_splitk_kernel<4, TOK, kPaged>, 256, lds);
+    case 8: return hipOccupancyMaxActiveBlocksPerMultiprocessor(per, attn_splitk_kernel<8, TOK, kPaged>, 256, lds);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t attn_resident_grid(int G, int n_groups, bool paged, int* grid) {
   int dev = 0, cus = 0, per = 0;
   const size_t lds = ((size_t)n_groups + 1) * sizeof(int64_t);
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return e;
-  switch (G) {
-    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<1, TOK>, 256, lds); break;
-    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<2, TOK>, 256, lds); break;
-    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<4, TOK>, 256, lds); break;
-    case 8: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_splitk_kernel<8, TOK>, 256, lds); break;
-    default: return hipErrorInvalidValue;
-  }
+  e = paged ? resident_t<true>(G, lds, &per) : resident_t<false>(G, lds, &per);
   *grid = (per > 0 ? per : 1) * (cus > 0 ? cus : 1);
   return e;
 }

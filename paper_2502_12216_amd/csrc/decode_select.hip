@@ -605,6 +605,7 @@ __device__ __forceinline__ double wave_max_d(double v) {
   return v;
 }
 
+template <bool kPaged>
 __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
   __shared__ double s_lg[kSampleChunk];
   constexpr int kRW = kSampleChunk / kWave;  // waves that reduce the chunk, one sample per lane
@@ -641,12 +642,22 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
       qf[2 * e + 1] = bf16hi(w[e]);
     }
   }
-  const uint16_t* kbase = a.K + ((int64_t)g * a.total + a.kv_indptr[b]) * kHeadDim + sl * 8;
+  const int64_t kvb = a.kv_indptr[b];
   double* lg = a.logits + (int64_t)bh * a.S_cap;
+  int64_t roff[kR];  // row index of every sample in the K array
+  if constexpr (kPaged) {
+    const int n_c = hm[0];
+#pragma unroll
+    for (int k = 0; k < kR; ++k)
+      roff[k] = r[k] >= 0 ? paged_row(a.pk, a.Hkv, a.total, kvb, b, g, r[k], n_c) : -1;
+  } else {
+#pragma unroll
+    for (int k = 0; k < kR; ++k) roff[k] = r[k] >= 0 ? (int64_t)g * a.total + kvb + r[k] : -1;
+  }
   uint4 kv[kR];
 #pragma unroll
   for (int k = 0; k < kR; ++k)
-    kv[k] = r[k] >= 0 ? load_stream16(kbase + (int64_t)r[k] * kHeadDim) : make_uint4(0, 0, 0, 0);
+    kv[k] = roff[k] >= 0 ? load_stream16(a.K + roff[k] * kHeadDim + sl * 8) : make_uint4(0, 0, 0, 0);
 #pragma unroll
   for (int k = 0; k < kR; ++k) {
     const uint32_t w[4] = {kv[k].x, kv[k].y, kv[k].z, kv[k].w};
@@ -1014,8 +1025,9 @@ hipError_t launch_sort(const SortArgs& a, bool lds, int n_heads, hipStream_t st)
   return hipGetLastError();
 }
 
-hipError_t launch_sample(const FitArgs& a, int split, int n_heads, hipStream_t st) {
-  hipLaunchKernelGGL(sample_logits_kernel, dim3(split, n_heads), dim3(256), 0, st, a);
+hipError_t launch_sample(const FitArgs& a, int split, int n_heads, bool paged, hipStream_t st) {
+  if (paged) hipLaunchKernelGGL(sample_logits_kernel<true>, dim3(split, n_heads), dim3(256), 0, st, a);
+  else hipLaunchKernelGGL(sample_logits_kernel<false>, dim3(split, n_heads), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

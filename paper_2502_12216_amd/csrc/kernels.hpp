@@ -8,6 +8,30 @@
 
 namespace tactic {
 
+// A paged K/V cache: page p holds page_size consecutive tokens of one
+// sequence for every KV head, bf16 [num_pages][Hkv][page_size][128]; the
+// page of a sequence's tokens [i * page_size, (i + 1) * page_size) is
+// page_table[b * max_pages + i].  perm (or null for the identity) maps a
+// cluster-sorted row of the first c_b rows to its token; rows from c_b on
+// (the recent tokens) are their own tokens.
+struct PagedKV {
+  const int32_t* page_table;  // [B][max_pages]
+  const int32_t* perm;        // [Hkv][total] sequence-relative token per cluster-sorted row, or null
+  int page_size, max_pages;
+  int64_t num_pages;
+};
+
+// Element offset of the 128-wide K/V row of (sequence b, KV head kvh) at
+// cluster-sorted row `row` (the token itself when dense); n_c = clustered rows.
+__device__ __forceinline__ int64_t paged_row(const PagedKV& pk, int Hkv, int64_t total, int64_t kvb, int b,
+                                             int kvh, int row, int n_c) {
+  int tok = (pk.perm && row < n_c) ? pk.perm[(int64_t)kvh * total + kvb + row] : row;
+  tok = min(max(tok, 0), pk.max_pages * pk.page_size - 1);  // in bounds whatever the tables hold
+  int64_t page = pk.page_table[(int64_t)b * pk.max_pages + tok / pk.page_size];
+  page = min(max(page, (int64_t)0), pk.num_pages - 1);
+  return (page * Hkv + kvh) * pk.page_size + tok % pk.page_size;
+}
+
 struct ScoreArgs {
   const uint16_t* q;          // bf16 [B][Hq][128]
   const uint16_t* centroids;  // bf16 [Hkv][Ct][128]
@@ -66,6 +90,7 @@ struct FitArgs {
   int32_t* rstart;            // [B*NV][Cm+2]: first row of each selected range
   int32_t* rupos;             // [B*NV][Cm+2]: its first position in the group's token list
   int32_t* cfr;               // [B*NV][max_chunks]
+  PagedKV pk;                 // used by the paged launches (K then points at the pages)
 };
 
 struct AttnArgs {
@@ -83,15 +108,17 @@ struct AttnArgs {
   const int32_t* cfr;
   float* partials;            // [B*NV + grid][GV*130]: one slot per (group, workgroup) pair
   int64_t* ameta;             // [B*NV + 2]: tokens per workgroup, then the groups' token offsets
+  const int32_t* head_meta;   // [B*Hq][16] (sparse, paged: clustered rows per head in field 0)
+  PagedKV pk;                 // used by the paged launches (K, V then point at the pages)
   float* out;                 // [B][Hq][128]
 };
 
 hipError_t launch_score(const ScoreArgs& a, int G, int grid_x, int grid_y, hipStream_t st);
 hipError_t launch_sort(const SortArgs& a, bool lds, int n_heads, hipStream_t st);
-hipError_t launch_sample(const FitArgs& a, int split, int n_heads, hipStream_t st);
+hipError_t launch_sample(const FitArgs& a, int split, int n_heads, bool paged, hipStream_t st);
 hipError_t launch_fit_union(const FitArgs& a, int G, int n_groups, hipStream_t st);
-hipError_t launch_attn(const AttnArgs& a, int G, int grid, hipStream_t st);
+hipError_t launch_attn(const AttnArgs& a, int G, int grid, bool paged, hipStream_t st);
 hipError_t launch_combine(const AttnArgs& a, int G, hipStream_t st);
-hipError_t attn_resident_grid(int G, int n_groups, int* grid);
+hipError_t attn_resident_grid(int G, int n_groups, bool paged, int* grid);
 
 }  // namespace tactic

@@ -102,6 +102,55 @@ def decode_params(target_frac: float = 0.9, **kw) -> C.DecodeParams:
     return p
 
 
+class PagedCache:
+    """A paged K/V cache (see tactic_paged_kv): K_pages, V_pages bf16
+    [num_pages][Hkv][page_size][128], page_table int32 [B][max_pages], and
+    optionally perm int32 [Hkv][total] mapping cluster-sorted rows to tokens."""
+
+    def __init__(self, K_pages: torch.Tensor, V_pages: torch.Tensor, page_table: torch.Tensor,
+                 perm: Optional[torch.Tensor] = None):
+        _check_tensor(K_pages, "K_pages", torch.bfloat16)
+        _check_tensor(V_pages, "V_pages", torch.bfloat16, tuple(K_pages.shape))
+        _check_tensor(page_table, "page_table", torch.int32)
+        if perm is not None:
+            _check_tensor(perm, "perm", torch.int32)
+        self.K_pages, self.V_pages, self.page_table, self.perm = K_pages, V_pages, page_table, perm
+        self.num_pages, _, self.page_size, _ = K_pages.shape
+        self.max_pages = page_table.shape[1]
+
+    @staticmethod
+    def from_token_order(K: torch.Tensor, V: torch.Tensor, batch: RaggedBatch, page_size: int,
+                         page_order: Optional[torch.Tensor] = None, perm: Optional[torch.Tensor] = None
+                         ) -> "PagedCache":
+        """Pages holding K, V [Hkv][total][128] (token order per sequence), placed
+        at the page ids `page_order` gives (default: in order)."""
+        B, Hkv = batch.batch, batch.n_kv_heads
+        lens = [int(batch.kv_indptr_host[b + 1] - batch.kv_indptr_host[b]) for b in range(B)]
+        npg = [(n + page_size - 1) // page_size for n in lens]
+        max_pages = max(1, max(npg) if npg else 1)
+        total_pages = max(1, sum(npg))
+        ids = torch.arange(total_pages, dtype=torch.int64) if page_order is None else page_order.cpu().long()
+        table = torch.zeros(B, max_pages, dtype=torch.int32)
+        Kp = torch.zeros(total_pages, Hkv, page_size, 128, dtype=torch.bfloat16, device=K.device)
+        Vp = torch.zeros_like(Kp)
+        nxt = 0
+        for b in range(B):
+            s0 = int(batch.kv_indptr_host[b])
+            for i in range(npg[b]):
+                pid = int(ids[nxt])
+                nxt += 1
+                table[b, i] = pid
+                t0, t1 = s0 + i * page_size, min(s0 + lens[b], s0 + (i + 1) * page_size)
+                Kp[pid, :, :t1 - t0] = K[:, t0:t1]
+                Vp[pid, :, :t1 - t0] = V[:, t0:t1]
+        return PagedCache(Kp, Vp, table.to(K.device), perm)
+
+    def struct(self) -> C.PagedKV:
+        return C.PagedKV(self.K_pages.data_ptr(), self.V_pages.data_ptr(), self.page_table.data_ptr(),
+                         None if self.perm is None else self.perm.data_ptr(), int(self.page_size),
+                         int(self.max_pages), int(self.num_pages))
+
+
 class SparseDecoder:
     """Tactic's decode for one batch shape: holds the launch plan and the
     workspace, so repeated calls (layers, decode steps) allocate nothing."""
@@ -143,6 +192,29 @@ class SparseDecoder:
             ctypes.byref(meta), ctypes.byref(self.params), ctypes.byref(self.plan), out.data_ptr(),
             sel_q.data_ptr(), sel_kv.data_ptr(), self.workspace.data_ptr(), self.workspace.numel(),
             _stream(stream)), "tactic_sparse_decode")
+        return out, sel_q, sel_kv
+
+    def paged(self, q: torch.Tensor, cache: PagedCache, clusters: ClusterSet, target_frac: Optional[float] = None,
+              stream=None, out=None, sel_q=None, sel_kv=None):
+        """The same decode over a paged cache (tactic_sparse_decode_paged)."""
+        b = self.batch
+        _check_tensor(q, "q", torch.bfloat16, (b.batch, b.n_q_heads, 128))
+        if clusters.n_clusters != self.n_clusters:
+            raise ValueError("cluster counts differ from the ones the decoder was planned for")
+        if cache.perm is not None:
+            _check_tensor(cache.perm, "perm", torch.int32, (b.n_kv_heads, b.total))
+        out = self.out if out is None else out
+        sel_q = self.sel_q if sel_q is None else sel_q
+        sel_kv = self.sel_kv if sel_kv is None else sel_kv
+        if target_frac is not None:
+            self.params.target_frac = float(target_frac)
+        meta = clusters.struct()
+        kv = cache.struct()
+        C.check(C.lib().tactic_sparse_decode_paged(
+            q.data_ptr(), ctypes.byref(kv), ctypes.byref(self._shape), ctypes.byref(meta),
+            ctypes.byref(self.params), ctypes.byref(self.plan), out.data_ptr(), sel_q.data_ptr(),
+            sel_kv.data_ptr(), self.workspace.data_ptr(), self.workspace.numel(), _stream(stream)),
+            "tactic_sparse_decode_paged")
         return out, sel_q, sel_kv
 
     def view(self) -> dict:
@@ -192,6 +264,18 @@ class DenseDecoder:
         C.check(C.lib().tactic_dense_decode(q.data_ptr(), K.data_ptr(), V.data_ptr(), ctypes.byref(self._shape),
                                             out.data_ptr(), self.workspace.data_ptr(), self.workspace.numel(),
                                             _stream(stream)), "tactic_dense_decode")
+        return out
+
+    def paged(self, q: torch.Tensor, cache: PagedCache, stream=None, out=None):
+        """Dense decode over a paged cache (tactic_dense_decode_paged)."""
+        b = self.batch
+        _check_tensor(q, "q", torch.bfloat16, (b.batch, b.n_q_heads, 128))
+        out = self.out if out is None else out
+        kv = cache.struct()
+        C.check(C.lib().tactic_dense_decode_paged(q.data_ptr(), ctypes.byref(kv), ctypes.byref(self._shape),
+                                                  out.data_ptr(), self.workspace.data_ptr(),
+                                                  self.workspace.numel(), _stream(stream)),
+                "tactic_dense_decode_paged")
         return out
 
 

@@ -316,3 +316,41 @@ def test_spare_room_layout_matches_packed_layout():
     d2 = T.DenseDecoder(spaced)(q, spread(inp.K), spread(inp.V))
     torch.cuda.synchronize()
     assert torch.allclose(d1, d2, atol=1e-5, rtol=0)
+
+
+@pytest.mark.parametrize("page_size", [16, 1, 64])
+def test_paged_cache_matches_cluster_sorted_copy(page_size):
+    """Decode from a paged cache in token order (cluster order reached through
+    perm, pages scattered at random) and from pages already in cluster order:
+    the same rows in the same order as the cluster-sorted copy, so the same
+    bits.  Includes recent tokens past the clusters and an empty sequence."""
+    T = _tactic()
+    wl = _small("ctx32k_llama8b", [2100, 0, 900, 1337])
+    inp = synth.make_layer(wl, 0)
+    tail = [50, 0, 0, 137]
+    lay = synth.label_layout(inp, tail=tail)
+    lens = list(wl.seq_lens)
+    ncl = [int(lay.cl_indptr[i + 1] - lay.cl_indptr[i]) for i in range(len(lens))]
+    batch = T.RaggedBatch(lens, wl.n_q_heads, wl.n_kv_heads)
+    g = torch.Generator().manual_seed(page_size)
+    npg = sum((n + page_size - 1) // page_size for n in lens)
+    scattered = torch.randperm(npg, generator=g)
+    q = inp.q.to(DEV)
+    K, V, Ks, Vs = (x.to(DEV) for x in (inp.K, inp.V, lay.K_sorted, lay.V_sorted))
+    perm = lay.perm.to(DEV).contiguous()
+    token_pages = T.PagedCache.from_token_order(K, V, batch, page_size, page_order=scattered, perm=perm)
+    sorted_pages = T.PagedCache.from_token_order(Ks, Vs, batch, page_size)
+    cl = T.ClusterSet(lay.centroids.to(DEV), lay.offsets.to(DEV), ncl)
+    for P in (0.5, 0.95):
+        dec = T.SparseDecoder(batch, ncl, T.decode_params(P, max_tail=256))
+        ref = [x.clone() for x in dec(q, Ks, Vs, cl)]
+        for pages in (token_pages, sorted_pages):
+            got = dec.paged(q, pages, cl)
+            torch.cuda.synchronize()
+            for a, b in zip(ref, got):
+                assert torch.equal(a, b)
+    den = T.DenseDecoder(batch)
+    d_ref = den(q, K, V).clone()
+    d_pg = den.paged(q, token_pages)
+    torch.cuda.synchronize()
+    assert torch.equal(d_ref, d_pg)
