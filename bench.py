@@ -78,6 +78,7 @@ def parse():
     ap.add_argument("--cpu-groups", type=int, default=4, help="(b, g) groups the CPU oracle times")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-ablation", action="store_true", help="skip the per-head (no-union) comparison")
+    ap.add_argument("--no-paged", action="store_true", help="skip the paged-cache comparison")
     ap.add_argument("--calibrate", action="store_true",
                     help="also run a plain 1 GiB device copy (reference dispatch for HBM counters)")
     return ap.parse_args()
@@ -105,6 +106,8 @@ def main():
 
     # ---------------------------------------------------------------- inputs + clustering
     qs, Ks, Vs, cls = [], [], [], []
+    keep = 0 if args.no_paged else min(layers, 4)  # layers whose token-order K/V the paged run needs
+    K_tok, V_tok, perms = [], [], []
     kmeans_ms = 0.0
     builder = T.ClusterBuilder(batch, ncl, max_iters=wl.kmeans_iters) if args.clusters == "kmeans" else None
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -122,6 +125,10 @@ def main():
             Ks.append(cb.K_sorted)
             Vs.append(cb.V_sorted)
             cls.append(cb.clusters)
+            if l < keep:
+                K_tok.append(inp.K)
+                V_tok.append(inp.V)
+                perms.append(cb.perm)
             del cb
         else:
             lay = synth.label_layout(inp)
@@ -129,6 +136,10 @@ def main():
             Ks.append(lay.K_sorted)
             Vs.append(lay.V_sorted)
             cls.append(T.ClusterSet(lay.centroids, lay.offsets, ncl))
+            if l < keep:
+                K_tok.append(inp.K)
+                V_tok.append(inp.V)
+                perms.append(lay.perm)
             del lay
         del inp
         if l % 4 == 3 or l == layers - 1:
@@ -182,15 +193,16 @@ def main():
     from paper_2502_12216_amd import _capi as C
     arr = (ctypes.c_void_p * (NS + 1))(*[e.cuda_event for e in stage_ev])
 
-    def stage_times(decoder):
+    def stage_times(decoder, call=None, n_layers=None):
         """Mean per-kernel milliseconds over args.steps passes of every layer, from
         events the library records between its launches on the decode stream."""
+        call = call or (lambda l: decoder(qs[l], Ks[l], Vs[l], cls[l]))
         C.check(C.lib().tactic_sparse_decode_plan_set_events(ctypes.byref(decoder.plan), arr), "set_events")
         acc = np.zeros(NS)
         nrep = 0
         for _ in range(args.steps):
-            for l in range(layers):
-                decoder(qs[l], Ks[l], Vs[l], cls[l])
+            for l in range(n_layers or layers):
+                call(l)
                 torch.cuda.synchronize()
                 for i in range(NS):
                     acc[i] += stage_ev[i].elapsed_time(stage_ev[i + 1])
@@ -226,6 +238,49 @@ def main():
                     "kv_rows_per_head_over_union": round(rows_ph / max(1, rows_un), 3)}
         del dec_ph
         log(f"per-head step {ms_ph:.3f} ms")
+
+    # ---------------------------------------------------------------- paged cache (Sec. 4.6)
+    paged = None
+    if keep:
+        PS = 16
+        g_pages = torch.Generator().manual_seed(11)
+        pcs = []
+        for l in range(keep):
+            npg = sum((n + PS - 1) // PS for n in wl.seq_lens)
+            pcs.append(T.PagedCache.from_token_order(K_tok[l], V_tok[l], batch, PS,
+                                                     page_order=torch.randperm(npg, generator=g_pages),
+                                                     perm=perms[l].contiguous()))
+        del K_tok, V_tok
+
+        def contiguous_part():
+            for l in range(keep):
+                dec(qs[l], Ks[l], Vs[l], cls[l])
+
+        def paged_part():
+            for l in range(keep):
+                dec.paged(qs[l], pcs[l], cls[l])
+
+        paged_part()
+        ms_c = timed(contiguous_part, args.steps)
+        ms_p = timed(paged_part, args.steps)
+        st_c = stage_times(dec, n_layers=keep)
+        st_p = stage_times(dec, call=lambda l: dec.paged(qs[l], pcs[l], cls[l]), n_layers=keep)
+        ub = []
+        for l in range(keep):
+            _, _, skv = dec(qs[l], Ks[l], Vs[l], cls[l])
+            ub.append(float(skv.sum()) * 512)
+        ub = float(np.mean(ub))
+        paged = {"page_size": PS, "layers": keep, "placement": "pages in token order at random page ids, "
+                 "cluster order through perm",
+                 "sparse_us_per_layer": round(ms_p * 1000 / keep, 2),
+                 "sparse_us_per_layer_cluster_sorted": round(ms_c * 1000 / keep, 2),
+                 "attn_us": round(float(st_p[4]) * 1000, 2), "attn_us_cluster_sorted": round(float(st_c[4]) * 1000, 2),
+                 "sample_us": round(float(st_p[2]) * 1000, 2),
+                 "sample_us_cluster_sorted": round(float(st_c[2]) * 1000, 2),
+                 "attn_gbps": round(ub / (float(st_p[4]) * 1e6), 1),
+                 "attn_gbps_cluster_sorted": round(ub / (float(st_c[4]) * 1e6), 1)}
+        del pcs
+        log(f"paged step ({keep} layers) {ms_p:.3f} ms vs {ms_c:.3f} ms cluster-sorted")
 
     # ---------------------------------------------------------------- selection statistics, bytes
     sel_q, sel_kv, samples = [], [], []
@@ -330,6 +385,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "union_ablation": ablation,
+        "paged_kv": paged,
     }
     if args.clusters == "kmeans":
         res["kmeans"] = {"seconds_all_layers": round(kmeans_ms / 1000, 3), "layers": layers,

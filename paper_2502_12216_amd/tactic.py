@@ -125,24 +125,28 @@ class PagedCache:
         """Pages holding K, V [Hkv][total][128] (token order per sequence), placed
         at the page ids `page_order` gives (default: in order)."""
         B, Hkv = batch.batch, batch.n_kv_heads
-        lens = [int(batch.kv_indptr_host[b + 1] - batch.kv_indptr_host[b]) for b in range(B)]
+        lens = ([int(batch.kv_indptr_host[b + 1] - batch.kv_indptr_host[b]) for b in range(B)]
+                if batch.seq_len is None else list(batch.seq_lens))
         npg = [(n + page_size - 1) // page_size for n in lens]
         max_pages = max(1, max(npg) if npg else 1)
         total_pages = max(1, sum(npg))
-        ids = torch.arange(total_pages, dtype=torch.int64) if page_order is None else page_order.cpu().long()
-        table = torch.zeros(B, max_pages, dtype=torch.int32)
+        ids = (torch.arange(total_pages, dtype=torch.int64) if page_order is None
+               else page_order.cpu().long()).to(K.device)
+        table = torch.zeros(B, max_pages, dtype=torch.int32, device=K.device)
         Kp = torch.zeros(total_pages, Hkv, page_size, 128, dtype=torch.bfloat16, device=K.device)
         Vp = torch.zeros_like(Kp)
         nxt = 0
         for b in range(B):
-            s0 = int(batch.kv_indptr_host[b])
-            for i in range(npg[b]):
-                pid = int(ids[nxt])
-                nxt += 1
-                table[b, i] = pid
-                t0, t1 = s0 + i * page_size, min(s0 + lens[b], s0 + (i + 1) * page_size)
-                Kp[pid, :, :t1 - t0] = K[:, t0:t1]
-                Vp[pid, :, :t1 - t0] = V[:, t0:t1]
+            if npg[b] == 0:
+                continue
+            s0, n = int(batch.kv_indptr_host[b]), lens[b]
+            pid = ids[nxt:nxt + npg[b]]
+            nxt += npg[b]
+            table[b, :npg[b]] = pid.to(torch.int32)
+            for X, Xp in ((K, Kp), (V, Vp)):
+                seq = torch.zeros(Hkv, npg[b] * page_size, 128, dtype=X.dtype, device=X.device)
+                seq[:, :n] = X[:, s0:s0 + n]
+                Xp[pid] = seq.view(Hkv, npg[b], page_size, 128).transpose(0, 1)
         return PagedCache(Kp, Vp, table.to(K.device), perm)
 
     def struct(self) -> C.PagedKV:
