@@ -354,3 +354,28 @@ def test_paged_cache_matches_cluster_sorted_copy(page_size):
     d_pg = den.paged(q, token_pages)
     torch.cuda.synchronize()
     assert torch.equal(d_ref, d_pg)
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(8, 8), (8, 4), (16, 2)])
+def test_sparse_other_group_sizes(Hq, Hkv):
+    """Group sizes G = 1 (multi-head), 2 and 8: the kernels' per-group code
+    (head-splitting reduction, per-head broadcasts, union over G heads) for
+    every G they support, in union and per-head modes, with a recent tail."""
+    import dataclasses
+    T = _tactic()
+    base = _small("ctx32k_llama8b", [1500, 640])
+    wl = dataclasses.replace(base, n_q_heads=Hq, n_kv_heads=Hkv, name=f"{base.name}_h{Hq}x{Hkv}")
+    inp = synth.make_layer(wl, 0)
+    lay = synth.label_layout(inp, tail=[40, 0])
+    for union in (1, 0):
+        for P in (0.6, 0.95):
+            res = run_sparse(inp, lay, P, T.decode_params(P, use_union=union, max_tail=64))
+            check_layer(inp, lay, P, res, label=f"G={Hq // Hkv} union={union} P={P}")
+    den = T.DenseDecoder(T.RaggedBatch(list(wl.seq_lens), Hq, Hkv))
+    out = den(inp.q.to(DEV), lay.K_sorted.to(DEV), lay.V_sorted.to(DEV)).cpu()
+    for b in range(len(wl.seq_lens)):
+        s0, s1 = int(inp.kv_indptr[b]), int(inp.kv_indptr[b + 1])
+        for h in range(Hq):
+            g = h // (Hq // Hkv)
+            ref = OA.dense_attention(np64(inp.q[b, h]), np64(lay.K_sorted[g, s0:s1]), np64(lay.V_sorted[g, s0:s1]))
+            assert float(np.max(np.abs(np64(out[b, h]) - ref))) <= 2e-3
