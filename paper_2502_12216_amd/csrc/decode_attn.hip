@@ -33,6 +33,16 @@ __device__ __forceinline__ int64_t group_tokens(const AttnArgs& a, int bg) {
   return (int64_t)a.gmeta[bg * 4 + 1];
 }
 
+// The attention splits "units" evenly over its workgroups: a group's tokens
+// plus kSegmentCost units standing for the fixed work of a group segment
+// (query load, range lookup, merge, partial store; about the time of 96
+// streamed tokens), so a workgroup that straddles groups gets fewer tokens.
+constexpr int64_t kSegmentCost = 96;
+__device__ __forceinline__ int64_t split_units(const AttnArgs& a, int bg) {
+  const int64_t n = group_tokens(a, bg);
+  return n > 0 ? n + kSegmentCost : 0;
+}
+
 __device__ __forceinline__ void load_words(const uint16_t* p, uint32_t* w) {
   const uint4 v = load_stream16(p);
   w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
@@ -131,7 +141,7 @@ void attn_splitk_kernel(AttnArgs a) {
   constexpr int GPW = kWave / LPR;        // lane-groups per wave
   constexpr int NG = 4 * GPW;             // lane-groups per workgroup
   constexpr int kTileTok = NG * TOK;      // tokens per workgroup tile
-  extern __shared__ int64_t s_prefix[];  // [B * NV + 1] tokens before each selection group
+  extern __shared__ int64_t s_prefix[];  // [B * NV + 1] split units before each selection group
   // the row table of a sub-range is dead once the merge starts, so the
   // merge's partial sums reuse its storage
   union ItemShared {
@@ -156,12 +166,13 @@ void attn_splitk_kernel(AttnArgs a) {
   const int gid = wave * GPW + grp;
   const int BG = a.B * a.NV;
 
-  // exclusive prefix of the groups' token counts: every thread sums a
-  // contiguous run of groups, then a wave scan and the four wave totals
+  // exclusive prefix of the groups' split units (tokens plus kSegmentCost for
+  // a non-empty group): every thread sums a contiguous run of groups, then a
+  // wave scan and the four wave totals
   {
     const int per = (BG + 255) / 256, g0 = min(BG, tid * per), g1 = min(BG, g0 + per);
     int64_t loc = 0;
-    for (int bg = g0; bg < g1; ++bg) loc += group_tokens(a, bg);
+    for (int bg = g0; bg < g1; ++bg) loc += split_units(a, bg);
     int64_t incl = loc;
     for (int o = 1; o < kWave; o <<= 1) {
       const int64_t y = __shfl_up(incl, o, kWave);
@@ -173,7 +184,7 @@ void attn_splitk_kernel(AttnArgs a) {
     for (int w = 0; w < wave; ++w) run += s_wsum[w];
     for (int bg = g0; bg < g1; ++bg) {
       s_prefix[bg] = run;
-      run += group_tokens(a, bg);
+      run += split_units(a, bg);
     }
     if (tid == 255) s_prefix[BG] = run;
     __syncthreads();
@@ -194,9 +205,11 @@ void attn_splitk_kernel(AttnArgs a) {
   }
 
   for (int bg = bg0; bg < BG && s_prefix[bg] < t1; ++bg) {
-    const int64_t seg_lo = max(t0, s_prefix[bg]) - s_prefix[bg];
-    const int64_t seg_hi = min(t1, s_prefix[bg + 1]) - s_prefix[bg];
-    if (seg_lo >= seg_hi) continue;  // empty group
+    // the group's tokens follow its kSegmentCost units of setup in the split
+    const int64_t first = s_prefix[bg] + kSegmentCost;
+    const int64_t seg_lo = max(t0, first) - first;
+    const int64_t seg_hi = min(t1, s_prefix[bg + 1]) - first;
+    if (seg_lo >= seg_hi) continue;  // no token of this group in the range
     const int b = bg / a.NV, jg = bg % a.NV, kvh = jg / a.kv_div;
     const int64_t kvb = a.kv_indptr[b];
     const int nseq = (int)seq_tokens(a.kv_indptr, a.seq_len, b);
@@ -319,16 +332,28 @@ void attn_splitk_kernel(AttnArgs a) {
           if (i < nr) s_rstart[i] = rst[i];
         }
         __syncthreads();
-        for (int t = tid; t < cnt; t += 256) {
-          const int pos = (int)(p + t);
-          int l2 = 0, h2 = nr - 1;  // largest i with s_rupos[i] <= pos
+        // each thread fills a run of consecutive positions: one binary search for
+        // the run's first position, then a walk along the ranges
+        constexpr int kRun = kMaxChunkTokens / 256;
+        const int t_lo = tid * kRun, t_hi = min(cnt, t_lo + kRun);
+        if (t_lo < t_hi) {
+          const int pos0 = (int)(p + t_lo);
+          int l2 = 0, h2 = nr - 1;  // largest i with s_rupos[i] <= pos0
           while (l2 < h2) {
             const int mid = (l2 + h2 + 1) >> 1;
-            if (s_rupos[mid] <= pos) l2 = mid;
+            if (s_rupos[mid] <= pos0) l2 = mid;
             else h2 = mid - 1;
           }
-          const int row = min(max(s_rstart[l2] + (pos - s_rupos[l2]), 0), nseq - 1);  // clamp: bad meta only
-          s_rows[t] = kPaged ? (int)paged_row(a.pk, a.Hkv, a.total, kvb, b, kvh, row, n_c) : row;
+          int next = l2 + 1 < nr ? s_rupos[l2 + 1] : 0x7fffffff;
+          for (int t = t_lo; t < t_hi; ++t) {
+            const int pos = (int)(p + t);
+            while (pos >= next) {  // the ranges cover positions without gaps
+              ++l2;
+              next = l2 + 1 < nr ? s_rupos[l2 + 1] : 0x7fffffff;
+            }
+            const int row = min(max(s_rstart[l2] + (pos - s_rupos[l2]), 0), nseq - 1);  // clamp: bad meta only
+            s_rows[t] = kPaged ? (int)paged_row(a.pk, a.Hkv, a.total, kvb, b, kvh, row, n_c) : row;
+          }
         }
         __syncthreads();
       }
@@ -444,7 +469,7 @@ __global__ __launch_bounds__(512) void combine_kernel(AttnArgs a) {
     if (slice == 0) out[d] = 0.f;
     return;
   }
-  const int64_t w0 = P0 / share, w1 = (P1 - 1) / share;
+  const int64_t w0 = (P0 + kSegmentCost) / share, w1 = (P1 - 1) / share;
   const int nchunks = (int)(w1 - w0 + 1);
   const float* pb = a.partials + (bg + w0) * kPart;
   float M = -INFINITY, num = 0.f, den = 0.f;
