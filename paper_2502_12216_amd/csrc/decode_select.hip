@@ -165,15 +165,18 @@ __device__ __forceinline__ uint32_t desc_key_bits(float s) {
   return ~ord;
 }
 
-// Monotone non-increasing in s (NaN last): every step below is a correctly
-// rounded operation that is monotone in its input (fp32 subtract and scale by
-// a positive constant, fp64 add, divide and subtract, truncation, clamp).
+// Monotone non-increasing in s (NaN last).  With r = 1 / (1 + |z|) in (0, 1]
+// the bucket is (nb / 2) r for z >= 0 and nb - (nb / 2) r for z < 0, i.e.
+// (1 - u) nb for u = 1/2 + sign(z) (1 - r) / 2.  Every step is monotone in its
+// input: fp32 subtract, scale by a positive constant, absolute value, add,
+// correctly rounded divide, scale by a power of two (exact), subtract from
+// nb, truncation and clamp; the two branches meet at nb / 2.
 __device__ __forceinline__ int squash_bucket(float s, float mu, float inv_sd, int nb) {
   if (!(s == s)) return nb - 1;
-  const double z = (double)((s - mu) * inv_sd);
-  const double t = 1.0 - 1.0 / (1.0 + fabs(z));  // [0, 1), non-decreasing in |z|
-  const double u = z >= 0.0 ? 0.5 + 0.5 * t : 0.5 - 0.5 * t;  // non-decreasing in z
-  const int bk = (int)((1.0 - u) * (double)nb);
+  const float z = (s - mu) * inv_sd;
+  const float half = 0.5f * (float)nb;
+  const float x = half * (1.0f / (1.0f + fabsf(z)));  // (0, nb/2], non-increasing in |z|
+  const int bk = (int)(z >= 0.f ? x : (float)nb - x);
   return min(max(bk, 0), nb - 1);
 }
 
@@ -897,8 +900,43 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
 
 // 3b. Fit of the G heads of a group (one wave each), then the union of their
 //     selections (Sec. 4.5) and the attention work list.  grid B*Hkv, 1024
-//     threads (the first G waves fit); the per-cluster union lengths are
-//     staged in LDS when they fit.
+//     threads (the first G waves fit).  Staged form (G <= 4, Cm <= 8192):
+//     while the first G waves fit, the other waves copy the heads' cluster
+//     ranks (u16) and the cluster offsets to LDS; then every thread takes 8
+//     consecutive clusters and keeps their union lengths and offsets in
+//     registers through the scan and the range list.  Otherwise the union
+//     lengths are staged in LDS (or the output array) between the passes.
+constexpr int kUnionSeg = 8;              // clusters per thread in the staged union
+constexpr int kUnionStagedMax = 8 * 1024;  // clusters of the staged union (kUnionSeg per thread)
+__host__ __device__ inline bool union_staged(int G, int64_t Cm) { return G <= 4 && Cm <= kUnionStagedMax; }
+
+// The group's range list ends with the recent tokens (rows n_c .. n_c + tail
+// - 1, the same for every head of the group) as one more range; then the
+// group's counts.  tot = (cluster ranges << 32) | their tokens.
+__device__ void union_close(const FitArgs& a, int bg, int b, int kvh, int h0, uint64_t tot, int32_t* rstart,
+                            int32_t* rupos, int32_t* cfr) {
+  const int64_t T = kCfrTokens;
+  int R = (int)(tot >> 32);
+  const int64_t U = (int64_t)(tot & 0xffffffffu);
+  int64_t Ut = U;
+  const int32_t* hm0 = a.head_meta + (int64_t)h0 * 16;
+  const int tail = hm0[11];
+  if (tail > 0) {
+    rstart[R] = hm0[0];
+    rupos[R] = (int32_t)U;
+    for (int64_t c = (U + T - 1) / T; c * T < U + tail && c < a.max_chunks; ++c) cfr[c] = R;
+    ++R;
+    Ut += tail;
+  }
+  rupos[R] = (int32_t)Ut;
+  a.gmeta[bg * 4 + 0] = R;
+  a.gmeta[bg * 4 + 1] = (int32_t)Ut;
+  a.gmeta[bg * 4 + 2] = (int32_t)((Ut + T - 1) / T);
+  a.gmeta[bg * 4 + 3] = (int32_t)T;
+  if (a.per_head) atomicAdd(&a.sel_count_kv[b * a.Hkv + kvh], (int32_t)Ut);  // rows loaded per KV head
+  else a.sel_count_kv[bg] = (int32_t)Ut;
+}
+
 template <int G>
 __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -909,13 +947,109 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
   const int bg = blockIdx.x;  // selection group: G query heads reading KV head kvh
   const int b = bg / a.NV, jg = bg % a.NV, kvh = jg / a.kv_div;
   const int h0 = b * a.Hq + jg * G;  // first query head of the group
-  if (wave < G) fit_head_wave(a, h0 + wave, lane, s_cut[wave]);
-  __syncthreads();
-
   const int64_t cb = a.cl_indptr[b];
   const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
   const int32_t* off = a.offsets + (int64_t)kvh * (a.Ct + a.B) + cb + b;
   int32_t* ulen = a.union_len + (int64_t)jg * a.Ct + cb;
+  const int64_t T = kCfrTokens;
+  int32_t* rstart = a.rstart + (int64_t)bg * (a.Cm + 2);
+  int32_t* rupos = a.rupos + (int64_t)bg * (a.Cm + 2);
+  int32_t* cfr = a.cfr + (int64_t)bg * a.max_chunks;
+
+  if (union_staged(G, a.Cm)) {
+    const int Cp = (a.Cm + kUnionSeg - 1) / kUnionSeg * kUnionSeg;
+    uint16_t* s_rk = reinterpret_cast<uint16_t*>(smem_raw);        // [G][Cp]
+    int32_t* s_off = reinterpret_cast<int32_t*>(s_rk + G * Cp);  // [Cp + 1]
+    if (wave < G) {
+      fit_head_wave(a, h0 + wave, lane, s_cut[wave]);
+    } else {
+      // all loads of a thread are issued before its LDS stores
+      constexpr int nw = 1024 - G * kWave;
+      constexpr int kW = (kUnionStagedMax + nw) / nw;  // covers j in [0, C] for C <= kUnionStagedMax
+      const int w = tid - G * kWave;
+      int32_t ov[kW];
+#pragma unroll
+      for (int i = 0; i < kW; ++i) ov[i] = w + i * nw <= C ? off[w + i * nw] : 0;
+      int32_t rv[G][kW];
+#pragma unroll
+      for (int hh = 0; hh < G; ++hh)
+#pragma unroll
+        for (int i = 0; i < kW; ++i)
+          rv[hh][i] = w + i * nw < C ? a.rank_of[(int64_t)(h0 + hh) * a.Cm + w + i * nw] : 0;
+#pragma unroll
+      for (int i = 0; i < kW; ++i)
+        if (w + i * nw <= C) s_off[w + i * nw] = ov[i];
+#pragma unroll
+      for (int hh = 0; hh < G; ++hh)
+#pragma unroll
+        for (int i = 0; i < kW; ++i)
+          if (w + i * nw < C) s_rk[hh * Cp + w + i * nw] = (uint16_t)rv[hh][i];
+    }
+    __syncthreads();
+    // union length of the thread's clusters j0 .. j0 + 7: max over the heads
+    const int j0 = tid * kUnionSeg;
+    int32_t o[kUnionSeg + 1], L[kUnionSeg];
+    uint64_t loc = 0;  // (ranges << 32) | tokens
+    if (j0 < C) {
+#pragma unroll
+      for (int e = 0; e <= kUnionSeg; ++e) o[e] = j0 + e <= C ? s_off[j0 + e] : 0;
+#pragma unroll
+      for (int e = 0; e < kUnionSeg; ++e) L[e] = 0;
+#pragma unroll
+      for (int hh = 0; hh < G; ++hh) {
+        const uint4 rw = *reinterpret_cast<const uint4*>(s_rk + hh * Cp + j0);
+        const uint32_t r2[4] = {rw.x, rw.y, rw.z, rw.w};
+#pragma unroll
+        for (int e = 0; e < kUnionSeg; ++e) {
+          const int r = (int)((r2[e >> 1] >> (16 * (e & 1))) & 0xffffu);
+          const int size = o[e + 1] - o[e];
+          const int len = r < s_cut[hh][0] ? size : (r == s_cut[hh][0] ? s_cut[hh][1] : 0);
+          L[e] = max(L[e], len);
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < kUnionSeg; ++e) {
+        if (j0 + e < C) {
+          ulen[j0 + e] = L[e];
+          if (L[e] > 0) loc += (1ull << 32) | (uint64_t)L[e];
+        } else {
+          L[e] = 0;
+        }
+      }
+    }
+    uint64_t incl = loc;
+    for (int o2 = 1; o2 < kWave; o2 <<= 1) {
+      const uint64_t y = __shfl_up(incl, o2, kWave);
+      if (lane >= o2) incl += y;
+    }
+    if (lane == kWave - 1) s_wave_u[wave] = incl;
+    __syncthreads();
+    uint64_t base = incl - loc, tot = 0;
+    for (int w = 0; w < 16; ++w) {
+      const uint64_t t = s_wave_u[w];
+      if (w < wave) base += t;
+      tot += t;
+    }
+    if (j0 < C) {
+      int idx = (int)(base >> 32);
+      int64_t upos = (int64_t)(base & 0xffffffffu);
+#pragma unroll
+      for (int e = 0; e < kUnionSeg; ++e) {
+        if (L[e] > 0) {
+          rstart[idx] = o[e];
+          rupos[idx] = (int32_t)upos;
+          for (int64_t c = (upos + T - 1) / T; c * T < upos + L[e] && c < a.max_chunks; ++c) cfr[c] = idx;
+          ++idx;
+          upos += L[e];
+        }
+      }
+    }
+    if (tid == 0) union_close(a, bg, b, kvh, h0, tot, rstart, rupos, cfr);
+    return;
+  }
+
+  if (wave < G) fit_head_wave(a, h0 + wave, lane, s_cut[wave]);
+  __syncthreads();
   int32_t* Ls = a.Cm <= kUnionLdsMax ? reinterpret_cast<int32_t*>(smem_raw) : ulen;
   // pass 1 (coalesced): selected prefix length of every cluster = max over heads
 #pragma unroll 4
@@ -959,14 +1093,9 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
   __syncthreads();
   const uint64_t base = s_wave_u[wave] + incl - loc;
   const uint64_t tot = s_wave_u[16];
-  const int64_t U = (int64_t)(tot & 0xffffffffu);
   // position -> range index of the union, one entry per kCfrTokens positions
-  const int64_t T = kCfrTokens;
   int idx = (int)(base >> 32);
   int64_t upos = (int64_t)(base & 0xffffffffu);
-  int32_t* rstart = a.rstart + (int64_t)bg * (a.Cm + 2);
-  int32_t* rupos = a.rupos + (int64_t)bg * (a.Cm + 2);
-  int32_t* cfr = a.cfr + (int64_t)bg * a.max_chunks;
   for (int j = beg; j < end; ++j) {
     const int L = Ls[j];
     if (L <= 0) continue;
@@ -976,28 +1105,7 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
     ++idx;
     upos += L;
   }
-  if (tid == 0) {
-    int R = (int)(tot >> 32);
-    int64_t Ut = U;
-    // the recent tokens (rows n_c .. n_c + tail - 1, the same for every head of
-    // the group) close the list as one more range
-    const int32_t* hm0 = a.head_meta + (int64_t)h0 * 16;
-    const int tail = hm0[11];
-    if (tail > 0) {
-      rstart[R] = hm0[0];
-      rupos[R] = (int32_t)U;
-      for (int64_t c = (U + T - 1) / T; c * T < U + tail && c < a.max_chunks; ++c) cfr[c] = R;
-      ++R;
-      Ut += tail;
-    }
-    rupos[R] = (int32_t)Ut;
-    a.gmeta[bg * 4 + 0] = R;
-    a.gmeta[bg * 4 + 1] = (int32_t)Ut;
-    a.gmeta[bg * 4 + 2] = (int32_t)((Ut + T - 1) / T);
-    a.gmeta[bg * 4 + 3] = (int32_t)T;
-    if (a.per_head) atomicAdd(&a.sel_count_kv[b * a.Hkv + kvh], (int32_t)Ut);  // rows loaded per KV head
-    else a.sel_count_kv[bg] = (int32_t)Ut;
-  }
+  if (tid == 0) union_close(a, bg, b, kvh, h0, tot, rstart, rupos, cfr);
 }
 
 // ============================================================================
@@ -1032,7 +1140,9 @@ hipError_t launch_sample(const FitArgs& a, int split, int n_heads, bool paged, h
 }
 
 hipError_t launch_fit_union(const FitArgs& a, int G, int n_groups, hipStream_t st) {
-  const size_t lds = a.Cm <= kUnionLdsMax ? (size_t)a.Cm * 4 : 0;
+  const int64_t Cp = (a.Cm + kUnionSeg - 1) / kUnionSeg * kUnionSeg;
+  const size_t lds = union_staged(G, a.Cm) ? (size_t)(G * Cp * 2 + (Cp + 1) * 4)
+                                           : (a.Cm <= kUnionLdsMax ? (size_t)a.Cm * 4 : 0);
   switch (G) {
     case 1: hipLaunchKernelGGL(fit_union_kernel<1>, dim3(n_groups), dim3(1024), lds, st, a); break;
     case 2: hipLaunchKernelGGL(fit_union_kernel<2>, dim3(n_groups), dim3(1024), lds, st, a); break;

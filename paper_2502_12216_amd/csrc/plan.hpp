@@ -19,7 +19,10 @@ constexpr int kFitFields = 16;
 constexpr int kStageEvents = 7;        // start + after each of the six decode kernels
 constexpr int kUnionLdsMax = 32768;     // clusters whose union lengths are staged in LDS
 constexpr int kScoreRows = 128;        // centroids per scoring workgroup
-constexpr int kSampleChunk = 128;      // sampled rows per sampling workgroup
+#ifndef TACTIC_SAMPLE_CHUNK
+#define TACTIC_SAMPLE_CHUNK 128
+#endif
+constexpr int kSampleChunk = TACTIC_SAMPLE_CHUNK;  // sampled rows per sampling workgroup
 
 struct DecodePlan {
   int64_t magic;
