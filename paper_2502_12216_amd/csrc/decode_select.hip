@@ -731,10 +731,18 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
   const int32_t* hm = a.head_meta + (int64_t)bh * 16;
   const double* lg = a.logits + (int64_t)bh * a.S_cap;
   const double* lse = a.lse + (int64_t)bh * a.split * (2 * kRg);
-  // the partials of the first 64 chunks load together with the head's metadata
+  // the partials of the first 64 chunks, the first chunk's logits and the
+  // first 64 rank-prefix entries load together with the head's metadata (a
+  // small budget ends in the first chunk and the first clusters)
   double pre[2 * kRg];
 #pragma unroll
   for (int i = 0; i < 2 * kRg; ++i) pre[i] = lane < a.split ? lse[lane * 2 * kRg + i] : 0.0;
+  constexpr int kLg0 = kSampleChunk / kWave;
+  double lg0[kLg0];
+#pragma unroll
+  for (int i = 0; i < kLg0; ++i) lg0[i] = i * kWave + lane < a.S_cap ? lg[i * kWave + lane] : 0.0;
+  const int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
+  const int rp0 = lane <= a.Cm ? rpre[lane] : 0;
   const int n = hm[0];          // clustered tokens (the list of Algorithm 1)
   const int64_t S = hm[9];      // sampled rows, the recent tokens included
   const int tail = hm[11];      // recent tokens, all selected
@@ -804,8 +812,9 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
         int cstar = nhc - 1;
         for (int c0 = 0; c0 < nhc; c0 += kWave) {
           const int c = c0 + lane;
-          const double mc = c < nhc ? lse[(c * kRg) * 2] : -INFINITY;
-          const double v = (c < nhc && mc != -INFINITY) ? lse[(c * kRg) * 2 + 1] * exp(mc - m) : 0.0;
+          const double mc = c < nhc ? (c0 == 0 ? pre[0] : lse[(c * kRg) * 2]) : -INFINITY;
+          const double sc = c0 == 0 ? pre[1] : (c < nhc ? lse[(c * kRg) * 2 + 1] : 0.0);
+          const double v = (c < nhc && mc != -INFINITY) ? sc * exp(mc - m) : 0.0;
           double incl = v;
           for (int o = 1; o < kWave; o <<= 1) {
             const double y = __shfl_up(incl, o, kWave);
@@ -825,7 +834,15 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
         double run = base;
         for (int64_t v0 = ub; v0 < ue && cand == 0x7fffffff; v0 += kWave) {
           const int64_t u = v0 + lane;
-          const double e = u < ue ? exp(lg[u] - m) : 0.0;
+          double lu = 0.0;
+          if (cstar == 0) {
+#pragma unroll
+            for (int i = 0; i < kLg0; ++i)
+              if (v0 == i * kWave) lu = lg0[i];
+          } else if (u < ue) {
+            lu = lg[u];
+          }
+          const double e = u < ue ? exp(lu - m) : 0.0;
           double incl = e;
           for (int o = 1; o < kWave; o <<= 1) {
             const double y = __shfl_up(incl, o, kWave);
@@ -871,8 +888,15 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
   int cut_r = -1, cut_len = 0;
   if (k > 0) {
     const int C = hm[10];
-    const int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
     int lo = 0, hi = C, vlo = 0;
+    // the first 64 entries settle it when prefix[63] >= k or C <= 63
+    const int v63 = __shfl(rp0, kWave - 1, kWave);
+    if (C <= kWave - 1 || v63 >= k) {
+      const uint64_t ok = __ballot(lane <= C && rp0 < k);
+      const int j = 63 - __clzll((long long)ok);
+      vlo = __shfl(rp0, j, kWave);
+      lo = hi = j;
+    }
     while (lo < hi) {
       const int step = (hi - lo + kWave) / kWave;
       const int cand = lo + lane * step;
@@ -947,10 +971,6 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
   const int bg = blockIdx.x;  // selection group: G query heads reading KV head kvh
   const int b = bg / a.NV, jg = bg % a.NV, kvh = jg / a.kv_div;
   const int h0 = b * a.Hq + jg * G;  // first query head of the group
-  const int64_t cb = a.cl_indptr[b];
-  const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
-  const int32_t* off = a.offsets + (int64_t)kvh * (a.Ct + a.B) + cb + b;
-  int32_t* ulen = a.union_len + (int64_t)jg * a.Ct + cb;
   const int64_t T = kCfrTokens;
   int32_t* rstart = a.rstart + (int64_t)bg * (a.Cm + 2);
   int32_t* rupos = a.rupos + (int64_t)bg * (a.Cm + 2);
@@ -960,9 +980,13 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
     const int Cp = (a.Cm + kUnionSeg - 1) / kUnionSeg * kUnionSeg;
     uint16_t* s_rk = reinterpret_cast<uint16_t*>(smem_raw);        // [G][Cp]
     int32_t* s_off = reinterpret_cast<int32_t*>(s_rk + G * Cp);  // [Cp + 1]
+    int32_t* s_L = s_off + Cp + 4;                                // [Cp]: union lengths (16-byte aligned)
     if (wave < G) {
       fit_head_wave(a, h0 + wave, lane, s_cut[wave]);
     } else {
+      const int64_t cb = a.cl_indptr[b];
+      const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
+      const int32_t* off = a.offsets + (int64_t)kvh * (a.Ct + a.B) + cb + b;
       // all loads of a thread are issued before its LDS stores
       constexpr int nw = 1024 - G * kWave;
       constexpr int kW = (kUnionStagedMax + nw) / nw;  // covers j in [0, C] for C <= kUnionStagedMax
@@ -986,36 +1010,54 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
           if (w + i * nw < C) s_rk[hh * Cp + w + i * nw] = (uint16_t)rv[hh][i];
     }
     __syncthreads();
-    // union length of the thread's clusters j0 .. j0 + 7: max over the heads
+    const int64_t cb = a.cl_indptr[b];
+    const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
+    int32_t* ulen = a.union_len + (int64_t)jg * a.Ct + cb;
+    // union length of the thread's clusters j0 .. j0 + 7: the whole cluster
+    // when some head ranks it before its cut (rank - cut < 0), the largest
+    // cut length among the heads whose cut cluster it is (rank - cut = 0)
     const int j0 = tid * kUnionSeg;
     int32_t o[kUnionSeg + 1], L[kUnionSeg];
     uint64_t loc = 0;  // (ranges << 32) | tokens
     if (j0 < C) {
+      {  // two 16-byte LDS reads (j0 is a multiple of 8) and the next thread's first entry
+        const int4 x = *reinterpret_cast<const int4*>(s_off + j0);
+        const int4 y = *reinterpret_cast<const int4*>(s_off + j0 + 4);
+        o[0] = x.x; o[1] = x.y; o[2] = x.z; o[3] = x.w;
+        o[4] = y.x; o[5] = y.y; o[6] = y.z; o[7] = y.w;
+      }
+      o[kUnionSeg] = j0 + kUnionSeg <= C ? s_off[j0 + kUnionSeg] : 0;
+      int dmin[kUnionSeg];
 #pragma unroll
-      for (int e = 0; e <= kUnionSeg; ++e) o[e] = j0 + e <= C ? s_off[j0 + e] : 0;
-#pragma unroll
-      for (int e = 0; e < kUnionSeg; ++e) L[e] = 0;
+      for (int e = 0; e < kUnionSeg; ++e) dmin[e] = 0x7fffffff;
 #pragma unroll
       for (int hh = 0; hh < G; ++hh) {
         const uint4 rw = *reinterpret_cast<const uint4*>(s_rk + hh * Cp + j0);
         const uint32_t r2[4] = {rw.x, rw.y, rw.z, rw.w};
+        const int c0 = s_cut[hh][0];
 #pragma unroll
-        for (int e = 0; e < kUnionSeg; ++e) {
-          const int r = (int)((r2[e >> 1] >> (16 * (e & 1))) & 0xffffu);
-          const int size = o[e + 1] - o[e];
-          const int len = r < s_cut[hh][0] ? size : (r == s_cut[hh][0] ? s_cut[hh][1] : 0);
-          L[e] = max(L[e], len);
+        for (int e = 0; e < kUnionSeg; ++e)
+          dmin[e] = min(dmin[e], (int)((r2[e >> 1] >> (16 * (e & 1))) & 0xffffu) - c0);
+      }
+#pragma unroll
+      for (int e = 0; e < kUnionSeg; ++e) {
+        L[e] = dmin[e] < 0 ? o[e + 1] - o[e] : 0;
+        if (dmin[e] == 0) {  // some head's cut cluster (at most G per group)
+          for (int hh = 0; hh < G; ++hh)
+            if ((int)s_rk[hh * Cp + j0 + e] == s_cut[hh][0]) L[e] = max(L[e], s_cut[hh][1]);
         }
       }
 #pragma unroll
       for (int e = 0; e < kUnionSeg; ++e) {
         if (j0 + e < C) {
-          ulen[j0 + e] = L[e];
           if (L[e] > 0) loc += (1ull << 32) | (uint64_t)L[e];
         } else {
           L[e] = 0;
         }
       }
+      // the lengths go out through LDS so that the global stores are contiguous
+      *reinterpret_cast<int4*>(s_L + j0) = make_int4(L[0], L[1], L[2], L[3]);
+      *reinterpret_cast<int4*>(s_L + j0 + 4) = make_int4(L[4], L[5], L[6], L[7]);
     }
     uint64_t incl = loc;
     for (int o2 = 1; o2 < kWave; o2 <<= 1) {
@@ -1030,6 +1072,9 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
       if (w < wave) base += t;
       tot += t;
     }
+#pragma unroll
+    for (int i = 0; i < kUnionSeg; ++i)
+      if (tid + i * 1024 < C) ulen[tid + i * 1024] = s_L[tid + i * 1024];
     if (j0 < C) {
       int idx = (int)(base >> 32);
       int64_t upos = (int64_t)(base & 0xffffffffu);
@@ -1050,6 +1095,10 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
 
   if (wave < G) fit_head_wave(a, h0 + wave, lane, s_cut[wave]);
   __syncthreads();
+  const int64_t cb = a.cl_indptr[b];
+  const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
+  const int32_t* off = a.offsets + (int64_t)kvh * (a.Ct + a.B) + cb + b;
+  int32_t* ulen = a.union_len + (int64_t)jg * a.Ct + cb;
   int32_t* Ls = a.Cm <= kUnionLdsMax ? reinterpret_cast<int32_t*>(smem_raw) : ulen;
   // pass 1 (coalesced): selected prefix length of every cluster = max over heads
 #pragma unroll 4
@@ -1141,7 +1190,7 @@ hipError_t launch_sample(const FitArgs& a, int split, int n_heads, bool paged, h
 
 hipError_t launch_fit_union(const FitArgs& a, int G, int n_groups, hipStream_t st) {
   const int64_t Cp = (a.Cm + kUnionSeg - 1) / kUnionSeg * kUnionSeg;
-  const size_t lds = union_staged(G, a.Cm) ? (size_t)(G * Cp * 2 + (Cp + 1) * 4)
+  const size_t lds = union_staged(G, a.Cm) ? (size_t)(G * Cp * 2 + (Cp + 4) * 4 + Cp * 4)
                                            : (a.Cm <= kUnionLdsMax ? (size_t)a.Cm * 4 : 0);
   switch (G) {
     case 1: hipLaunchKernelGGL(fit_union_kernel<1>, dim3(n_groups), dim3(1024), lds, st, a); break;
