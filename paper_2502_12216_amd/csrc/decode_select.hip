@@ -582,13 +582,14 @@ __device__ double tail_sum(double a, double b, int64_t lo, int64_t hi) {
   return a * (harmonic(R) - harmonic(L - 1)) + b * (double)(R - L + 1);
 }
 
-// 3a. Exact logits of the sampled rows, fp64 (products of bf16 values are
-//     exact in fp64).  grid (ceil(S_cap/128), B*Hq), 256 threads: workgroup c
-//     owns samples [128c, 128c + 128); 16 lanes per row, each wave gathers 32
-//     rows with all loads in flight together.  The workgroup also reduces its
-//     logits per region (exact head, window 1, window 2) to (max, sum of
-//     exp(l - max)), so the fit needs one exponential per chunk instead of one
-//     per sample.
+// 3a. Logits of the sampled rows: each lane sums its 8 bf16 products in fp32
+//     (v_dot2, error at most a few ulp of the lane's sum of |products|), the
+//     16 lane sums add in fp64.  grid (ceil(S_cap/128), B*Hq), 256 threads:
+//     workgroup c owns samples [128c, 128c + 128); 16 lanes per row, each wave
+//     gathers 32 rows with all loads in flight together.  The workgroup also
+//     reduces its logits per region (exact head, window 1, window 2, recent
+//     tokens) to (max, sum of exp(l - max)), so the fit needs one exponential
+//     per chunk instead of one per sample.
 // wave-wide fp64 sum / max, identical in every lane: DPP within rows of 16
 // lanes, then two cross-row exchanges
 __device__ __forceinline__ double wave_sum_d(double v) {
@@ -635,16 +636,7 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
 #pragma unroll
   for (int k = 0; k < kR; ++k)
     if (u0 + wave * (kSampleChunk / 4) + k * 4 + grp >= S) r[k] = -1;
-  float qf[8];
-  {
-    const uint4 v = *reinterpret_cast<const uint4*>(a.q + (int64_t)bh * kHeadDim + sl * 8);
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      qf[2 * e] = bf16lo(w[e]);
-      qf[2 * e + 1] = bf16hi(w[e]);
-    }
-  }
+  const uint4 qv = *reinterpret_cast<const uint4*>(a.q + (int64_t)bh * kHeadDim + sl * 8);
   const int64_t kvb = a.kv_indptr[b];
   double* lg = a.logits + (int64_t)bh * a.S_cap;
   int64_t roff[kR];  // row index of every sample in the K array
@@ -663,16 +655,12 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
     kv[k] = roff[k] >= 0 ? load_stream16(a.K + roff[k] * kHeadDim + sl * 8) : make_uint4(0, 0, 0, 0);
 #pragma unroll
   for (int k = 0; k < kR; ++k) {
-    const uint32_t w[4] = {kv[k].x, kv[k].y, kv[k].z, kv[k].w};
-    // a product of two bf16 values has at most 16 significant bits, so it is
-    // exact in fp32 (short of fp32 underflow); the sum runs in fp64
-    double acc = 0.0;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      acc += (double)(qf[2 * e] * bf16lo(w[e]));
-      acc += (double)(qf[2 * e + 1] * bf16hi(w[e]));
-    }
-    acc = sum16d(acc) * 0.088388347648318440550;  // 1 / sqrt(128), within 1 ulp of the quotient
+    // the lane's 8 products summed in fp32 (v_dot2), the 16 lane sums in fp64
+    float d = dot2_bf16(kv[k].x, qv.x, 0.f);
+    d = dot2_bf16(kv[k].y, qv.y, d);
+    d = dot2_bf16(kv[k].z, qv.z, d);
+    d = dot2_bf16(kv[k].w, qv.w, d);
+    const double acc = sum16d((double)d) * 0.088388347648318440550;  // 1 / sqrt(128), within 1 ulp of the quotient
     const int t = wave * (kSampleChunk / 4) + k * 4 + grp;
     if (sl == 0) {
       s_lg[t] = acc;
