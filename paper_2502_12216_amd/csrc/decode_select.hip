@@ -121,8 +121,19 @@ __global__ __launch_bounds__(256) void score_clusters_kernel(ScoreArgs a) {
   const uint16_t* cbase = a.centroids + ((int64_t)g * a.Ct + cb) * kHeadDim + sl * 8;
   float* sc = a.scores + ((int64_t)b * a.Hq + g * G) * a.Cm;
   constexpr int kPerWave = kScoreRows / 4;  // rows per wave, 4 per step
-#pragma unroll 1
-  for (int it0 = 0; it0 < kPerWave / 4; it0 += 4) {
+  constexpr int kSteps = kPerWave / 4;
+  // after sum16 all 16 lanes of a row hold its G scores; lane sl keeps the
+  // score of head sl % G of step sl / G of a window of P steps, and the
+  // window goes out as one store of P * 4 consecutive rows per head
+  constexpr int P = 16 / G;
+  float keep = 0.f;
+  auto flush = [&](int s0, int ns) {
+    const int sp = sl / G, h = sl % G;
+    const int j = j0 + wave * kPerWave + (s0 + sp) * 4 + grp;
+    if (sp < ns && j < C) sc[(int64_t)h * a.Cm + j] = keep;
+  };
+#pragma unroll
+  for (int it0 = 0; it0 < kSteps; it0 += 4) {
     uint4 c[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -131,7 +142,7 @@ __global__ __launch_bounds__(256) void score_clusters_kernel(ScoreArgs a) {
     }
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      const int j = j0 + wave * kPerWave + (it0 + k) * 4 + grp;
+      const int st = it0 + k;
 #pragma unroll
       for (int h = 0; h < G; ++h) {
         float d = dot2_bf16(c[k].x, qw[h][0], 0.f);
@@ -139,8 +150,9 @@ __global__ __launch_bounds__(256) void score_clusters_kernel(ScoreArgs a) {
         d = dot2_bf16(c[k].z, qw[h][2], d);
         d = dot2_bf16(c[k].w, qw[h][3], d);
         d = sum16(d);
-        if (sl == h && j < C) sc[(int64_t)h * a.Cm + j] = d;
+        if (sl == (st % P) * G + h) keep = d;
       }
+      if ((st + 1) % P == 0 || st + 1 == kSteps) flush(st - st % P, st % P + 1);
     }
   }
 }
@@ -662,12 +674,10 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
     d = dot2_bf16(kv[k].w, qv.w, d);
     const double acc = sum16d((double)d) * 0.088388347648318440550;  // 1 / sqrt(128), within 1 ulp of the quotient
     const int t = wave * (kSampleChunk / 4) + k * 4 + grp;
-    if (sl == 0) {
-      s_lg[t] = acc;
-      if (u0 + t < S) lg[u0 + t] = acc;
-    }
+    if (sl == 0) s_lg[t] = acc;
   }
   __syncthreads();
+  if (tid < kSampleChunk && u0 + tid < S) lg[u0 + tid] = s_lg[tid];  // contiguous stores
   // per-region (max, sum exp(l - max)) of this chunk, one sample per lane of
   // the first waves; regions: exact head, window 1, window 2, recent tokens
   const int64_t S_main = hm[12];
