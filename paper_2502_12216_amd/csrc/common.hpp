@@ -124,6 +124,50 @@ __device__ __forceinline__ double sum16d(double v) {
   return v;
 }
 
+// Lane shift / broadcast by DPP with zero fill: lanes whose source lies
+// outside their row (row_shr) or whose row is masked off (row_bcast) get 0.
+template <int CTRL, int RM>
+__device__ __forceinline__ uint32_t dpp_zero(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, RM, 0xF, true);
+}
+template <int CTRL, int RM>
+__device__ __forceinline__ uint64_t dpp_zero(uint64_t v) {
+  return ((uint64_t)dpp_zero<CTRL, RM>((uint32_t)(v >> 32)) << 32) | dpp_zero<CTRL, RM>((uint32_t)v);
+}
+template <int CTRL, int RM>
+__device__ __forceinline__ int dpp_zero(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, RM, 0xF, true);
+}
+template <int CTRL, int RM>
+__device__ __forceinline__ int64_t dpp_zero(int64_t v) {
+  return (int64_t)dpp_zero<CTRL, RM>((uint64_t)v);
+}
+template <int CTRL, int RM>
+__device__ __forceinline__ double dpp_zero(double v) {
+  return __builtin_bit_cast(double, dpp_zero<CTRL, RM>(__builtin_bit_cast(uint64_t, v)));
+}
+
+// Inclusive scan over the 16 lanes of each DPP row (row_shr 1, 2, 4, 8).
+template <typename T>
+__device__ __forceinline__ T row_incl_scan(T v) {
+  v += dpp_zero<0x111, 0xF>(v);
+  v += dpp_zero<0x112, 0xF>(v);
+  v += dpp_zero<0x114, 0xF>(v);
+  v += dpp_zero<0x118, 0xF>(v);
+  return v;
+}
+
+// Inclusive scan over the 64 lanes of a wave without LDS: the row scans, then
+// lane 15 of rows 0 and 2 added to rows 1 and 3 (row_bcast:15) and lane 31 to
+// rows 2 and 3 (row_bcast:31).
+template <typename T>
+__device__ __forceinline__ T wave_incl_scan(T v) {
+  v = row_incl_scan(v);
+  v += dpp_zero<0x142, 0xA>(v);
+  v += dpp_zero<0x143, 0xC>(v);
+  return v;
+}
+
 __device__ __forceinline__ float wave_max(float v) {
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
   return v;

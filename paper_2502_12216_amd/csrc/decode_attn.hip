@@ -173,11 +173,7 @@ void attn_splitk_kernel(AttnArgs a) {
     const int per = (BG + 255) / 256, g0 = min(BG, tid * per), g1 = min(BG, g0 + per);
     int64_t loc = 0;
     for (int bg = g0; bg < g1; ++bg) loc += split_units(a, bg);
-    int64_t incl = loc;
-    for (int o = 1; o < kWave; o <<= 1) {
-      const int64_t y = __shfl_up(incl, o, kWave);
-      if (lane >= o) incl += y;
-    }
+    int64_t incl = wave_incl_scan(loc);  // DPP, no LDS
     if (lane == kWave - 1) s_wsum[wave] = incl;
     __syncthreads();
     int64_t run = incl - loc;

@@ -30,11 +30,7 @@ __device__ T block_exclusive_scan(T* a, int count, T* s_wave) {
   const int beg = min(count, tid * seg), end = min(count, beg + seg);
   T local = 0;
   for (int i = beg; i < end; ++i) local += a[i];
-  T incl = local;
-  for (int o = 1; o < kWave; o <<= 1) {
-    const T y = __shfl_up(incl, o, kWave);
-    if ((tid & (kWave - 1)) >= o) incl += y;
-  }
+  T incl = wave_incl_scan(local);  // DPP, no LDS
   if ((tid & (kWave - 1)) == kWave - 1) s_wave[tid / kWave] = incl;
   __syncthreads();
   if (tid == 0) {
@@ -202,20 +198,12 @@ __device__ uint32_t scan8k_lds(uint32_t* a, uint32_t* s_wave) {
   uint32_t local = 0;
 #pragma unroll
   for (int e = 0; e < 8; ++e) local += v[e];
-  uint32_t incl = local;
-  for (int o = 1; o < kWave; o <<= 1) {
-    const uint32_t t = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += t;
-  }
+  uint32_t incl = wave_incl_scan(local);  // DPP, no LDS
   if (lane == kWave - 1) s_wave[wave] = incl;
   __syncthreads();
   if (wave == 0) {
     const uint32_t w = lane < 16 ? s_wave[lane] : 0u;
-    uint32_t wi = w;
-    for (int o = 1; o < 16; o <<= 1) {
-      const uint32_t t = __shfl_up(wi, o, kWave);
-      if (lane >= o) wi += t;
-    }
+    uint32_t wi = row_incl_scan(w);  // DPP, no LDS
     if (lane < 16) s_wave[lane] = wi - w;
     if (lane == 15) s_wave[16] = wi;
   }
@@ -813,13 +801,10 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
           const double mc = c < nhc ? (c0 == 0 ? pre[0] : lse[(c * kRg) * 2]) : -INFINITY;
           const double sc = c0 == 0 ? pre[1] : (c < nhc ? lse[(c * kRg) * 2 + 1] : 0.0);
           const double v = (c < nhc && mc != -INFINITY) ? sc * exp(mc - m) : 0.0;
-          double incl = v;
-          for (int o = 1; o < kWave; o <<= 1) {
-            const double y = __shfl_up(incl, o, kWave);
-            if (lane >= o) incl += y;
-          }
-          int hit = (c < nhc && base + incl >= Tc) ? c : 0x7fffffff;
-          for (int o = kWave / 2; o > 0; o >>= 1) hit = min(hit, __shfl_xor(hit, o, kWave));
+          double incl = wave_incl_scan(v);  // DPP, no LDS
+          // the running sum only grows, so the crossing is the first lane that reaches Tc
+          const uint64_t hb = __ballot(c < nhc && base + incl >= Tc);
+          const int hit = hb ? c0 + __ffsll((long long)hb) - 1 : 0x7fffffff;
           if (hit != 0x7fffffff) {
             cstar = hit;
             base += __shfl(incl - v, hit - c0, kWave);
@@ -841,14 +826,9 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
             lu = lg[u];
           }
           const double e = u < ue ? exp(lu - m) : 0.0;
-          double incl = e;
-          for (int o = 1; o < kWave; o <<= 1) {
-            const double y = __shfl_up(incl, o, kWave);
-            if (lane >= o) incl += y;
-          }
-          int c2 = (u < ue && run + incl >= Tc) ? (int)(u + 1) : 0x7fffffff;
-          for (int o = kWave / 2; o > 0; o >>= 1) c2 = min(c2, __shfl_xor(c2, o, kWave));
-          cand = c2;
+          double incl = wave_incl_scan(e);  // DPP, no LDS
+          const uint64_t hb = __ballot(u < ue && run + incl >= Tc);
+          cand = hb ? (int)(v0 + __ffsll((long long)hb)) : 0x7fffffff;  // u + 1 of the first such lane
           run += __shfl(incl, kWave - 1, kWave);
         }
         k = cand == 0x7fffffff ? (int)ue : cand;  // ue only if rounding lost the crossing
@@ -1057,11 +1037,7 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
       *reinterpret_cast<int4*>(s_L + j0) = make_int4(L[0], L[1], L[2], L[3]);
       *reinterpret_cast<int4*>(s_L + j0 + 4) = make_int4(L[4], L[5], L[6], L[7]);
     }
-    uint64_t incl = loc;
-    for (int o2 = 1; o2 < kWave; o2 <<= 1) {
-      const uint64_t y = __shfl_up(incl, o2, kWave);
-      if (lane >= o2) incl += y;
-    }
+    uint64_t incl = wave_incl_scan(loc);  // DPP, no LDS
     if (lane == kWave - 1) s_wave_u[wave] = incl;
     __syncthreads();
     uint64_t base = incl - loc, tot = 0;
@@ -1121,11 +1097,7 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
     const int L = Ls[j];
     if (L > 0) loc += (1ull << 32) | (uint64_t)L;
   }
-  uint64_t incl = loc;
-  for (int o = 1; o < kWave; o <<= 1) {
-    const uint64_t y = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += y;
-  }
+  uint64_t incl = wave_incl_scan(loc);  // DPP, no LDS
   if (lane == kWave - 1) s_wave_u[wave] = incl;
   __syncthreads();
   if (tid == 0) {

@@ -321,11 +321,7 @@ __global__ __launch_bounds__(1024) void km_scan3_kernel(KmArgs a) {
     v[e] = b0 + e < b1 ? tab[b0 + e] : 0;
     loc += v[e];
   }
-  int incl = loc;
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(incl, o, 64);
-    if (lane >= o) incl += y;
-  }
+  int incl = wave_incl_scan(loc);  // DPP, no LDS
   if (lane == 63) s_w[wave] = incl;
   __syncthreads();
   if (tid == 0) {
