@@ -576,11 +576,13 @@ __device__ bool positive_interval(double a, double b, int64_t lo, int64_t hi, in
 
 // sum_{i=lo}^{hi} max(0, a/i + b) in closed form: a (H(R) - H(L-1)) + b (R - L + 1)
 // over the positive interval [L, R].
-__device__ double tail_sum(double a, double b, int64_t lo, int64_t hi) {
-  int64_t L, R;
-  if (!positive_interval(a, b, lo, hi, &L, &R)) return 0.0;
-  return a * (harmonic(R) - harmonic(L - 1)) + b * (double)(R - L + 1);
+__device__ __forceinline__ double readlane_d(double v, int lane) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), lane);
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
 }
+
 
 // 3a. Logits of the sampled rows: each lane sums its 8 bf16 products in fp32
 //     (v_dot2, error at most a few ulp of the lane's sum of |products|), the
@@ -766,6 +768,11 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
     mu2 = R[2];
   }
   double Tc = 0.0;  // the part of the target the clustered list must supply
+  // positive interval [L, R] of the fitted curve over (N, n] and H(R), H(L - 1):
+  // the tail sum S_n and the budget search share them
+  bool any = false;
+  int64_t L = 0, Rr = 0;
+  double HL = 0.0, HR = 0.0;
   if (n > 0) {
     if (exact) {
       Sn = EN;
@@ -776,7 +783,13 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
       const double x1 = (double)(hm[4] + hm[5]) / 2.0, x2 = (double)(hm[6] + hm[7]) / 2.0;
       fa = (mu1 - mu2) / (1.0 / x1 - 1.0 / x2);
       fb = mu1 - fa / x1;
-      Sn = EN + tail_sum(fa, fb, N + 1, n);
+      any = positive_interval(fa, fb, N + 1, n, &L, &Rr);
+      if (any) {  // the two harmonic numbers in two lanes at once
+        const double hx = harmonic(lane == 0 ? Rr : L - 1);
+        HR = readlane_d(hx, 0);
+        HL = readlane_d(hx, 1);
+      }
+      Sn = EN + (any ? fa * (HR - HL) + fb * (double)(Rr - L + 1) : 0.0);  // the tail sum over (N, n]
     }
   } else {
     mu1 = mu2 = 0.0;
@@ -835,9 +848,6 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
       } else {
         // minimal k in (N, n] with E_N + tail(N+1..k) >= Tc: 64-way parallel
         // search on the closed form over the positive interval [L, R]
-        int64_t L, Rr;
-        const bool any = positive_interval(fa, fb, N + 1, n, &L, &Rr);
-        const double HL = any ? harmonic(L - 1) : 0.0;
         auto reached = [&](int64_t kk) -> bool {
           const int64_t r = min(kk, Rr);
           const double t = (!any || r < L) ? 0.0 : fa * (harmonic(r) - HL) + fb * (double)(r - L + 1);
@@ -847,8 +857,8 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
         while (lo < hi) {
           const int64_t step = (hi - lo + kWave) / kWave;
           const int64_t cand = min(hi, lo + (int64_t)lane * step);
-          int first = reached(cand) ? lane : kWave;
-          for (int o = kWave / 2; o > 0; o >>= 1) first = min(first, __shfl_xor(first, o, kWave));
+          const uint64_t rb = __ballot(reached(cand));  // the first reached candidate
+          const int first = rb ? __ffsll((long long)rb) - 1 : kWave;
           const int64_t chi = first < kWave ? min(hi, lo + (int64_t)first * step) : hi;
           // a reached candidate bounds the answer above; if rounding left none
           // reached, the clamp ends the search at hi
