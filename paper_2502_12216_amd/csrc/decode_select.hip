@@ -614,9 +614,8 @@ __device__ __forceinline__ double wave_max_d(double v) {
 template <bool kPaged>
 __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
   __shared__ double s_lg[kSampleChunk];
-  constexpr int kRW = kSampleChunk / kWave;  // waves that reduce the chunk, one sample per lane
-  static_assert(kSampleChunk % kWave == 0 && kRW <= 4, "chunk must fit the workgroup's waves");
-  __shared__ double s_part[kRW][4][2];
+  constexpr int kRW = kSampleChunk / kWave;  // samples per lane in the chunk reduction
+  static_assert(kSampleChunk % kWave == 0 && kRW <= 4, "chunk must be 1 to 4 waves of samples");
   const int tid = threadIdx.x;
   const int bh = blockIdx.y;
   const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
@@ -668,8 +667,9 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
   }
   __syncthreads();
   if (tid < kSampleChunk && u0 + tid < S) lg[u0 + tid] = s_lg[tid];  // contiguous stores
-  // per-region (max, sum exp(l - max)) of this chunk, one sample per lane of
-  // the first waves; regions: exact head, window 1, window 2, recent tokens
+  // per-region (max, sum exp(l - max)) of this chunk by the first wave, kRW
+  // samples per lane; regions: exact head, window 1, window 2, recent tokens
+  if (wave != 0) return;
   const int64_t S_main = hm[12];
   const int64_t N = hm[8] ? S_main : hm[1];
   const int64_t N1 = N + hm[2];
@@ -677,35 +677,30 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
     return u < N ? 0 : (u < N1 ? 1 : (u < S_main ? 2 : (u < S ? 3 : 4)));
   };
   const int rg_lo = region(u0), rg_hi = region(min(S, u0 + kSampleChunk) - 1);  // regions present
-  if (wave < kRW) {
-    const int t = wave * kWave + lane;
-    const int reg = region(u0 + t);
-    const double l = s_lg[t];
-    for (int rg = rg_lo; rg <= rg_hi; ++rg) {
-      const double mx = wave_max_d(reg == rg ? l : -INFINITY);
-      const double sm = wave_sum_d(reg == rg ? exp(l - mx) : 0.0);
-      if (lane == 0) {
-        s_part[wave][rg][0] = mx;
-        s_part[wave][rg][1] = mx == -INFINITY ? 0.0 : sm;
-      }
-    }
+  double l[kRW];
+  int reg[kRW];
+#pragma unroll
+  for (int i = 0; i < kRW; ++i) {
+    l[i] = s_lg[i * kWave + lane];
+    reg[i] = region(u0 + i * kWave + lane);
   }
-  __syncthreads();
-  if (tid < 4) {
-    double M = -INFINITY, Ssum = 0.0;
-    if (tid >= rg_lo && tid <= rg_hi) {
+  double* out = a.lse + ((int64_t)bh * a.split + blockIdx.x) * 8;
+  for (int rg = 0; rg < 4; ++rg) {
+    double mx = -INFINITY, sm = 0.0;
+    if (rg >= rg_lo && rg <= rg_hi) {
+      double m0 = -INFINITY;
 #pragma unroll
-      for (int w = 0; w < kRW; ++w) M = fmax(M, s_part[w][tid][0]);
-      if (M != -INFINITY)
+      for (int i = 0; i < kRW; ++i) m0 = fmax(m0, reg[i] == rg ? l[i] : -INFINITY);
+      mx = wave_max_d(m0);
+      double e = 0.0;
 #pragma unroll
-        for (int w = 0; w < kRW; ++w) {
-          const double mw = s_part[w][tid][0];
-          if (mw != -INFINITY) Ssum += s_part[w][tid][1] * exp(mw - M);
-        }
+      for (int i = 0; i < kRW; ++i) e += reg[i] == rg ? exp(l[i] - mx) : 0.0;
+      sm = wave_sum_d(e);
     }
-    double* out = a.lse + (((int64_t)bh * a.split + blockIdx.x) * 4 + tid) * 2;
-    out[0] = M;
-    out[1] = Ssum;
+    if (lane == 0) {
+      out[rg * 2] = mx;
+      out[rg * 2 + 1] = mx == -INFINITY ? 0.0 : sm;
+    }
   }
 }
 
