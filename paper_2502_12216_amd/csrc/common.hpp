@@ -168,6 +168,18 @@ __device__ __forceinline__ T wave_incl_scan(T v) {
   return v;
 }
 
+// Inclusive max-scan over the 64 lanes of a wave of non-negative values (the
+// zero fill of the shifts is neutral): the same steps as wave_incl_scan.
+__device__ __forceinline__ int wave_incl_max(int v) {
+  v = max(v, dpp_zero<0x111, 0xF>(v));
+  v = max(v, dpp_zero<0x112, 0xF>(v));
+  v = max(v, dpp_zero<0x114, 0xF>(v));
+  v = max(v, dpp_zero<0x118, 0xF>(v));
+  v = max(v, dpp_zero<0x142, 0xA>(v));
+  v = max(v, dpp_zero<0x143, 0xC>(v));
+  return v;
+}
+
 __device__ __forceinline__ float wave_max(float v) {
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
   return v;

@@ -152,7 +152,7 @@ void attn_splitk_kernel(AttnArgs a) {
     } r;
     float red[4][G][kHeadDim];
   };
-  __shared__ ItemShared sh;
+  __shared__ __align__(16) ItemShared sh;  // 16-byte LDS accesses to the row table
   int* s_rows = sh.r.rows;
   int* s_rupos = sh.r.rupos;
   int* s_rstart = sh.r.rstart;
@@ -160,6 +160,7 @@ void attn_splitk_kernel(AttnArgs a) {
   __shared__ float s_ml[NG][2][G];
   __shared__ float s_M[G], s_L[G];
   __shared__ int64_t s_wsum[4];
+  __shared__ int s_wmax[4];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, sl = lane % LPR, grp = lane / LPR;
@@ -317,40 +318,63 @@ void attn_splitk_kernel(AttnArgs a) {
       } else {
         const int64_t c = p / kCfrTokens, in = p - c * kCfrTokens;
         cnt = (int)min(seg_hi - p, (int64_t)kMaxChunkTokens - in);
-        // ranges that can touch [p, p + cnt): from the one holding position c * kCfrTokens
-        const int R = a.gmeta[bg * 4 + 0];
-        const int r0 = a.cfr[(int64_t)bg * a.max_chunks + c];
-        const int nr = max(1, min(R - r0, (int)(in + cnt)));
+        // ranges that can touch [p, p + cnt): from the one holding position
+        // c * kCfrTokens to the one holding the first position of the chunk
+        // after the sub-range's last (or the group's last range), at most
+        // in + cnt of them (every range after r0 starts at its own position)
+        const int R = a.gmeta[bg * 4 + 0], nchunk = a.gmeta[bg * 4 + 2];
+        const int64_t c_end = (p + cnt - 1) / kCfrTokens + 1;
+        const int32_t* cf = a.cfr + (int64_t)bg * a.max_chunks;
+        const int r0 = cf[c];
+        const int r_hi = c_end < min((int64_t)nchunk, a.max_chunks) ? cf[c_end] : R - 1;
+        const int nr = max(1, min(min(R - r0, r_hi - r0 + 1), (int)(in + cnt)));
         const int32_t* rup = a.rupos + (int64_t)bg * (a.Cm + 2) + r0;
         const int32_t* rst = a.rstart + (int64_t)bg * (a.Cm + 2) + r0;
+        constexpr int kRun = kMaxChunkTokens / 256;  // positions per thread
+        const int t_lo = tid * kRun;
+        // the row table starts as range markers: all zero, then each range's
+        // index at its first position (the ranges starting at or before p
+        // all mark position 0, and the largest index wins)
+        *reinterpret_cast<int4*>(s_rows + t_lo) = make_int4(0, 0, 0, 0);
+        *reinterpret_cast<int4*>(s_rows + t_lo + 4) = make_int4(0, 0, 0, 0);
+#pragma unroll 4
         for (int i = tid; i <= nr; i += 256) {
           s_rupos[i] = rup[i];
           if (i < nr) s_rstart[i] = rst[i];
         }
         __syncthreads();
-        // each thread fills a run of consecutive positions: one binary search for
-        // the run's first position, then a walk along the ranges
-        constexpr int kRun = kMaxChunkTokens / 256;
-        const int t_lo = tid * kRun, t_hi = min(cnt, t_lo + kRun);
-        if (t_lo < t_hi) {
-          const int pos0 = (int)(p + t_lo);
-          int l2 = 0, h2 = nr - 1;  // largest i with s_rupos[i] <= pos0
-          while (l2 < h2) {
-            const int mid = (l2 + h2 + 1) >> 1;
-            if (s_rupos[mid] <= pos0) l2 = mid;
-            else h2 = mid - 1;
-          }
-          int next = l2 + 1 < nr ? s_rupos[l2 + 1] : 0x7fffffff;
-          for (int t = t_lo; t < t_hi; ++t) {
-            const int pos = (int)(p + t);
-            while (pos >= next) {  // the ranges cover positions without gaps
-              ++l2;
-              next = l2 + 1 < nr ? s_rupos[l2 + 1] : 0x7fffffff;
-            }
-            const int row = min(max(s_rstart[l2] + (pos - s_rupos[l2]), 0), nseq - 1);  // clamp: bad meta only
-            s_rows[t] = kPaged ? (int)paged_row(a.pk, a.Hkv, a.total, kvb, b, kvh, row, n_c) : row;
-          }
+        for (int i = tid; i < nr; i += 256) {
+          const int64_t q = (int64_t)s_rupos[i] - p;
+          if (q < cnt) atomicMax(&s_rows[max(q, (int64_t)0)], i);
         }
+        __syncthreads();
+        // each position's range is the largest marker at or before it: a
+        // running max over the thread's positions, a DPP max-scan over the
+        // wave, the maxima of the earlier waves
+        int mk[kRun];
+        {
+          const int4 x = *reinterpret_cast<const int4*>(s_rows + t_lo);
+          const int4 y = *reinterpret_cast<const int4*>(s_rows + t_lo + 4);
+          mk[0] = x.x; mk[1] = x.y; mk[2] = x.z; mk[3] = x.w;
+          mk[4] = y.x; mk[5] = y.y; mk[6] = y.z; mk[7] = y.w;
+        }
+#pragma unroll
+        for (int e = 1; e < kRun; ++e) mk[e] = max(mk[e], mk[e - 1]);
+        const int wincl = wave_incl_max(mk[kRun - 1]);
+        if (lane == kWave - 1) s_wmax[wave] = wincl;
+        __syncthreads();
+        int run = dpp_zero<0x138, 0xF>(wincl);  // wave_shr:1, the lanes before this one
+        for (int w = 0; w < wave; ++w) run = max(run, s_wmax[w]);
+        int rw[kRun];
+#pragma unroll
+        for (int e = 0; e < kRun; ++e) {
+          const int idx = max(mk[e], run);
+          const int pos = (int)(p + t_lo + e);
+          const int row = min(max(s_rstart[idx] + (pos - s_rupos[idx]), 0), nseq - 1);  // clamp: bad meta only
+          rw[e] = kPaged ? (int)paged_row(a.pk, a.Hkv, a.total, kvb, b, kvh, row, n_c) : row;
+        }
+        *reinterpret_cast<int4*>(s_rows + t_lo) = make_int4(rw[0], rw[1], rw[2], rw[3]);
+        *reinterpret_cast<int4*>(s_rows + t_lo + 4) = make_int4(rw[4], rw[5], rw[6], rw[7]);
         __syncthreads();
       }
       const int ntile = (cnt + kTileTok - 1) / kTileTok;
