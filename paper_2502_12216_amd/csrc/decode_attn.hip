@@ -150,7 +150,9 @@ void attn_splitk_kernel(AttnArgs a) {
       int rupos[kMaxChunkTokens + 1];
       int rstart[kMaxChunkTokens + 1];
     } r;
-    float red[4][G][kHeadDim];
+    // the merge: every lane-group's rescaled accumulators (G <= 4), else the
+    // four waves' sums after an in-wave reduction
+    float red[G <= 4 ? NG : 4][G][kHeadDim];
   };
   __shared__ __align__(16) ItemShared sh;  // 16-byte LDS accesses to the row table
   int* s_rows = sh.r.rows;
@@ -439,28 +441,55 @@ void attn_splitk_kernel(AttnArgs a) {
     }
     __syncthreads();
     const float sc_own = m == -INFINITY ? 0.f : fast_exp2(m - s_M[hl]);
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float sc = head_value<G>(sc_own, h);
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) {
-        float v = acc[h][e] * sc;
-        v += __shfl_xor(v, 16, 64);
-        v += __shfl_xor(v, 32, 64);
-        acc[h][e] = v;
-      }
-    }
-    if (grp == 0) {
-#pragma unroll
-      for (int h = 0; h < G; ++h)
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) s_red[wave][h][sl * EPL + e] = acc[h][e];
-    }
-    __syncthreads();
     float* part = a.partials + ((int64_t)bg + blockIdx.x) * kPart;  // slot bg + w is unique
-    for (int i = tid; i < G * kHeadDim; i += 256) {
-      const int h = i / kHeadDim, d = i % kHeadDim;
-      part[i] = s_red[0][h][d] + s_red[1][h][d] + s_red[2][h][d] + s_red[3][h][d];
+    if constexpr (G <= 4) {
+      // every lane-group's rescaled accumulators to LDS, then 4 consecutive
+      // outputs per thread summed over the NG lane-groups
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float sc = head_value<G>(sc_own, h);
+#pragma unroll
+        for (int e = 0; e < EPL; e += 4)
+          *reinterpret_cast<float4*>(&s_red[gid][h][sl * EPL + e]) =
+              make_float4(acc[h][e] * sc, acc[h][e + 1] * sc, acc[h][e + 2] * sc, acc[h][e + 3] * sc);
+      }
+      __syncthreads();
+      if (tid * 4 < G * kHeadDim) {
+        const int h = tid * 4 / kHeadDim, d = tid * 4 % kHeadDim;
+        float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int q2 = 0; q2 < NG; ++q2) {
+          const float4 v = *reinterpret_cast<const float4*>(&s_red[q2][h][d]);
+          sum.x += v.x;
+          sum.y += v.y;
+          sum.z += v.z;
+          sum.w += v.w;
+        }
+        *reinterpret_cast<float4*>(part + tid * 4) = sum;
+      }
+    } else {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float sc = head_value<G>(sc_own, h);
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) {
+          float v = acc[h][e] * sc;
+          v += __shfl_xor(v, 16, 64);
+          v += __shfl_xor(v, 32, 64);
+          acc[h][e] = v;
+        }
+      }
+      if (grp == 0) {
+#pragma unroll
+        for (int h = 0; h < G; ++h)
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) s_red[wave][h][sl * EPL + e] = acc[h][e];
+      }
+      __syncthreads();
+      for (int i = tid; i < G * kHeadDim; i += 256) {
+        const int h = i / kHeadDim, d = i % kHeadDim;
+        part[i] = s_red[0][h][d] + s_red[1][h][d] + s_red[2][h][d] + s_red[3][h][d];
+      }
     }
     if (tid < G) {
       part[G * kHeadDim + tid] = s_M[tid];
