@@ -143,6 +143,10 @@ __device__ __forceinline__ int64_t dpp_zero(int64_t v) {
   return (int64_t)dpp_zero<CTRL, RM>((uint64_t)v);
 }
 template <int CTRL, int RM>
+__device__ __forceinline__ float dpp_zero(float v) {
+  return __builtin_bit_cast(float, dpp_zero<CTRL, RM>(__builtin_bit_cast(uint32_t, v)));
+}
+template <int CTRL, int RM>
 __device__ __forceinline__ double dpp_zero(double v) {
   return __builtin_bit_cast(double, dpp_zero<CTRL, RM>(__builtin_bit_cast(uint64_t, v)));
 }
@@ -179,6 +183,59 @@ __device__ __forceinline__ int wave_incl_max(int v) {
   v = max(v, dpp_zero<0x143, 0xC>(v));
   return v;
 }
+
+// Lane shift / broadcast by DPP that keeps the lane's own value where the
+// source lies outside its row or the row is masked off (neutral for max/min).
+template <int CTRL, int RM>
+__device__ __forceinline__ float dpp_self(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v),
+                                                               CTRL, RM, 0xF, false));
+}
+template <int CTRL, int RM>
+__device__ __forceinline__ double dpp_self(double v) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const int lo = __builtin_amdgcn_update_dpp((int)(uint32_t)u, (int)(uint32_t)u, CTRL, RM, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp((int)(uint32_t)(u >> 32), (int)(uint32_t)(u >> 32), CTRL, RM, 0xF, false);
+  return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+__device__ __forceinline__ float readlane_f(float v, int lane) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
+}
+__device__ __forceinline__ double readlane_d(double v, int lane) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), lane);
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+// Wave-wide reductions without LDS, the same value in every lane: the DPP
+// inclusive scan (sum) or max/min scan, read from the last lane.
+template <typename T>
+__device__ __forceinline__ T wave_scan_max(T v) {
+  v = fmax(v, dpp_self<0x111, 0xF>(v));
+  v = fmax(v, dpp_self<0x112, 0xF>(v));
+  v = fmax(v, dpp_self<0x114, 0xF>(v));
+  v = fmax(v, dpp_self<0x118, 0xF>(v));
+  v = fmax(v, dpp_self<0x142, 0xA>(v));
+  v = fmax(v, dpp_self<0x143, 0xC>(v));
+  return v;
+}
+template <typename T>
+__device__ __forceinline__ T wave_scan_min(T v) {
+  v = fmin(v, dpp_self<0x111, 0xF>(v));
+  v = fmin(v, dpp_self<0x112, 0xF>(v));
+  v = fmin(v, dpp_self<0x114, 0xF>(v));
+  v = fmin(v, dpp_self<0x118, 0xF>(v));
+  v = fmin(v, dpp_self<0x142, 0xA>(v));
+  v = fmin(v, dpp_self<0x143, 0xC>(v));
+  return v;
+}
+__device__ __forceinline__ double wave_allsum_d(double v) { return readlane_d(wave_incl_scan(v), kWave - 1); }
+__device__ __forceinline__ double wave_allmax_d(double v) { return readlane_d(wave_scan_max(v), kWave - 1); }
+__device__ __forceinline__ float wave_allsum_f(float v) { return readlane_f(wave_incl_scan(v), kWave - 1); }
+__device__ __forceinline__ float wave_allmax_f(float v) { return readlane_f(wave_scan_max(v), kWave - 1); }
+__device__ __forceinline__ float wave_allmin_f(float v) { return readlane_f(wave_scan_min(v), kWave - 1); }
 
 __device__ __forceinline__ float wave_max(float v) {
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));

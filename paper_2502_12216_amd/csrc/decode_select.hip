@@ -278,13 +278,11 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
         nf += 1.f;
       }
     }
-    for (int o = kWave / 2; o > 0; o >>= 1) {
-      sm += __shfl_xor(sm, o, kWave);
-      sq += __shfl_xor(sq, o, kWave);
-      nf += __shfl_xor(nf, o, kWave);
-      lo = fminf(lo, __shfl_xor(lo, o, kWave));
-      hi = fmaxf(hi, __shfl_xor(hi, o, kWave));
-    }
+    sm = wave_allsum_f(sm);  // DPP, no LDS
+    sq = wave_allsum_f(sq);
+    nf = wave_allsum_f(nf);
+    lo = wave_allmin_f(lo);
+    hi = wave_allmax_f(hi);
     if ((tid & (kWave - 1)) == 0) {
       s_red[tid / kWave][0] = sm;
       s_red[tid / kWave][1] = sq;
@@ -576,13 +574,6 @@ __device__ bool positive_interval(double a, double b, int64_t lo, int64_t hi, in
 
 // sum_{i=lo}^{hi} max(0, a/i + b) in closed form: a (H(R) - H(L-1)) + b (R - L + 1)
 // over the positive interval [L, R].
-__device__ __forceinline__ double readlane_d(double v, int lane) {
-  const uint64_t u = __builtin_bit_cast(uint64_t, v);
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, lane);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), lane);
-  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
-}
-
 
 // 3a. Logits of the sampled rows: each lane sums its 8 bf16 products in fp32
 //     (v_dot2, error at most a few ulp of the lane's sum of |products|), the
@@ -592,24 +583,9 @@ __device__ __forceinline__ double readlane_d(double v, int lane) {
 //     reduces its logits per region (exact head, window 1, window 2, recent
 //     tokens) to (max, sum of exp(l - max)), so the fit needs one exponential
 //     per chunk instead of one per sample.
-// wave-wide fp64 sum / max, identical in every lane: DPP within rows of 16
-// lanes, then two cross-row exchanges
-__device__ __forceinline__ double wave_sum_d(double v) {
-  v = sum16d(v);
-  v += __shfl_xor(v, 16, kWave);
-  v += __shfl_xor(v, 32, kWave);
-  return v;
-}
-
-__device__ __forceinline__ double wave_max_d(double v) {
-  v = fmax(v, dpp<0x140>(v));
-  v = fmax(v, dpp<0x141>(v));
-  v = fmax(v, dpp<0x4E>(v));
-  v = fmax(v, dpp<0xB1>(v));
-  v = fmax(v, __shfl_xor(v, 16, kWave));
-  v = fmax(v, __shfl_xor(v, 32, kWave));
-  return v;
-}
+// wave-wide fp64 sum / max, identical in every lane (DPP scans, no LDS)
+__device__ __forceinline__ double wave_sum_d(double v) { return wave_allsum_d(v); }
+__device__ __forceinline__ double wave_max_d(double v) { return wave_allmax_d(v); }
 
 template <bool kPaged>
 __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
