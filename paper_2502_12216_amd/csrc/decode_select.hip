@@ -334,8 +334,12 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
         if (j < C) {
           const uint64_t key = ((uint64_t)desc_key_bits(v[e]) << 32) | (uint32_t)j;
           const uint32_t end = start[bk[e]], beg = end - cnt[bk[e]];
-          uint32_t r = 0;
-          for (uint32_t t = beg; t < end; ++t) r += keys[t] < key ? 1u : 0u;
+          uint32_t r = 0, t = beg;
+          for (; t + 1 < end; t += 2) {  // two LDS reads in flight per step
+            const uint64_t k0 = keys[t], k1 = keys[t + 1];
+            r += (k0 < key ? 1u : 0u) + (k1 < key ? 1u : 0u);
+          }
+          if (t < end) r += keys[t] < key ? 1u : 0u;
           pos[e] = (int)(beg + r);
         }
       }
