@@ -379,3 +379,30 @@ def test_sparse_other_group_sizes(Hq, Hkv):
             g = h // (Hq // Hkv)
             ref = OA.dense_attention(np64(inp.q[b, h]), np64(lay.K_sorted[g, s0:s1]), np64(lay.V_sorted[g, s0:s1]))
             assert float(np.max(np.abs(np64(out[b, h]) - ref))) <= 2e-3
+
+
+@pytest.mark.parametrize("P", [0.5, 0.9])
+def test_sparse_degenerate_scores(P):
+    """Score ties end to end: a zero query (every cluster score 0: the sort's
+    equal-scores shortcut, uniform logits, a flat fit with a = 0) and
+    centroids repeated every 8 clusters (each score shared by an eighth of
+    the clusters: crowded sort buckets, order by cluster id within a tie)."""
+    wl = _small("ctx32k_llama8b", [3000, 1500])
+    inp = synth.make_layer(wl, 0)
+    lay = synth.label_layout(inp)
+    G = wl.n_q_heads // wl.n_kv_heads
+    q = inp.q.clone()
+    q[0, ::G] = 0  # the first query head of every group of sequence 0
+    inp.q = q
+    cent = lay.centroids.clone()
+    c0, c1 = int(lay.cl_indptr[1]), int(lay.cl_indptr[2])
+    idx = c0 + (torch.arange(c1 - c0) % 8)
+    cent[:, c0:c1] = cent[:, idx]
+    lay.centroids = cent
+    res = run_sparse(inp, lay, P)
+    st = check_layer(inp, lay, P, res, label=f"degenerate P={P}")
+    order = res["view"]["order"]
+    for g in range(wl.n_kv_heads):  # equal scores: the order is the cluster id
+        C0 = int(lay.cl_indptr[1] - lay.cl_indptr[0])
+        assert torch.equal(order[0, g * G, :C0], torch.arange(C0, dtype=order.dtype))
+    print(f"degenerate P={P}: ties(order)={sum(s['order_ties'] for s in st)} k={[s['k'] for s in st][:2]}")
