@@ -237,14 +237,5 @@ __device__ __forceinline__ float wave_allsum_f(float v) { return readlane_f(wave
 __device__ __forceinline__ float wave_allmax_f(float v) { return readlane_f(wave_scan_max(v), kWave - 1); }
 __device__ __forceinline__ float wave_allmin_f(float v) { return readlane_f(wave_scan_min(v), kWave - 1); }
 
-__device__ __forceinline__ float wave_max(float v) {
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
-}
-
-__device__ __forceinline__ float wave_sum(float v) {
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
 
 }  // namespace tactic

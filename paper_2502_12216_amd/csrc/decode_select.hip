@@ -54,29 +54,6 @@ __device__ T block_exclusive_scan(T* a, int count, T* s_wave) {
   return total;
 }
 
-template <typename T>
-__device__ T block_sum(T v, T* s_wave) {
-  for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-  const int nw = blockDim.x / kWave;
-  if ((threadIdx.x & (kWave - 1)) == 0) s_wave[threadIdx.x / kWave] = v;
-  __syncthreads();
-  T r = 0;
-  for (int w = 0; w < nw; ++w) r += s_wave[w];
-  __syncthreads();
-  return r;
-}
-
-__device__ double block_max_d(double v, double* s_wave) {
-  for (int o = kWave / 2; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, kWave));
-  const int nw = blockDim.x / kWave;
-  if ((threadIdx.x & (kWave - 1)) == 0) s_wave[threadIdx.x / kWave] = v;
-  __syncthreads();
-  double r = s_wave[0];
-  for (int w = 1; w < nw; ++w) r = fmax(r, s_wave[w]);
-  __syncthreads();
-  return r;
-}
-
 __device__ float block_minmax(float v, bool want_max, float* s_wave) {
   for (int o = kWave / 2; o > 0; o >>= 1) {
     const float y = __shfl_xor(v, o, kWave);
