@@ -553,9 +553,6 @@ __device__ bool positive_interval(double a, double b, int64_t lo, int64_t hi, in
   return true;
 }
 
-// sum_{i=lo}^{hi} max(0, a/i + b) in closed form: a (H(R) - H(L-1)) + b (R - L + 1)
-// over the positive interval [L, R].
-
 // 3a. Logits of the sampled rows: each lane sums its 8 bf16 products in fp32
 //     (v_dot2, error at most a few ulp of the lane's sum of |products|), the
 //     16 lane sums add in fp64.  grid (ceil(S_cap/128), B*Hq), 256 threads:
@@ -579,38 +576,40 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
   const int32_t* hm = a.head_meta + (int64_t)bh * 16;
   const int64_t u0 = (int64_t)blockIdx.x * kSampleChunk;
   const int lane = tid & 63, wave = tid >> 6, sl = lane & 15, grp = lane >> 4;
-  // the row indices load together with the head's metadata: entries past the
-  // head's sample count (but inside its S_cap) are read and then ignored
+  // one sampled row per lane, coalesced (the wave's kSpw samples), loaded
+  // together with the head's metadata: entries past the head's sample count
+  // (but inside its S_cap) are read and then ignored.  Each lane-group then
+  // takes its rows from the lanes that hold them (cross-lane permute), so
+  // only the K data stays in registers while every load is in flight.
+  constexpr int kSpw = kSampleChunk / 4;  // samples per wave
+  constexpr int kR = kSampleChunk / 16;   // rows per lane-group
+  static_assert(kSpw <= kWave, "one sample per lane");
+  const int64_t uw = u0 + wave * kSpw + lane;  // this lane's sample
   const int32_t* rows = a.sample_rows + (int64_t)bh * a.S_cap;
-  constexpr int kR = kSampleChunk / 16;  // rows per lane-group
-  int32_t r[kR];
-#pragma unroll
-  for (int k = 0; k < kR; ++k) {
-    const int64_t u = u0 + wave * (kSampleChunk / 4) + k * 4 + grp;
-    r[k] = u < a.S_cap ? rows[u] : -1;
-  }
+  int32_t rl = (lane < kSpw && uw < a.S_cap) ? rows[uw] : -1;
   const int64_t S = hm[9];
   if (u0 >= S) return;
-#pragma unroll
-  for (int k = 0; k < kR; ++k)
-    if (u0 + wave * (kSampleChunk / 4) + k * 4 + grp >= S) r[k] = -1;
+  if (uw >= S) rl = -1;
   const uint4 qv = *reinterpret_cast<const uint4*>(a.q + (int64_t)bh * kHeadDim + sl * 8);
   const int64_t kvb = a.kv_indptr[b];
   double* lg = a.logits + (int64_t)bh * a.S_cap;
-  int64_t roff[kR];  // row index of every sample in the K array
+  uint4 kv[kR];  // sample wave * kSpw + k * 4 + grp of the chunk
   if constexpr (kPaged) {
-    const int n_c = hm[0];
+    const int64_t ro = rl >= 0 ? paged_row(a.pk, a.Hkv, a.total, kvb, b, g, rl, hm[0]) : -1;
+    const uint16_t* Kl = a.K + sl * 8;
 #pragma unroll
-    for (int k = 0; k < kR; ++k)
-      roff[k] = r[k] >= 0 ? paged_row(a.pk, a.Hkv, a.total, kvb, b, g, r[k], n_c) : -1;
+    for (int k = 0; k < kR; ++k) {
+      const int64_t rk = __shfl(ro, k * 4 + grp, kWave);
+      kv[k] = rk >= 0 ? load_stream16(Kl + rk * kHeadDim) : make_uint4(0, 0, 0, 0);
+    }
   } else {
+    const uint16_t* Kg = a.K + ((int64_t)g * a.total + kvb) * kHeadDim + sl * 8;
 #pragma unroll
-    for (int k = 0; k < kR; ++k) roff[k] = r[k] >= 0 ? (int64_t)g * a.total + kvb + r[k] : -1;
+    for (int k = 0; k < kR; ++k) {
+      const int rk = __shfl(rl, k * 4 + grp, kWave);
+      kv[k] = rk >= 0 ? load_stream16(Kg + (int64_t)rk * kHeadDim) : make_uint4(0, 0, 0, 0);
+    }
   }
-  uint4 kv[kR];
-#pragma unroll
-  for (int k = 0; k < kR; ++k)
-    kv[k] = roff[k] >= 0 ? load_stream16(a.K + roff[k] * kHeadDim + sl * 8) : make_uint4(0, 0, 0, 0);
 #pragma unroll
   for (int k = 0; k < kR; ++k) {
     // the lane's 8 products summed in fp32 (v_dot2), the 16 lane sums in fp64
@@ -619,7 +618,7 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
     d = dot2_bf16(kv[k].z, qv.z, d);
     d = dot2_bf16(kv[k].w, qv.w, d);
     const double acc = sum16d((double)d) * 0.088388347648318440550;  // 1 / sqrt(128), within 1 ulp of the quotient
-    const int t = wave * (kSampleChunk / 4) + k * 4 + grp;
+    const int t = wave * kSpw + k * 4 + grp;
     if (sl == 0) s_lg[t] = acc;
   }
   __syncthreads();
