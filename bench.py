@@ -66,6 +66,42 @@ def profiled_traffic(stage: str):
     return None
 
 
+def dense_sdpa(q, K, V, wl, reps: int, own_out=None) -> dict:
+    """torch's scaled_dot_product_attention (GQA) as a second dense decode on
+    one layer's bf16 inputs, restricted to the fused flash / memory-efficient
+    backends; the result says why when neither takes the shape."""
+    if len(set(wl.seq_lens)) != 1:
+        return {"us_per_layer": None, "error": "ragged batch: SDPA needs equal lengths"}
+    try:
+        from torch.nn.attention import SDPBackend, sdpa_kernel
+        B, Hq, d = q.shape
+        Hkv, n = K.shape[0], wl.seq_lens[0]
+        qS = q.view(B, Hq, 1, d)
+        KS = K.view(Hkv, B, n, d).transpose(0, 1).contiguous()
+        VS = V.view(Hkv, B, n, d).transpose(0, 1).contiguous()
+        backends = [SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION]
+
+        def call():
+            with sdpa_kernel(backends):
+                return torch.nn.functional.scaled_dot_product_attention(qS, KS, VS, enable_gqa=True)
+
+        o = call().view(B, Hq, d).float()
+        diff = float((o - own_out).abs().max()) if own_out is not None else None
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            call()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1000 / reps
+        del KS, VS
+        return {"us_per_layer": round(us, 2), "backends": "flash, efficient", "reps": reps,
+                "max_abs_diff_vs_own_dense": diff}
+    except Exception as e:  # no fused backend for this shape on this build
+        return {"us_per_layer": None, "error": f"{type(e).__name__}: {str(e)[:160]}"}
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -166,22 +202,32 @@ def main():
         for l in range(layers):
             dense(qs[l], Ks[l], Vs[l])
 
-    def timed(step, n):
+    def timed(step, n, per_step=None):
+        """Mean milliseconds per step over n steps; per_step, if given, receives
+        every step's own time (events between the steps, same stream)."""
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
         torch.cuda.synchronize()
         ev0.record()
-        for _ in range(n):
+        evs[0].record()
+        for i in range(n):
             step()
+            evs[i + 1].record()
         ev1.record()
         torch.cuda.synchronize()
+        if per_step is not None:
+            per_step.extend(evs[i].elapsed_time(evs[i + 1]) for i in range(n))
         return ev0.elapsed_time(ev1) / n
 
     for _ in range(args.warmup):
         sparse_step()
         dense_step()
-    ms_sparse = timed(sparse_step, args.steps)
+    step_ms = []
+    ms_sparse = timed(sparse_step, args.steps, step_ms)
     log(f"sparse step {ms_sparse:.3f} ms")
     ms_dense = timed(dense_step, args.steps)
     log(f"dense step {ms_dense:.3f} ms")
+    sdpa = dense_sdpa(qs[0], Ks[0], Vs[0], wl, max(3, args.steps), dense(qs[0], Ks[0], Vs[0]).clone())
+    log(f"torch SDPA dense layer: {sdpa}")
 
     # ---------------------------------------------------------------- per-stage timing (HIP events)
     NS = 6
@@ -193,9 +239,10 @@ def main():
     from paper_2502_12216_amd import _capi as C
     arr = (ctypes.c_void_p * (NS + 1))(*[e.cuda_event for e in stage_ev])
 
-    def stage_times(decoder, call=None, n_layers=None):
+    def stage_times(decoder, call=None, n_layers=None, per_layer=None):
         """Mean per-kernel milliseconds over args.steps passes of every layer, from
-        events the library records between its launches on the decode stream."""
+        events the library records between its launches on the decode stream;
+        per_layer, if given, receives each call's first-to-last event time."""
         call = call or (lambda l: decoder(qs[l], Ks[l], Vs[l], cls[l]))
         C.check(C.lib().tactic_sparse_decode_plan_set_events(ctypes.byref(decoder.plan), arr), "set_events")
         acc = np.zeros(NS)
@@ -206,11 +253,14 @@ def main():
                 torch.cuda.synchronize()
                 for i in range(NS):
                     acc[i] += stage_ev[i].elapsed_time(stage_ev[i + 1])
+                if per_layer is not None:
+                    per_layer.append(stage_ev[0].elapsed_time(stage_ev[NS]))
                 nrep += 1
         C.check(C.lib().tactic_sparse_decode_plan_set_events(ctypes.byref(decoder.plan), None), "set_events")
         return acc / nrep
 
-    stage_ms = stage_times(dec)
+    layer_ms = []
+    stage_ms = stage_times(dec, per_layer=layer_ms)
     stage_names = ["score_clusters", "sort_clusters", "sample_logits", "fit_union", "attn_splitk", "combine"]
 
     # ---------------------------------------------------------------- GQA-union ablation (Sec. 4.5)
@@ -300,6 +350,7 @@ def main():
     dense_bytes_layer = float(lens.sum()) * Hkv * 512
     us_sparse = ms_sparse * 1000 / layers
     us_dense = ms_dense * 1000 / layers
+    us_dense_best = min(us_dense, sdpa["us_per_layer"]) if sdpa.get("us_per_layer") else us_dense
     gbps = float(bytes_layer.mean()) / (us_sparse * 1e3)
     stage_us = stage_ms * 1000
     stage_bytes = [bytes_centroids, 0.0, float(bytes_samples.mean()), 0.0, float(bytes_union.mean()), 0.0]
@@ -371,8 +422,19 @@ def main():
         "config": {"workload": wl.name, "batch": B, "seq_len": int(wl.seq_lens[0]), "layers": layers,
                    "n_q_heads": Hq, "n_kv_heads": Hkv, "head_dim": 128, "clusters_per_seq": int(ncl[0]),
                    "target_frac": args.target_frac, "clustering": args.clusters},
+        "us_per_layer_dist": {
+            "steps_p10": round(float(np.percentile(step_ms, 10)) * 1000 / layers, 2),
+            "steps_median": round(float(np.median(step_ms)) * 1000 / layers, 2),
+            "steps_p90": round(float(np.percentile(step_ms, 90)) * 1000 / layers, 2),
+            "layer_calls_p10": round(float(np.percentile(layer_ms, 10)) * 1000, 2),
+            "layer_calls_median": round(float(np.median(layer_ms)) * 1000, 2),
+            "layer_calls_p90": round(float(np.percentile(layer_ms, 90)) * 1000, 2),
+            "note": "steps: each timed step / layers; layer_calls: one layer's six launches between "
+                    "library events, synchronised per call (layers differ in their selected fraction)"},
         "dense_us_per_layer": round(us_dense, 2),
-        "speedup_vs_dense": round(us_dense / us_sparse, 3),
+        "dense_sdpa": sdpa,
+        "speedup_vs_dense": round(us_dense_best / us_sparse, 3),
+        "speedup_vs_own_dense": round(us_dense / us_sparse, 3),
         "hbm_gbps": round(gbps, 1),
         "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
         "dense_hbm_gbps": round(dense_bytes_layer / (us_dense * 1e3), 1),
