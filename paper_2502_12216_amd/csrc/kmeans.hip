@@ -2,9 +2,9 @@
 //
 // One problem per (sequence b, KV head g): n_b keys, C_b clusters, started
 // from the keys of the sampled tokens init_idx.  Each iteration:
-//   km_assign   nearest stored centroid of every key: ||c||^2 - 2 k.c with
-//               the k.c contraction on MFMA (v_mfma_f32_32x32x16_bf16, fp32
-//               accumulation) and a fused argmin (ties to the smaller id);
+//   km_assign   nearest stored centroid of every key: the largest
+//               k.c - ||c||^2 / 2, contracted on MFMA (v_mfma_f32_32x32x16_bf16,
+//               fp32 accumulation) with a fused argmax (ties to the smaller id);
 //               counts assignments that changed.
 //   km_hist     per tile of 2048 tokens: sort (cluster, token) keys in LDS,
 //               giving each token its rank among same-cluster tokens of the
@@ -32,7 +32,7 @@ constexpr int kKmTile = 2048;       // tokens per counting tile
 constexpr int kKmChunk = 16384;     // table entries per scan chunk
 constexpr int kKmMaxIters = 1000;
 constexpr int kAsgTok = 256;        // tokens per assignment workgroup (4 waves x 64)
-constexpr int kAsgCen = 128;        // centroids staged in LDS per step
+constexpr int kAsgCen = 64;         // centroids staged in LDS per step
 constexpr int kLdsRow = kHeadDim + 8;  // padded LDS row (bf16): 272 bytes, 2-way bank conflicts
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -117,11 +117,21 @@ __global__ __launch_bounds__(256) void km_init_kernel(KmArgs a) {
 // ---------------------------------------------------------------------------
 // assignment: grid (ceil(nmax/256), BG), 256 threads.  A wave owns 64 tokens
 // (two 32-token MFMA B operands held in registers for the whole pass);
-// centroids stream through LDS 128 at a time as the A operand.
+// centroids stream through LDS 64 at a time as the A operand, each tile
+// loaded into registers while the one before it is contracted.  The nearest
+// centroid maximises s = k.c - ||c||^2 / 2; the -||c||^2 / 2 term enters the
+// contraction as one more K step (the A operand holds it split into two bf16
+// parts, hi + lo, within about 2^-17 of the fp32 value; the B operand holds
+// ones there), so the epilogue reads finished scores: a 3-input max over each
+// lane's 16 scores of a block, and the search for the row that holds it only
+// when some lane of the wave improved on its best (strict, so the smaller
+// centroid id wins a tie).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void km_assign_kernel(KmArgs a) {
+// three waves per SIMD: the accumulators then live in VGPRs next to the
+// prefetched tile, without spills
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void km_assign_kernel(KmArgs a) {
   __shared__ __align__(16) uint16_t s_c[kAsgCen * kLdsRow];
-  __shared__ float s_cn[kAsgCen];
+  __shared__ uint32_t s_hl[kAsgCen];  // bf16 pair (hi, lo) of -||c||^2 / 2
   const int p = blockIdx.y;
   if (a.done[p]) return;
   const Problem q = problem(a, p);
@@ -142,39 +152,81 @@ __global__ __launch_bounds__(256) void km_assign_kernel(KmArgs a) {
       bt[bb][s] = __builtin_bit_cast(bf16x8, v);
     }
   }
-  float best_v[2] = {INFINITY, INFINITY};
+  // the extra K step: ones against (hi, lo) in the first two K slots of the
+  // lanes of half 0, zeros elsewhere
+  const bf16x8 ones = __builtin_bit_cast(bf16x8, half == 0 ? make_uint4(0x3F803F80u, 0, 0, 0) : make_uint4(0, 0, 0, 0));
+  float best_v[2] = {-INFINITY, -INFINITY};
   int best_j[2] = {0x7fffffff, 0x7fffffff};
   const uint16_t* cbase = a.centroids + q.cl_base * kHeadDim;
+  // the next tile's centroids and norms load during this tile's contraction
+  constexpr int kPieces = kAsgCen * 16 / 256;  // 16-byte pieces per thread
+  uint4 pf[kPieces];
+  float pfn = 0.f;
+  auto fetch = [&](int c0) {
+#pragma unroll
+    for (int k = 0; k < kPieces; ++k) {
+      const int idx = tid + 256 * k, row = idx >> 4, pc = idx & 15;
+      pf[k] = c0 + row < q.C ? *reinterpret_cast<const uint4*>(cbase + (int64_t)(c0 + row) * kHeadDim + pc * 8)
+                             : make_uint4(0, 0, 0, 0);
+    }
+    if (tid < kAsgCen && c0 + tid < q.C) pfn = a.cnorm[q.cl_base + c0 + tid];
+  };
+  fetch(0);
   for (int c0 = 0; c0 < q.C; c0 += kAsgCen) {
     __syncthreads();
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int idx = tid + 256 * k;  // 16-byte piece: row idx / 16, piece idx % 16
-      const int row = idx >> 4, pc = idx & 15;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (c0 + row < q.C) v = *reinterpret_cast<const uint4*>(cbase + (int64_t)(c0 + row) * kHeadDim + pc * 8);
-      *reinterpret_cast<uint4*>(s_c + row * kLdsRow + pc * 8) = v;
+    for (int k = 0; k < kPieces; ++k) {
+      const int idx = tid + 256 * k, row = idx >> 4, pc = idx & 15;
+      *reinterpret_cast<uint4*>(s_c + row * kLdsRow + pc * 8) = pf[k];
     }
-    if (tid < kAsgCen) s_cn[tid] = c0 + tid < q.C ? a.cnorm[q.cl_base + c0 + tid] : INFINITY;
+    if (tid < kAsgCen) {
+      uint32_t hl = 0xFF80u;  // rows past the last centroid score -inf (hi = -inf, zero data)
+      if (c0 + tid < q.C) {
+        const float x = -0.5f * pfn;
+        const uint16_t hi = f32_to_bf16_rne(x);
+        hl = (uint32_t)hi | ((uint32_t)f32_to_bf16_rne(x - bf16lo(hi)) << 16);
+      }
+      s_hl[tid] = hl;
+    }
     __syncthreads();
-    const int nblk = min(4, (q.C - c0 + 31) / 32);
+    if (c0 + kAsgCen < q.C) fetch(c0 + kAsgCen);
+    const int nblk = min(kAsgCen / 32, (q.C - c0 + 31) / 32);
     for (int cb = 0; cb < nblk; ++cb) {
-      f32x16 acc0 = {}, acc1 = {};
+      f32x16 acc[2] = {{}, {}};
       const uint16_t* arow = s_c + (cb * 32 + col) * kLdsRow + 64 * half;
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
         const bf16x8 av = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(arow + 8 * s));
-        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bt[0][s], acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bt[1][s], acc1, 0, 0, 0);
+        acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bt[0][s], acc[0], 0, 0, 0);
+        acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bt[1][s], acc[1], 0, 0, 0);
+      }
+      {
+        const uint32_t hl = half == 0 ? s_hl[cb * 32 + col] : 0u;
+        const bf16x8 av = __builtin_bit_cast(bf16x8, make_uint4(hl, 0, 0, 0));
+        acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, ones, acc[0], 0, 0, 0);
+        acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, ones, acc[1], 0, 0, 0);
       }
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int r = 8 * (i / 4) + 4 * half + (i % 4);  // centroid row of this accumulator
-        const float cn = s_cn[cb * 32 + r];
-        const int j = c0 + cb * 32 + r;
-        const float d0 = fmaf(-2.f, acc0[i], cn), d1 = fmaf(-2.f, acc1[i], cn);
-        if (d0 < best_v[0]) { best_v[0] = d0; best_j[0] = j; }
-        if (d1 < best_v[1]) { best_v[1] = d1; best_j[1] = j; }
+      for (int bb = 0; bb < 2; ++bb) {
+        const f32x16 v = acc[bb];
+        float m = fmaxf(fmaxf(v[0], v[1]), v[2]);
+        m = fmaxf(fmaxf(m, v[3]), v[4]);
+        m = fmaxf(fmaxf(m, v[5]), v[6]);
+        m = fmaxf(fmaxf(m, v[7]), v[8]);
+        m = fmaxf(fmaxf(m, v[9]), v[10]);
+        m = fmaxf(fmaxf(m, v[11]), v[12]);
+        m = fmaxf(fmaxf(m, v[13]), v[14]);
+        m = fmaxf(m, v[15]);
+        const bool imp = m > best_v[bb];
+        if (__any(imp)) {
+          int r = 0;  // the smallest row of this lane that holds m
+#pragma unroll
+          for (int i = 15; i >= 0; --i) r = v[i] == m ? 8 * (i / 4) + 4 * half + (i % 4) : r;
+          if (imp) {
+            best_v[bb] = m;
+            best_j[bb] = c0 + cb * 32 + r;
+          }
+        }
       }
     }
   }
@@ -183,7 +235,7 @@ __global__ __launch_bounds__(256) void km_assign_kernel(KmArgs a) {
   for (int bb = 0; bb < 2; ++bb) {
     const float ov = __shfl_xor(best_v[bb], 32, 64);
     const int oj = __shfl_xor(best_j[bb], 32, 64);
-    if (ov < best_v[bb] || (ov == best_v[bb] && oj < best_j[bb])) {
+    if (ov > best_v[bb] || (ov == best_v[bb] && oj < best_j[bb])) {
       best_v[bb] = ov;
       best_j[bb] = oj;
     }
