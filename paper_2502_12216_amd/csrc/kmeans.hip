@@ -264,8 +264,11 @@ __device__ __forceinline__ int lower_bound_u32(const uint32_t* s, int n, uint32_
   return lo;
 }
 
+constexpr int kHistLdsCounts = 8192;  // clusters whose tile counts are gathered in LDS
+
 __global__ __launch_bounds__(1024) void km_hist_kernel(KmArgs a) {
   __shared__ uint32_t s_key[kKmTile];
+  __shared__ int32_t s_cnt[kHistLdsCounts];
   const int p = blockIdx.y;
   if (a.done[p]) return;
   if (a.iter > 1 && a.changed[(int64_t)a.iter * a.B * a.Hkv + p] == 0) {
@@ -278,6 +281,9 @@ __global__ __launch_bounds__(1024) void km_hist_kernel(KmArgs a) {
   if (i0 >= q.n) return;
   const int m = min(kKmTile, q.n - i0);
   const int tid = threadIdx.x;
+  const bool lds_counts = q.C <= kHistLdsCounts;
+  if (lds_counts)
+    for (int c = tid; c < q.C; c += 1024) s_cnt[c] = 0;  // ordered before use by the sort's barriers
   for (int x = tid; x < kKmTile; x += 1024)
     s_key[x] = x < m ? ((uint32_t)a.assign[q.tok_base + i0 + x] << 11) | (uint32_t)x : 0xffffffffu;
   // bitonic sort of 2048 keys, one compare-exchange per thread per step
@@ -295,23 +301,35 @@ __global__ __launch_bounds__(1024) void km_hist_kernel(KmArgs a) {
     }
   }
   __syncthreads();
+  // rank of each token among the tile's tokens of its cluster (offset from
+  // the start of its run of equal clusters); the last token of a run holds
+  // the cluster's count in this tile
   for (int s = tid; s < m; s += 1024) {
     const uint32_t key = s_key[s];
     const uint32_t c = key >> 11;
     const int lb = lower_bound_u32(s_key, m, c << 11);
     a.local_rank[q.tok_base + i0 + (key & 2047u)] = s - lb;
+    if (lds_counts && (s == m - 1 || (s_key[s + 1] >> 11) != c)) s_cnt[c] = s - lb + 1;
   }
-  int32_t* tab = a.table + (int64_t)p * a.Cm * a.tiles_max;
-  for (int c = tid; c < q.C; c += 1024) {
-    const int lo = lower_bound_u32(s_key, m, (uint32_t)c << 11);
-    const int hi = lower_bound_u32(s_key, m, (uint32_t)(c + 1) << 11);
-    tab[(int64_t)c * q.tiles + t] = hi - lo;
+  int32_t* tab = a.table + (int64_t)p * a.Cm * a.tiles_max + (int64_t)t * q.C;  // this tile's row
+  if (lds_counts) {
+    __syncthreads();
+    for (int c = tid; c < q.C; c += 1024) tab[c] = s_cnt[c];
+  } else {
+    for (int c = tid; c < q.C; c += 1024) {
+      const int lo = lower_bound_u32(s_key, m, (uint32_t)c << 11);
+      const int hi = lower_bound_u32(s_key, m, (uint32_t)(c + 1) << 11);
+      tab[c] = hi - lo;
+    }
   }
 }
 
 // ---------------------------------------------------------------------------
-// exclusive scan of the (cluster, tile) counts, cluster-major
+// exclusive scan of the (cluster, tile) counts in cluster-major order
+// (x = c * tiles + t); the table is stored tile-major (entry t * C + c), so
+// that each counting tile writes one contiguous row
 // ---------------------------------------------------------------------------
+
 __device__ __forceinline__ bool km_active(const KmArgs& a, int p) {
   return !a.done[p];
 }
@@ -325,8 +343,16 @@ __global__ __launch_bounds__(1024) void km_scan1_kernel(KmArgs a) {
   const int64_t x0 = (int64_t)blockIdx.x * kKmChunk;
   if (x0 >= E) return;
   const int32_t* tab = a.table + (int64_t)p * a.Cm * a.tiles_max;
+  // 16 consecutive entries per thread, their (tile, cluster) stepped from
+  // the first one's
+  const int64_t b0 = x0 + (int64_t)threadIdx.x * 16, b1 = min(E, b0 + 16);
+  const int t0 = (int)(b0 % q.tiles), c0 = (int)(b0 / q.tiles);
   int s = 0;
-  for (int64_t x = x0 + threadIdx.x; x < min(E, x0 + kKmChunk); x += 1024) s += tab[x];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const int te = t0 + e;
+    if (b0 + e < b1) s += tab[(int64_t)(te % q.tiles) * q.C + c0 + te / q.tiles];
+  }
   for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
   if ((threadIdx.x & 63) == 0) s_w[threadIdx.x >> 6] = s;
   __syncthreads();
@@ -366,11 +392,17 @@ __global__ __launch_bounds__(1024) void km_scan3_kernel(KmArgs a) {
   int32_t* tab = a.table + (int64_t)p * a.Cm * a.tiles_max;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t b0 = x0 + (int64_t)tid * 16, b1 = min(E, b0 + 16);
+  // the 16 entries' (tile, cluster), stepped from the first one's
+  const int t0 = (int)(b0 % q.tiles), c0 = (int)(b0 / q.tiles);
+  int64_t ix[16];
   int v[16];
   int loc = 0;
 #pragma unroll
   for (int e = 0; e < 16; ++e) {
-    v[e] = b0 + e < b1 ? tab[b0 + e] : 0;
+    const int te = t0 + e;  // e < 16: at most ceil(16 / tiles) wraps, folded below
+    const int ce = c0 + te / q.tiles;
+    ix[e] = (int64_t)(te % q.tiles) * q.C + ce;
+    v[e] = b0 + e < b1 ? tab[ix[e]] : 0;
     loc += v[e];
   }
   int incl = wave_incl_scan(loc);  // DPP, no LDS
@@ -390,7 +422,7 @@ __global__ __launch_bounds__(1024) void km_scan3_kernel(KmArgs a) {
   for (int e = 0; e < 16; ++e) {
     const int64_t x = b0 + e;
     if (x < b1) {
-      tab[x] = run;
+      tab[ix[e]] = run;
       if (x % q.tiles == 0) a.offsets[q.off_base + x / q.tiles] = run;  // start of cluster x / tiles
       run += v[e];
     }
@@ -411,7 +443,7 @@ __global__ __launch_bounds__(1024) void km_perm_kernel(KmArgs a) {
   for (int x = threadIdx.x; x < min(kKmTile, q.n - i0); x += 1024) {
     const int i = i0 + x;
     const int c = a.assign[q.tok_base + i];
-    const int row = tab[(int64_t)c * q.tiles + t] + a.local_rank[q.tok_base + i];
+    const int row = tab[(int64_t)t * q.C + c] + a.local_rank[q.tok_base + i];
     a.perm[q.tok_base + min(max(row, 0), q.n - 1)] = i;
   }
 }
