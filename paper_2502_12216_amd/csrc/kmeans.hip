@@ -460,15 +460,30 @@ __global__ __launch_bounds__(256) void km_mean_kernel(KmArgs a) {
   if (j >= q.C) return;
   const int o0 = a.offsets[q.off_base + j], o1 = a.offsets[q.off_base + j + 1];
   if (o1 <= o0) return;  // empty cluster keeps its centroid
+  // lane-group grp sums rows grp, grp + 4, grp + 8, ... in that order; 16
+  // rows per step, their token ids and then their key rows loaded together
   float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int r = o0 + grp; r < o1; r += 4) {
-    const int tok = a.perm[q.tok_base + r];
-    const uint4 v = *reinterpret_cast<const uint4*>(a.K + (q.tok_base + tok) * kHeadDim + sl * 8);
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  for (int r0 = o0; r0 < o1; r0 += 16) {
+    int tok[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      s[2 * e] += bf16lo(w[e]);
-      s[2 * e + 1] += bf16hi(w[e]);
+    for (int k = 0; k < 4; ++k) {
+      const int r = r0 + grp + 4 * k;
+      tok[k] = r < o1 ? a.perm[q.tok_base + r] : -1;
+    }
+    uint4 v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      v[k] = tok[k] >= 0 ? *reinterpret_cast<const uint4*>(a.K + (q.tok_base + tok[k]) * kHeadDim + sl * 8)
+                         : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (tok[k] < 0) continue;
+      const uint32_t w[4] = {v[k].x, v[k].y, v[k].z, v[k].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        s[2 * e] += bf16lo(w[e]);
+        s[2 * e + 1] += bf16hi(w[e]);
+      }
     }
   }
   const float inv = 1.f / (float)(o1 - o0);
