@@ -347,10 +347,15 @@ def test_kmeans_one_cluster_per_token_is_identity():
 
 def test_kmeans_matches_scipy_lloyd():
     """Without bf16 storage the iteration is Lloyd's algorithm, which
-    scipy.cluster.vq.kmeans2(minit='matrix') also runs (same empty-cluster
-    rule); data without empty clusters must give identical results."""
+    scipy.cluster.vq.kmeans2(minit='matrix') also runs.  Its default for a
+    cluster that loses all members (missing='warn': warn, keep the previous
+    centroid) is the empty-cluster reading of Sec. 4.2 taken here, so trials
+    with and without an emptied cluster must both give identical results;
+    the seeds below produce both kinds."""
+    import warnings
     from scipy.cluster.vq import kmeans2
     rng = np.random.default_rng(11)
+    kinds = set()
     for trial in range(5):
         C, per = 12, 30
         cen = rng.standard_normal((C, 16)) * 4
@@ -358,9 +363,16 @@ def test_kmeans_matches_scipy_lloyd():
         K = K[rng.permutation(len(K))]
         init = rng.choice(len(K), C, replace=False)
         r = KM.kmeans(K, init, max_iters=10, round_storage=False)
-        cb, lab = kmeans2(K, K[init].copy(), iter=10, minit="matrix")
+        with warnings.catch_warnings(record=True) as caught:
+            warnings.simplefilter("always")
+            cb, lab = kmeans2(K, K[init].copy(), iter=10, minit="matrix")
+        emptied = any("empty" in str(w.message) for w in caught)
+        kinds.add(emptied)
+        if not emptied:
+            assert np.bincount(r.assign, minlength=C).min() > 0
         np.testing.assert_array_equal(r.assign, lab)
         np.testing.assert_allclose(r.centroids, cb, atol=1e-12)
+    assert kinds == {True, False}
 
 
 def test_kmeans_inertia_non_increasing():
