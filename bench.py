@@ -115,6 +115,7 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-ablation", action="store_true", help="skip the per-head (no-union) comparison")
     ap.add_argument("--no-paged", action="store_true", help="skip the paged-cache comparison")
+    ap.add_argument("--no-recent", action="store_true", help="skip the recent-token / re-clustering run")
     ap.add_argument("--calibrate", action="store_true",
                     help="also run a plain 1 GiB device copy (reference dispatch for HBM counters)")
     return ap.parse_args()
@@ -332,6 +333,59 @@ def main():
         del pcs
         log(f"paged step ({keep} layers) {ms_p:.3f} ms vs {ms_c:.3f} ms cluster-sorted")
 
+    # ---------------------------------------------------------------- recent tokens + re-clustering (Sec. 1)
+    recent = None
+    if not args.no_recent and len(set(wl.seq_lens)) == 1:
+        T_rec = 2048
+        n = int(wl.seq_lens[0])
+        kvp = batch.kv_indptr_host
+        inp0 = synth.make_layer(wl, 0, device=dev)  # layer 0 in token order
+        cache = T.RecentTailCache(Hq, Hkv, list(wl.seq_lens), recluster_every=T_rec, cluster_div=n // ncl[0],
+                                  kmeans_iters=wl.kmeans_iters, target_frac=P, seed=5, device=dev)
+        cut = n - T_rec
+
+        def timed_once(fn):
+            torch.cuda.synchronize()
+            ev0.record()
+            fn()
+            ev1.record()
+            torch.cuda.synchronize()
+            return ev0.elapsed_time(ev1)
+
+        ms_prefill = timed_once(lambda: cache.prefill([inp0.K[:, kvp[b]:kvp[b] + cut] for b in range(B)],
+                                                      [inp0.V[:, kvp[b]:kvp[b] + cut] for b in range(B)]))
+        for i in range(T_rec - 1):
+            rows = [int(kvp[b]) + cut + i for b in range(B)]
+            cache.append(inp0.K[:, rows].transpose(0, 1), inp0.V[:, rows].transpose(0, 1))
+        q0 = qs[0]
+
+        def decode_us():
+            cache.decode(q0)
+            return timed(lambda: cache.decode(q0), 20) * 1000
+
+        us_tail = decode_us()
+        tail_now = cache.recent[0]
+        rows = [int(kvp[b]) + n - 1 for b in range(B)]
+        ms_warm = timed_once(lambda: cache.append(inp0.K[:, rows].transpose(0, 1), inp0.V[:, rows].transpose(0, 1)))
+        assert cache.recent[0] == 0, "the last append re-clusters"
+        us_fresh = decode_us()
+        cache.warm_start = False
+        ms_cold = timed_once(cache.recluster)
+        us_cold_fresh = decode_us()
+        recent = {"layer": 0, "tail_tokens": tail_now, "recluster_every": T_rec,
+                  "sparse_us_with_tail": round(us_tail, 2), "sparse_us_after_recluster": round(us_fresh, 2),
+                  "sparse_us_after_cold_recluster": round(us_cold_fresh, 2),
+                  "prefill_cluster_ms": round(ms_prefill, 2),
+                  "recluster_warm_ms": round(ms_warm, 2), "recluster_cold_ms": round(ms_cold, 2),
+                  "amortized_us_per_step_warm": round(ms_warm * 1000 / T_rec, 2),
+                  "amortized_us_per_step_cold": round(ms_cold * 1000 / T_rec, 2),
+                  "note": "one layer of the workload; prefill of n - 2048 tokens, 2047 appended, the 2048th "
+                          "append re-clusters from the previous centroids (warm), then a cold re-clustering of "
+                          "the same cache for comparison; the warm time includes the append"}
+        del cache, inp0
+        log(f"recent tail: decode {us_tail:.1f} us with {tail_now} recent tokens, re-clustering warm {ms_warm:.1f} ms "
+            f"cold {ms_cold:.1f} ms")
+
     # ---------------------------------------------------------------- selection statistics, bytes
     sel_q, sel_kv, samples = [], [], []
     for l in range(layers):
@@ -448,6 +502,7 @@ def main():
         "cpu_baseline": cpu,
         "union_ablation": ablation,
         "paged_kv": paged,
+        "recent_tail": recent,
     }
     if args.clusters == "kmeans":
         res["kmeans"] = {"seconds_all_layers": round(kmeans_ms / 1000, 3), "layers": layers,

@@ -247,7 +247,7 @@ tactic_status tactic_dense_decode_paged(const uint16_t* q, const tactic_paged_kv
  *   K, V          bf16 [Hkv][total_tokens][128], original token order
  *   cl_indptr     device [B+1] (C_b = cl_indptr[b+1] - cl_indptr[b], 1 <= C_b <= n_b)
  *   init_idx      device int32 [Hkv][total_clusters]: C_b distinct sequence-relative
- *                 token ids per (b, g)
+ *                 token ids per (b, g) (entries of warm-started centroids are ignored)
  * Outputs: centroids bf16 [Hkv][total_clusters][128], assign int32 [Hkv][total_tokens]
  * (cluster of each original token), offsets int32 [Hkv][total_clusters + B] and perm
  * int32 [Hkv][total_tokens] (original token of each cluster-sorted row, ascending
@@ -255,6 +255,18 @@ tactic_status tactic_dense_decode_paged(const uint16_t* q, const tactic_paged_kv
  * be null to skip it). */
 typedef struct {
   int32_t max_iters;           /* default 10 (Sec. 4.2) */
+  int32_t reserved;            /* 0 */
+  /* Warm start (re-clustering, Sec. 1: the cache is re-clustered periodically
+   * while decoding).  NULL: every centroid starts from init_idx.  Otherwise a
+   * previous clustering of the same sequences and KV heads: prev_cl_indptr is
+   * device int64 [B+1] (prev C_b = prev_cl_indptr[b+1] - prev_cl_indptr[b]) and
+   * prev_centroids bf16 [Hkv][prev_cl_indptr[B]][128]; centroid j of (b, g)
+   * starts from previous centroid j of (b, g) for j < min(C_b, prev C_b) (its
+   * init_idx entry is ignored) and from the key init_idx names for the rest.
+   * Both pointers are set or both are NULL; the arrays are read by the first
+   * kernel only.  An all-zero struct with max_iters set is a cold start. */
+  const uint16_t* prev_centroids;
+  const int64_t* prev_cl_indptr;
 } tactic_kmeans_params;
 
 size_t tactic_build_clusters_workspace_size(const tactic_kv_shape* shape, int64_t total_clusters,

@@ -61,10 +61,19 @@ class KMeansResult:
     inertia: List[float] = field(default_factory=list)  # sum of squared distances after each assignment
 
 
-def kmeans(K: np.ndarray, init_idx, max_iters: int = 10, round_storage: bool = True) -> KMeansResult:
-    """Lloyd iterations from the keys of the sampled tokens (Sec. 4.2)."""
+def kmeans(K: np.ndarray, init_idx, max_iters: int = 10, round_storage: bool = True,
+           prev_centroids=None) -> KMeansResult:
+    """Lloyd iterations from the keys of the sampled tokens (Sec. 4.2).
+
+    prev_centroids (re-clustering, Sec. 1): the stored centroids of a previous
+    clustering; centroid j starts from prev_centroids[j] for j below both
+    counts and from the key of token init_idx[j] otherwise."""
     init_idx = np.asarray(init_idx, dtype=np.int64)
-    C = K[init_idx].copy()
+    m = 0 if prev_centroids is None else min(len(init_idx), len(prev_centroids))
+    C = np.empty((len(init_idx), K.shape[1]))
+    if m:
+        C[:m] = np.asarray(prev_centroids, dtype=np.float64)[:m]
+    C[m:] = K[init_idx[m:]]
     prev = None
     inertia = []
     it = 0

@@ -58,7 +58,8 @@ class PagedKV(ctypes.Structure):
 
 
 class KMeansParams(ctypes.Structure):
-    _fields_ = [("max_iters", c_int32)]
+    _fields_ = [("max_iters", c_int32), ("reserved", c_int32), ("prev_centroids", c_void_p),
+                ("prev_cl_indptr", c_void_p)]
 
 
 class TacticError(RuntimeError):

@@ -29,13 +29,14 @@ class RecentTailCache:
 
     def __init__(self, n_q_heads: int, n_kv_heads: int, capacities: Sequence[int], recluster_every: int = 2048,
                  cluster_div: int = 16, kmeans_iters: int = 10, target_frac: float = 0.9, seed: int = 0,
-                 device="cuda"):
+                 warm_start: bool = True, device="cuda"):
         self.capacities = [int(c) for c in capacities]
         self.Hq, self.Hkv = int(n_q_heads), int(n_kv_heads)
         self.recluster_every = int(recluster_every)
         self.cluster_div = int(cluster_div)
         self.kmeans_iters = int(kmeans_iters)
         self.target_frac = float(target_frac)
+        self.warm_start = bool(warm_start)
         self.device = device
         self.rng = np.random.default_rng(seed)
         B = len(self.capacities)
@@ -90,16 +91,26 @@ class RecentTailCache:
 
     def recluster(self) -> None:
         """K-means over every held token of every sequence (prompt and recent),
-        then the cache is the cluster-sorted copy and no token is recent."""
+        then the cache is the cluster-sorted copy and no token is recent.
+
+        With warm_start and a previous clustering, centroid j of every
+        (sequence, KV head) starts from the previous centroid j (j below both
+        cluster counts) and the added clusters from distinct recent tokens, so
+        the iterations only have to absorb the recent tokens; otherwise every
+        centroid starts from a distinct sampled token."""
         ncl = [self.n_clusters(n) for n in self.lens]
+        prev = self.clusters if (self.warm_start and self.clusters is not None) else None
         init = np.zeros((self.Hkv, int(sum(ncl))), dtype=np.int32)
         c0 = 0
         for b, (n, C) in enumerate(zip(self.lens, ncl)):
+            m = min(C, prev.n_clusters[b]) if prev is not None else 0
+            lo = self.clustered[b] if C - m <= n - self.clustered[b] else 0  # seed from the recent tokens
             for g in range(self.Hkv):
-                init[g, c0:c0 + C] = self.rng.choice(max(n, 1), size=C, replace=n < C) if n else 0
+                if n and C > m:
+                    init[g, c0 + m:c0 + C] = lo + self.rng.choice(n - lo, size=C - m, replace=n - lo < C - m)
             c0 += C
         builder = ClusterBuilder(self.batch, ncl, max_iters=self.kmeans_iters, device=self.device)
-        res = builder(self.K, self.V, torch.as_tensor(init, device=self.device))
+        res = builder(self.K, self.V, torch.as_tensor(init, device=self.device), prev=prev)
         self.K, self.V = res.K_sorted, res.V_sorted
         self.clusters = res.clusters
         self.clustered = list(self.lens)

@@ -532,12 +532,15 @@ tactic_status tactic_build_clusters(const uint16_t* K, const uint16_t* V, const 
   if (params->max_iters < 1 || params->max_iters > 1000)
     return fail(TACTIC_ERR_INVALID_ARG, "max_iters must be in [1, 1000]");
   if (max_clusters >= (1 << 21)) return fail(TACTIC_ERR_UNSUPPORTED, "more than 2^21 - 1 clusters");
+  if ((params->prev_centroids == nullptr) != (params->prev_cl_indptr == nullptr))
+    return fail(TACTIC_ERR_INVALID_ARG, "prev_centroids and prev_cl_indptr must be set together");
   const size_t need = tactic_build_clusters_workspace_size(shape, total_clusters, max_clusters);
   if (!workspace || workspace_bytes < need)
     return fail(TACTIC_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
   hipError_t e = tactic::run_kmeans(K, V, shape->kv_indptr, shape->seq_len, cl_indptr, shape->batch, shape->n_kv_heads,
                                     shape->total_tokens, shape->max_seq_len, total_clusters, max_clusters,
-                                    init_idx, params->max_iters, centroids, assign, offsets, perm, K_sorted,
+                                    init_idx, params->max_iters, params->prev_centroids, params->prev_cl_indptr,
+                                    centroids, assign, offsets, perm, K_sorted,
                                     V_sorted, workspace, stream);
   if (e != hipSuccess) return hip_fail(e, "k-means launch");
   return TACTIC_OK;

@@ -47,6 +47,8 @@ struct KmArgs {
   int B, Hkv, Cm, tiles_max, chunks_max, iter, max_iters;
   int64_t total, Ct;
   const int32_t* init_idx;
+  const uint16_t* prev_centroids;  // warm start, or null
+  const int64_t* prev_cl_indptr;
   uint16_t* centroids;
   float* cnorm;
   int32_t* assign;
@@ -87,7 +89,8 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
 }
 
 // ---------------------------------------------------------------------------
-// init: c0 = K[init_idx], ||c0||^2, per-problem flags.  grid (ceil(Cm/4), BG)
+// init: c0 = K[init_idx] (or the previous clustering's centroid j for a warm
+// start), ||c0||^2, per-problem flags.  grid (ceil(Cm/4), BG)
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void km_init_kernel(KmArgs a) {
   const int p = blockIdx.y;
@@ -99,8 +102,17 @@ __global__ __launch_bounds__(256) void km_init_kernel(KmArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, sl = lane & 15, grp = lane >> 4;
   const int j = blockIdx.x * 4 + wave;
   if (j >= q.C || grp != 0 || q.n == 0) return;
-  const int t = min(max(a.init_idx[q.cl_base + j], 0), q.n - 1);
-  const uint4 v = *reinterpret_cast<const uint4*>(a.K + (q.tok_base + t) * kHeadDim + sl * 8);
+  uint4 v;
+  const int64_t pc0 = a.prev_centroids ? a.prev_cl_indptr[q.b] : 0;
+  const int64_t pc1 = a.prev_centroids ? a.prev_cl_indptr[q.b + 1] : 0;
+  if (j < pc1 - pc0) {
+    // warm start: the previous clustering's centroid j of this (b, g)
+    const int64_t prev_total = a.prev_cl_indptr[a.B];
+    v = *reinterpret_cast<const uint4*>(a.prev_centroids + ((int64_t)q.g * prev_total + pc0 + j) * kHeadDim + sl * 8);
+  } else {
+    const int t = min(max(a.init_idx[q.cl_base + j], 0), q.n - 1);
+    v = *reinterpret_cast<const uint4*>(a.K + (q.tok_base + t) * kHeadDim + sl * 8);
+  }
   *reinterpret_cast<uint4*>(a.centroids + (q.cl_base + j) * kHeadDim + sl * 8) = v;
   const uint32_t w[4] = {v.x, v.y, v.z, v.w};
   float s = 0.f;
@@ -561,7 +573,7 @@ size_t kmeans_workspace_bytes(int B, int Hkv, int64_t total, int64_t Ct, int Cm,
 hipError_t run_kmeans(const uint16_t* K, const uint16_t* V, const int64_t* kv_indptr, const int64_t* seq_len,
                       const int64_t* cl_indptr, int B, int Hkv, int64_t total, int64_t nmax,
                       int64_t Ct, int Cm, const int32_t* init_idx, int max_iters,
-                      uint16_t* centroids, int32_t* assign, int32_t* offsets, int32_t* perm,
+                      const uint16_t* prev_centroids, const int64_t* prev_cl_indptr, uint16_t* centroids, int32_t* assign, int32_t* offsets, int32_t* perm,
                       uint16_t* K_sorted, uint16_t* V_sorted, void* workspace, hipStream_t st) {
   if (max_iters > kKmMaxIters) return hipErrorInvalidValue;
   const KmLayout L = km_layout(B, Hkv, total, Ct, Cm, nmax);
@@ -582,6 +594,8 @@ hipError_t run_kmeans(const uint16_t* K, const uint16_t* V, const int64_t* kv_in
   a.total = total;
   a.Ct = Ct;
   a.init_idx = init_idx;
+  a.prev_centroids = prev_centroids;
+  a.prev_cl_indptr = prev_cl_indptr;
   a.centroids = centroids;
   a.cnorm = reinterpret_cast<float*>(ws + L.off_cnorm);
   a.assign = assign;

@@ -311,13 +311,25 @@ class ClusterBuilder:
         self.device = device
 
     def __call__(self, K: torch.Tensor, V: Optional[torch.Tensor], init_idx: torch.Tensor, sort_kv: bool = True,
-                 stream=None) -> ClusterBuild:
+                 stream=None, prev: Optional[ClusterSet] = None) -> ClusterBuild:
+        """prev: a previous clustering of the same sequences to start from (its
+        centroid j of every (sequence, KV head) for j below both cluster counts;
+        see tactic_kmeans_params)."""
         b = self.batch
         Hkv = b.n_kv_heads
         _check_tensor(K, "K", torch.bfloat16, (Hkv, b.total, 128))
         if V is not None:
             _check_tensor(V, "V", torch.bfloat16, (Hkv, b.total, 128))
         _check_tensor(init_idx, "init_idx", torch.int32, (Hkv, self.total_c))
+        if prev is not None:
+            if len(prev.n_clusters) != b.batch:
+                raise ValueError("prev clustering has another batch size")
+            _check_tensor(prev.centroids, "prev.centroids", torch.bfloat16, (Hkv, prev.total, 128))
+            self.params.prev_centroids = prev.centroids.data_ptr()
+            self.params.prev_cl_indptr = prev.cl_indptr.data_ptr()
+        else:
+            self.params.prev_centroids = None
+            self.params.prev_cl_indptr = None
         dev = K.device
         cent = torch.empty(Hkv, self.total_c, 128, dtype=torch.bfloat16, device=dev)
         assign = torch.empty(Hkv, b.total, dtype=torch.int32, device=dev)

@@ -137,6 +137,13 @@ def test_dense_and_kmeans_validation():
     st = L.tactic_build_clusters(FAKE, FAKE, ctypes.byref(shape), FAKE, 100, 256, FAKE, ctypes.byref(kp),
                                  FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, m, None)
     assert st == 1
+    # a warm start needs both the previous centroids and their cluster offsets
+    for pc, pi in ((FAKE, None), (None, FAKE)):
+        kp2 = C.KMeansParams(10, 0, pc, pi)
+        st = L.tactic_build_clusters(FAKE, FAKE, ctypes.byref(shape), FAKE, 256, 256, FAKE, ctypes.byref(kp2),
+                                     FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, m, None)
+        assert st == 1
+        assert b"together" in L.tactic_last_error()
 
 
 def test_status_strings():

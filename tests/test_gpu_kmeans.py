@@ -189,3 +189,68 @@ def test_kmeans_spare_room_layout_matches_packed():
         s0, d0 = packed.kv_indptr_host[b], spaced.kv_indptr_host[b]
         assert torch.equal(r1.assign[:, s0:s0 + n], r2.assign[:, d0:d0 + n])
         assert torch.equal(r1.K_sorted[:, s0:s0 + n], r2.K_sorted[:, d0:d0 + n])
+
+
+@pytest.mark.parametrize("iters", [1, 10])
+def test_kmeans_warm_start_parity(iters):
+    """Re-clustering from a previous clustering (tactic_kmeans_params
+    prev_centroids / prev_cl_indptr): centroid j of (b, g) starts from the
+    previous centroid j below both cluster counts, from the init_idx key
+    otherwise.  The previous centroids are the oracle's own CPU clustering
+    (3 iterations, bf16 storage) with fewer, more and as many clusters as the
+    new one, so no oracle input comes from the GPU.  One step: assignment
+    from the warm start identical except near ties, update within 1 bf16 ulp;
+    ten steps: inertia within 0.1% of the oracle's warm run."""
+    T = _tactic()
+    wl = synth.small_workload(synth.WORKLOADS["ctx4k_gqa4"], [3000, 1500, 700])
+    inp = synth.make_layer(wl, 0)
+    lens = [int(inp.kv_indptr[i + 1] - inp.kv_indptr[i]) for i in range(len(inp.kv_indptr) - 1)]
+    ncl = [wl.n_clusters(n) for n in lens]
+    prev_ncl = [ncl[0] - 7, ncl[1] + 5, ncl[2]]
+    Hkv = wl.n_kv_heads
+    kv = np.concatenate([[0], np.cumsum(lens)])
+    pcl = np.concatenate([[0], np.cumsum(prev_ncl)])
+    cl = np.concatenate([[0], np.cumsum(ncl)])
+    rng = np.random.default_rng(31)
+    prev_cent = np.zeros((Hkv, int(pcl[-1]), 128))
+    for b in range(len(lens)):
+        for g in range(Hkv):
+            K = np64(inp.K[g, int(kv[b]):int(kv[b + 1])])
+            r = OK.kmeans(K, rng.choice(lens[b], prev_ncl[b], replace=False), max_iters=3)
+            prev_cent[g, int(pcl[b]):int(pcl[b + 1])] = r.centroids
+    prev = T.ClusterSet(torch.tensor(prev_cent, dtype=torch.bfloat16, device=DEV),
+                        torch.zeros(Hkv, int(pcl[-1]) + len(lens), dtype=torch.int32, device=DEV), prev_ncl)
+    batch = T.RaggedBatch(lens, wl.n_q_heads, Hkv)
+    builder = T.ClusterBuilder(batch, ncl, max_iters=iters)
+    init_np = synth.kmeans_init_all(wl, inp.layer)
+    res = builder(inp.K.to(DEV).contiguous(), inp.V.to(DEV).contiguous(), torch.as_tensor(init_np, device=DEV),
+                  prev=prev)
+    torch.cuda.synchronize()
+    ties = 0
+    for b, g in _groups(lens, Hkv):
+        sl = _slices(inp, res, lens, ncl, b, g)
+        K = sl["K"]
+        ini = init_np[g, int(cl[b]):int(cl[b + 1])].astype(np.int64)
+        pc = prev_cent[g, int(pcl[b]):int(pcl[b + 1])]
+        m = min(ncl[b], prev_ncl[b])
+        c_start = np.concatenate([pc[:m], K[ini[m:]]])
+        if iters == 1:
+            D = OK.sq_distances(K, c_start)
+            a_or = np.argmin(D, axis=1)
+            a_gpu = sl["assign"]
+            diff = np.nonzero(a_or != a_gpu)[0]
+            if len(diff):
+                kk = np.einsum("ij,ij->i", K[diff], K[diff])
+                cc = np.einsum("ij,ij->i", c_start[a_or[diff]], c_start[a_or[diff]])
+                gap = np.abs(D[diff, a_gpu[diff]] - D[diff, a_or[diff]])
+                assert np.all(gap <= 1e-4 * (kk + cc)), f"b={b} g={g}: {len(diff)} assignments differ beyond ties"
+                ties += len(diff)
+            c_or = OK.update_step(K, a_gpu, c_start, round_storage=True)
+            assert np.max(np.abs(_bf16_bits(c_or) - _bf16_bits(sl["cent"]))) <= 1, f"b={b} g={g}"
+        else:
+            r = OK.kmeans(K, ini, max_iters=10, prev_centroids=pc)
+            in_or = OK.inertia(K, r.assign, r.centroids)
+            in_gpu = OK.inertia(K, sl["assign"], sl["cent"])
+            assert abs(in_gpu - in_or) <= 1e-3 * in_or, f"b={b} g={g}: inertia gpu {in_gpu} oracle {in_or}"
+    print(f"kmeans warm start, {iters} iteration(s): near-tie assignment differences {ties}")
+

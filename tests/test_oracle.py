@@ -375,6 +375,46 @@ def test_kmeans_matches_scipy_lloyd():
     assert kinds == {True, False}
 
 
+def test_kmeans_warm_start_from_converged_clustering_is_a_fixed_point():
+    """Re-clustering (Sec. 1) from a clustering that has converged (its last
+    assignment step changed nothing) must stop at the second assignment of
+    the new run with the same assignment and the same stored centroids."""
+    rng = np.random.default_rng(21)
+    C, per = 16, 40
+    cen = rng.standard_normal((C, 16)) * 3
+    K = NUM.round_bf16(np.concatenate([cen[j] + rng.standard_normal((per, 16)) for j in range(C)]))
+    r0 = KM.kmeans(K, rng.choice(len(K), C, replace=False), max_iters=200)
+    assert r0.iters < 200, "the cold run must converge for this pin"
+    garbage = np.full(C, len(K) - 1)  # ignored: every centroid is warm-started
+    r1 = KM.kmeans(K, garbage, max_iters=10, prev_centroids=r0.centroids)
+    assert r1.iters == 2
+    np.testing.assert_array_equal(r1.assign, r0.assign)
+    np.testing.assert_array_equal(r1.centroids, r0.centroids)
+
+
+def test_kmeans_warm_start_takes_the_prefix_from_the_previous_centroids():
+    """Centroid j starts from the previous clustering's centroid j below both
+    counts and from init_idx above: previous centroids equal to the keys of
+    the first init tokens reproduce the cold run whatever init_idx holds
+    there, with previous clusterings shorter and longer than the new one."""
+    rng = np.random.default_rng(22)
+    K = NUM.round_bf16(rng.standard_normal((600, 32)))
+    C = 24
+    init = rng.choice(len(K), C, replace=False)
+    cold = KM.kmeans(K, init, max_iters=6)
+    for m in (1, 10, C):
+        init2 = init.copy()
+        init2[:m] = rng.integers(0, len(K), m)  # ignored entries
+        prev = np.concatenate([K[init[:m]], rng.standard_normal((3, 32))]) if m == C else K[init[:m]]
+        warm = KM.kmeans(K, init2, max_iters=6, prev_centroids=prev)
+        np.testing.assert_array_equal(warm.assign, cold.assign)
+        np.testing.assert_array_equal(warm.centroids, cold.centroids)
+    # and a previous centroid that differs from the key changes the run
+    prev = K[init[:1]] + 5.0
+    assert not np.array_equal(KM.kmeans(K, init, max_iters=1, prev_centroids=prev).assign,
+                              KM.kmeans(K, init, max_iters=1).assign)
+
+
 def test_kmeans_inertia_non_increasing():
     rng = np.random.default_rng(12)
     K = rng.standard_normal((2000, 128))
