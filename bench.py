@@ -111,7 +111,8 @@ def parse():
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (0: the workload's)")
     ap.add_argument("--target-frac", type=float, default=0.9)
     ap.add_argument("--clusters", choices=["kmeans", "labels"], default="kmeans")
-    ap.add_argument("--cpu-groups", type=int, default=4, help="(b, g) groups the CPU oracle times")
+    ap.add_argument("--cpu-groups", type=int, default=96,
+                    help="(sequence, KV head) groups the CPU oracle times, all groups of layer 0, then layer 1, ...")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-ablation", action="store_true", help="skip the per-head (no-union) comparison")
     ap.add_argument("--no-paged", action="store_true", help="skip the paged-cache comparison")
@@ -430,24 +431,26 @@ def main():
     cpu = None
     if not args.no_cpu:
         from oracle import tactic as OT
-        rng = np.random.default_rng(17)
-        groups = [(int(rng.integers(0, B)), int(rng.integers(0, Hkv))) for _ in range(args.cpu_groups)]
-        cl0 = cls[0]
+        n_groups = max(1, min(args.cpu_groups, layers * B * Hkv))
         kvp = batch.kv_indptr_host
-        clp = cl0.cl_indptr_host
         t_or = 0.0
-        for b, g in groups:
+        for idx in range(n_groups):
+            l, r = divmod(idx, B * Hkv)
+            b, g = divmod(r, Hkv)
+            cl_l = cls[l]
+            clp = cl_l.cl_indptr_host
             s0, s1 = int(kvp[b]), int(kvp[b + 1])
             c0, c1 = int(clp[b]), int(clp[b + 1])
-            Qg = qs[0][b, g * G:(g + 1) * G].double().cpu().numpy()
-            Kg = Ks[0][g, s0:s1].double().cpu().numpy()
-            Vg = Vs[0][g, s0:s1].double().cpu().numpy()
-            cent = cl0.centroids[g, c0:c1].double().cpu().numpy()
-            off = cl0.offsets[g, c0 + b:c1 + b + 1].cpu().numpy().astype(np.int64)
+            Qg = qs[l][b, g * G:(g + 1) * G].double().cpu().numpy()
+            Kg = Ks[l][g, s0:s1].double().cpu().numpy()
+            Vg = Vs[l][g, s0:s1].double().cpu().numpy()
+            cent = cl_l.centroids[g, c0:c1].double().cpu().numpy()
+            off = cl_l.offsets[g, c0 + b:c1 + b + 1].cpu().numpy().astype(np.int64)
             t0 = time.perf_counter()
             OT.decode_group(Qg, Kg, Vg, cent, off, P)
             t_or += time.perf_counter() - t0
-        per_group = t_or / len(groups)
+            del Qg, Kg, Vg, cent, off
+        per_group = t_or / n_groups
         try:
             from threadpoolctl import threadpool_info
             blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
@@ -455,8 +458,9 @@ def main():
             blas_threads = 1
         cpu = {"value": round(per_group * B * Hkv * 1e6, 1), "unit": "us/layer", "cores": int(blas_threads),
                "kind": "oracle",
-               "sample": f"{len(groups)} of the {B * Hkv} (sequence, KV head) groups of layer 0, fp64 NumPy "
-                         f"oracle decode_group each ({t_or:.1f} s total), scaled to one layer; "
+               "sample": f"{n_groups} (sequence, KV head) groups (every group of layer 0, then layer 1, ...; "
+                         f"{B * Hkv} per layer), fp64 NumPy oracle decode_group each, {t_or:.1f} s in total, "
+                         f"mean per group x {B * Hkv} groups = one layer; "
                          f"host {platform.processor() or platform.machine()}, "
                          f"{len(os.sched_getaffinity(0))} cores visible"}
         log(f"cpu oracle {per_group:.2f} s per group")
