@@ -263,8 +263,10 @@ typedef struct {
    * prev_centroids bf16 [Hkv][prev_cl_indptr[B]][128]; centroid j of (b, g)
    * starts from previous centroid j of (b, g) for j < min(C_b, prev C_b) (its
    * init_idx entry is ignored) and from the key init_idx names for the rest.
-   * Both pointers are set or both are NULL; the arrays are read by the first
-   * kernel only.  An all-zero struct with max_iters set is a cold start. */
+   * Both pointers are set or both are NULL (else TACTIC_ERR_INVALID_ARG); the
+   * arrays are read by the first kernel only and must not overlap the
+   * centroids output; prev C_b may be smaller or larger than C_b.  An all-zero
+   * struct with max_iters set is a cold start. */
   const uint16_t* prev_centroids;
   const int64_t* prev_cl_indptr;
 } tactic_kmeans_params;
