@@ -98,7 +98,7 @@ def dense_sdpa(q, K, V, wl, reps: int, own_out=None) -> dict:
         del KS, VS
         return {"us_per_layer": round(us, 2), "backends": "flash, efficient", "reps": reps,
                 "max_abs_diff_vs_own_dense": diff}
-    except Exception as e:  # no fused backend for this shape on this build
+    except Exception as e:  # no fused backend for this shape in the installed torch
         return {"us_per_layer": None, "error": f"{type(e).__name__}: {str(e)[:160]}"}
 
 
@@ -126,8 +126,9 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: this build runs on a single MI355X and has no multi-GPU path "
-              "(the decode shards by (sequence, KV head) with no exchange; see the design notes).",
+        print("bench.py measures one GPU: the library runs on a single MI355X and has no multi-GPU path "
+              "(the decode shards by (sequence, KV head) with no exchange, so each GPU would run its share "
+              "of the KV heads at the same shape).",
               file=sys.stderr)
         sys.exit(2)
     import paper_2502_12216_amd as T

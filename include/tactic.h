@@ -43,7 +43,7 @@ extern "C" {
 typedef enum {
   TACTIC_OK = 0,
   TACTIC_ERR_INVALID_ARG = 1,  /* a null pointer, a size out of range, P outside (0, 1] ... */
-  TACTIC_ERR_UNSUPPORTED = 2,  /* a valid request this build does not implement (e.g. head_dim != 128) */
+  TACTIC_ERR_UNSUPPORTED = 2,  /* a valid request the library does not implement (e.g. head_dim != 128) */
   TACTIC_ERR_WORKSPACE = 3,    /* workspace smaller than the size query returned */
   TACTIC_ERR_HIP = 4           /* a HIP launch failed; tactic_last_error() has the message */
 } tactic_status;
