@@ -876,16 +876,14 @@ __host__ __device__ inline bool union_staged(int G, int64_t Cm) { return G <= 4 
 // The group's range list ends with the recent tokens (rows n_c .. n_c + tail
 // - 1, the same for every head of the group) as one more range; then the
 // group's counts.  tot = (cluster ranges << 32) | their tokens.
-__device__ void union_close(const FitArgs& a, int bg, int b, int kvh, int h0, uint64_t tot, int32_t* rstart,
-                            int32_t* rupos, int32_t* cfr) {
+__device__ void union_close(const FitArgs& a, int bg, int b, int kvh, int n_c, int tail, uint64_t tot,
+                            int32_t* rstart, int32_t* rupos, int32_t* cfr) {
   const int64_t T = kCfrTokens;
   int R = (int)(tot >> 32);
   const int64_t U = (int64_t)(tot & 0xffffffffu);
   int64_t Ut = U;
-  const int32_t* hm0 = a.head_meta + (int64_t)h0 * 16;
-  const int tail = hm0[11];
   if (tail > 0) {
-    rstart[R] = hm0[0];
+    rstart[R] = n_c;
     rupos[R] = (int32_t)U;
     for (int64_t c = (U + T - 1) / T; c * T < U + tail && c < a.max_chunks; ++c) cfr[c] = R;
     ++R;
@@ -914,6 +912,12 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
   int32_t* rstart = a.rstart + (int64_t)bg * (a.Cm + 2);
   int32_t* rupos = a.rupos + (int64_t)bg * (a.Cm + 2);
   int32_t* cfr = a.cfr + (int64_t)bg * a.max_chunks;
+  // the sequence's clusters and the group's clustered rows / recent tokens
+  // (the same for every head of the group), loaded before the fit so that
+  // no global load waits behind it
+  const int64_t cb = a.cl_indptr[b];
+  const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
+  const int n_c = a.head_meta[(int64_t)h0 * 16 + 0], tail = a.head_meta[(int64_t)h0 * 16 + 11];
 
   if (union_staged(G, a.Cm)) {
     const int Cp = (a.Cm + kUnionSeg - 1) / kUnionSeg * kUnionSeg;
@@ -923,8 +927,6 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
     if (wave < G) {
       fit_head_wave(a, h0 + wave, lane, s_cut[wave]);
     } else {
-      const int64_t cb = a.cl_indptr[b];
-      const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
       const int32_t* off = a.offsets + (int64_t)kvh * (a.Ct + a.B) + cb + b;
       // all loads of a thread are issued before its LDS stores
       constexpr int nw = 1024 - G * kWave;
@@ -949,8 +951,6 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
           if (w + i * nw < C) s_rk[hh * Cp + w + i * nw] = (uint16_t)rv[hh][i];
     }
     __syncthreads();
-    const int64_t cb = a.cl_indptr[b];
-    const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
     int32_t* ulen = a.union_len + (int64_t)jg * a.Ct + cb;
     // union length of the thread's clusters j0 .. j0 + 7: the whole cluster
     // when some head ranks it before its cut (rank - cut < 0), the largest
@@ -1024,14 +1024,12 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
         }
       }
     }
-    if (tid == 0) union_close(a, bg, b, kvh, h0, tot, rstart, rupos, cfr);
+    if (tid == 0) union_close(a, bg, b, kvh, n_c, tail, tot, rstart, rupos, cfr);
     return;
   }
 
   if (wave < G) fit_head_wave(a, h0 + wave, lane, s_cut[wave]);
   __syncthreads();
-  const int64_t cb = a.cl_indptr[b];
-  const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
   const int32_t* off = a.offsets + (int64_t)kvh * (a.Ct + a.B) + cb + b;
   int32_t* ulen = a.union_len + (int64_t)jg * a.Ct + cb;
   int32_t* Ls = a.Cm <= kUnionLdsMax ? reinterpret_cast<int32_t*>(smem_raw) : ulen;
@@ -1085,7 +1083,7 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
     ++idx;
     upos += L;
   }
-  if (tid == 0) union_close(a, bg, b, kvh, h0, tot, rstart, rupos, cfr);
+  if (tid == 0) union_close(a, bg, b, kvh, n_c, tail, tot, rstart, rupos, cfr);
 }
 
 // ============================================================================
