@@ -75,11 +75,18 @@ class RecentTailCache:
 
     def append(self, k: torch.Tensor, v: torch.Tensor) -> bool:
         """k, v: bf16 [B][Hkv][128], the new token of every sequence.  Returns
-        True when the call re-clustered the batch."""
-        rows = self.starts + torch.as_tensor(np.asarray(self.lens, dtype=np.int64), device=self.device)
-        self._set_lens([n + 1 for n in self.lens])
+        True when the call re-clustered the batch.  Only device work is
+        enqueued (no host-device copy): the rows come from the device lengths,
+        which are then advanced in place."""
+        lens = [n + 1 for n in self.lens]
+        if any(n > c for n, c in zip(lens, self.capacities)):
+            raise ValueError("a sequence outgrew its capacity")
+        rows = self.starts + self.batch.seq_len  # the next free row of every sequence
         self.K[:, rows] = k.transpose(0, 1).to(self.K.dtype)
         self.V[:, rows] = v.transpose(0, 1).to(self.V.dtype)
+        self.batch.seq_len += 1
+        self.lens = lens
+        self.batch.seq_lens = list(lens)
         if max(n - c for n, c in zip(self.lens, self.clustered)) >= self.recluster_every:
             self.recluster()
             return True
