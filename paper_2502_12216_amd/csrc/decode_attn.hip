@@ -38,6 +38,7 @@ __device__ __forceinline__ int64_t group_tokens(const AttnArgs& a, int bg) {
 // (query load, range lookup, merge, partial store; about the time of 96
 // streamed tokens), so a workgroup that straddles groups gets fewer tokens.
 constexpr int64_t kSegmentCost = 96;
+constexpr int64_t kMinShare = 256;  // smallest split share (units) of a workgroup
 __device__ __forceinline__ int64_t split_units(const AttnArgs& a, int bg) {
   const int64_t n = group_tokens(a, bg);
   return n > 0 ? n + kSegmentCost : 0;
@@ -189,7 +190,10 @@ void attn_splitk_kernel(AttnArgs a) {
     __syncthreads();
   }
   const int64_t total = s_prefix[BG];
-  const int64_t share = (total + gridDim.x - 1) / gridDim.x;
+  // a small selection is not spread thinner than kMinShare units per
+  // workgroup: below that the fixed work of a workgroup and the partials the
+  // combine must merge cost more than the extra workgroups stream
+  const int64_t share = max((total + gridDim.x - 1) / gridDim.x, kMinShare);
   if (blockIdx.x == 0) {  // for the combine: the split and the group offsets
     if (tid == 0) a.ameta[0] = share;
     for (int bg = tid; bg <= BG; bg += 256) a.ameta[1 + bg] = s_prefix[bg];
@@ -501,16 +505,25 @@ void attn_splitk_kernel(AttnArgs a) {
 
 // Combine the partials of every (b, g): out = sum_c acc_c 2^(m_c - M) /
 // sum_c l_c 2^(m_c - M).  grid (B*NV, G), 512 threads: four slices of the
-// chunks (c = slice mod 4) x 128 output dimensions, each slice a single pass
-// with a running maximum, merged in slice order.  Groups without tokens get
-// zeros.
+// partials (c = slice mod 4) x 128 output dimensions.  The partials'
+// (maximum, sum) pairs go to LDS and a block reduction gives M; each
+// partial's weight 2^(m_c - M) then replaces its maximum in LDS and a block
+// reduction gives the denominator; each slice sums weight x accumulator over
+// its partials in ascending order (the first eight loaded before the
+// reductions, all loads independent of one another) and the slices add in
+// order.  Every sum has a fixed order, so results do not depend on
+// scheduling.  Groups without tokens get zeros.
 template <int G>
 __global__ __launch_bounds__(512) void combine_kernel(AttnArgs a) {
   constexpr int kPart = G * (kHeadDim + 2);
-  __shared__ float s_m[4][kHeadDim], s_num[4][kHeadDim], s_den[4][kHeadDim];
+  __shared__ float s_w[kMaxAttnGrid];     // running maximum, then weight, of each partial
+  __shared__ float s_l[kMaxAttnGrid];     // running sum of each partial
+  __shared__ float s_num[4][kHeadDim];
+  __shared__ float s_red[8];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
   const int bg = blockIdx.x, h = blockIdx.y;
   const int b = bg / a.NV, jg = bg % a.NV;
-  const int d = threadIdx.x & (kHeadDim - 1), slice = threadIdx.x >> 7;
+  const int d = tid & (kHeadDim - 1), slice = tid >> 7;
   float* out = a.out + ((int64_t)b * a.Hq + jg * G + h) * kHeadDim;
   // workgroups w0..w1 covered this group's tokens; their partials sit in slots bg + w
   const int64_t share = a.ameta[0], P0 = a.ameta[1 + bg], P1 = a.ameta[2 + bg];
@@ -519,37 +532,58 @@ __global__ __launch_bounds__(512) void combine_kernel(AttnArgs a) {
     return;
   }
   const int64_t w0 = (P0 + kSegmentCost) / share, w1 = (P1 - 1) / share;
-  const int nchunks = (int)(w1 - w0 + 1);
+  const int np = (int)min(w1 - w0 + 1, (int64_t)kMaxAttnGrid);
   const float* pb = a.partials + (bg + w0) * kPart;
-  float M = -INFINITY, num = 0.f, den = 0.f;
-#pragma unroll 4
-  for (int c = slice; c < nchunks; c += 4) {
-    const float* pc = pb + (int64_t)c * kPart;
-    const float mc = pc[G * kHeadDim + h], lc = pc[G * kHeadDim + G + h], ac = pc[h * kHeadDim + d];
-    if (mc > M) {
-      const float sc = fast_exp2(M - mc);
-      num *= sc;
-      den *= sc;
-      M = mc;
-    }
-    const float w = fast_exp2(mc - M);
-    num = fmaf(ac, w, num);
-    den = fmaf(lc, w, den);
+  const float* pd = pb + h * kHeadDim + d;  // this thread's output dimension of partial 0
+  constexpr int kPre = 8;                   // numerator loads issued before the reductions
+  float pre[kPre];
+#pragma unroll
+  for (int i = 0; i < kPre; ++i) {
+    const int c = slice + 4 * i;
+    pre[i] = c < np ? pd[(int64_t)c * kPart] : 0.f;
   }
-  s_m[slice][d] = M;
+  // 1. every partial's (maximum, sum) to LDS, and the common maximum
+  float mx = -INFINITY;
+  for (int c = tid; c < np; c += 512) {
+    const float mc = pb[(int64_t)c * kPart + G * kHeadDim + h];
+    s_w[c] = mc;
+    s_l[c] = pb[(int64_t)c * kPart + G * kHeadDim + G + h];
+    mx = fmaxf(mx, mc);
+  }
+  mx = wave_allmax_f(mx);
+  if (lane == 0) s_red[wave] = mx;
+  __syncthreads();
+  float M = s_red[0];
+#pragma unroll
+  for (int w = 1; w < 8; ++w) M = fmaxf(M, s_red[w]);
+  __syncthreads();  // s_red is reused below
+  // 2. weights and denominator
+  float den = 0.f;
+  for (int c = tid; c < np; c += 512) {  // the entries this thread wrote
+    const float mc = s_w[c];
+    const float wc = mc == -INFINITY ? 0.f : fast_exp2(mc - M);
+    s_w[c] = wc;
+    den = fmaf(s_l[c], wc, den);
+  }
+  den = wave_allsum_f(den);
+  if (lane == 0) s_red[wave] = den;
+  __syncthreads();
+  // 3. numerator: slice s sums partials s, s + 4, ... for dimension d
+  float num = 0.f;
+#pragma unroll
+  for (int i = 0; i < kPre; ++i) {
+    const int c = slice + 4 * i;
+    if (c < np) num = fmaf(s_w[c], pre[i], num);
+  }
+#pragma unroll 8
+  for (int c = slice + 4 * kPre; c < np; c += 4) num = fmaf(s_w[c], pd[(int64_t)c * kPart], num);
   s_num[slice][d] = num;
-  s_den[slice][d] = den;
   __syncthreads();
   if (slice == 0) {
-    float mm = -INFINITY;
-    for (int q = 0; q < 4; ++q) mm = fmaxf(mm, s_m[q][d]);
-    float nn = 0.f, dd = 0.f;
-    for (int q = 0; q < 4; ++q) {
-      const float w = s_m[q][d] == -INFINITY ? 0.f : fast_exp2(s_m[q][d] - mm);
-      nn = fmaf(s_num[q][d], w, nn);
-      dd = fmaf(s_den[q][d], w, dd);
-    }
-    out[d] = nn / dd;
+    float dd = 0.f;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) dd += s_red[w];
+    out[d] = (((s_num[0][d] + s_num[1][d]) + s_num[2][d]) + s_num[3][d]) / dd;
   }
 }
 
