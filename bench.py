@@ -117,6 +117,7 @@ def parse():
     ap.add_argument("--no-ablation", action="store_true", help="skip the per-head (no-union) comparison")
     ap.add_argument("--no-paged", action="store_true", help="skip the paged-cache comparison")
     ap.add_argument("--no-recent", action="store_true", help="skip the recent-token / re-clustering run")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the query-concentration sweep")
     ap.add_argument("--calibrate", action="store_true",
                     help="also run a plain 1 GiB device copy (reference dispatch for HBM counters)")
     return ap.parse_args()
@@ -389,6 +390,42 @@ def main():
         log(f"recent tail: decode {us_tail:.1f} us with {tail_now} recent tokens, re-clustering warm {ms_warm:.1f} ms "
             f"cold {ms_cold:.1f} ms")
 
+    # ---------------------------------------------------------------- query-concentration sweep
+    sweep = None
+    if not args.no_sweep:
+        points = []
+        for wl_s in synth.sweep_workloads():
+            inp_s = synth.make_layer(wl_s, 0, device=dev)
+            ncl_s = list(wl_s.cluster_counts)
+            n_s = int(wl_s.seq_lens[0])
+            batch_s = T.RaggedBatch(wl_s.seq_lens, wl_s.n_q_heads, wl_s.n_kv_heads)
+            bld = T.ClusterBuilder(batch_s, ncl_s, max_iters=wl_s.kmeans_iters)
+            cb_s = bld(inp_s.K, inp_s.V, torch.as_tensor(synth.kmeans_init_all(wl_s, 0), device=dev))
+            dec_s = T.SparseDecoder(batch_s, ncl_s, T.decode_params(P))
+            den_s = T.DenseDecoder(batch_s)
+            args_s = (inp_s.q, cb_s.K_sorted, cb_s.V_sorted)
+            for _ in range(5):
+                dec_s(*args_s, cb_s.clusters)
+                den_s(*args_s)
+            us_s = timed(lambda: dec_s(*args_s, cb_s.clusters), 30) * 1000
+            us_d = timed(lambda: den_s(*args_s), 30) * 1000
+            _, sq_s, skv_s = dec_s(*args_s, cb_s.clusters)
+            smp = float(dec_s.view()["fit"][..., 11].sum())
+            C_s = float(ncl_s[0])
+            b_sparse = wl_s.n_kv_heads * (C_s * 256 + (C_s + 1) * 4) + smp * 256 + float(skv_s.sum()) * 512
+            b_dense = float(n_s) * wl_s.n_kv_heads * 512
+            points.append({"beta": wl_s.beta, "reading": "mean" if wl_s.q_mean else "sum",
+                           "head_frac_mean": round(float(sq_s.double().mean()) / n_s, 5),
+                           "union_frac_mean": round(float(skv_s.double().mean()) / n_s, 5),
+                           "sparse_us": round(us_s, 2), "dense_us": round(us_d, 2),
+                           "speedup": round(us_d / us_s, 3), "byte_bound_speedup": round(b_dense / b_sparse, 3)})
+            del inp_s, cb_s, dec_s, den_s, bld, args_s
+        sweep = {"workload": "1 x 131072 tokens, 32 query / 8 KV heads, 8192 K-means clusters (10 iterations), "
+                             "P = 0.9; query = beta (sum or mean of k_h in 1..8 centres + noise)",
+                 "points": points}
+        log("concentration sweep: " + ", ".join(f"b={p['beta']:g}/{p['reading']} U={p['union_frac_mean']:.3f} "
+                                                f"x{p['speedup']:.2f}" for p in points))
+
     # ---------------------------------------------------------------- selection statistics, bytes
     sel_q, sel_kv, samples = [], [], []
     for l in range(layers):
@@ -509,6 +546,7 @@ def main():
         "union_ablation": ablation,
         "paged_kv": paged,
         "recent_tail": recent,
+        "concentration_sweep": sweep,
     }
     if args.clusters == "kmeans":
         res["kmeans"] = {"seconds_all_layers": round(kmeans_ms / 1000, 3), "layers": layers,

@@ -18,7 +18,12 @@ Recipe (per sequence b, layer l, KV head g; n tokens, d = 128):
 * Query head h of group g picks k_h distinct centres S_h of group g and is
   q_h = beta_h * (sum_{j in S_h} c_j + sigma * eps).  k_h is fixed (3) for the
   smallest workload and uniform in {1..8} otherwise; beta_h = 2, or
-  2 * LogNormal(0, 1) per (layer, head) for the 32-layer workload.
+  2 * LogNormal(0, 1) per (layer, head) for the 32-layer workload.  The
+  "mean of centres" reading (q_mean) divides the centre sum by k_h.
+* The concentration sweep (sweep_workloads): one 131072-token sequence, 32 /
+  8 heads, fixed beta in {0.25, 0.5, 1, 2} under both readings, all points on
+  the same keys, values and centres (one workload id), so only the query's
+  concentration changes from point to point.
 * Everything is cast to bf16 (round to nearest even) before use.
 
 Sub-seeds are derived from (workload id, b, layer, head, tag) with NumPy's
@@ -60,6 +65,7 @@ class Workload:
     q_k_range: tuple = (1, 8)         # centres mixed into one query head
     beta: float = 2.0
     beta_lognormal: bool = False      # beta = 2 * LogNormal(0, 1) per (layer, head)
+    q_mean: bool = False              # query = beta * (mean of its centres + noise) instead of the sum
     target_fracs: tuple = (0.9,)
     kmeans_iters: int = 10
 
@@ -108,6 +114,21 @@ WORKLOADS = {
         name="ctx128k_b4_32layer", wid=5, seq_lens=(131072,) * 4, n_q_heads=32,
         n_kv_heads=8, layers=32, beta_lognormal=True),
 }
+
+
+SWEEP_BETAS = (0.25, 0.5, 1.0, 2.0)
+
+
+def sweep_workloads() -> list:
+    """The concentration sweep: selected fraction, and so the speedup, as a
+    function of how concentrated the queries are (not one of the workloads
+    above: every point shares workload id 6)."""
+    out = []
+    for mean in (False, True):
+        for beta in SWEEP_BETAS:
+            out.append(Workload(name=f"sweep_b{beta:g}_{'mean' if mean else 'sum'}", wid=6, seq_lens=(131072,),
+                                n_q_heads=32, n_kv_heads=8, beta=beta, q_mean=mean))
+    return out
 
 
 def indptr(lengths: Sequence[int]) -> np.ndarray:
@@ -194,6 +215,8 @@ def make_layer(wl: Workload, layer: int = 0, device="cpu", seq_subset=None) -> L
                     beta = wl.beta * float(brng.lognormal(0.0, 1.0))
                 qg = _gen(sub_seed(wl.wid, b, layer, 1000 + h), device)
                 qv = cen[torch.as_tensor(S, device=device)].sum(0)
+                if wl.q_mean:
+                    qv = qv / float(len(S))
                 qv = qv + wl.noise * torch.randn(d, generator=qg, device=device)
                 q[bi, h] = (beta * qv).to(torch.bfloat16)
                 q_centres.append([int(x) for x in S])
