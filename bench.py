@@ -394,10 +394,12 @@ def main():
     sweep = None
     if not args.no_sweep:
         points = []
-        for wl_s in synth.sweep_workloads():
+        # one sequence at every point, then the two concentrated points at the timed batch of 4
+        for wl_s in synth.sweep_workloads() + synth.sweep_workloads(4, betas=(1.0, 2.0), readings=(False,)):
             inp_s = synth.make_layer(wl_s, 0, device=dev)
             ncl_s = list(wl_s.cluster_counts)
             n_s = int(wl_s.seq_lens[0])
+            B_s = len(wl_s.seq_lens)
             batch_s = T.RaggedBatch(wl_s.seq_lens, wl_s.n_q_heads, wl_s.n_kv_heads)
             bld = T.ClusterBuilder(batch_s, ncl_s, max_iters=wl_s.kmeans_iters)
             cb_s = bld(inp_s.K, inp_s.V, torch.as_tensor(synth.kmeans_init_all(wl_s, 0), device=dev))
@@ -412,18 +414,19 @@ def main():
             _, sq_s, skv_s = dec_s(*args_s, cb_s.clusters)
             smp = float(dec_s.view()["fit"][..., 11].sum())
             C_s = float(ncl_s[0])
-            b_sparse = wl_s.n_kv_heads * (C_s * 256 + (C_s + 1) * 4) + smp * 256 + float(skv_s.sum()) * 512
-            b_dense = float(n_s) * wl_s.n_kv_heads * 512
-            points.append({"beta": wl_s.beta, "reading": "mean" if wl_s.q_mean else "sum",
+            b_sparse = B_s * wl_s.n_kv_heads * (C_s * 256 + (C_s + 1) * 4) + smp * 256 + float(skv_s.sum()) * 512
+            b_dense = float(n_s) * B_s * wl_s.n_kv_heads * 512
+            points.append({"batch": B_s, "beta": wl_s.beta, "reading": "mean" if wl_s.q_mean else "sum",
                            "head_frac_mean": round(float(sq_s.double().mean()) / n_s, 5),
                            "union_frac_mean": round(float(skv_s.double().mean()) / n_s, 5),
                            "sparse_us": round(us_s, 2), "dense_us": round(us_d, 2),
                            "speedup": round(us_d / us_s, 3), "byte_bound_speedup": round(b_dense / b_sparse, 3)})
             del inp_s, cb_s, dec_s, den_s, bld, args_s
-        sweep = {"workload": "1 x 131072 tokens, 32 query / 8 KV heads, 8192 K-means clusters (10 iterations), "
-                             "P = 0.9; query = beta (sum or mean of k_h in 1..8 centres + noise)",
+        sweep = {"workload": "batch x 131072 tokens (batch 1 at every point, 4 at two), 32 query / 8 KV heads, "
+                             "8192 K-means clusters per sequence (10 iterations), P = 0.9; query = beta (sum or "
+                             "mean of k_h in 1..8 centres + noise)",
                  "points": points}
-        log("concentration sweep: " + ", ".join(f"b={p['beta']:g}/{p['reading']} U={p['union_frac_mean']:.3f} "
+        log("concentration sweep: " + ", ".join(f"B={p['batch']} b={p['beta']:g}/{p['reading']} U={p['union_frac_mean']:.3f} "
                                                 f"x{p['speedup']:.2f}" for p in points))
 
     # ---------------------------------------------------------------- selection statistics, bytes

@@ -119,15 +119,17 @@ WORKLOADS = {
 SWEEP_BETAS = (0.25, 0.5, 1.0, 2.0)
 
 
-def sweep_workloads() -> list:
+def sweep_workloads(batch: int = 1, betas=SWEEP_BETAS, readings=(False, True)) -> list:
     """The concentration sweep: selected fraction, and so the speedup, as a
     function of how concentrated the queries are (not one of the workloads
-    above: every point shares workload id 6)."""
+    above: every point shares workload id 6, so sequence b has the same keys
+    at every point and batch size)."""
     out = []
-    for mean in (False, True):
-        for beta in SWEEP_BETAS:
-            out.append(Workload(name=f"sweep_b{beta:g}_{'mean' if mean else 'sum'}", wid=6, seq_lens=(131072,),
-                                n_q_heads=32, n_kv_heads=8, beta=beta, q_mean=mean))
+    for mean in readings:
+        for beta in betas:
+            name = f"sweep_b{beta:g}_{'mean' if mean else 'sum'}" + (f"_x{batch}" if batch > 1 else "")
+            out.append(Workload(name=name, wid=6, seq_lens=(131072,) * batch, n_q_heads=32, n_kv_heads=8,
+                                beta=beta, q_mean=mean))
     return out
 
 
