@@ -66,6 +66,35 @@ def profiled_traffic(stage: str):
     return None
 
 
+class TimingEvents:
+    """HIP events for timing only, created with hipEventDisableSystemFence:
+    recording one does not write back and invalidate the caches (which would
+    also slow the kernel after it), and they are read after a full device
+    synchronisation.  `array` is what tactic_sparse_decode_plan_set_events
+    takes."""
+
+    FLAGS = 0x20000000  # hipEventDisableSystemFence
+
+    def __init__(self, n: int):
+        import ctypes
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.events = []
+        for _ in range(n):
+            ev = ctypes.c_void_p()
+            if self.hip.hipEventCreateWithFlags(ctypes.byref(ev), ctypes.c_uint(self.FLAGS)) != 0:
+                raise RuntimeError("hipEventCreateWithFlags failed")
+            self.events.append(ev)
+        self.array = (ctypes.c_void_p * n)(*[e.value for e in self.events])
+
+    def elapsed(self, i: int, j: int) -> float:
+        """Milliseconds from event i to event j (both recorded and complete)."""
+        import ctypes
+        ms = ctypes.c_float()
+        if self.hip.hipEventElapsedTime(ctypes.byref(ms), self.events[i], self.events[j]) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+
 def dense_sdpa(q, K, V, wl, reps: int, own_out=None) -> dict:
     """torch's scaled_dot_product_attention (GQA) as a second dense decode on
     one layer's bf16 inputs, restricted to the fused flash / memory-efficient
@@ -235,13 +264,10 @@ def main():
 
     # ---------------------------------------------------------------- per-stage timing (HIP events)
     NS = 6
-    stage_ev = [torch.cuda.Event(enable_timing=True) for _ in range(NS + 1)]
-    for e in stage_ev:
-        e.record()
-    torch.cuda.synchronize()
     import ctypes
     from paper_2502_12216_amd import _capi as C
-    arr = (ctypes.c_void_p * (NS + 1))(*[e.cuda_event for e in stage_ev])
+    stage_ev = TimingEvents(NS + 1)
+    arr = stage_ev.array
 
     def stage_times(decoder, call=None, n_layers=None, per_layer=None):
         """Mean per-kernel milliseconds over args.steps passes of every layer, from
@@ -256,9 +282,9 @@ def main():
                 call(l)
                 torch.cuda.synchronize()
                 for i in range(NS):
-                    acc[i] += stage_ev[i].elapsed_time(stage_ev[i + 1])
+                    acc[i] += stage_ev.elapsed(i, i + 1)
                 if per_layer is not None:
-                    per_layer.append(stage_ev[0].elapsed_time(stage_ev[NS]))
+                    per_layer.append(stage_ev.elapsed(0, NS))
                 nrep += 1
         C.check(C.lib().tactic_sparse_decode_plan_set_events(ctypes.byref(decoder.plan), None), "set_events")
         return acc / nrep
@@ -541,6 +567,8 @@ def main():
         "bytes_per_layer": {"centroids": bytes_centroids, "samples": float(bytes_samples.mean()),
                             "union_kv": float(bytes_union.mean()), "dense_kv": dense_bytes_layer},
         "stages_us_per_layer": {n: round(float(t), 2) for n, t in zip(stage_names, stage_us)},
+        "stage_timing": "HIP events recorded by the library between its launches on the decode stream, "
+                        "created with hipEventDisableSystemFence (no cache flush at each event)",
         "selected_frac": {"head_mean": round(float(kq.mean()), 5), "head_median": round(float(np.median(kq)), 5),
                           "head_max": round(float(kq.max()), 5), "union_mean": round(float(ku.mean()), 5),
                           "union_max": round(float(ku.max()), 5)},
