@@ -208,11 +208,19 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
   const int tid = threadIdx.x, nt = blockDim.x;
   const int bh = blockIdx.x;
   const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
+  const float* sc = a.scores + (int64_t)bh * a.Cm;
+  // LDS path: the head's scores, loaded first and unconditionally at indices
+  // clamped to the stride Cm (>= C; the entries past C are masked later), so
+  // that they travel with the cluster-count load instead of after it
+  float raw[8];
+  if constexpr (kLds) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) raw[e] = sc[min(tid + e * 1024, a.Cm - 1)];
+  }
   const int64_t cb = a.cl_indptr[b];
   const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
   const int n = (int)seq_tokens(a.kv_indptr, a.seq_len, b);
   const int32_t* off = a.offsets + (int64_t)g * (a.Ct + a.B) + cb + b;
-  const float* sc = a.scores + (int64_t)bh * a.Cm;
   int32_t* rank_of = a.rank_of + (int64_t)bh * a.Cm;
   int32_t* order = a.order + (int64_t)bh * a.Cm;
 
@@ -231,12 +239,28 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     // every thread keeps its 8 elements in registers (C <= 8192 = 8 * 1024)
     float v[8];
     int sz[8], o0[8], bk[8], pos[8];
+    // the offsets too are loaded unconditionally, at indices clamped into the
+    // (b, g) list, so that all of them are in flight together (a guarded load
+    // whose value is used inside its guard waits there)
+    {
+      int o1[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int j = tid + e * 1024;
-      v[e] = j < C ? sc[j] : NAN;
-      o0[e] = j < C ? off[j] : 0;
-      sz[e] = j < C ? off[j + 1] - o0[e] : 0;
+      for (int e = 0; e < 8; ++e) o0[e] = o1[e] = 0;
+      if (C > 0) {  // uniform: the offsets hold C + 1 entries
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int jc = min(tid + e * 1024, C - 1);
+          o0[e] = off[jc];
+          o1[e] = off[jc + 1];
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const bool in = tid + e * 1024 < C;
+        v[e] = in ? raw[e] : NAN;
+        sz[e] = in ? o1[e] - o0[e] : 0;
+        o0[e] = in ? o0[e] : 0;
+      }
     }
     {
       uint4* c4 = reinterpret_cast<uint4*>(cnt) + tid * 2;
