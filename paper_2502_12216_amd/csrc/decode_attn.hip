@@ -332,7 +332,10 @@ void attn_splitk_kernel(AttnArgs a) {
         const int64_t c_end = (p + cnt - 1) / kCfrTokens + 1;
         const int32_t* cf = a.cfr + (int64_t)bg * a.max_chunks;
         const int r0 = cf[c];
-        const int r_hi = c_end < min((int64_t)nchunk, a.max_chunks) ? cf[c_end] : R - 1;
+        // loaded unconditionally (clamped into the group's chunk index) so that
+        // it travels with the group's metadata instead of after it
+        const int cf_end = cf[min(c_end, a.max_chunks - 1)];
+        const int r_hi = c_end < min((int64_t)nchunk, a.max_chunks) ? cf_end : R - 1;
         const int nr = max(1, min(min(R - r0, r_hi - r0 + 1), (int)(in + cnt)));
         const int32_t* rup = a.rupos + (int64_t)bg * (a.Cm + 2) + r0;
         const int32_t* rst = a.rstart + (int64_t)bg * (a.Cm + 2) + r0;
@@ -343,10 +346,14 @@ void attn_splitk_kernel(AttnArgs a) {
         // all mark position 0, and the largest index wins)
         *reinterpret_cast<int4*>(s_rows + t_lo) = make_int4(0, 0, 0, 0);
         *reinterpret_cast<int4*>(s_rows + t_lo + 4) = make_int4(0, 0, 0, 0);
+        // loads and stores unconditional so that the two loads are in flight
+        // together: entry nr of the starts (a copy of range nr - 1's) is
+        // never read, since every marker is a range index below nr
 #pragma unroll 4
         for (int i = tid; i <= nr; i += 256) {
-          s_rupos[i] = rup[i];
-          if (i < nr) s_rstart[i] = rst[i];
+          const int up = rup[i], st = rst[min(i, nr - 1)];
+          s_rupos[i] = up;
+          s_rstart[i] = st;
         }
         __syncthreads();
         for (int i = tid; i < nr; i += 256) {
