@@ -359,11 +359,15 @@ __global__ __launch_bounds__(1024) void km_scan1_kernel(KmArgs a) {
   // the first one's
   const int64_t b0 = x0 + (int64_t)threadIdx.x * 16, b1 = min(E, b0 + 16);
   const int t0 = (int)(b0 % q.tiles), c0 = (int)(b0 / q.tiles);
+  // every load unconditional (entries past the end read entry 0 and count
+  // nothing) so that the 16 are in flight together
   int s = 0;
 #pragma unroll
   for (int e = 0; e < 16; ++e) {
     const int te = t0 + e;
-    if (b0 + e < b1) s += tab[(int64_t)(te % q.tiles) * q.C + c0 + te / q.tiles];
+    const bool in = b0 + e < b1;
+    const int v = tab[in ? (int64_t)(te % q.tiles) * q.C + c0 + te / q.tiles : 0];
+    s += in ? v : 0;
   }
   for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
   if ((threadIdx.x & 63) == 0) s_w[threadIdx.x >> 6] = s;
