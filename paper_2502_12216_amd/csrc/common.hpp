@@ -28,8 +28,9 @@ __host__ __device__ inline int64_t ceil_div64(int64_t a, int64_t b) { return (a 
 // Tokens of sequence b: its span [indptr[b], indptr[b+1]) or, with a length
 // array, the first len[b] rows of that span.
 __device__ __forceinline__ int64_t seq_tokens(const int64_t* indptr, const int64_t* len, int b) {
+  const int64_t l = len ? len[b] : 0;  // issued before the span is formed, so the loads overlap
   const int64_t span = indptr[b + 1] - indptr[b];
-  return len ? max((int64_t)0, min(len[b], span)) : span;
+  return len ? max((int64_t)0, min(l, span)) : span;
 }
 
 __host__ __device__ inline Geometry make_geometry(int64_t n, const SelParams& p) {

@@ -383,8 +383,13 @@ void attn_splitk_kernel(AttnArgs a) {
         for (int e = 0; e < kRun; ++e) {
           const int idx = max(mk[e], run);
           const int pos = (int)(p + t_lo + e);
-          const int row = min(max(s_rstart[idx] + (pos - s_rupos[idx]), 0), nseq - 1);  // clamp: bad meta only
-          rw[e] = kPaged ? (int)paged_row(a.pk, a.Hkv, a.total, kvb, b, kvh, row, n_c) : row;
+          rw[e] = min(max(s_rstart[idx] + (pos - s_rupos[idx]), 0), nseq - 1);  // clamp: bad meta only
+        }
+        if constexpr (kPaged) {  // the group holds tokens here, so nseq >= 1 and every row is valid
+          int64_t pr[kRun];
+          paged_rows(a.pk, a.Hkv, a.total, kvb, b, kvh, rw, n_c, pr);
+#pragma unroll
+          for (int e = 0; e < kRun; ++e) rw[e] = (int)pr[e];
         }
         *reinterpret_cast<int4*>(s_rows + t_lo) = make_int4(rw[0], rw[1], rw[2], rw[3]);
         *reinterpret_cast<int4*>(s_rows + t_lo + 4) = make_int4(rw[4], rw[5], rw[6], rw[7]);

@@ -32,6 +32,36 @@ __device__ __forceinline__ int64_t paged_row(const PagedKV& pk, int Hkv, int64_t
   return (page * Hkv + kvh) * pk.page_size + tok % pk.page_size;
 }
 
+// paged_row for K rows at once, each row in [0, n) of a sequence of n tokens
+// (kvb + n <= total): the K permutation loads are issued together (row >= n_c
+// reads an entry it then ignores, so no load sits behind a per-row guard),
+// then the K page-table loads.  Same clamps and results as paged_row.
+template <int K>
+__device__ __forceinline__ void paged_rows(const PagedKV& pk, int Hkv, int64_t total, int64_t kvb, int b,
+                                           int kvh, const int (&row)[K], int n_c, int64_t (&out)[K]) {
+  int tok[K];
+  if (pk.perm) {
+#pragma unroll
+    for (int e = 0; e < K; ++e) tok[e] = pk.perm[(int64_t)kvh * total + kvb + row[e]];
+#pragma unroll
+    for (int e = 0; e < K; ++e) tok[e] = row[e] < n_c ? tok[e] : row[e];
+  } else {
+#pragma unroll
+    for (int e = 0; e < K; ++e) tok[e] = row[e];
+  }
+  int64_t page[K];
+#pragma unroll
+  for (int e = 0; e < K; ++e) {
+    tok[e] = min(max(tok[e], 0), pk.max_pages * pk.page_size - 1);
+    page[e] = pk.page_table[(int64_t)b * pk.max_pages + tok[e] / pk.page_size];
+  }
+#pragma unroll
+  for (int e = 0; e < K; ++e) {
+    const int64_t pg = min(max(page[e], (int64_t)0), pk.num_pages - 1);
+    out[e] = (pg * Hkv + kvh) * pk.page_size + tok[e] % pk.page_size;
+  }
+}
+
 struct ScoreArgs {
   const uint16_t* q;          // bf16 [B][Hq][128]
   const uint16_t* centroids;  // bf16 [Hkv][Ct][128]
