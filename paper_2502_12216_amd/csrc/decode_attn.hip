@@ -318,8 +318,17 @@ void attn_splitk_kernel(AttnArgs a) {
       } else if (a.dense) {
         // paged dense: the row table holds each position's page row
         cnt = (int)min(seg_hi - p, (int64_t)kMaxChunkTokens);
-        for (int t = tid; t < cnt; t += 256)
-          s_rows[t] = (int)paged_row(a.pk, a.Hkv, a.total, kvb, b, kvh, (int)(p + t), 0);
+        // a thread's positions (stride 256; cnt >= 1) looked up as one batch
+        // of loads, those past the sub-range at its last position
+        constexpr int kPer = kMaxChunkTokens / 256;
+        int rr[kPer];
+        int64_t pr[kPer];
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) rr[e] = (int)(p + min(tid + e * 256, cnt - 1));
+        paged_rows(a.pk, a.Hkv, a.total, kvb, b, kvh, rr, 0, pr);
+#pragma unroll
+        for (int e = 0; e < kPer; ++e)
+          if (tid + e * 256 < cnt) s_rows[tid + e * 256] = (int)pr[e];
         __syncthreads();
       } else {
         const int64_t c = p / kCfrTokens, in = p - c * kCfrTokens;
