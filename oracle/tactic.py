@@ -271,10 +271,18 @@ def selection_report(q: np.ndarray, Ks: np.ndarray, Vs: np.ndarray, r: GroupResu
     s = softmax_weights(_logits(q, Ks))
     p_sel = float(s[r.sel[h]].sum())
     p_union = float(s[r.union].sum())
-    desc = np.sort(s)[::-1]
-    k_opt = int(np.argmax(np.add.accumulate(desc) >= P)) + 1
+
+    def first_reaching(cum: np.ndarray, target: float) -> int:
+        # fewest leading tokens whose mass reaches the target; all of them
+        # when rounding leaves the full sum a hair below it (P = 1)
+        hit = np.nonzero(cum >= target)[0]
+        return int(hit[0]) + 1 if len(hit) else len(cum)
+
+    k_opt = first_reaching(np.add.accumulate(np.sort(s)[::-1]), P)
+    # Cluster-Optimal: the true scores of the clustered tokens taken in the
+    # head's cluster order, against P of their total
     cs = np.add.accumulate(s[r.rows[h]])
-    k_cluster = int(np.argmax(cs >= P * cs[-1])) + 1
+    k_cluster = first_reaching(cs, P * cs[-1]) if len(cs) else 0
     o = s @ Vs
     eps = float(np.linalg.norm(o - r.out[h]))
     bound = 2.0 * (1.0 - p_union) * float(np.max(np.linalg.norm(Vs, axis=1)))

@@ -134,6 +134,69 @@ def test_fit_recovers_exact_curve_and_cutoff_matches_rational_arithmetic():
             assert k == k_exact, (n, P, k, k_exact)
 
 
+def _window_mean_exact(a: Fraction, b: Fraction, s: int, t: int) -> Fraction:
+    """Mean of a/i + b over the integers s..t: (a (H_t - H_{s-1}) + b W) / W."""
+    W = t - s + 1
+    return (a * sum((Fraction(1, i) for i in range(s, t + 1)), Fraction(0)) + b * W) / W
+
+
+WINDOWED_CASES = [
+    (600, dict()),                                     # W = 8 (the minimum)
+    (1700, dict()),                                    # W = 9
+    (2000, dict(win_bp=400)),                          # W = 80
+    (1200, dict(exact_bp=200, win_bp=300, p1_bp=1500, p2_bp=5000)),
+]
+
+
+def pin_windowed_fit_exact(T):
+    """Algorithm 1 with real windows (W >= 8) on a list whose tail follows
+    y = a/x + b exactly.  Each window's point is the mean of the scores over
+    its positions placed at the window's middle position (Sec. 4.4: means
+    within windows around p1 and p2).  Since 1/x is convex that mean is not
+    a/x_mid + b, so the fit gives other coefficients (a', b'); they, the two
+    means and the budget must equal the values exact rational arithmetic
+    gives from those definitions."""
+    checked = 0
+    for n, kw in WINDOWED_CASES:
+        prm = T.FitParams(**kw)
+        g = T.geometry(n, prm)
+        assert not g.exact and g.t1 - g.s1 + 1 >= 8 and g.t2 - g.s2 + 1 >= 8
+        a, b = Fraction(g.N, 2), Fraction(1, 64)
+        m = 3.0
+        head = [m] + [m - 0.05 - 0.6 * i / g.N for i in range(1, g.N)]
+        tail = [m + math.log(float(a) / i + float(b)) for i in range(g.N + 1, n + 1)]
+        l_pos = np.array(head + tail)
+        mu1 = _window_mean_exact(a, b, g.s1, g.t1)
+        mu2 = _window_mean_exact(a, b, g.s2, g.t2)
+        x1, x2 = Fraction(g.s1 + g.t1, 2), Fraction(g.s2 + g.t2, 2)
+        a2 = (mu1 - mu2) / (1 / x1 - 1 / x2)
+        b2 = mu1 - a2 / x1
+        E = [Fraction(math.exp(x - m)) for x in head]
+        w = E + [max(Fraction(0), a2 / i + b2) for i in range(g.N + 1, n + 1)]
+        S, acc = [], Fraction(0)
+        for x in w:
+            acc += x
+            S.append(acc)
+        for P in (0.3, 0.5, 0.7, 0.8, 0.9, 0.97):
+            k, info = T.estimate_budget(l_pos, P, prm)
+            assert abs(info["mu1"] - float(mu1)) <= 1e-12 * float(mu1), (n, kw, info["mu1"], float(mu1))
+            assert abs(info["mu2"] - float(mu2)) <= 1e-12 * float(mu2), (n, kw, info["mu2"], float(mu2))
+            assert abs(info["a"] - float(a2)) <= 1e-9 * abs(float(a2)), (n, kw, info["a"], float(a2))
+            assert abs(info["b"] - float(b2)) <= 1e-9 * abs(float(a2)) / n, (n, kw, info["b"], float(b2))
+            target = Fraction(P) * S[-1]
+            k_exact = next(i for i, x in enumerate(S, start=1) if x >= target)
+            # compare only where no cumulative sum lies within 1e-9 of the target
+            margin = min(abs(S[k_exact - 1] - target), abs(target - S[k_exact - 2]) if k_exact > 1 else 1)
+            if margin > Fraction(1, 10 ** 9) * S[-1]:
+                assert k == k_exact, (n, kw, P, k, k_exact)
+                checked += 1
+    assert checked >= 20
+
+
+def test_windowed_fit_matches_exact_arithmetic():
+    pin_windowed_fit_exact(T)
+
+
 def test_constant_tail_budget_closed_form():
     """a = 0: w is constant b beyond the head, so the budget is
     N + ceil((P S_n - E_N) / b) when the target lies beyond the head."""
@@ -205,7 +268,7 @@ def _golden_inputs(fx):
     return Q, K, V, cent, np.array(fx["offsets"])
 
 
-def test_golden_tiny_exact_pipeline():
+def pin_golden_pipeline(T):
     with open(os.path.join(GOLDEN, "tiny_exact.json")) as f:
         fx = json.load(f)
     Q, K, V, cent, off = _golden_inputs(fx)
@@ -217,6 +280,33 @@ def test_golden_tiny_exact_pipeline():
             exp = np.array([[_frac(x) for x in row] for row in case[key]])
             np.testing.assert_allclose(r.out[:, :4], exp, rtol=0, atol=1e-12)
             assert np.all(r.out[:, 4:] == 0)
+
+
+def pin_golden_report(T):
+    """Sec. 5.2's diagnostics on the worked example: p(I_h) and p(U) (Eq. 5),
+    the Optimal and Cluster-Optimal budgets, the attention distance (Eq. 4)
+    and its bound (Eq. 6), each derived by hand in tests/golden."""
+    with open(os.path.join(GOLDEN, "tiny_exact.json")) as f:
+        fx = json.load(f)
+    Q, K, V, cent, off = _golden_inputs(fx)
+    for case in fx["cases"]:
+        r = T.decode_group(Q, K, V, cent, off, case["P"])
+        for h, want in enumerate(case["report"]):
+            got = T.selection_report(Q[h], K, V, r, case["P"], h)
+            assert got["k_optimal"] == want["k_optimal"], (case["P"], h, got)
+            assert got["k_cluster_optimal"] == want["k_cluster_optimal"], (case["P"], h, got)
+            assert abs(got["p_sel"] - _frac(want["p_sel"])) <= 1e-12, (case["P"], h, got)
+            assert abs(got["p_union"] - _frac(want["p_union"])) <= 1e-12, (case["P"], h, got)
+            assert abs(got["eps"] ** 2 - _frac(want["eps_sq"])) <= 1e-12, (case["P"], h, got)
+            assert abs(got["bound"] - _frac(want["bound"])) <= 1e-12, (case["P"], h, got)
+
+
+def test_golden_tiny_exact_pipeline():
+    pin_golden_pipeline(T)
+
+
+def test_golden_tiny_exact_report():
+    pin_golden_report(T)
 
 
 def _random_clustered_group(rng, n, C, G=4, d=128):
