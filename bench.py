@@ -14,7 +14,14 @@ separately), or from the generator's mixture labels with --clusters labels.
 Prints one JSON line: sparse microseconds per layer (lower is better), the
 same-GPU dense decode time and speedup, the HBM rate on the bytes the
 kernels must read, a roofline record of the dominant kernel and the CPU
-oracle's time on a bounded sample.
+oracle's time on a bounded sample.  The same line carries one record per
+other workload (4K, 32K at three target fractions, the ragged batch of 16,
+1M tokens): single-layer timings with the caches flushed before every rep,
+and the device's measured streaming-read ceiling.
+
+Bytes "touched" per layer: every centroid row and cluster offset, every K and
+V row of each group's union, and the distinct sampled key rows of a group
+that lie outside its union (the ones inside are read again by the attention).
 """
 from __future__ import annotations
 
@@ -95,6 +102,68 @@ class TimingEvents:
         return ms.value
 
 
+class Flusher:
+    """Evicts L2 and the 256 MB Infinity Cache between timed reps by writing a
+    1 GiB buffer (untimed: it runs between the events of two reps)."""
+
+    def __init__(self, dev, nbytes: int = 1 << 30):
+        self.buf = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        self.v = 0
+
+    def __call__(self):
+        self.v ^= 1
+        self.buf.fill_(self.v)
+
+
+def timed_reps(fn, reps: int, flush=None) -> list:
+    """Milliseconds of each of `reps` calls of fn, from events around the call
+    alone on the current stream; `flush`, if given, runs before every rep."""
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    torch.cuda.synchronize()
+    for e0, e1 in evs:
+        if flush is not None:
+            flush()
+        e0.record()
+        fn()
+        e1.record()
+    torch.cuda.synchronize()
+    return [e0.elapsed_time(e1) for e0, e1 in evs]
+
+
+def samples_outside_union(view: dict, clusters, G: int) -> int:
+    """Distinct sampled key rows of every (sequence, KV head) group that lie
+    outside the group's union: the sampled rows the attention does not read
+    again.  Rows past a sequence's clusters (recent tokens) are always in it."""
+    rows = view["sample_rows"].cpu().numpy()
+    cnt = view["fit"][..., 11].cpu().numpy().astype(np.int64)
+    ulen = view["union_len"].cpu().numpy()
+    off = clusters.offsets.cpu().numpy()
+    clp = clusters.cl_indptr_host
+    B, Hq = cnt.shape
+    total = 0
+    for b in range(B):
+        c0, c1 = int(clp[b]), int(clp[b + 1])
+        for g in range(Hq // G):
+            o = off[g, c0 + b:c1 + b + 1].astype(np.int64)
+            r = np.unique(np.concatenate([rows[b, g * G + j, :cnt[b, g * G + j]] for j in range(G)]))
+            r = r[r < o[-1]]
+            c = np.searchsorted(o, r, side="right") - 1
+            total += int(np.count_nonzero((r - o[c]) >= ulen[g, c0 + c]))
+    return total
+
+
+def touched_bytes(view: dict, clusters, sel_kv: torch.Tensor, G: int) -> dict:
+    """Bytes one sparse decode call must move: centroids and offsets, the
+    union's K and V rows, and the sampled key rows outside the union."""
+    Hkv, Ct = clusters.centroids.shape[0], clusters.total
+    B = len(clusters.n_clusters)
+    cent = Hkv * Ct * 256 + Hkv * (Ct + B) * 4
+    samples = samples_outside_union(view, clusters, G) * 256
+    union = float(sel_kv.sum()) * 512
+    return {"centroids": float(cent), "samples_outside_union": float(samples), "union_kv": union,
+            "total": float(cent + samples + union)}
+
+
 def dense_sdpa(q, K, V, wl, reps: int, own_out=None) -> dict:
     """torch's scaled_dot_product_attention (GQA) as a second dense decode on
     one layer's bf16 inputs, restricted to the fused flash / memory-efficient
@@ -131,6 +200,129 @@ def dense_sdpa(q, K, V, wl, reps: int, own_out=None) -> dict:
         return {"us_per_layer": None, "error": f"{type(e).__name__}: {str(e)[:160]}"}
 
 
+STAGE_NAMES = ["score_clusters", "sort_clusters", "sample_logits", "fit_union", "attn_splitk", "combine"]
+
+
+def config_record(T, wl, Ps, dev, flush, reps: int, stage_ev, ceiling, host_groups=None):
+    """One layer of workload `wl` on the library's K-means clusters: sparse and
+    dense decode times (medians of `reps` calls, caches flushed before each),
+    per-kernel times (library events, flushed), touched bytes and rates,
+    selected fractions.  host_groups: (sequence, KV head) groups whose fp64
+    inputs are returned for the CPU oracle legs."""
+    import ctypes
+    from paper_2502_12216_amd import _capi as C
+    B, Hq, Hkv = wl.batch, wl.n_q_heads, wl.n_kv_heads
+    G = Hq // Hkv
+    ncl = list(wl.cluster_counts)
+    lens = np.asarray(wl.seq_lens, dtype=np.float64)
+    batch = T.RaggedBatch(wl.seq_lens, Hq, Hkv)
+    inp = synth.make_layer(wl, 0, device=dev)
+    init = torch.as_tensor(synth.kmeans_init_all(wl, 0), device=dev)
+    bld = T.ClusterBuilder(batch, ncl, max_iters=wl.kmeans_iters)
+    built = []
+    km_ms = timed_reps(lambda: built.append(bld(inp.K, inp.V, init)), 1)[0]
+    cb = built[0]
+    q, Ks, Vs, cl = inp.q, cb.K_sorted, cb.V_sorted, cb.clusters
+    host = None
+    if host_groups:
+        kvp, clp = batch.kv_indptr_host, cl.cl_indptr_host
+        host = {"G": G, "groups": []}
+        for b, g in host_groups:
+            s0, s1, c0, c1 = int(kvp[b]), int(kvp[b + 1]), int(clp[b]), int(clp[b + 1])
+            host["groups"].append(dict(
+                Q=q[b, g * G:(g + 1) * G].double().cpu().numpy(), Ks=Ks[g, s0:s1].double().cpu().numpy(),
+                Vs=Vs[g, s0:s1].double().cpu().numpy(), cent=cl.centroids[g, c0:c1].double().cpu().numpy(),
+                off=cl.offsets[g, c0 + b:c1 + b + 1].cpu().numpy().astype(np.int64),
+                K=inp.K[g, s0:s1].double().cpu().numpy(), init=init[g, c0:c1].cpu().numpy().astype(np.int64)))
+        host["groups_per_layer"] = B * Hkv
+    del inp, built
+    den = T.DenseDecoder(batch)
+    for _ in range(3):
+        den(q, Ks, Vs)
+    us_dense = float(np.median(timed_reps(lambda: den(q, Ks, Vs), reps, flush))) * 1000
+    dense_bytes = float(lens.sum()) * Hkv * 512
+    points = []
+    for P in Ps:
+        dec = T.SparseDecoder(batch, ncl, T.decode_params(P))
+        for _ in range(3):
+            dec(q, Ks, Vs, cl)
+        us = float(np.median(timed_reps(lambda: dec(q, Ks, Vs, cl), reps, flush))) * 1000
+        C.check(C.lib().tactic_sparse_decode_plan_set_events(ctypes.byref(dec.plan), stage_ev.array), "set_events")
+        acc = np.zeros(len(STAGE_NAMES))
+        n_ev = 5
+        for _ in range(n_ev):
+            flush()
+            dec(q, Ks, Vs, cl)
+            torch.cuda.synchronize()
+            acc += [stage_ev.elapsed(i, i + 1) for i in range(len(STAGE_NAMES))]
+        C.check(C.lib().tactic_sparse_decode_plan_set_events(ctypes.byref(dec.plan), None), "set_events")
+        stage_us = acc / n_ev * 1000
+        _, sq, skv = dec(q, Ks, Vs, cl)
+        torch.cuda.synchronize()
+        tb = touched_bytes(dec.view(), cl, skv, G)
+        kq = sq.cpu().numpy() / lens[:, None]
+        ku = skv.cpu().numpy() / lens[:, None]
+        gbps = tb["total"] / (us * 1e3)
+        rec = {"target_frac": P, "sparse_us": round(us, 2), "dense_us": round(us_dense, 2),
+               "speedup_vs_dense": round(us_dense / us, 3),
+               "touched_mb": round(tb["total"] / 1e6, 3),
+               "touched_parts_mb": {k: round(v / 1e6, 3) for k, v in tb.items() if k != "total"},
+               "hbm_gbps": round(gbps, 1), "hbm_frac_peak": round(gbps / HBM_PEAK_GBPS, 4),
+               "hbm_frac_read_ceiling": round(gbps / ceiling, 4) if ceiling else None,
+               "byte_bound_speedup": round(dense_bytes / tb["total"], 3),
+               "stages_us": {n: round(float(t), 2) for n, t in zip(STAGE_NAMES, stage_us)},
+               "attn_gbps": round(tb["union_kv"] / (float(stage_us[4]) * 1e3), 1),
+               "selected_frac": {"head_mean": round(float(kq.mean()), 5),
+                                 "head_median": round(float(np.median(kq)), 5),
+                                 "head_max": round(float(kq.max()), 5), "union_mean": round(float(ku.mean()), 5),
+                                 "union_max": round(float(ku.max()), 5)}}
+        if B == 1 and Hq <= 32 and lens[0] >= 1 << 20:
+            rec["k_per_query_head"] = [int(x) for x in sq.cpu().numpy()[0]]
+            rec["union_per_kv_head"] = [int(x) for x in skv.cpu().numpy()[0]]
+        points.append(rec)
+        del dec
+    sort_path = "LDS" if max(ncl) <= 8192 else "workspace (out of LDS)"
+    out = {"batch": B, "seq_lens": (list(map(int, wl.seq_lens)) if B > 1 else int(wl.seq_lens[0])),
+           "n_q_heads": Hq, "n_kv_heads": Hkv, "clusters_per_seq": (list(map(int, ncl)) if B > 1 else int(ncl[0])),
+           "cluster_sort": sort_path, "kmeans_ms": round(km_ms, 2), "dense_us": round(us_dense, 2),
+           "dense_gbps": round(dense_bytes / (us_dense * 1e3), 1), "points": points}
+    del den, q, Ks, Vs, cl, cb
+    torch.cuda.empty_cache()
+    return out, host
+
+
+def oracle_config_timings(hosts: dict, P: float) -> dict:
+    """The fp64 oracle's decode (per group, scaled to one layer) on the host
+    cores, with all BLAS threads and with one, and its K-means (10
+    iterations) on one group, for the small workloads."""
+    from threadpoolctl import threadpool_info, threadpool_limits
+
+    from oracle import kmeans as OK
+    from oracle import tactic as OT
+    all_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    res = {}
+    for name, host in hosts.items():
+        r = {"groups_timed": len(host["groups"]), "groups_per_layer": host["groups_per_layer"]}
+        for label, th in (("all_threads", all_threads), ("one_thread", 1)):
+            with threadpool_limits(limits=th):
+                t = 0.0
+                for gi in host["groups"]:
+                    t0 = time.perf_counter()
+                    OT.decode_group(gi["Q"], gi["Ks"], gi["Vs"], gi["cent"], gi["off"], P)
+                    t += time.perf_counter() - t0
+            r[f"decode_us_per_layer_{label}"] = round(t / len(host["groups"]) * host["groups_per_layer"] * 1e6, 1)
+        gi = host["groups"][0]
+        with threadpool_limits(limits=all_threads):
+            t0 = time.perf_counter()
+            km = OK.kmeans(gi["K"], gi["init"], max_iters=10)
+            t = time.perf_counter() - t0
+        r["kmeans_s_per_group_all_threads"] = round(t, 3)
+        r["kmeans_iters"] = int(km.iters)
+        r["threads"] = {"all": int(all_threads), "one": 1}
+        res[name] = r
+    return res
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -149,6 +341,9 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true", help="skip the query-concentration sweep")
     ap.add_argument("--calibrate", action="store_true",
                     help="also run a plain 1 GiB device copy (reference dispatch for HBM counters)")
+    ap.add_argument("--no-configs", action="store_true", help="skip the records of the other workloads")
+    ap.add_argument("--config-reps", type=int, default=20, help="timed calls per point of those records")
+    ap.add_argument("--no-ceiling", action="store_true", help="skip the streaming-read ceiling measurement")
     return ap.parse_args()
 
 
@@ -226,6 +421,7 @@ def main():
     params = T.decode_params(P)
     dec = T.SparseDecoder(batch, ncl, params)
     dense = T.DenseDecoder(batch)
+    flush = Flusher(dev)
 
     def sparse_step():
         for l in range(layers):
@@ -291,7 +487,7 @@ def main():
 
     layer_ms = []
     stage_ms = stage_times(dec, per_layer=layer_ms)
-    stage_names = ["score_clusters", "sort_clusters", "sample_logits", "fit_union", "attn_splitk", "combine"]
+    stage_names = STAGE_NAMES
 
     # ---------------------------------------------------------------- GQA-union ablation (Sec. 4.5)
     ablation = None
@@ -391,7 +587,7 @@ def main():
         def decode_us():
             for _ in range(20):  # warm-up (the appends before leave the GPU lightly loaded)
                 cache.decode(q0)
-            return timed(lambda: cache.decode(q0), 50) * 1000
+            return float(np.median(timed_reps(lambda: cache.decode(q0), 30, flush))) * 1000
 
         us_tail = decode_us()
         tail_now = cache.recent[0]
@@ -411,7 +607,8 @@ def main():
                   "amortized_us_per_step_cold": round(ms_cold * 1000 / T_rec, 2),
                   "note": "one layer of the workload; prefill of n - 2048 tokens, 2047 appended, the 2048th "
                           "append re-clusters from the previous centroids (warm), then a cold re-clustering of "
-                          "the same cache for comparison; the warm time includes the append"}
+                          "the same cache for comparison; the warm time includes the append; decode times are "
+                          "medians of 30 calls, caches flushed before each"}
         del cache, inp0
         log(f"recent tail: decode {us_tail:.1f} us with {tail_now} recent tokens, re-clustering warm {ms_warm:.1f} ms "
             f"cold {ms_cold:.1f} ms")
@@ -435,12 +632,10 @@ def main():
             for _ in range(5):
                 dec_s(*args_s, cb_s.clusters)
                 den_s(*args_s)
-            us_s = timed(lambda: dec_s(*args_s, cb_s.clusters), 30) * 1000
-            us_d = timed(lambda: den_s(*args_s), 30) * 1000
+            us_s = float(np.median(timed_reps(lambda: dec_s(*args_s, cb_s.clusters), 30, flush))) * 1000
+            us_d = float(np.median(timed_reps(lambda: den_s(*args_s), 30, flush))) * 1000
             _, sq_s, skv_s = dec_s(*args_s, cb_s.clusters)
-            smp = float(dec_s.view()["fit"][..., 11].sum())
-            C_s = float(ncl_s[0])
-            b_sparse = B_s * wl_s.n_kv_heads * (C_s * 256 + (C_s + 1) * 4) + smp * 256 + float(skv_s.sum()) * 512
+            b_sparse = touched_bytes(dec_s.view(), cb_s.clusters, skv_s, wl_s.n_q_heads // wl_s.n_kv_heads)["total"]
             b_dense = float(n_s) * B_s * wl_s.n_kv_heads * 512
             points.append({"batch": B_s, "beta": wl_s.beta, "reading": "mean" if wl_s.q_mean else "sum",
                            "head_frac_mean": round(float(sq_s.double().mean()) / n_s, 5),
@@ -451,24 +646,26 @@ def main():
         sweep = {"workload": "batch x 131072 tokens (batch 1 at every point, 4 at two), 32 query / 8 KV heads, "
                              "8192 K-means clusters per sequence (10 iterations), P = 0.9; query = beta (sum or "
                              "mean of k_h in 1..8 centres + noise)",
+                 "timing": "median of 30 calls of one layer, L2 and Infinity Cache flushed before each",
                  "points": points}
         log("concentration sweep: " + ", ".join(f"B={p['batch']} b={p['beta']:g}/{p['reading']} U={p['union_frac_mean']:.3f} "
                                                 f"x{p['speedup']:.2f}" for p in points))
 
     # ---------------------------------------------------------------- selection statistics, bytes
-    sel_q, sel_kv, samples = [], [], []
+    sel_q, sel_kv, tb = [], [], []
     for l in range(layers):
         _, sq, skv = dec(qs[l], Ks[l], Vs[l], cls[l])
-        v = dec.view()
+        torch.cuda.synchronize()
         sel_q.append(sq.cpu().numpy().copy())
         sel_kv.append(skv.cpu().numpy().copy())
-        samples.append(v["fit"][..., 11].cpu().numpy().copy())
-    sel_q, sel_kv, samples = np.array(sel_q), np.array(sel_kv), np.array(samples)
+        v = dec.view()
+        tb.append(touched_bytes(v, cls[l], skv, G))
+        tb[-1]["sampled_all"] = float(v["fit"][..., 11].sum()) * 256  # what the sampling kernel reads
+    sel_q, sel_kv = np.array(sel_q), np.array(sel_kv)
     lens = np.array(wl.seq_lens, dtype=np.float64)
-    Csum = float(sum(ncl))
-    bytes_centroids = Hkv * Csum * 256 + Hkv * (Csum + B) * 4
-    bytes_samples = samples.sum(axis=(1, 2)) * 256            # per layer
-    bytes_union = sel_kv.sum(axis=(1, 2)) * 512               # per layer
+    bytes_centroids = tb[0]["centroids"]
+    bytes_samples = np.array([t["samples_outside_union"] for t in tb])   # per layer
+    bytes_union = np.array([t["union_kv"] for t in tb])                  # per layer
     bytes_layer = bytes_centroids + bytes_samples + bytes_union
     dense_bytes_layer = float(lens.sum()) * Hkv * 512
     us_sparse = ms_sparse * 1000 / layers
@@ -476,7 +673,9 @@ def main():
     us_dense_best = min(us_dense, sdpa["us_per_layer"]) if sdpa.get("us_per_layer") else us_dense
     gbps = float(bytes_layer.mean()) / (us_sparse * 1e3)
     stage_us = stage_ms * 1000
-    stage_bytes = [bytes_centroids, 0.0, float(bytes_samples.mean()), 0.0, float(bytes_union.mean()), 0.0]
+    # each kernel's own algorithmic bytes: the sampler reads every sampled row
+    stage_bytes = [bytes_centroids, 0.0, float(np.mean([t["sampled_all"] for t in tb])), 0.0,
+                   float(bytes_union.mean()), 0.0]
     dom = int(np.argmax(stage_us))
     dom_bytes = stage_bytes[dom]
     roof = {
@@ -493,6 +692,31 @@ def main():
     roof["traffic"] = profiled_traffic(stage_names[dom])
     kq = sel_q.astype(np.float64) / lens[None, :, None]
     ku = sel_kv.astype(np.float64) / lens[None, :, None]
+
+    # ---------------------------------------------------------------- streaming-read ceiling
+    ceiling = None
+    if not args.no_ceiling:
+        buf = torch.empty(4 << 30, dtype=torch.uint8, device=dev)
+        ceiling = T.stream_read_gbps(buf, reps=10)
+        del buf
+        log(f"streaming-read ceiling {ceiling:.0f} GB/s")
+
+    # ---------------------------------------------------------------- the other workloads, one layer each
+    configs, hosts = None, {}
+    if not args.no_configs:
+        configs = {}
+        for name, Ps, hg in (("ctx4k_gqa4", (0.9,), [(0, 0), (0, 1)]),
+                             ("ctx32k_llama8b", (0.8, 0.9, 0.95), [(0, 0), (0, 5)]),
+                             ("ragged16_16k_128k", (0.9,), None),
+                             ("ctx1m", (0.9,), None)):
+            rec, host = config_record(T, synth.WORKLOADS[name], Ps, dev, flush, args.config_reps, stage_ev, ceiling,
+                                      host_groups=None if args.no_cpu else hg)
+            configs[name] = rec
+            if host is not None:
+                hosts[name] = host
+            log(f"{name}: " + ", ".join(f"P={p['target_frac']} {p['sparse_us']:.1f} us vs dense {p['dense_us']:.1f} us "
+                                        f"(x{p['speedup_vs_dense']:.2f}, union {p['selected_frac']['union_mean']:.3f})"
+                                        for p in rec["points"]))
 
     # ---------------------------------------------------------------- CPU oracle on a bounded sample
     cpu = None
@@ -531,6 +755,9 @@ def main():
                          f"host {platform.processor() or platform.machine()}, "
                          f"{len(os.sched_getaffinity(0))} cores visible"}
         log(f"cpu oracle {per_group:.2f} s per group")
+        if hosts:
+            cpu["configs"] = oracle_config_timings(hosts, P)
+            log(f"cpu oracle on the small workloads: {cpu['configs']}")
 
     res = {
         "metric": METRIC,
@@ -564,8 +791,10 @@ def main():
         "hbm_gbps": round(gbps, 1),
         "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
         "dense_hbm_gbps": round(dense_bytes_layer / (us_dense * 1e3), 1),
-        "bytes_per_layer": {"centroids": bytes_centroids, "samples": float(bytes_samples.mean()),
-                            "union_kv": float(bytes_union.mean()), "dense_kv": dense_bytes_layer},
+        "bytes_per_layer": {"centroids": bytes_centroids, "samples_outside_union": float(bytes_samples.mean()),
+                            "union_kv": float(bytes_union.mean()), "dense_kv": dense_bytes_layer,
+                            "note": "touched bytes: centroids + offsets, distinct sampled key rows of a group "
+                                    "outside its union, and the union's K and V rows; mean over layers"},
         "stages_us_per_layer": {n: round(float(t), 2) for n, t in zip(stage_names, stage_us)},
         "stage_timing": "HIP events recorded by the library between its launches on the decode stream, "
                         "created with hipEventDisableSystemFence (no cache flush at each event)",
@@ -573,7 +802,10 @@ def main():
                           "head_max": round(float(kq.max()), 5), "union_mean": round(float(ku.mean()), 5),
                           "union_max": round(float(ku.max()), 5)},
         "roofline": roof,
+        "hbm_read_ceiling_gbps": round(ceiling, 1) if ceiling else None,
+        "attn_frac_of_read_ceiling": (round(stage_bytes[4] / (stage_us[4] * 1e3) / ceiling, 4) if ceiling else None),
         "cpu_baseline": cpu,
+        "configs": configs,
         "union_ablation": ablation,
         "paged_kv": paged,
         "recent_tail": recent,

@@ -125,7 +125,11 @@ void tactic_decode_params_default(tactic_decode_params* p);
 
 /* Validates shape, cluster counts and parameters and fills `plan`.
  * *workspace_bytes receives the workspace size tactic_sparse_decode needs.
- * meta's device pointers are not read and may be null here.
+ * meta's device pointers are not read and may be null here.  The plan also
+ * records how many attention workgroups fit at once on the device current at
+ * this call, so that decode calls on that device make no occupancy query
+ * (calls on another device make it).  At most 4096 selection groups: B * Hkv,
+ * or B * Hq with use_union = 0.
  * Errors: TACTIC_ERR_INVALID_ARG, TACTIC_ERR_UNSUPPORTED. */
 tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape,
                                         const tactic_cluster_meta* meta,
@@ -184,6 +188,10 @@ typedef struct {
                                   [Hq][total_clusters] (use_union = 0): rows of each cluster
                                   in the group's union or the head's selection (a prefix of
                                   the cluster) */
+  const int32_t* sample_rows;  /* [B][Hq][sample_cap]: sequence-relative cache rows whose keys the
+                                  head sampled (exact head 1..N, window 1, window 2, then the
+                                  recent tokens); the first `sampled rows` (fit field 11) are valid */
+  int64_t sample_cap;
 } tactic_decode_view;
 
 tactic_status tactic_sparse_decode_view(const tactic_decode_plan* plan, const void* workspace,
@@ -280,6 +288,14 @@ tactic_status tactic_build_clusters(const uint16_t* K, const uint16_t* V,
                                     uint16_t* centroids, int32_t* assign, int32_t* offsets,
                                     int32_t* perm, uint16_t* K_sorted, uint16_t* V_sorted,
                                     void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Measurement helper, not part of the method: reads every 16-byte word of
+ * `buf` (bytes, a multiple of 16) once with streaming loads from a grid of
+ * resident workgroups and stores nothing unless a read value equals a magic
+ * word (then one word to *sink, a device uint32).  Its rate is the device's
+ * practical streaming-read ceiling, the yardstick of the bandwidth-bound
+ * decode kernels.  Errors: TACTIC_ERR_INVALID_ARG, TACTIC_ERR_HIP. */
+tactic_status tactic_probe_stream_read(const void* buf, size_t bytes, uint32_t* sink, hipStream_t stream);
 
 /* Static description of a status code. */
 const char* tactic_status_string(tactic_status s);

@@ -21,6 +21,7 @@ EXPORTS = (
     "tactic_sparse_decode_plan_set_events",
     "tactic_sparse_decode_view", "tactic_dense_decode_workspace_size", "tactic_dense_decode",
     "tactic_sparse_decode_paged", "tactic_dense_decode_paged",
+    "tactic_probe_stream_read",
     "tactic_build_clusters_workspace_size", "tactic_build_clusters", "tactic_status_string",
     "tactic_last_error",
 )
@@ -49,7 +50,7 @@ class DecodePlan(ctypes.Structure):
 
 class DecodeView(ctypes.Structure):
     _fields_ = [("scores", c_void_p), ("order", c_void_p), ("rank_prefix", c_void_p),
-                ("fit", c_void_p), ("union_len", c_void_p)]
+                ("fit", c_void_p), ("union_len", c_void_p), ("sample_rows", c_void_p), ("sample_cap", c_int64)]
 
 
 class PagedKV(ctypes.Structure):
@@ -109,6 +110,8 @@ def lib() -> ctypes.CDLL:
                                         c_void_p, POINTER(KMeansParams), c_void_p, c_void_p, c_void_p,
                                         c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
     L.tactic_build_clusters.restype = c_int
+    L.tactic_probe_stream_read.argtypes = [c_void_p, c_size_t, c_void_p, c_void_p]
+    L.tactic_probe_stream_read.restype = c_int
     L.tactic_status_string.argtypes = [c_int]
     L.tactic_status_string.restype = c_char_p
     L.tactic_last_error.argtypes = []

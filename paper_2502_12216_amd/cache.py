@@ -16,7 +16,8 @@ from typing import List, Optional, Sequence
 import numpy as np
 import torch
 
-from .tactic import ClusterBuilder, ClusterSet, DenseDecoder, RaggedBatch, SparseDecoder, decode_params
+from .tactic import (ClusterBuilder, ClusterSet, DenseDecoder, RaggedBatch, SparseDecoder, decode_params,
+                     sparse_decode_workspace_bytes)
 
 
 class RecentTailCache:
@@ -46,8 +47,11 @@ class RecentTailCache:
         self.starts = torch.as_tensor(self.batch.kv_indptr_host[:-1], device=device)
         self.K = torch.zeros(self.Hkv, self.batch.total, 128, dtype=torch.bfloat16, device=device)
         self.V = torch.zeros_like(self.K)
+        self.K_alt = torch.empty_like(self.K)  # the next clustering writes here, then the two swap
+        self.V_alt = torch.empty_like(self.V)
         self.clusters: Optional[ClusterSet] = None
         self.decoder: Optional[SparseDecoder] = None
+        self.builder: Optional[ClusterBuilder] = None
         self.dense = DenseDecoder(self.batch, device=device)
         self.reclusterings = 0
 
@@ -116,13 +120,23 @@ class RecentTailCache:
                 if n and C > m:
                     init[g, c0 + m:c0 + C] = lo + self.rng.choice(n - lo, size=C - m, replace=n - lo < C - m)
             c0 += C
-        builder = ClusterBuilder(self.batch, ncl, max_iters=self.kmeans_iters, device=self.device)
-        res = builder(self.K, self.V, torch.as_tensor(init, device=self.device), prev=prev)
-        self.K, self.V = res.K_sorted, res.V_sorted
+        if self.builder is None:  # one workspace, sized for the counts of full sequences
+            self.builder = ClusterBuilder(self.batch, ncl, max_iters=self.kmeans_iters, device=self.device,
+                                          workspace_clusters=[self.n_clusters(c) for c in self.capacities])
+        res = self.builder(self.K, self.V, torch.as_tensor(init, device=self.device), prev=prev, n_clusters=ncl,
+                           K_out=self.K_alt, V_out=self.V_alt)
+        self.K, self.K_alt = self.K_alt, self.K
+        self.V, self.V_alt = self.V_alt, self.V
         self.clusters = res.clusters
         self.clustered = list(self.lens)
-        self.decoder = SparseDecoder(self.batch, ncl, decode_params(self.target_frac, max_tail=self.recluster_every),
-                                     device=self.device)
+        params = decode_params(self.target_frac, max_tail=self.recluster_every)
+        if self.decoder is None:  # one workspace, sized for the counts of full sequences
+            cap = [self.n_clusters(c) for c in self.capacities]
+            ws = torch.empty(sparse_decode_workspace_bytes(self.batch, cap, params), dtype=torch.uint8,
+                             device=self.device)
+        else:
+            ws = self.decoder.workspace
+        self.decoder = SparseDecoder(self.batch, ncl, params, device=self.device, workspace=ws)
         self.reclusterings += 1
 
     # ------------------------------------------------------------------ attention

@@ -184,6 +184,11 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape, const tact
   p.max_tail = params->max_tail;
   p.NV = p.use_union ? p.Hkv : p.Hq;
   p.GV = p.use_union ? p.G : 1;
+  // the attention keeps one prefix entry per selection group in LDS
+  if (p.B * p.NV > tactic::kMaxGroups)
+    return fail(TACTIC_ERR_UNSUPPORTED, "batch * %s = %lld selection groups > %d",
+                p.use_union ? "n_kv_heads" : "n_q_heads (use_union = 0)", (long long)(p.B * p.NV),
+                tactic::kMaxGroups);
   // sampled rows per head: the largest list any length <= nmax can need
   const tactic::SelParams sp = sel_params(params);
   int64_t S_cap = 1;
@@ -229,6 +234,19 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape, const tact
     p.off_sort_start = L.take(BH * (p.nb_max + 4) * 4);
   }
   p.ws_bytes = L.cur;
+  // resident attention workgroups on the current device, so that decode calls
+  // on it need no occupancy query; without a usable device the calls query
+  p.attn_dev = -1;
+  int dev = -1, g0 = 0, g1 = 0;
+  if (hipGetDevice(&dev) == hipSuccess &&
+      tactic::attn_resident_grid((int)p.GV, (int)(p.B * p.NV), false, &g0) == hipSuccess &&
+      tactic::attn_resident_grid((int)p.GV, (int)(p.B * p.NV), true, &g1) == hipSuccess) {
+    p.attn_dev = dev;
+    p.attn_res[0] = g0;
+    p.attn_res[1] = g1;
+  } else {
+    (void)hipGetLastError();  // leave no error behind for the next launch check
+  }
   memcpy(plan_out, &p, sizeof(p));
   *workspace_bytes = (size_t)p.ws_bytes;
   return TACTIC_OK;
@@ -382,9 +400,15 @@ static tactic_status sparse_decode_impl(const uint16_t* q, const uint16_t* K_sor
   aa.head_meta = so.head_meta;
   if (pk) aa.pk = *pk;
   aa.out = out;
-  int grid = 0;
-  e = tactic::attn_resident_grid((int)p.GV, BV, pk != nullptr, &grid);
-  if (e != hipSuccess) return hip_fail(e, "attention occupancy query");
+  int grid = 0, dev = -1;
+  e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev == p.attn_dev) {
+    grid = (int)p.attn_res[pk != nullptr ? 1 : 0];
+  } else {
+    e = tactic::attn_resident_grid((int)p.GV, BV, pk != nullptr, &grid);
+    if (e != hipSuccess) return hip_fail(e, "attention occupancy query");
+  }
   grid = (int)std::min<int64_t>(grid, p.attn_grid);  // the partials are sized for attn_grid
   e = tactic::launch_attn(aa, (int)p.GV, grid, pk != nullptr, stream);
   if (e == hipSuccess) e = record(5);
@@ -439,6 +463,8 @@ tactic_status tactic_sparse_decode_view(const tactic_decode_plan* plan_in, const
   view->rank_prefix = reinterpret_cast<const int32_t*>(ws + p.off_rprefix);
   view->fit = reinterpret_cast<const double*>(ws + p.off_fit);
   view->union_len = reinterpret_cast<const int32_t*>(ws + p.off_union_len);
+  view->sample_rows = reinterpret_cast<const int32_t*>(ws + p.off_rows);
+  view->sample_cap = p.S_cap;
   return TACTIC_OK;
 }
 
@@ -505,6 +531,14 @@ tactic_status tactic_dense_decode_paged(const uint16_t* q, const tactic_paged_kv
   if ((st = paged_args(kv, shape, &pk)) != TACTIC_OK) return st;
   pk.perm = nullptr;  // dense decode reads positions: no cluster order
   return dense_decode_impl(q, kv->K_pages, kv->V_pages, &pk, shape, out, workspace, workspace_bytes, stream);
+}
+
+tactic_status tactic_probe_stream_read(const void* buf, size_t bytes, uint32_t* sink, hipStream_t stream) {
+  if (!buf || !sink || bytes == 0 || bytes % 16 != 0)
+    return fail(TACTIC_ERR_INVALID_ARG, "stream read probe: null pointer or a size that is not a multiple of 16");
+  const hipError_t e = tactic::launch_stream_read(buf, bytes / 16, sink, stream);
+  if (e != hipSuccess) return hip_fail(e, "stream read launch");
+  return TACTIC_OK;
 }
 
 size_t tactic_build_clusters_workspace_size(const tactic_kv_shape* shape, int64_t total_clusters,

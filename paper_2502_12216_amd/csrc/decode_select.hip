@@ -54,20 +54,6 @@ __device__ T block_exclusive_scan(T* a, int count, T* s_wave) {
   return total;
 }
 
-__device__ float block_minmax(float v, bool want_max, float* s_wave) {
-  for (int o = kWave / 2; o > 0; o >>= 1) {
-    const float y = __shfl_xor(v, o, kWave);
-    v = want_max ? fmaxf(v, y) : fminf(v, y);
-  }
-  const int nw = blockDim.x / kWave;
-  if ((threadIdx.x & (kWave - 1)) == 0) s_wave[threadIdx.x / kWave] = v;
-  __syncthreads();
-  float r = s_wave[0];
-  for (int w = 1; w < nw; ++w) r = want_max ? fmaxf(r, s_wave[w]) : fminf(r, s_wave[w]);
-  __syncthreads();
-  return r;
-}
-
 // ============================================================================
 // 1. Centroid scoring: s[b][h][j] = q_h . c_{b,g,j}, fp32 accumulation of
 //    bf16 products (v_dot2).  grid (ceil(Cm/kScoreRows), B*Hkv), 256 threads;
@@ -382,43 +368,76 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     int nb = 1;
     while (nb < C) nb <<= 1;
     for (int i = tid; i < nb + 1; i += nt) cnt[i] = 0;
-    float lo = INFINITY, hi = -INFINITY;
+    // moments and range of the finite scores, as in the LDS path
+    float sm = 0.f, sq = 0.f, lo = INFINITY, hi = -INFINITY, nf = 0.f;
     for (int j = tid; j < C; j += nt) {
       const float sv = sc[j];
       if (sv == sv) {
+        sm += sv;
+        sq += sv * sv;
         lo = fminf(lo, sv);
         hi = fmaxf(hi, sv);
+        nf += 1.f;
       }
     }
-    lo = block_minmax(lo, false, s_wave_f);
-    hi = block_minmax(hi, true, s_wave_f);
-    const float range = hi - lo;
-    auto bucket_of = [&](float sv) -> int {
-      if (!(sv == sv)) return nb - 1;
-      if (!(range > 0.f)) return 0;
-      return (int)fminf((float)(nb - 1), fmaxf(0.f, floorf((hi - sv) / range * (float)nb)));
-    };
-    __syncthreads();
-    for (int j = tid; j < C; j += nt) atomicAdd(&cnt[bucket_of(sc[j])], 1u);
-    __syncthreads();
-    for (int i = tid; i < nb; i += nt) start[i] = cnt[i];
-    __syncthreads();
-    block_exclusive_scan<uint32_t>(start, nb, s_wave_u);
-    for (int j = tid; j < C; j += nt) {
-      const float sv = sc[j];
-      keys[atomicAdd(&start[bucket_of(sv)], 1u)] = ((uint64_t)desc_key_bits(sv) << 32) | (uint32_t)j;
+    sm = wave_allsum_f(sm);  // DPP, no LDS
+    sq = wave_allsum_f(sq);
+    nf = wave_allsum_f(nf);
+    lo = wave_allmin_f(lo);
+    hi = wave_allmax_f(hi);
+    if ((tid & (kWave - 1)) == 0) {
+      s_red[tid / kWave][0] = sm;
+      s_red[tid / kWave][1] = sq;
+      s_red[tid / kWave][2] = lo;
+      s_red[tid / kWave][3] = hi;
+      s_wave_f[tid / kWave] = nf;
     }
-    __syncthreads();
-    for (int j = tid; j < C; j += nt) {
-      const float sv = sc[j];
-      const uint64_t key = ((uint64_t)desc_key_bits(sv) << 32) | (uint32_t)j;
-      const int b2 = bucket_of(sv);
-      const uint32_t end = start[b2], beg = end - cnt[b2];
-      uint32_t r = 0;
-      for (uint32_t t = beg; t < end; ++t) r += keys[t] < key ? 1u : 0u;
-      const int p2 = (int)(beg + r);
-      order[p2] = j;
-      rank_of[j] = p2;
+    __syncthreads();  // also orders the count clears before the counting below
+    sm = 0.f, sq = 0.f, lo = INFINITY, hi = -INFINITY, nf = 0.f;
+    for (int w = 0; w < nt / kWave; ++w) {
+      sm += s_red[w][0];
+      sq += s_red[w][1];
+      lo = fminf(lo, s_red[w][2]);
+      hi = fmaxf(hi, s_red[w][3]);
+      nf += s_wave_f[w];
+    }
+    if (lo == hi && nf == (float)C) {
+      // all scores equal: the order is the cluster id
+      for (int j = tid; j < C; j += nt) {
+        order[j] = j;
+        rank_of[j] = j;
+      }
+    } else {
+      const float mu = nf > 0.f ? sm / nf : 0.f;
+      const float var = nf > 0.f ? fmaxf(sq / nf - mu * mu, 0.f) : 0.f;
+      const float sd = sqrtf(var);
+      const float inv_sd = sd > 0.f ? 1.f / sd : (hi > lo ? 1.f / (hi - lo) : 1.f);
+      for (int j = tid; j < C; j += nt) atomicAdd(&cnt[squash_bucket(sc[j], mu, inv_sd, nb)], 1u);
+      __syncthreads();
+      for (int i = tid; i < nb; i += nt) start[i] = cnt[i];
+      __syncthreads();
+      block_exclusive_scan<uint32_t>(start, nb, s_wave_u);
+      for (int j = tid; j < C; j += nt) {
+        const float sv = sc[j];
+        keys[atomicAdd(&start[squash_bucket(sv, mu, inv_sd, nb)], 1u)] =
+            ((uint64_t)desc_key_bits(sv) << 32) | (uint32_t)j;
+      }
+      __syncthreads();
+      for (int j = tid; j < C; j += nt) {
+        const float sv = sc[j];
+        const uint64_t key = ((uint64_t)desc_key_bits(sv) << 32) | (uint32_t)j;
+        const int b2 = squash_bucket(sv, mu, inv_sd, nb);
+        const uint32_t end = start[b2], beg = end - cnt[b2];
+        uint32_t r = 0, t = beg;
+        for (; t + 1 < end; t += 2) {  // two reads in flight per step
+          const uint64_t k0 = keys[t], k1 = keys[t + 1];
+          r += (k0 < key ? 1u : 0u) + (k1 < key ? 1u : 0u);
+        }
+        if (t < end) r += keys[t] < key ? 1u : 0u;
+        const int p2 = (int)(beg + r);
+        order[p2] = j;
+        rank_of[j] = p2;
+      }
     }
     __syncthreads();
     for (int j = tid; j < C; j += nt) {

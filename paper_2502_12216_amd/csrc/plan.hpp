@@ -44,7 +44,9 @@ struct DecodePlan {
   int64_t use_union;     // 1: GQA union (Sec. 4.5); 0: every query head over its own selection
   int64_t NV, GV;        // selection groups per sequence, query heads per selection group
   int64_t max_tail;      // capacity for recent (unclustered) tokens per sequence
-  int64_t pad[64 - 53];
+  int64_t attn_dev;      // device the resident attention grids below were measured on (-1: none)
+  int64_t attn_res[2];   // attention workgroups resident at once on it: contiguous, paged
+  int64_t pad[64 - 56];
 };
 static_assert(sizeof(DecodePlan) == 64 * sizeof(int64_t), "plan must fill tactic_decode_plan");
 

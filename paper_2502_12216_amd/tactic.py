@@ -155,12 +155,47 @@ class PagedCache:
                          int(self.max_pages), int(self.num_pages))
 
 
+def sparse_decode_workspace_bytes(batch: RaggedBatch, n_clusters: Sequence[int],
+                                  params: Optional[C.DecodeParams] = None) -> int:
+    """Workspace bytes tactic_sparse_decode needs for this shape (its plan call)."""
+    params = params if params is not None else decode_params()
+    ncl = [int(x) for x in n_clusters]
+    meta = C.ClusterMeta(int(sum(ncl)), max(ncl), None, None, None)
+    plan, nbytes = C.DecodePlan(), ctypes.c_size_t()
+    shape = batch.struct()
+    C.check(C.lib().tactic_sparse_decode_plan(ctypes.byref(shape), ctypes.byref(meta), ctypes.byref(params),
+                                              ctypes.byref(plan), ctypes.byref(nbytes)), "tactic_sparse_decode_plan")
+    return int(nbytes.value)
+
+
+def stream_read_gbps(buf: torch.Tensor, reps: int = 10, stream=None) -> float:
+    """Streaming-read rate (GB/s) of the device over `buf` (tactic_probe_stream_read),
+    median of `reps` timed reads; a measurement helper, not part of the method."""
+    if not buf.is_cuda or not buf.is_contiguous():
+        raise ValueError("buf must be a contiguous device tensor")
+    nbytes = buf.numel() * buf.element_size() // 16 * 16
+    sink = torch.zeros(1, dtype=torch.int32, device=buf.device)
+    s = stream if stream is not None else torch.cuda.current_stream()
+    times = []
+    for _ in range(reps + 1):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        C.check(C.lib().tactic_probe_stream_read(buf.data_ptr(), nbytes, sink.data_ptr(), int(s.cuda_stream)),
+                "tactic_probe_stream_read")
+        e1.record(s)
+        e1.synchronize()
+        times.append(e0.elapsed_time(e1))
+    return nbytes / (float(np.median(times[1:])) * 1e6)
+
+
 class SparseDecoder:
     """Tactic's decode for one batch shape: holds the launch plan and the
     workspace, so repeated calls (layers, decode steps) allocate nothing."""
 
     def __init__(self, batch: RaggedBatch, n_clusters: Sequence[int], params: Optional[C.DecodeParams] = None,
-                 device="cuda"):
+                 device="cuda", workspace: Optional[torch.Tensor] = None):
+        """workspace: a uint8 device tensor to use if it is large enough (for
+        instance a previous decoder's), else a new one is allocated."""
         self.batch = batch
         self.params = params if params is not None else decode_params()
         self.n_clusters = [int(x) for x in n_clusters]
@@ -171,7 +206,11 @@ class SparseDecoder:
         C.check(C.lib().tactic_sparse_decode_plan(ctypes.byref(self._shape), ctypes.byref(meta),
                                                   ctypes.byref(self.params), ctypes.byref(self.plan),
                                                   ctypes.byref(nbytes)), "tactic_sparse_decode_plan")
-        self.workspace = torch.empty(max(1, nbytes.value), dtype=torch.uint8, device=device)
+        need = max(1, nbytes.value)
+        if workspace is not None and workspace.dtype == torch.uint8 and workspace.is_cuda and workspace.numel() >= need:
+            self.workspace = workspace
+        else:
+            self.workspace = torch.empty(need, dtype=torch.uint8, device=device)
         B, Hq, Hkv = batch.batch, batch.n_q_heads, batch.n_kv_heads
         self.out = torch.empty(B, Hq, 128, dtype=torch.float32, device=device)
         self.sel_q = torch.empty(B, Hq, dtype=torch.int32, device=device)
@@ -244,6 +283,7 @@ class SparseDecoder:
             "rank_prefix": sl(v.rank_prefix, BH * (Cm + 1), torch.int32, (b.batch, b.n_q_heads, Cm + 1)),
             "fit": sl(v.fit, BH * C.FIT_FIELDS, torch.float64, (b.batch, b.n_q_heads, C.FIT_FIELDS)),
             "union_len": sl(v.union_len, nv * Ct, torch.int32, (nv, Ct)),
+            "sample_rows": sl(v.sample_rows, BH * v.sample_cap, torch.int32, (b.batch, b.n_q_heads, v.sample_cap)),
         }
 
 
@@ -295,26 +335,38 @@ class ClusterBuild:
 class ClusterBuilder:
     """Prefill K-means (tactic_build_clusters) for one batch shape."""
 
-    def __init__(self, batch: RaggedBatch, n_clusters: Sequence[int], max_iters: int = 10, device="cuda"):
+    def __init__(self, batch: RaggedBatch, n_clusters: Sequence[int], max_iters: int = 10, device="cuda",
+                 workspace_clusters: Optional[Sequence[int]] = None):
+        """workspace_clusters: the largest cluster counts later calls will use
+        (default n_clusters); the workspace is sized for them once."""
         self.batch = batch
+        self.device = device
+        self.params = C.KMeansParams(int(max_iters))
+        self._shape = batch.struct()
+        ws = [int(x) for x in (workspace_clusters if workspace_clusters is not None else n_clusters)]
+        n = C.lib().tactic_build_clusters_workspace_size(ctypes.byref(self._shape), int(sum(ws)), max(ws))
+        if n == 0:
+            raise C.TacticError("tactic_build_clusters_workspace_size rejected the shape")
+        self.workspace = torch.empty(n, dtype=torch.uint8, device=device)
+        self._set_clusters(n_clusters)
+
+    def _set_clusters(self, n_clusters: Sequence[int]) -> None:
         self.n_clusters = [int(x) for x in n_clusters]
         self.total_c = int(sum(self.n_clusters))
         self.max_c = max(self.n_clusters)
         self.cl_indptr_host = _indptr(self.n_clusters)
-        self.cl_indptr = torch.as_tensor(self.cl_indptr_host, device=device)
-        self.params = C.KMeansParams(int(max_iters))
-        self._shape = batch.struct()
-        n = C.lib().tactic_build_clusters_workspace_size(ctypes.byref(self._shape), self.total_c, self.max_c)
-        if n == 0:
-            raise C.TacticError("tactic_build_clusters_workspace_size rejected the shape")
-        self.workspace = torch.empty(n, dtype=torch.uint8, device=device)
-        self.device = device
+        self.cl_indptr = torch.as_tensor(self.cl_indptr_host, device=self.device)
 
     def __call__(self, K: torch.Tensor, V: Optional[torch.Tensor], init_idx: torch.Tensor, sort_kv: bool = True,
-                 stream=None, prev: Optional[ClusterSet] = None) -> ClusterBuild:
+                 stream=None, prev: Optional[ClusterSet] = None, n_clusters: Optional[Sequence[int]] = None,
+                 K_out: Optional[torch.Tensor] = None, V_out: Optional[torch.Tensor] = None) -> ClusterBuild:
         """prev: a previous clustering of the same sequences to start from (its
         centroid j of every (sequence, KV head) for j below both cluster counts;
-        see tactic_kmeans_params)."""
+        see tactic_kmeans_params).  n_clusters: this call's cluster counts (the
+        workspace must have room for them).  K_out, V_out: where the
+        cluster-sorted rows go (default: new tensors; never K or V)."""
+        if n_clusters is not None and [int(x) for x in n_clusters] != self.n_clusters:
+            self._set_clusters(n_clusters)
         b = self.batch
         Hkv = b.n_kv_heads
         _check_tensor(K, "K", torch.bfloat16, (Hkv, b.total, 128))
@@ -335,8 +387,16 @@ class ClusterBuilder:
         assign = torch.empty(Hkv, b.total, dtype=torch.int32, device=dev)
         offsets = torch.empty(Hkv, self.total_c + b.batch, dtype=torch.int32, device=dev)
         perm = torch.empty(Hkv, b.total, dtype=torch.int32, device=dev)
-        Ks = torch.empty_like(K) if sort_kv else None
-        Vs = torch.empty_like(V) if (sort_kv and V is not None) else None
+        Ks = Vs = None
+        if sort_kv:
+            Ks = torch.empty_like(K) if K_out is None else K_out
+            if V is not None:
+                Vs = torch.empty_like(V) if V_out is None else V_out
+            for name, out in (("K_out", Ks), ("V_out", Vs)):
+                if out is not None:
+                    _check_tensor(out, name, torch.bfloat16, (Hkv, b.total, 128))
+                    if out.data_ptr() in (K.data_ptr(), V.data_ptr() if V is not None else 0):
+                        raise ValueError(f"{name} must not be the input it is sorted from")
         C.check(C.lib().tactic_build_clusters(
             K.data_ptr(), V.data_ptr() if V is not None else None, ctypes.byref(self._shape),
             self.cl_indptr.data_ptr(), self.total_c, self.max_c, init_idx.data_ptr(), ctypes.byref(self.params),

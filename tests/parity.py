@@ -3,8 +3,10 @@
 Stages (each later stage is evaluated on the GPU's own result of the earlier
 ones, so a tie resolved differently upstream cannot fail a later stage):
   1. cluster scores q . c within fp32 accumulation error;
-  2. cluster order: a permutation, sorted by the oracle's scores up to the
-     tie tolerance (1e-5 * |q| * max |c|); identical when no near-tie exists;
+  2. cluster order: exactly the order of the GPU's own fp32 scores (score
+     descending, ties by ascending cluster id); against the oracle's fp64
+     scores it may differ only inside blocks of near-tied scores (within the
+     score tolerance 1e-5 * |q| * max |c|);
   3. budget k of every head, with the oracle run on the GPU's order: equal,
      or the oracle's cumulative sum at the GPU's k is within 1e-5 (relative)
      of the target on both sides of the cutoff;
@@ -78,9 +80,10 @@ def check_group(inp: dict, P: float, prm: OT.FitParams, gpu: dict, label: str = 
         err = float(np.max(np.abs(sg - s_or))) if C else 0.0
         assert err <= tol, f"{label} head {h}: score error {err} > {tol}"
         og = np.asarray(gpu["order"][h][:C], dtype=np.int64)
-        assert np.array_equal(np.sort(og), np.arange(C)), f"{label} head {h}: order is not a permutation"
-        s_in = s_or[og]
-        assert np.all(s_in[:-1] >= s_in[1:] - tol), f"{label} head {h}: order not sorted by score"
+        # the GPU sorts its own fp32 scores: that order is unique (ties by id)
+        own = np.lexsort((np.arange(C), -np.asarray(sg, dtype=np.float64)))
+        assert np.array_equal(og, own), \
+            f"{label} head {h}: order differs from the sort of the GPU's scores at {int(np.argmax(og != own))}"
         _, oo = OT.rank_clusters(Q[h], cent)
         if np.array_equal(oo, og):
             stats["order_equal"] += 1
@@ -120,7 +123,7 @@ def check_group(inp: dict, P: float, prm: OT.FitParams, gpu: dict, label: str = 
             err = max(err, float(np.max(np.abs(gpu["out"][h] - ref))))
         assert int(gpu["sel_kv"]) == loaded, f"{label}: loaded gpu {int(gpu['sel_kv'])} oracle {loaded}"
         assert err <= OUT_ATOL, f"{label}: output max-abs error {err} > {OUT_ATOL}"
-        stats.update(out_err=err, k=k_gpu.tolist(), union=loaded, n=n)
+        stats.update(out_err=err, k=k_gpu.tolist(), union=loaded, n=n, result=r)
         return stats
     U = np.unique(np.concatenate(sel_rows)) if G else np.zeros(0, np.int64)
     clus = np.searchsorted(off, U, side="right") - 1 if len(U) else np.zeros(0, np.int64)
@@ -138,4 +141,5 @@ def check_group(inp: dict, P: float, prm: OT.FitParams, gpu: dict, label: str = 
     stats["k"] = k_gpu.tolist()
     stats["union"] = len(U)
     stats["n"] = n
+    stats["result"] = r  # the oracle's decode on the GPU's order (GroupResult)
     return stats

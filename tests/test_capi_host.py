@@ -119,6 +119,21 @@ def test_decode_rejects_small_workspace_and_mismatched_plan():
     assert "null" in L.tactic_last_error().decode()
 
 
+def test_plan_rejects_more_selection_groups_than_the_attention_holds():
+    """The attention keeps one prefix entry per selection group in LDS (at most
+    4096 groups): per-head mode has B * Hq groups and is rejected at plan time,
+    before any kernel runs, where the union's B * Hkv groups still fit."""
+    B, Hq, Hkv = 200, 32, 8
+    shape = _shape(B=B, Hq=Hq, Hkv=Hkv, total=B * 64, nmax=64)
+    meta = C.ClusterMeta(B * 4, 4, FAKE, FAKE, FAKE)
+    st, _, _ = _plan(shape, meta, _params())
+    assert st == 0, C.lib().tactic_last_error()
+    ph = _params()
+    ph.use_union = 0
+    st, _, _ = _plan(shape, meta, ph)
+    assert st == 2 and b"selection groups" in C.lib().tactic_last_error()
+
+
 def test_dense_and_kmeans_validation():
     L = C.lib()
     shape = _shape()

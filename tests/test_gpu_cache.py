@@ -35,6 +35,9 @@ def test_recent_tail_cache_decode_loop_matches_oracle():
     P = 0.8
     prm = fit_params(T.decode_params(P))
     checked = 0
+    # buffers the re-clusterings reuse: two K/V buffers in turn, one builder and one decoder workspace
+    kv_bufs = {cache.K.data_ptr(), cache.K_alt.data_ptr()}
+    ws_ptrs = (cache.builder.workspace.data_ptr(), cache.decoder.workspace.data_ptr())
     for step in range(new + 1):
         if step in (0, 1, 30, 47, 48, 49, 96, new):
             out, sq, skv = cache.decode(q, target_frac=P)
@@ -65,6 +68,8 @@ def test_recent_tail_cache_decode_loop_matches_oracle():
         assert reclustered == ((step + 1) % 48 == 0)
         if reclustered:
             assert cache.recent == [0, 0]
+            assert {cache.K.data_ptr(), cache.K_alt.data_ptr()} == kv_bufs
+            assert (cache.builder.workspace.data_ptr(), cache.decoder.workspace.data_ptr()) == ws_ptrs
     assert cache.reclusterings == 1 + new // 48
     # every token is still held once, in the cluster-sorted rows or the recent tail
     for b in range(len(lens)):

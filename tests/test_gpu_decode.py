@@ -342,13 +342,18 @@ def test_paged_cache_matches_cluster_sorted_copy(page_size):
     sorted_pages = T.PagedCache.from_token_order(Ks, Vs, batch, page_size)
     cl = T.ClusterSet(lay.centroids.to(DEV), lay.offsets.to(DEV), ncl)
     for P in (0.5, 0.95):
-        dec = T.SparseDecoder(batch, ncl, T.decode_params(P, max_tail=256))
+        params = T.decode_params(P, max_tail=256)
+        dec = T.SparseDecoder(batch, ncl, params)
         ref = [x.clone() for x in dec(q, Ks, Vs, cl)]
-        for pages in (token_pages, sorted_pages):
+        for name, pages in (("token order + perm", token_pages), ("cluster order", sorted_pages)):
             got = dec.paged(q, pages, cl)
             torch.cuda.synchronize()
             for a, b in zip(ref, got):
                 assert torch.equal(a, b)
+            # and the paged call's own selection and output against the oracle
+            res = dict(out=got[0].clone().cpu(), sel_q=got[1].clone().cpu(), sel_kv=got[2].clone().cpu(),
+                       view={k: v.clone().cpu() for k, v in dec.view().items()}, params=params)
+            check_layer(inp, lay, P, res, label=f"paged ps={page_size} {name} P={P}")
     den = T.DenseDecoder(batch)
     d_ref = den(q, K, V).clone()
     d_pg = den.paged(q, token_pages)
@@ -406,3 +411,97 @@ def test_sparse_degenerate_scores(P):
         C0 = int(lay.cl_indptr[1] - lay.cl_indptr[0])
         assert torch.equal(order[0, g * G, :C0], torch.arange(C0, dtype=order.dtype))
     print(f"degenerate P={P}: ties(order)={sum(s['order_ties'] for s in st)} k={[s['k'] for s in st][:2]}")
+
+
+def test_sparse_empty_clusters_parity():
+    """Empty clusters (Sec. 4.2 keeps a centroid that lost its members): the
+    tokens of every odd mixture component are filed under the even one below
+    it, so half the clusters hold no token but keep their centroid and are
+    ranked like the others (the query's own centres among them)."""
+    wl = _small("ctx32k_llama8b", [3000, 1700, 260])
+    inp = synth.make_layer(wl, 0)
+    inp.labels = (inp.labels // 2) * 2
+    lay = synth.label_layout(inp, tail=[0, 45, 0])
+    off = lay.offsets.long()
+    empty = int(((off[:, 1:] - off[:, :-1]) == 0).sum())
+    assert empty >= lay.centroids.shape[1] // 2 - 1
+    T = _tactic()
+    for P in (0.5, 0.9, 1.0):
+        res = run_sparse(inp, lay, P, T.decode_params(P, max_tail=64))
+        check_layer(inp, lay, P, res, label=f"empty clusters P={P}")
+
+
+def test_sparse_target_one_at_128k_matches_dense_and_paged():
+    """P = 1 selects every token (Eq. 2 from Eq. 3): at the timed shape
+    (4 x 131072 tokens, one layer) the sparse decode must agree with the
+    dense decode and with the fp64 oracle on sampled heads.  Every
+    attention workgroup then streams ~5.5K tokens of one group, several
+    2048-row sub-ranges starting inside a 256-position chunk, so the
+    sub-range walk and the paged row lookups past position 256 are
+    exercised; paged and contiguous caches give the same bits."""
+    T = _tactic()
+    wl = synth.WORKLOADS["ctx128k_b4_32layer"]
+    inp = synth.make_layer(wl, 0, device=DEV)
+    lay = synth.label_layout(inp)
+    ncl = list(wl.cluster_counts)
+    batch = T.RaggedBatch(wl.seq_lens, wl.n_q_heads, wl.n_kv_heads)
+    cl = T.ClusterSet(lay.centroids.contiguous(), lay.offsets.contiguous(), ncl)
+    dec = T.SparseDecoder(batch, ncl, T.decode_params(1.0))
+    out, sq, skv = (x.clone() for x in dec(inp.q, lay.K_sorted, lay.V_sorted, cl))
+    den = T.DenseDecoder(batch)
+    d_sorted = den(inp.q, lay.K_sorted, lay.V_sorted).clone()
+    d_tok = den(inp.q, inp.K, inp.V).clone()
+    torch.cuda.synchronize()
+    n = wl.seq_lens[0]
+    assert torch.all(sq == n) and torch.all(skv == n)
+    assert float((out - d_sorted).abs().max()) <= 1e-4
+    assert float((out - d_tok).abs().max()) <= 1e-4
+    # paged: 16-token pages at random page ids, cluster order through perm
+    npg = sum((x + 15) // 16 for x in wl.seq_lens)
+    pages = T.PagedCache.from_token_order(inp.K, inp.V, batch, 16,
+                                          page_order=torch.randperm(npg, generator=torch.Generator().manual_seed(3)),
+                                          perm=lay.perm.contiguous())
+    got = [x.clone() for x in dec.paged(inp.q, pages, cl)]
+    d_pg = den.paged(inp.q, pages).clone()
+    torch.cuda.synchronize()
+    assert torch.equal(got[0], out) and torch.equal(got[1], sq) and torch.equal(got[2], skv)
+    assert torch.equal(d_pg, d_tok)
+    # the fp64 oracle on a seeded sample of heads
+    G = wl.n_q_heads // wl.n_kv_heads
+    rng = np.random.default_rng(17)
+    err = 0.0
+    for b, h in zip(rng.integers(0, 4, 6), rng.integers(0, wl.n_q_heads, 6)):
+        g = int(h) // G
+        s0 = int(batch.kv_indptr_host[b])
+        ref = OA.dense_attention(np64(inp.q[b, h]), np64(inp.K[g, s0:s0 + n]), np64(inp.V[g, s0:s0 + n]))
+        err = max(err, float(np.max(np.abs(np64(out[b, h]) - ref))))
+    assert err <= 2e-3, err
+    print(f"128k P=1: sparse-dense {float((out - d_tok).abs().max()):.2e}, oracle max-abs {err:.2e}")
+
+
+@pytest.mark.parametrize("P", [0.5, 0.9])
+def test_sparse_degenerate_scores_out_of_lds_sort(P):
+    """The sort of more than 8192 clusters per head runs out of the
+    workspace: a zero query (all scores equal: identity order), centroids
+    repeated every 8 clusters (eight scores shared by an eighth of the
+    clusters each: crowded buckets, ties by cluster id) and ordinary heads,
+    with 9000 clusters of about two tokens each (many empty)."""
+    import dataclasses
+    base = _small("ctx32k_llama8b", [20000, 12000])
+    wl = dataclasses.replace(base, fixed_clusters=9000, name=base.name + "_c9000")
+    inp = synth.make_layer(wl, 0)
+    lay = synth.label_layout(inp)
+    G = wl.n_q_heads // wl.n_kv_heads
+    q = inp.q.clone()
+    q[0, ::G] = 0
+    inp.q = q
+    cent = lay.centroids.clone()
+    c0, c1 = int(lay.cl_indptr[1]), int(lay.cl_indptr[2])
+    cent[:, c0:c1] = cent[:, c0 + (torch.arange(c1 - c0) % 8)]
+    lay.centroids = cent
+    res = run_sparse(inp, lay, P)
+    st = check_layer(inp, lay, P, res, label=f"degenerate C=9000 P={P}")
+    order = res["view"]["order"]
+    for g in range(wl.n_kv_heads):
+        assert torch.equal(order[0, g * G, :9000], torch.arange(9000, dtype=order.dtype))
+    print(f"degenerate C=9000 P={P}: k={[s['k'] for s in st][:2]}")

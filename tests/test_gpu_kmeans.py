@@ -159,6 +159,45 @@ def test_decode_on_kmeans_clusters_invariants():
         assert torch.isfinite(out).all()
 
 
+def test_decode_on_kmeans_clusters_128k_sampled_parity():
+    """The timed shape as the benchmark runs it: one 4 x 131072-token layer
+    clustered by tactic_build_clusters (10 iterations, 8192 clusters per
+    sequence and KV head, some of them emptied by the iterations), then the
+    sparse decode at P = 0.9, staged parity on sampled groups (those with the
+    most empty clusters first).  The oracle reads the library's cluster
+    layout as its input, as a decode loop would hand it over."""
+    from tests.test_gpu_decode import check_layer
+    T = _tactic()
+    wl = synth.WORKLOADS["ctx128k_b4_32layer"]
+    inp = synth.make_layer(wl, 3, device=DEV)
+    res, lens, ncl, _ = _build(inp, wl, wl.kmeans_iters)
+    batch = T.RaggedBatch(lens, wl.n_q_heads, wl.n_kv_heads)
+    P = 0.9
+    params = T.decode_params(P)
+    dec = T.SparseDecoder(batch, ncl, params)
+    out, sq, skv = dec(inp.q, res.K_sorted, res.V_sorted, res.clusters)
+    torch.cuda.synchronize()
+    run = dict(out=out.clone().cpu(), sel_q=sq.clone().cpu(), sel_kv=skv.clone().cpu(),
+               view={k: v.clone().cpu() for k, v in dec.view().items()}, params=params)
+    kv_ip = np.concatenate([[0], np.cumsum(lens)])
+    cl_ip = np.concatenate([[0], np.cumsum(ncl)])
+    lay = synth.LabelLayout(K_sorted=res.K_sorted, V_sorted=res.V_sorted, centroids=res.clusters.centroids,
+                            offsets=res.clusters.offsets, perm=res.perm, kv_indptr=kv_ip, cl_indptr=cl_ip)
+    off = res.clusters.offsets.long().cpu()
+    empties = {}
+    for b in range(len(lens)):
+        o = off[:, cl_ip[b] + b:cl_ip[b + 1] + b + 1]
+        for g in range(wl.n_kv_heads):
+            empties[(b, g)] = int(((o[g, 1:] - o[g, :-1]) == 0).sum())
+    ranked = sorted(empties, key=lambda bg: -empties[bg])
+    rng = np.random.default_rng(23)
+    rest = [ranked[i] for i in rng.choice(np.arange(2, len(ranked)), 3, replace=False)]
+    groups = ranked[:2] + rest
+    st = check_layer(inp, lay, P, run, groups=groups, label="kmeans 128k")
+    print("kmeans 128k sampled:", [(bg, empties[bg], s["k"], s["union"]) for bg, s in zip(groups, st)],
+          "empty clusters in the layer:", sum(empties.values()))
+
+
 def test_kmeans_spare_room_layout_matches_packed():
     """K-means over sequences with spare rows (seq_len < span) touches only
     the sequences' tokens: same clusters and cluster-sorted rows as packed."""
