@@ -27,7 +27,8 @@
  *    undefined behaviour).
  *  - The library allocates no memory and keeps no global state: the caller
  *    owns every buffer, including the workspace.  Calls that share a
- *    workspace must be ordered on one stream.
+ *    workspace must be ordered on one stream.  The one exception is the
+ *    static scratch of tactic_sparse_decode_noalloc (see there).
  */
 #ifndef TACTIC_H_
 #define TACTIC_H_
@@ -160,6 +161,27 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted,
                                    int32_t* sel_count_q, int32_t* sel_count_kv,
                                    void* workspace, size_t workspace_bytes,
                                    hipStream_t stream);
+
+/* The same decode for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * it takes no workspace and calls no allocating routine.  Its workspace is a
+ * static scratch array of TACTIC_NOALLOC_SCRATCH_BYTES in the library's device
+ * code, one copy per GPU, held from the library's load on that GPU until the
+ * process ends (its device address is looked up once per device, at the first
+ * call there).  A plan whose workspace exceeds it gives TACTIC_ERR_WORKSPACE
+ * before any launch.  Every call on a GPU uses that GPU's one array, which
+ * keeps the last call's contents: calls that overlap on one GPU (other
+ * streams, other threads) race and must be ordered by the caller.  The
+ * decode needs no zeroed workspace.  Arguments, outputs and errors are those
+ * of tactic_sparse_decode. */
+#define TACTIC_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+tactic_status tactic_sparse_decode_noalloc(const uint16_t* q, const uint16_t* K_sorted,
+                                           const uint16_t* V_sorted, const tactic_kv_shape* shape,
+                                           const tactic_cluster_meta* meta,
+                                           const tactic_decode_params* params,
+                                           const tactic_decode_plan* plan, float* out,
+                                           int32_t* sel_count_q, int32_t* sel_count_kv,
+                                           hipStream_t stream);
 
 /* Optional per-stage timing: with events set (an array of 7 created events,
  * or NULL to clear), every tactic_sparse_decode with this plan records

@@ -11,6 +11,7 @@ from ctypes import POINTER, c_char_p, c_double, c_float, c_int, c_int32, c_int64
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtactic.so")
 
 TACTIC_OK = 0
+NOALLOC_SCRATCH_BYTES = 64 << 20  # TACTIC_NOALLOC_SCRATCH_BYTES
 FIT_FIELDS = 16
 FIT_NAMES = ("m", "mu1", "mu2", "a", "b", "S_n", "T", "k", "N", "n", "exact", "samples", "E_N",
              "cut_rank", "cut_len", "unused")
@@ -20,7 +21,7 @@ EXPORTS = (
     "tactic_decode_params_default", "tactic_sparse_decode_plan", "tactic_sparse_decode",
     "tactic_sparse_decode_plan_set_events",
     "tactic_sparse_decode_view", "tactic_dense_decode_workspace_size", "tactic_dense_decode",
-    "tactic_sparse_decode_paged", "tactic_dense_decode_paged",
+    "tactic_sparse_decode_paged", "tactic_dense_decode_paged", "tactic_sparse_decode_noalloc",
     "tactic_probe_stream_read",
     "tactic_build_clusters_workspace_size", "tactic_build_clusters", "tactic_status_string",
     "tactic_last_error",
@@ -92,6 +93,10 @@ def lib() -> ctypes.CDLL:
                                              POINTER(DecodeParams), POINTER(DecodePlan), c_void_p, c_void_p,
                                              c_void_p, c_void_p, c_size_t, c_void_p]
     L.tactic_sparse_decode_paged.restype = c_int
+    L.tactic_sparse_decode_noalloc.argtypes = [c_void_p, c_void_p, c_void_p, POINTER(KVShape), POINTER(ClusterMeta),
+                                               POINTER(DecodeParams), POINTER(DecodePlan), c_void_p, c_void_p,
+                                               c_void_p, c_void_p]
+    L.tactic_sparse_decode_noalloc.restype = c_int
     L.tactic_sparse_decode_plan_set_events.argtypes = [POINTER(DecodePlan), c_void_p]
     L.tactic_sparse_decode_plan_set_events.restype = c_int
     L.tactic_sparse_decode_view.argtypes = [POINTER(DecodePlan), c_void_p, POINTER(DecodeView)]
@@ -128,4 +133,5 @@ def check(status: int, what: str) -> None:
 
 
 __all__ = ["KVShape", "ClusterMeta", "DecodeParams", "DecodePlan", "DecodeView", "KMeansParams", "PagedKV",
-           "TacticError", "lib", "check", "EXPORTS", "LIB_PATH", "FIT_FIELDS", "FIT_NAMES", "c_double"]
+           "TacticError", "lib", "check", "EXPORTS", "LIB_PATH", "FIT_FIELDS", "FIT_NAMES", "NOALLOC_SCRATCH_BYTES",
+           "c_double"]

@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 
 #include "../../include/tactic.h"
@@ -426,6 +427,59 @@ tactic_status tactic_sparse_decode(const uint16_t* q, const uint16_t* K_sorted, 
                                    size_t workspace_bytes, hipStream_t stream) {
   return sparse_decode_impl(q, K_sorted, V_sorted, nullptr, shape, meta, params, plan_in, out, sel_count_q,
                             sel_count_kv, workspace, workspace_bytes, stream);
+}
+
+}  // extern "C"
+
+// Scratch of the no-alloc decode: one array per device, from the code object's
+// own data (allocated when the library is loaded on that device, held until the
+// process ends).  Host code never uses the array's name as an address: the
+// device address of each device's copy comes from hipGetSymbolAddress.
+namespace {
+constexpr size_t kScratchBytes = TACTIC_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxScratchDevices];  // device address of `scratch` per device, or null
+
+tactic_status scratch_on_current_device(void** addr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(TACTIC_ERR_UNSUPPORTED, "device %d: the scratch table holds %d devices", dev, kMaxScratchDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(TACTIC_ERR_HIP, "hipGetSymbolAddress(scratch) returned a null address");
+    g_scratch_addr[dev] = p;
+  }
+  *addr = g_scratch_addr[dev];
+  return TACTIC_OK;
+}
+}  // namespace
+
+extern "C" {
+
+tactic_status tactic_sparse_decode_noalloc(const uint16_t* q, const uint16_t* K_sorted, const uint16_t* V_sorted,
+                                           const tactic_kv_shape* shape, const tactic_cluster_meta* meta,
+                                           const tactic_decode_params* params, const tactic_decode_plan* plan_in,
+                                           float* out, int32_t* sel_count_q, int32_t* sel_count_kv,
+                                           hipStream_t stream) {
+  if (!plan_in) return fail(TACTIC_ERR_INVALID_ARG, "null plan");
+  const tactic::DecodePlan& p = *as_plan(plan_in);
+  if (p.magic != tactic::kPlanMagic) return fail(TACTIC_ERR_INVALID_ARG, "not a decode plan");
+  if (p.ws_bytes > (int64_t)kScratchBytes)
+    return fail(TACTIC_ERR_WORKSPACE, "the shape needs %lld bytes of workspace; the static scratch of "
+                "tactic_sparse_decode_noalloc holds %zu", (long long)p.ws_bytes, kScratchBytes);
+  void* ws = nullptr;
+  const tactic_status st = scratch_on_current_device(&ws);
+  if (st != TACTIC_OK) return st;
+  // the decode needs no zeroed workspace: every kernel writes what it reads later
+  return sparse_decode_impl(q, K_sorted, V_sorted, nullptr, shape, meta, params, plan_in, out, sel_count_q,
+                            sel_count_kv, ws, kScratchBytes, stream);
 }
 
 tactic_status tactic_sparse_decode_paged(const uint16_t* q, const tactic_paged_kv* kv,

@@ -237,6 +237,29 @@ class SparseDecoder:
             _stream(stream)), "tactic_sparse_decode")
         return out, sel_q, sel_kv
 
+    def noalloc(self, q: torch.Tensor, K_sorted: torch.Tensor, V_sorted: torch.Tensor, clusters: ClusterSet,
+                target_frac: Optional[float] = None, stream=None, out=None, sel_q=None, sel_kv=None):
+        """The same decode through tactic_sparse_decode_noalloc: the library's
+        static scratch instead of this decoder's workspace (calls on one GPU
+        must not overlap)."""
+        b = self.batch
+        _check_tensor(q, "q", torch.bfloat16, (b.batch, b.n_q_heads, 128))
+        _check_tensor(K_sorted, "K_sorted", torch.bfloat16, (b.n_kv_heads, b.total, 128))
+        _check_tensor(V_sorted, "V_sorted", torch.bfloat16, (b.n_kv_heads, b.total, 128))
+        if clusters.n_clusters != self.n_clusters:
+            raise ValueError("cluster counts differ from the ones the decoder was planned for")
+        out = self.out if out is None else out
+        sel_q = self.sel_q if sel_q is None else sel_q
+        sel_kv = self.sel_kv if sel_kv is None else sel_kv
+        if target_frac is not None:
+            self.params.target_frac = float(target_frac)
+        meta = clusters.struct()
+        C.check(C.lib().tactic_sparse_decode_noalloc(
+            q.data_ptr(), K_sorted.data_ptr(), V_sorted.data_ptr(), ctypes.byref(self._shape),
+            ctypes.byref(meta), ctypes.byref(self.params), ctypes.byref(self.plan), out.data_ptr(),
+            sel_q.data_ptr(), sel_kv.data_ptr(), _stream(stream)), "tactic_sparse_decode_noalloc")
+        return out, sel_q, sel_kv
+
     def paged(self, q: torch.Tensor, cache: PagedCache, clusters: ClusterSet, target_frac: Optional[float] = None,
               stream=None, out=None, sel_q=None, sel_kv=None):
         """The same decode over a paged cache (tactic_sparse_decode_paged)."""

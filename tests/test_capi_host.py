@@ -134,6 +134,28 @@ def test_plan_rejects_more_selection_groups_than_the_attention_holds():
     assert st == 2 and b"selection groups" in C.lib().tactic_last_error()
 
 
+def test_noalloc_decode_rejects_a_plan_beyond_its_scratch():
+    """tactic_sparse_decode_noalloc checks the plan's workspace against its
+    static scratch before any device work: 16 x 131072 tokens need ~100 MiB."""
+    L = C.lib()
+    B, n = 16, 131072
+    shape = _shape(B=B, Hq=32, Hkv=8, total=B * n, nmax=n)
+    meta = C.ClusterMeta(B * 8192, 8192, FAKE, FAKE, FAKE)
+    params = _params()
+    st, plan, nbytes = _plan(shape, meta, params)
+    assert st == 0 and nbytes > C.NOALLOC_SCRATCH_BYTES
+    st = L.tactic_sparse_decode_noalloc(FAKE, FAKE, FAKE, ctypes.byref(shape), ctypes.byref(meta),
+                                        ctypes.byref(params), ctypes.byref(plan), FAKE, FAKE, FAKE, None)
+    assert st == 3 and b"static scratch" in L.tactic_last_error()
+    st = L.tactic_sparse_decode_noalloc(FAKE, FAKE, FAKE, ctypes.byref(shape), ctypes.byref(meta),
+                                        ctypes.byref(params), None, FAKE, FAKE, FAKE, None)
+    assert st == 1
+    # the timed shape (4 x 131072 tokens, 8192 clusters) fits
+    shape = _shape(B=4, Hq=32, Hkv=8, total=4 * n, nmax=n)
+    st, _, nbytes = _plan(shape, C.ClusterMeta(4 * 8192, 8192, FAKE, FAKE, FAKE), params)
+    assert st == 0 and nbytes <= C.NOALLOC_SCRATCH_BYTES
+
+
 def test_dense_and_kmeans_validation():
     L = C.lib()
     shape = _shape()
