@@ -65,10 +65,8 @@ def profiled_traffic(stage: str):
         shas = summ.get("_source_sha256", {})
         if any(shas.get(n) != h for n, h in src.items()):
             continue
-        key = {"attn_splitk": "attn_splitk", "score_clusters": "score_clusters", "sort_clusters": "sort_clusters",
-               "sample_logits": "sample_logits", "fit_union": "fit_union", "combine": "combine"}[stage]
         for k, v in summ.items():
-            if k.startswith(key) and "[dense]" not in k:
+            if k.startswith(stage) and "[dense]" not in k:
                 return v.get("traffic_bytes")
     return None
 
@@ -200,7 +198,10 @@ def dense_sdpa(q, K, V, wl, reps: int, own_out=None) -> dict:
         return {"us_per_layer": None, "error": f"{type(e).__name__}: {str(e)[:160]}"}
 
 
+# the decode's kernels in launch order (one library event after each)
 STAGE_NAMES = ["score_clusters", "sort_clusters", "sample_logits", "fit_union", "attn_splitk", "combine"]
+STAGE_KERNEL = {n: n for n in STAGE_NAMES}
+SEL, ATT, COMB = STAGE_NAMES.index("sample_logits"), STAGE_NAMES.index("attn_splitk"), STAGE_NAMES.index("combine")
 
 
 def config_record(T, wl, Ps, dev, flush, reps: int, stage_ev, ceiling, host_groups=None):
@@ -271,7 +272,7 @@ def config_record(T, wl, Ps, dev, flush, reps: int, stage_ev, ceiling, host_grou
                "hbm_frac_read_ceiling": round(gbps / ceiling, 4) if ceiling else None,
                "byte_bound_speedup": round(dense_bytes / tb["total"], 3),
                "stages_us": {n: round(float(t), 2) for n, t in zip(STAGE_NAMES, stage_us)},
-               "attn_gbps": round(tb["union_kv"] / (float(stage_us[4]) * 1e3), 1),
+               "attn_gbps": round(tb["union_kv"] / (float(stage_us[ATT]) * 1e3), 1),
                "selected_frac": {"head_mean": round(float(kq.mean()), 5),
                                  "head_median": round(float(np.median(kq)), 5),
                                  "head_max": round(float(kq.max()), 5), "union_mean": round(float(ku.mean()), 5),
@@ -459,7 +460,7 @@ def main():
     log(f"torch SDPA dense layer: {sdpa}")
 
     # ---------------------------------------------------------------- per-stage timing (HIP events)
-    NS = 6
+    NS = len(STAGE_NAMES)
     import ctypes
     from paper_2502_12216_amd import _capi as C
     stage_ev = TimingEvents(NS + 1)
@@ -508,9 +509,10 @@ def main():
             rows_ph += int(skv_ph.sum())
             rows_un += int(skv_un.sum())
         ablation = {"per_head_us_per_layer": round(ms_ph * 1000 / layers, 2),
-                    "per_head_attn_us": round(float(st_ph[4] + st_ph[5]) * 1000, 2),
-                    "union_attn_us": round(float(stage_ms[4] + stage_ms[5]) * 1000, 2),
-                    "attn_speedup_from_union": round(float((st_ph[4] + st_ph[5]) / (stage_ms[4] + stage_ms[5])), 3),
+                    "per_head_attn_us": round(float(st_ph[ATT] + st_ph[COMB]) * 1000, 2),
+                    "union_attn_us": round(float(stage_ms[ATT] + stage_ms[COMB]) * 1000, 2),
+                    "attn_speedup_from_union": round(float((st_ph[ATT] + st_ph[COMB]) /
+                                                           (stage_ms[ATT] + stage_ms[COMB])), 3),
                     "kv_rows_per_head_over_union": round(rows_ph / max(1, rows_un), 3)}
         del dec_ph
         log(f"per-head step {ms_ph:.3f} ms")
@@ -550,11 +552,12 @@ def main():
                  "cluster order through perm",
                  "sparse_us_per_layer": round(ms_p * 1000 / keep, 2),
                  "sparse_us_per_layer_cluster_sorted": round(ms_c * 1000 / keep, 2),
-                 "attn_us": round(float(st_p[4]) * 1000, 2), "attn_us_cluster_sorted": round(float(st_c[4]) * 1000, 2),
-                 "sample_us": round(float(st_p[2]) * 1000, 2),
-                 "sample_us_cluster_sorted": round(float(st_c[2]) * 1000, 2),
-                 "attn_gbps": round(ub / (float(st_p[4]) * 1e6), 1),
-                 "attn_gbps_cluster_sorted": round(ub / (float(st_c[4]) * 1e6), 1)}
+                 "attn_us": round(float(st_p[ATT]) * 1000, 2),
+                 "attn_us_cluster_sorted": round(float(st_c[ATT]) * 1000, 2),
+                 "sample_us": round(float(st_p[SEL]) * 1000, 2),
+                 "sample_us_cluster_sorted": round(float(st_c[SEL]) * 1000, 2),
+                 "attn_gbps": round(ub / (float(st_p[ATT]) * 1e6), 1),
+                 "attn_gbps_cluster_sorted": round(ub / (float(st_c[ATT]) * 1e6), 1)}
         del pcs
         log(f"paged step ({keep} layers) {ms_p:.3f} ms vs {ms_c:.3f} ms cluster-sorted")
 
@@ -674,8 +677,10 @@ def main():
     gbps = float(bytes_layer.mean()) / (us_sparse * 1e3)
     stage_us = stage_ms * 1000
     # each kernel's own algorithmic bytes: the sampler reads every sampled row
-    stage_bytes = [bytes_centroids, 0.0, float(np.mean([t["sampled_all"] for t in tb])), 0.0,
-                   float(bytes_union.mean()), 0.0]
+    stage_bytes = [0.0] * len(STAGE_NAMES)
+    stage_bytes[0] = bytes_centroids
+    stage_bytes[SEL] = float(np.mean([t["sampled_all"] for t in tb]))
+    stage_bytes[ATT] = float(bytes_union.mean())
     dom = int(np.argmax(stage_us))
     dom_bytes = stage_bytes[dom]
     roof = {
@@ -689,17 +694,19 @@ def main():
     }
     if stage_bytes[dom] == 0.0:
         roof["bound"] = "alu"
-    roof["traffic"] = profiled_traffic(stage_names[dom])
+    roof["traffic"] = profiled_traffic(STAGE_KERNEL[stage_names[dom]])
     kq = sel_q.astype(np.float64) / lens[None, :, None]
     ku = sel_kv.astype(np.float64) / lens[None, :, None]
 
     # ---------------------------------------------------------------- streaming-read ceiling
     ceiling = None
     if not args.no_ceiling:
-        buf = torch.empty(4 << 30, dtype=torch.uint8, device=dev)
-        ceiling = T.stream_read_gbps(buf, reps=10)
+        buf = torch.zeros(4 << 30, dtype=torch.uint8, device=dev)
+        probe = T.stream_read_gbps(buf, reps=10)
+        ceiling = probe["best_gbps"]
         del buf
-        log(f"streaming-read ceiling {ceiling:.0f} GB/s")
+        log(f"streaming-read ceiling {ceiling:.0f} GB/s (by workgroups: "
+            f"{ {k: round(v) for k, v in probe['gbps_by_workgroups'].items()} })")
 
     # ---------------------------------------------------------------- the other workloads, one layer each
     configs, hosts = None, {}
@@ -803,7 +810,10 @@ def main():
                           "union_max": round(float(ku.max()), 5)},
         "roofline": roof,
         "hbm_read_ceiling_gbps": round(ceiling, 1) if ceiling else None,
-        "attn_frac_of_read_ceiling": (round(stage_bytes[4] / (stage_us[4] * 1e3) / ceiling, 4) if ceiling else None),
+        "hbm_read_ceiling_note": ("best median of 10 reads of a 4 GiB buffer by tactic_probe_stream_read over "
+                                  "launch shapes " + str({k: round(v, 1) for k, v in probe["gbps_by_workgroups"].items()})
+                                  if ceiling else None),
+        "attn_frac_of_read_ceiling": (round(stage_bytes[ATT] / (stage_us[ATT] * 1e3) / ceiling, 4) if ceiling else None),
         "cpu_baseline": cpu,
         "configs": configs,
         "union_ablation": ablation,

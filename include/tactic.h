@@ -312,12 +312,14 @@ tactic_status tactic_build_clusters(const uint16_t* K, const uint16_t* V,
                                     void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Measurement helper, not part of the method: reads every 16-byte word of
- * `buf` (bytes, a multiple of 16) once with streaming loads from a grid of
- * resident workgroups and stores nothing unless a read value equals a magic
- * word (then one word to *sink, a device uint32).  Its rate is the device's
+ * `buf` (bytes, a multiple of 16) once with streaming loads from `workgroups`
+ * workgroups of 256 threads (0: as many as fit on the device at once) and
+ * stores nothing unless a read value equals a magic word (then one word to
+ * *sink, a device uint32).  Its best rate over launch shapes is the device's
  * practical streaming-read ceiling, the yardstick of the bandwidth-bound
  * decode kernels.  Errors: TACTIC_ERR_INVALID_ARG, TACTIC_ERR_HIP. */
-tactic_status tactic_probe_stream_read(const void* buf, size_t bytes, uint32_t* sink, hipStream_t stream);
+tactic_status tactic_probe_stream_read(const void* buf, size_t bytes, int32_t workgroups, uint32_t* sink,
+                                       hipStream_t stream);
 
 /* Static description of a status code. */
 const char* tactic_status_string(tactic_status s);

@@ -115,7 +115,7 @@ def lib() -> ctypes.CDLL:
                                         c_void_p, POINTER(KMeansParams), c_void_p, c_void_p, c_void_p,
                                         c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
     L.tactic_build_clusters.restype = c_int
-    L.tactic_probe_stream_read.argtypes = [c_void_p, c_size_t, c_void_p, c_void_p]
+    L.tactic_probe_stream_read.argtypes = [c_void_p, c_size_t, c_int32, c_void_p, c_void_p]
     L.tactic_probe_stream_read.restype = c_int
     L.tactic_status_string.argtypes = [c_int]
     L.tactic_status_string.restype = c_char_p

@@ -587,10 +587,12 @@ tactic_status tactic_dense_decode_paged(const uint16_t* q, const tactic_paged_kv
   return dense_decode_impl(q, kv->K_pages, kv->V_pages, &pk, shape, out, workspace, workspace_bytes, stream);
 }
 
-tactic_status tactic_probe_stream_read(const void* buf, size_t bytes, uint32_t* sink, hipStream_t stream) {
-  if (!buf || !sink || bytes == 0 || bytes % 16 != 0)
-    return fail(TACTIC_ERR_INVALID_ARG, "stream read probe: null pointer or a size that is not a multiple of 16");
-  const hipError_t e = tactic::launch_stream_read(buf, bytes / 16, sink, stream);
+tactic_status tactic_probe_stream_read(const void* buf, size_t bytes, int32_t workgroups, uint32_t* sink,
+                                       hipStream_t stream) {
+  if (!buf || !sink || bytes == 0 || bytes % 16 != 0 || workgroups < 0)
+    return fail(TACTIC_ERR_INVALID_ARG, "stream read probe: null pointer, a size that is not a multiple of 16 "
+                "or a negative workgroup count");
+  const hipError_t e = tactic::launch_stream_read(buf, bytes / 16, workgroups, sink, stream);
   if (e != hipSuccess) return hip_fail(e, "stream read launch");
   return TACTIC_OK;
 }

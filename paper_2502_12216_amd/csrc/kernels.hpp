@@ -150,6 +150,6 @@ hipError_t launch_fit_union(const FitArgs& a, int G, int n_groups, hipStream_t s
 hipError_t launch_attn(const AttnArgs& a, int G, int grid, bool paged, hipStream_t st);
 hipError_t launch_combine(const AttnArgs& a, int G, hipStream_t st);
 hipError_t attn_resident_grid(int G, int n_groups, bool paged, int* grid);
-hipError_t launch_stream_read(const void* buf, int64_t n16, uint32_t* sink, hipStream_t st);
+hipError_t launch_stream_read(const void* buf, int64_t n16, int workgroups, uint32_t* sink, hipStream_t st);
 
 }  // namespace tactic

@@ -168,24 +168,29 @@ def sparse_decode_workspace_bytes(batch: RaggedBatch, n_clusters: Sequence[int],
     return int(nbytes.value)
 
 
-def stream_read_gbps(buf: torch.Tensor, reps: int = 10, stream=None) -> float:
-    """Streaming-read rate (GB/s) of the device over `buf` (tactic_probe_stream_read),
-    median of `reps` timed reads; a measurement helper, not part of the method."""
+def stream_read_gbps(buf: torch.Tensor, reps: int = 10, workgroups=(0, 2048, 4096, 8192, 16384),
+                     stream=None) -> dict:
+    """Streaming-read rate (GB/s) of the device over `buf` (tactic_probe_stream_read):
+    the median of `reps` timed reads for each launch shape, and the best of them.
+    A measurement helper, not part of the method."""
     if not buf.is_cuda or not buf.is_contiguous():
         raise ValueError("buf must be a contiguous device tensor")
     nbytes = buf.numel() * buf.element_size() // 16 * 16
     sink = torch.zeros(1, dtype=torch.int32, device=buf.device)
     s = stream if stream is not None else torch.cuda.current_stream()
-    times = []
-    for _ in range(reps + 1):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(s)
-        C.check(C.lib().tactic_probe_stream_read(buf.data_ptr(), nbytes, sink.data_ptr(), int(s.cuda_stream)),
-                "tactic_probe_stream_read")
-        e1.record(s)
-        e1.synchronize()
-        times.append(e0.elapsed_time(e1))
-    return nbytes / (float(np.median(times[1:])) * 1e6)
+    rates = {}
+    for wg in workgroups:
+        times = []
+        for _ in range(reps + 1):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            C.check(C.lib().tactic_probe_stream_read(buf.data_ptr(), nbytes, int(wg), sink.data_ptr(),
+                                                     int(s.cuda_stream)), "tactic_probe_stream_read")
+            e1.record(s)
+            e1.synchronize()
+            times.append(e0.elapsed_time(e1))
+        rates[int(wg)] = nbytes / (float(np.median(times[1:])) * 1e6)
+    return {"best_gbps": max(rates.values()), "gbps_by_workgroups": rates, "bytes": nbytes}
 
 
 class SparseDecoder:
