@@ -361,23 +361,37 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
     for (int r = tid; r <= C; r += nt) rpre[r] = (int32_t)(r < C ? cnt[r] : total);
   } else {
+    // C > 8192: the bucket counts (8192 buckets) in LDS, the keys and the
+    // per-rank sizes / starts in the workspace.  Every loop over the elements
+    // takes 8 (4 in the ranking) per thread per step with their global loads
+    // issued together, so a step costs one memory round trip.
+    uint32_t* cnt_l = reinterpret_cast<uint32_t*>(smem_raw);
+    uint32_t* start_l = cnt_l + kSortLdsBuckets;
+    constexpr int nb = kSortLdsBuckets;
+    constexpr int kB = 8;
     uint64_t* keys = a.g_keys + (int64_t)bh * a.nb_max;
-    cnt = a.g_cnt + (int64_t)bh * (a.nb_max + 4);
-    uint32_t* start = a.g_start + (int64_t)bh * (a.nb_max + 4);
-    ostart = reinterpret_cast<int32_t*>(keys);
-    int nb = 1;
-    while (nb < C) nb <<= 1;
-    for (int i = tid; i < nb + 1; i += nt) cnt[i] = 0;
+    cnt = a.g_cnt + (int64_t)bh * (a.nb_max + 4);                                    // per rank: size, then prefix
+    ostart = reinterpret_cast<int32_t*>(a.g_start + (int64_t)bh * (a.nb_max + 4));  // per rank: first row
+    {
+      uint4* c4 = reinterpret_cast<uint4*>(cnt_l) + tid * 2;
+      c4[0] = make_uint4(0, 0, 0, 0);
+      c4[1] = make_uint4(0, 0, 0, 0);
+    }
     // moments and range of the finite scores, as in the LDS path
     float sm = 0.f, sq = 0.f, lo = INFINITY, hi = -INFINITY, nf = 0.f;
-    for (int j = tid; j < C; j += nt) {
-      const float sv = sc[j];
-      if (sv == sv) {
-        sm += sv;
-        sq += sv * sv;
-        lo = fminf(lo, sv);
-        hi = fmaxf(hi, sv);
-        nf += 1.f;
+    for (int j0 = tid; j0 < C; j0 += kB * nt) {
+      float v[kB];
+#pragma unroll
+      for (int e = 0; e < kB; ++e) v[e] = sc[min(j0 + e * nt, C - 1)];
+#pragma unroll
+      for (int e = 0; e < kB; ++e) {
+        if (j0 + e * nt < C && v[e] == v[e]) {
+          sm += v[e];
+          sq += v[e] * v[e];
+          lo = fminf(lo, v[e]);
+          hi = fmaxf(hi, v[e]);
+          nf += 1.f;
+        }
       }
     }
     sm = wave_allsum_f(sm);  // DPP, no LDS
@@ -401,54 +415,134 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
       hi = fmaxf(hi, s_red[w][3]);
       nf += s_wave_f[w];
     }
-    if (lo == hi && nf == (float)C) {
-      // all scores equal: the order is the cluster id
-      for (int j = tid; j < C; j += nt) {
-        order[j] = j;
-        rank_of[j] = j;
-      }
-    } else {
-      const float mu = nf > 0.f ? sm / nf : 0.f;
-      const float var = nf > 0.f ? fmaxf(sq / nf - mu * mu, 0.f) : 0.f;
-      const float sd = sqrtf(var);
-      const float inv_sd = sd > 0.f ? 1.f / sd : (hi > lo ? 1.f / (hi - lo) : 1.f);
-      for (int j = tid; j < C; j += nt) atomicAdd(&cnt[squash_bucket(sc[j], mu, inv_sd, nb)], 1u);
-      __syncthreads();
-      for (int i = tid; i < nb; i += nt) start[i] = cnt[i];
-      __syncthreads();
-      block_exclusive_scan<uint32_t>(start, nb, s_wave_u);
-      for (int j = tid; j < C; j += nt) {
-        const float sv = sc[j];
-        keys[atomicAdd(&start[squash_bucket(sv, mu, inv_sd, nb)], 1u)] =
-            ((uint64_t)desc_key_bits(sv) << 32) | (uint32_t)j;
+    const bool all_equal = lo == hi && nf == (float)C;  // then the order is the cluster id
+    const float mu = nf > 0.f ? sm / nf : 0.f;
+    const float var = nf > 0.f ? fmaxf(sq / nf - mu * mu, 0.f) : 0.f;
+    const float sd = sqrtf(var);
+    const float inv_sd = sd > 0.f ? 1.f / sd : (hi > lo ? 1.f / (hi - lo) : 1.f);
+    if (!all_equal) {
+      for (int j0 = tid; j0 < C; j0 += kB * nt) {
+        float v[kB];
+#pragma unroll
+        for (int e = 0; e < kB; ++e) v[e] = sc[min(j0 + e * nt, C - 1)];
+#pragma unroll
+        for (int e = 0; e < kB; ++e)
+          if (j0 + e * nt < C) atomicAdd(&cnt_l[squash_bucket(v[e], mu, inv_sd, nb)], 1u);
       }
       __syncthreads();
-      for (int j = tid; j < C; j += nt) {
-        const float sv = sc[j];
-        const uint64_t key = ((uint64_t)desc_key_bits(sv) << 32) | (uint32_t)j;
-        const int b2 = squash_bucket(sv, mu, inv_sd, nb);
-        const uint32_t end = start[b2], beg = end - cnt[b2];
-        uint32_t r = 0, t = beg;
-        for (; t + 1 < end; t += 2) {  // two reads in flight per step
-          const uint64_t k0 = keys[t], k1 = keys[t + 1];
-          r += (k0 < key ? 1u : 0u) + (k1 < key ? 1u : 0u);
+      {
+        const uint4* c4 = reinterpret_cast<const uint4*>(cnt_l) + tid * 2;
+        uint4* s4 = reinterpret_cast<uint4*>(start_l) + tid * 2;
+        s4[0] = c4[0];
+        s4[1] = c4[1];
+      }
+      scan8k_lds(start_l, s_wave_u);  // (each thread copied the entries it scans)
+      for (int j0 = tid; j0 < C; j0 += kB * nt) {
+        float v[kB];
+#pragma unroll
+        for (int e = 0; e < kB; ++e) v[e] = sc[min(j0 + e * nt, C - 1)];
+#pragma unroll
+        for (int e = 0; e < kB; ++e) {
+          const int j = j0 + e * nt;
+          if (j < C)
+            keys[atomicAdd(&start_l[squash_bucket(v[e], mu, inv_sd, nb)], 1u)] =
+                ((uint64_t)desc_key_bits(v[e]) << 32) | (uint32_t)j;
         }
-        if (t < end) r += keys[t] < key ? 1u : 0u;
-        const int p2 = (int)(beg + r);
-        order[p2] = j;
-        rank_of[j] = p2;
+      }
+      __syncthreads();  // the keys are visible to the workgroup; start_l holds the bucket ends
+    }
+    // rank of every element: its bucket start plus the smaller keys in its
+    // bucket.  Four elements per step: the first four keys of each one's
+    // bucket load together with the elements' cluster offsets; longer buckets
+    // are walked after.  Then its size and first row go to its rank.
+    {
+      constexpr int kE = 4, kK = 4;
+      for (int j0 = tid; j0 < C; j0 += kE * nt) {
+        uint64_t key[kE];
+        uint32_t beg[kE], end[kE], r[kE];
+        int o_lo[kE], o_hi[kE];
+#pragma unroll
+        for (int e = 0; e < kE; ++e) {
+          const int jc = min(j0 + e * nt, C - 1);
+          const float sv = sc[jc];
+          key[e] = ((uint64_t)desc_key_bits(sv) << 32) | (uint32_t)jc;
+          o_lo[e] = off[jc];
+          o_hi[e] = off[jc + 1];
+          const int bk = all_equal ? 0 : squash_bucket(sv, mu, inv_sd, nb);
+          end[e] = all_equal ? 1u : start_l[bk];
+          beg[e] = all_equal ? 0u : end[e] - cnt_l[bk];
+          r[e] = 0;
+        }
+        if (!all_equal) {
+          uint64_t kk[kE][kK];
+#pragma unroll
+          for (int e = 0; e < kE; ++e)
+#pragma unroll
+            for (int i = 0; i < kK; ++i) kk[e][i] = keys[min(beg[e] + i, end[e] - 1)];  // the element is in it
+#pragma unroll
+          for (int e = 0; e < kE; ++e) {
+#pragma unroll
+            for (int i = 0; i < kK; ++i) r[e] += (beg[e] + i < end[e] && kk[e][i] < key[e]) ? 1u : 0u;
+            for (uint32_t t = beg[e] + kK; t < end[e]; ++t) r[e] += keys[t] < key[e] ? 1u : 0u;
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < kE; ++e) {
+          const int j = j0 + e * nt;
+          if (j < C) {
+            const int p2 = all_equal ? j : (int)(beg[e] + r[e]);
+            order[p2] = j;
+            rank_of[j] = p2;
+            cnt[p2] = (uint32_t)(o_hi[e] - o_lo[e]);
+            ostart[p2] = o_lo[e];
+          }
+        }
       }
     }
-    __syncthreads();
-    for (int j = tid; j < C; j += nt) {
-      const int p2 = rank_of[j];
-      cnt[p2] = (uint32_t)(off[j + 1] - off[j]);
-      ostart[p2] = off[j];
+    __syncthreads();  // sizes and starts by rank are visible
+    // exclusive prefix of the sizes in rank order: 32 consecutive ranks per
+    // thread per pass, loaded together
+    {
+      constexpr int kS = 32;
+      uint32_t carry = 0;
+      for (int base = 0; base < C; base += kS * nt) {
+        const int r0 = base + tid * kS;
+        uint32_t v[kS];
+#pragma unroll
+        for (int e = 0; e < kS; ++e) v[e] = r0 + e < C ? cnt[r0 + e] : 0u;
+        uint32_t local = 0;
+#pragma unroll
+        for (int e = 0; e < kS; ++e) local += v[e];
+        const uint32_t incl = wave_incl_scan(local);  // DPP, no LDS
+        if ((tid & (kWave - 1)) == kWave - 1) s_wave_u[tid / kWave] = incl;
+        __syncthreads();
+        uint32_t run = carry + incl - local, tot = 0;
+        for (int w = 0; w < nt / kWave; ++w) {
+          const uint32_t t = s_wave_u[w];
+          if (w < tid / kWave) run += t;
+          tot += t;
+        }
+#pragma unroll
+        for (int e = 0; e < kS; ++e) {
+          if (r0 + e < C) cnt[r0 + e] = run;
+          run += v[e];
+        }
+        carry += tot;
+        __syncthreads();  // s_wave_u is reused; the prefix is visible
+      }
+      total = carry;
     }
-    __syncthreads();
-    total = block_exclusive_scan<uint32_t>(cnt, C, s_wave_u);
     int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
-    for (int r = tid; r <= C; r += nt) rpre[r] = (int32_t)(r < C ? cnt[r] : total);
+    for (int r0 = tid; r0 <= C; r0 += kB * nt) {
+      uint32_t v[kB];
+#pragma unroll
+      for (int e = 0; e < kB; ++e) v[e] = cnt[min(r0 + e * nt, C - 1)];
+#pragma unroll
+      for (int e = 0; e < kB; ++e) {
+        const int r = r0 + e * nt;
+        if (r <= C) rpre[r] = (int32_t)(r < C ? v[e] : total);
+      }
+    }
   }
 
   // the clusters hold the first n_c rows; the rest are recent tokens, sampled
@@ -481,6 +575,67 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
   const int64_t N = geo.exact ? n_c : geo.N;
   const int64_t W1 = geo.exact ? 0 : geo.t1 - geo.s1 + 1;
   auto prefix_at = [&](int r) -> uint32_t { return r < C ? cnt[r] : total; };  // r in [0, C]
+  if constexpr (!kLds) {
+    // workspace path: every kStr-th prefix entry in LDS (the bucket arrays are
+    // dead), a binary search there, then the last kStr entries from memory
+    uint32_t* s_pre = reinterpret_cast<uint32_t*>(smem_raw);
+    const int kStr = (C + 2 * kSortLdsBuckets - 1) / (2 * kSortLdsBuckets);  // 16384 LDS entries at most
+    const int nsp = (C + kStr - 1) / kStr;
+    for (int i0 = tid; i0 < nsp; i0 += 8 * nt) {
+      uint32_t v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = cnt[min((i0 + e * nt) * kStr, C - 1)];
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (i0 + e * nt < nsp) s_pre[i0 + e * nt] = v[e];
+    }
+    __syncthreads();
+    int top = 1;
+    while (top * 2 <= nsp) top <<= 1;
+    constexpr int kU = 4;  // independent searches in flight per thread
+    for (int64_t u0 = tid; u0 < S_main; u0 += (int64_t)kU * nt) {
+      int64_t iv[kU];
+      int li[kU];
+#pragma unroll
+      for (int k = 0; k < kU; ++k) {
+        const int64_t u = u0 + (int64_t)k * nt;
+        iv[k] = u < N ? u + 1 : (u < N + W1 ? geo.s1 + (u - N) : geo.s2 + (u - N - W1));
+        li[k] = 0;
+      }
+      // largest i with s_pre[i] < position (s_pre[0] = prefix[0] = 0)
+      for (int step = top; step > 0; step >>= 1) {
+#pragma unroll
+        for (int k = 0; k < kU; ++k) {
+          const int t = li[k] + step;
+          li[k] = (t < nsp && (int64_t)s_pre[t] < iv[k]) ? t : li[k];
+        }
+      }
+      // then the largest r in [li * kStr, li * kStr + kStr) with prefix[r] < position
+      int lr[kU];
+#pragma unroll
+      for (int k = 0; k < kU; ++k) lr[k] = li[k] * kStr;
+      for (int d = 1; d < kStr; ++d) {
+        uint32_t pv[kU];
+#pragma unroll
+        for (int k = 0; k < kU; ++k) pv[k] = cnt[min(li[k] * kStr + d, C - 1)];
+#pragma unroll
+        for (int k = 0; k < kU; ++k) {
+          const int t = li[k] * kStr + d;
+          lr[k] = (t < C && (int64_t)pv[k] < iv[k]) ? t : lr[k];
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < kU; ++k) {
+        const int64_t u = u0 + (int64_t)k * nt;
+        if (u < S_main) {
+          const int r = min(lr[k], C - 1);
+          const int32_t row = ostart[r] + (int32_t)(iv[k] - 1 - (int64_t)prefix_at(r));
+          rows[u] = min(max(row, 0), n - 1);
+        }
+      }
+    }
+    return;
+  }
   int top = 1;
   while (top * 2 <= C) top <<= 1;
   constexpr int kU = 4;  // independent searches in flight per thread
@@ -1149,7 +1304,8 @@ hipError_t launch_sort(const SortArgs& a, bool lds, int n_heads, hipStream_t st)
     const size_t bytes = (size_t)kSortLdsBuckets * 16;  // keys u64, cnt u32, start u32
     hipLaunchKernelGGL(sort_clusters_kernel<true>, dim3(n_heads), dim3(1024), bytes, st, a);
   } else {
-    hipLaunchKernelGGL(sort_clusters_kernel<false>, dim3(n_heads), dim3(1024), 0, st, a);
+    const size_t bytes = (size_t)kSortLdsBuckets * 8;  // bucket cnt u32, start u32; then the sampled prefix
+    hipLaunchKernelGGL(sort_clusters_kernel<false>, dim3(n_heads), dim3(1024), bytes, st, a);
   }
   return hipGetLastError();
 }
