@@ -151,16 +151,24 @@ __device__ __forceinline__ int squash_bucket(float s, float mu, float inv_sd, in
   return min(max(bk, 0), nb - 1);
 }
 
-// Exclusive scan in place of a[0..8192) in LDS by 1024 threads, 8 consecutive
-// entries each (two 16-byte LDS accesses); returns the total.  Ends with a barrier.
-__device__ uint32_t scan8k_lds(uint32_t* a, uint32_t* s_wave) {
+// Exclusive scan in place of a[0..1024 kPer) in LDS by 1024 threads, kPer
+// consecutive entries each (16-byte LDS accesses when kPer is 8); returns the
+// total.  Ends with a barrier.
+template <int kPer>
+__device__ uint32_t scan_lds(uint32_t* a, uint32_t* s_wave) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-  uint4* a4 = reinterpret_cast<uint4*>(a) + tid * 2;
-  const uint4 x = a4[0], y = a4[1];
-  const uint32_t v[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
+  uint32_t v[kPer];
+  if constexpr (kPer == 8) {
+    const uint4* a4 = reinterpret_cast<const uint4*>(a) + tid * 2;
+    const uint4 x = a4[0], y = a4[1];
+    v[0] = x.x, v[1] = x.y, v[2] = x.z, v[3] = x.w, v[4] = y.x, v[5] = y.y, v[6] = y.z, v[7] = y.w;
+  } else {
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) v[e] = a[tid * kPer + e];
+  }
   uint32_t local = 0;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) local += v[e];
+  for (int e = 0; e < kPer; ++e) local += v[e];
   uint32_t incl = wave_incl_scan(local);  // DPP, no LDS
   if (lane == kWave - 1) s_wave[wave] = incl;
   __syncthreads();
@@ -172,18 +180,47 @@ __device__ uint32_t scan8k_lds(uint32_t* a, uint32_t* s_wave) {
   }
   __syncthreads();
   uint32_t run = s_wave[wave] + incl - local;
-  uint32_t o[8];
+  uint32_t o[kPer];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
+  for (int e = 0; e < kPer; ++e) {
     o[e] = run;
     run += v[e];
   }
-  a4[0] = make_uint4(o[0], o[1], o[2], o[3]);
-  a4[1] = make_uint4(o[4], o[5], o[6], o[7]);
+  if constexpr (kPer == 8) {
+    uint4* a4 = reinterpret_cast<uint4*>(a) + tid * 2;
+    a4[0] = make_uint4(o[0], o[1], o[2], o[3]);
+    a4[1] = make_uint4(o[4], o[5], o[6], o[7]);
+  } else {
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) a[tid * kPer + e] = o[e];
+  }
   const uint32_t total = s_wave[16];
   __syncthreads();
   return total;
 }
+__device__ __forceinline__ uint32_t scan8k_lds(uint32_t* a, uint32_t* s_wave) { return scan_lds<8>(a, s_wave); }
+
+// Inverse of desc_key_bits: the score (with -0 read as +0; NaN bits kept).
+__device__ __forceinline__ float key_score(uint32_t k) {
+  const uint32_t ord = ~k;
+  return __uint_as_float((ord & 0x80000000u) ? (ord & 0x7fffffffu) : ~ord);
+}
+
+// Workspace sort of 8192 < C <= kPieceMaxC clusters: the scores and sizes of
+// a thread's 32 clusters stay in registers; the bucket counts (kPieceBuckets)
+// sit in LDS, and the buckets are taken in pieces of consecutive buckets
+// holding at most kPieceCap clusters, whose keys are staged in LDS: every
+// access of the rank computation is an LDS access, and the global accesses
+// are coalesced.  A piece's ranks are consecutive, so its order, rank-prefix
+// and size entries leave in order.
+constexpr int kPieceBuckets = 4096;
+constexpr int kPiecePer = 6;                    // entries per thread in the piece scan
+constexpr int kPieceCap = kPiecePer * 1024;     // clusters per piece
+constexpr int kPieceMaxC = 32 * 1024;           // 32 clusters per thread
+constexpr size_t kPieceLdsBytes = (size_t)kPieceBuckets * 8 + (size_t)kPieceCap * 20;
+// dynamic LDS of the workspace sort: the pieces, or 8192 bucket counts and
+// starts on the general path; then the rank prefix for the sample search
+constexpr size_t kSortWsLdsBytes = kPieceLdsBytes > (size_t)kSortLdsBuckets * 8 ? kPieceLdsBytes : (size_t)kSortLdsBuckets * 8;
 
 template <bool kLds>
 __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
@@ -361,31 +398,46 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
     for (int r = tid; r <= C; r += nt) rpre[r] = (int32_t)(r < C ? cnt[r] : total);
   } else {
-    // C > 8192: the bucket counts (8192 buckets) in LDS, the keys and the
-    // per-rank sizes / starts in the workspace.  Every loop over the elements
-    // takes 8 (4 in the ranking) per thread per step with their global loads
-    // issued together, so a step costs one memory round trip.
-    uint32_t* cnt_l = reinterpret_cast<uint32_t*>(smem_raw);
-    uint32_t* start_l = cnt_l + kSortLdsBuckets;
-    constexpr int nb = kSortLdsBuckets;
-    constexpr int kB = 8;
-    uint64_t* keys = a.g_keys + (int64_t)bh * a.nb_max;
-    cnt = a.g_cnt + (int64_t)bh * (a.nb_max + 4);                                    // per rank: size, then prefix
-    ostart = reinterpret_cast<int32_t*>(a.g_start + (int64_t)bh * (a.nb_max + 4));  // per rank: first row
-    {
-      uint4* c4 = reinterpret_cast<uint4*>(cnt_l) + tid * 2;
-      c4[0] = make_uint4(0, 0, 0, 0);
-      c4[1] = make_uint4(0, 0, 0, 0);
-    }
-    // moments and range of the finite scores, as in the LDS path
-    float sm = 0.f, sq = 0.f, lo = INFINITY, hi = -INFINITY, nf = 0.f;
-    for (int j0 = tid; j0 < C; j0 += kB * nt) {
-      float v[kB];
+    cnt = a.g_cnt + (int64_t)bh * (a.nb_max + 4);  // per rank: size, then prefix
+    ostart = nullptr;                              // the sample rows start from off[order[r]]
+    bool pieces_done = false;
+    if (C <= kPieceMaxC) {  // uniform
+      constexpr int nbk = kPieceBuckets, kE = kPieceMaxC / 1024;
+      uint32_t* cnt_l = reinterpret_cast<uint32_t*>(smem_raw);  // bucket sizes
+      uint32_t* cur_l = cnt_l + nbk;                            // bucket starts, then scatter cursors
+      uint64_t* s_keys = reinterpret_cast<uint64_t*>(cur_l + nbk);  // the piece's keys by bucket position
+      uint32_t* s_aux = reinterpret_cast<uint32_t*>(s_keys + kPieceCap);  // size by position, then rank
+      int32_t* s_ord = reinterpret_cast<int32_t*>(s_aux + kPieceCap);     // cluster by rank in the piece
+      uint32_t* s_sz = reinterpret_cast<uint32_t*>(s_ord + kPieceCap);    // size, then prefix, by rank
+      float v[kE];          // the score; the bucket position while its piece is ranked; then the rank
+      uint32_t sz2[kE / 2];  // cluster sizes, two 16-bit halves (larger sizes take the general path)
+      uint32_t size_or = 0;  // OR of the sizes: any bit above 15 sends the head to the general path
 #pragma unroll
-      for (int e = 0; e < kB; ++e) v[e] = sc[min(j0 + e * nt, C - 1)];
+      for (int e = 0; e < kE; ++e) v[e] = sc[min(tid + e * 1024, C - 1)];
 #pragma unroll
-      for (int e = 0; e < kB; ++e) {
-        if (j0 + e * nt < C && v[e] == v[e]) {
+      for (int e0 = 0; e0 < kE; e0 += 8) {  // sizes: 16 loads in flight per batch
+        int o0[8], o1[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int jc = min(tid + (e0 + e) * 1024, C - 1);
+          o0[e] = off[jc];
+          o1[e] = off[jc + 1];
+        }
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+          const uint32_t x = (uint32_t)(o1[e] - o0[e]), y = (uint32_t)(o1[e + 1] - o0[e + 1]);
+          size_or |= x | y;
+          uint32_t packed = x | (y << 16);
+          // packed (and OR-ed) now, so that the loaded offsets die here
+          asm volatile("" : "+v"(packed), "+v"(size_or));
+          sz2[(e0 + e) / 2] = packed;
+        }
+      }
+      reinterpret_cast<uint4*>(cnt_l)[tid] = make_uint4(0, 0, 0, 0);
+      float sm = 0.f, sq = 0.f, lo = INFINITY, hi = -INFINITY, nf = 0.f;
+#pragma unroll
+      for (int e = 0; e < kE; ++e) {
+        if (tid + e * 1024 < C && v[e] == v[e]) {
           sm += v[e];
           sq += v[e] * v[e];
           lo = fminf(lo, v[e]);
@@ -393,154 +445,302 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
           nf += 1.f;
         }
       }
-    }
-    sm = wave_allsum_f(sm);  // DPP, no LDS
-    sq = wave_allsum_f(sq);
-    nf = wave_allsum_f(nf);
-    lo = wave_allmin_f(lo);
-    hi = wave_allmax_f(hi);
-    if ((tid & (kWave - 1)) == 0) {
-      s_red[tid / kWave][0] = sm;
-      s_red[tid / kWave][1] = sq;
-      s_red[tid / kWave][2] = lo;
-      s_red[tid / kWave][3] = hi;
-      s_wave_f[tid / kWave] = nf;
-    }
-    __syncthreads();  // also orders the count clears before the counting below
-    sm = 0.f, sq = 0.f, lo = INFINITY, hi = -INFINITY, nf = 0.f;
-    for (int w = 0; w < nt / kWave; ++w) {
-      sm += s_red[w][0];
-      sq += s_red[w][1];
-      lo = fminf(lo, s_red[w][2]);
-      hi = fmaxf(hi, s_red[w][3]);
-      nf += s_wave_f[w];
-    }
-    const bool all_equal = lo == hi && nf == (float)C;  // then the order is the cluster id
-    const float mu = nf > 0.f ? sm / nf : 0.f;
-    const float var = nf > 0.f ? fmaxf(sq / nf - mu * mu, 0.f) : 0.f;
-    const float sd = sqrtf(var);
-    const float inv_sd = sd > 0.f ? 1.f / sd : (hi > lo ? 1.f / (hi - lo) : 1.f);
-    if (!all_equal) {
-      for (int j0 = tid; j0 < C; j0 += kB * nt) {
-        float v[kB];
-#pragma unroll
-        for (int e = 0; e < kB; ++e) v[e] = sc[min(j0 + e * nt, C - 1)];
-#pragma unroll
-        for (int e = 0; e < kB; ++e)
-          if (j0 + e * nt < C) atomicAdd(&cnt_l[squash_bucket(v[e], mu, inv_sd, nb)], 1u);
+      sm = wave_allsum_f(sm);  // DPP, no LDS
+      sq = wave_allsum_f(sq);
+      nf = wave_allsum_f(nf);
+      lo = wave_allmin_f(lo);
+      hi = wave_allmax_f(hi);
+      if ((tid & (kWave - 1)) == 0) {
+        s_red[tid / kWave][0] = sm;
+        s_red[tid / kWave][1] = sq;
+        s_red[tid / kWave][2] = lo;
+        s_red[tid / kWave][3] = hi;
+        s_wave_f[tid / kWave] = nf;
       }
-      __syncthreads();
+      __syncthreads();  // also orders the count clears before the counting below
+      sm = 0.f, sq = 0.f, lo = INFINITY, hi = -INFINITY, nf = 0.f;
+      for (int w = 0; w < 1024 / kWave; ++w) {
+        sm += s_red[w][0];
+        sq += s_red[w][1];
+        lo = fminf(lo, s_red[w][2]);
+        hi = fmaxf(hi, s_red[w][3]);
+        nf += s_wave_f[w];
+      }
+      const bool all_equal = lo == hi && nf == (float)C;  // the general path orders them by id
+      const float mu = nf > 0.f ? sm / nf : 0.f;
+      const float var = nf > 0.f ? fmaxf(sq / nf - mu * mu, 0.f) : 0.f;
+      const float sd = sqrtf(var);
+      const float inv_sd = sd > 0.f ? 1.f / sd : (hi > lo ? 1.f / (hi - lo) : 1.f);
+      if (!all_equal) {
+#pragma unroll
+        for (int e = 0; e < kE; ++e)
+          if (tid + e * 1024 < C) atomicAdd(&cnt_l[squash_bucket(v[e], mu, inv_sd, nbk)], 1u);
+        __syncthreads();
+        // the largest bucket must fit a piece
+        const uint4 c4 = reinterpret_cast<const uint4*>(cnt_l)[tid];
+        reinterpret_cast<uint4*>(cur_l)[tid] = c4;
+        float mb = (float)max(max(c4.x, c4.y), max(c4.z, c4.w));  // counts <= 2^15: exact
+        mb = wave_allmax_f(size_or > 0xffffu ? INFINITY : mb);
+        if ((tid & (kWave - 1)) == 0) s_wave_f[tid / kWave] = mb;
+        scan_lds<nbk / 1024>(cur_l, s_wave_u);  // bucket starts; its barriers publish s_wave_f
+        float maxb = 0.f;
+        for (int w = 0; w < 1024 / kWave; ++w) maxb = fmaxf(maxb, s_wave_f[w]);
+        pieces_done = maxb <= (float)kPieceCap;
+      }
+      if (pieces_done) {
+        int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
+        __shared__ int s_b1;
+        uint32_t carry = 0, ranked = 0;  // bit e: cluster e has its rank in v[e]
+        for (int b0 = 0; b0 < nbk;) {
+          // the piece: buckets [b0, b1), the last b1 whose start is within
+          // kPieceCap of the piece's start (buckets from b0 on still hold
+          // their start; the bucket b0 alone fits)
+          const uint32_t p0 = cur_l[b0];
+          if (tid == 0) {
+            int lo_b = b0 + 1, hi_b = nbk;
+            while (lo_b < hi_b) {
+              const int mid = (lo_b + hi_b + 1) >> 1;
+              const uint32_t st = mid < nbk ? cur_l[mid] : (uint32_t)C;
+              if (st - p0 <= (uint32_t)kPieceCap) lo_b = mid;
+              else hi_b = mid - 1;
+            }
+            s_b1 = lo_b;
+          }
+          __syncthreads();  // also: the previous piece's LDS reads are done
+          const int b1 = s_b1;
+          const uint32_t p1 = b1 < nbk ? cur_l[b1] : (uint32_t)C;
+#pragma unroll
+          for (int e = 0; e < kPiecePer; ++e) s_sz[tid * kPiecePer + e] = 0u;
+          // the owners place the piece's keys and sizes at their bucket positions
+          uint32_t mine = 0;
+#pragma unroll
+          for (int e = 0; e < kE; ++e) {
+            const int j = tid + e * 1024;
+            if (j < C && !((ranked >> e) & 1u)) {
+              const int bk = squash_bucket(v[e], mu, inv_sd, nbk);
+              if (bk >= b0 && bk < b1) {
+                const uint32_t pos = atomicAdd(&cur_l[bk], 1u) - p0;
+                s_keys[pos] = ((uint64_t)desc_key_bits(v[e]) << 32) | (uint32_t)j;
+                s_aux[pos] = (sz2[e / 2] >> (16 * (e & 1))) & 0xffffu;
+                v[e] = __uint_as_float(pos);
+                mine |= 1u << e;
+              }
+            }
+          }
+          __syncthreads();  // cur_l now holds the piece's bucket ends
+          // by position: rank = bucket start + smaller keys of the bucket
+          for (int t = tid; t < (int)(p1 - p0); t += nt) {
+            const uint64_t key = s_keys[t];
+            const int bk = squash_bucket(key_score((uint32_t)(key >> 32)), mu, inv_sd, nbk);
+            const uint32_t end = cur_l[bk] - p0, beg = end - cnt_l[bk];
+            uint32_t r = beg;
+            for (uint32_t i = beg; i < end; ++i) r += s_keys[i] < key ? 1u : 0u;
+            s_ord[r] = (int32_t)(uint32_t)key;
+            s_sz[r] = s_aux[t];
+            s_aux[t] = p0 + r;
+          }
+          __syncthreads();
+#pragma unroll
+          for (int e = 0; e < kE; ++e)
+            if ((mine >> e) & 1u) v[e] = __uint_as_float(s_aux[__float_as_uint(v[e])]);
+          ranked |= mine;
+          const uint32_t tot = scan_lds<kPiecePer>(s_sz, s_wave_u);
+          for (int t = tid; t < (int)(p1 - p0); t += nt) {
+            const uint32_t pf = carry + s_sz[t];
+            order[p0 + t] = s_ord[t];
+            cnt[p0 + t] = pf;
+            rpre[p0 + t] = (int32_t)pf;
+          }
+          carry += tot;
+          b0 = b1;
+        }
+#pragma unroll
+        for (int e = 0; e < kE; ++e)
+          if (tid + e * 1024 < C) rank_of[tid + e * 1024] = (int32_t)__float_as_uint(v[e]);
+        total = carry;
+        if (tid == 0) rpre[C] = (int32_t)total;
+      }
+      __syncthreads();  // the general path below reuses the LDS and s_red
+    }
+    if (!pieces_done) {
+      // C > 8192: the bucket counts (8192 buckets) in LDS, the keys and the
+      // per-rank sizes / starts in the workspace.  Every loop over the elements
+      // takes 8 (4 in the ranking) per thread per step with their global loads
+      // issued together, so a step costs one memory round trip.
+      uint32_t* cnt_l = reinterpret_cast<uint32_t*>(smem_raw);
+      uint32_t* start_l = cnt_l + kSortLdsBuckets;
+      constexpr int nb = kSortLdsBuckets;
+      constexpr int kB = 8;
+      uint64_t* keys = a.g_keys + (int64_t)bh * a.nb_max;
       {
-        const uint4* c4 = reinterpret_cast<const uint4*>(cnt_l) + tid * 2;
-        uint4* s4 = reinterpret_cast<uint4*>(start_l) + tid * 2;
-        s4[0] = c4[0];
-        s4[1] = c4[1];
+        uint4* c4 = reinterpret_cast<uint4*>(cnt_l) + tid * 2;
+        c4[0] = make_uint4(0, 0, 0, 0);
+        c4[1] = make_uint4(0, 0, 0, 0);
       }
-      scan8k_lds(start_l, s_wave_u);  // (each thread copied the entries it scans)
+      // moments and range of the finite scores, as in the LDS path
+      float sm = 0.f, sq = 0.f, lo = INFINITY, hi = -INFINITY, nf = 0.f;
       for (int j0 = tid; j0 < C; j0 += kB * nt) {
         float v[kB];
 #pragma unroll
         for (int e = 0; e < kB; ++e) v[e] = sc[min(j0 + e * nt, C - 1)];
 #pragma unroll
         for (int e = 0; e < kB; ++e) {
-          const int j = j0 + e * nt;
-          if (j < C)
-            keys[atomicAdd(&start_l[squash_bucket(v[e], mu, inv_sd, nb)], 1u)] =
-                ((uint64_t)desc_key_bits(v[e]) << 32) | (uint32_t)j;
+          if (j0 + e * nt < C && v[e] == v[e]) {
+            sm += v[e];
+            sq += v[e] * v[e];
+            lo = fminf(lo, v[e]);
+            hi = fmaxf(hi, v[e]);
+            nf += 1.f;
+          }
         }
       }
-      __syncthreads();  // the keys are visible to the workgroup; start_l holds the bucket ends
-    }
-    // rank of every element: its bucket start plus the smaller keys in its
-    // bucket.  Four elements per step: the first four keys of each one's
-    // bucket load together with the elements' cluster offsets; longer buckets
-    // are walked after.  Then its size and first row go to its rank.
-    {
-      constexpr int kE = 4, kK = 4;
-      for (int j0 = tid; j0 < C; j0 += kE * nt) {
-        uint64_t key[kE];
-        uint32_t beg[kE], end[kE], r[kE];
-        int o_lo[kE], o_hi[kE];
+      sm = wave_allsum_f(sm);  // DPP, no LDS
+      sq = wave_allsum_f(sq);
+      nf = wave_allsum_f(nf);
+      lo = wave_allmin_f(lo);
+      hi = wave_allmax_f(hi);
+      if ((tid & (kWave - 1)) == 0) {
+        s_red[tid / kWave][0] = sm;
+        s_red[tid / kWave][1] = sq;
+        s_red[tid / kWave][2] = lo;
+        s_red[tid / kWave][3] = hi;
+        s_wave_f[tid / kWave] = nf;
+      }
+      __syncthreads();  // also orders the count clears before the counting below
+      sm = 0.f, sq = 0.f, lo = INFINITY, hi = -INFINITY, nf = 0.f;
+      for (int w = 0; w < nt / kWave; ++w) {
+        sm += s_red[w][0];
+        sq += s_red[w][1];
+        lo = fminf(lo, s_red[w][2]);
+        hi = fmaxf(hi, s_red[w][3]);
+        nf += s_wave_f[w];
+      }
+      const bool all_equal = lo == hi && nf == (float)C;  // then the order is the cluster id
+      const float mu = nf > 0.f ? sm / nf : 0.f;
+      const float var = nf > 0.f ? fmaxf(sq / nf - mu * mu, 0.f) : 0.f;
+      const float sd = sqrtf(var);
+      const float inv_sd = sd > 0.f ? 1.f / sd : (hi > lo ? 1.f / (hi - lo) : 1.f);
+      if (!all_equal) {
+        for (int j0 = tid; j0 < C; j0 += kB * nt) {
+          float v[kB];
 #pragma unroll
-        for (int e = 0; e < kE; ++e) {
-          const int jc = min(j0 + e * nt, C - 1);
-          const float sv = sc[jc];
-          key[e] = ((uint64_t)desc_key_bits(sv) << 32) | (uint32_t)jc;
-          o_lo[e] = off[jc];
-          o_hi[e] = off[jc + 1];
-          const int bk = all_equal ? 0 : squash_bucket(sv, mu, inv_sd, nb);
-          end[e] = all_equal ? 1u : start_l[bk];
-          beg[e] = all_equal ? 0u : end[e] - cnt_l[bk];
-          r[e] = 0;
+          for (int e = 0; e < kB; ++e) v[e] = sc[min(j0 + e * nt, C - 1)];
+#pragma unroll
+          for (int e = 0; e < kB; ++e)
+            if (j0 + e * nt < C) atomicAdd(&cnt_l[squash_bucket(v[e], mu, inv_sd, nb)], 1u);
         }
-        if (!all_equal) {
-          uint64_t kk[kE][kK];
+        __syncthreads();
+        {
+          const uint4* c4 = reinterpret_cast<const uint4*>(cnt_l) + tid * 2;
+          uint4* s4 = reinterpret_cast<uint4*>(start_l) + tid * 2;
+          s4[0] = c4[0];
+          s4[1] = c4[1];
+        }
+        scan8k_lds(start_l, s_wave_u);  // (each thread copied the entries it scans)
+        for (int j0 = tid; j0 < C; j0 += kB * nt) {
+          float v[kB];
 #pragma unroll
-          for (int e = 0; e < kE; ++e)
+          for (int e = 0; e < kB; ++e) v[e] = sc[min(j0 + e * nt, C - 1)];
 #pragma unroll
-            for (int i = 0; i < kK; ++i) kk[e][i] = keys[min(beg[e] + i, end[e] - 1)];  // the element is in it
+          for (int e = 0; e < kB; ++e) {
+            const int j = j0 + e * nt;
+            if (j < C)
+              keys[atomicAdd(&start_l[squash_bucket(v[e], mu, inv_sd, nb)], 1u)] =
+                  ((uint64_t)desc_key_bits(v[e]) << 32) | (uint32_t)j;
+          }
+        }
+        __syncthreads();  // the keys are visible to the workgroup; start_l holds the bucket ends
+      }
+      // rank of every element: its bucket start plus the smaller keys in its
+      // bucket.  Four elements per step: the first four keys of each one's
+      // bucket load together with the elements' cluster offsets; longer buckets
+      // are walked after.  Then its size and first row go to its rank.
+      {
+        constexpr int kE = 4, kK = 4;
+        for (int j0 = tid; j0 < C; j0 += kE * nt) {
+          uint64_t key[kE];
+          uint32_t beg[kE], end[kE], r[kE];
+          int o_lo[kE], o_hi[kE];
 #pragma unroll
           for (int e = 0; e < kE; ++e) {
-#pragma unroll
-            for (int i = 0; i < kK; ++i) r[e] += (beg[e] + i < end[e] && kk[e][i] < key[e]) ? 1u : 0u;
-            for (uint32_t t = beg[e] + kK; t < end[e]; ++t) r[e] += keys[t] < key[e] ? 1u : 0u;
+            const int jc = min(j0 + e * nt, C - 1);
+            const float sv = sc[jc];
+            key[e] = ((uint64_t)desc_key_bits(sv) << 32) | (uint32_t)jc;
+            o_lo[e] = off[jc];
+            o_hi[e] = off[jc + 1];
+            const int bk = all_equal ? 0 : squash_bucket(sv, mu, inv_sd, nb);
+            end[e] = all_equal ? 1u : start_l[bk];
+            beg[e] = all_equal ? 0u : end[e] - cnt_l[bk];
+            r[e] = 0;
           }
-        }
+          if (!all_equal) {
+            uint64_t kk[kE][kK];
 #pragma unroll
-        for (int e = 0; e < kE; ++e) {
-          const int j = j0 + e * nt;
-          if (j < C) {
-            const int p2 = all_equal ? j : (int)(beg[e] + r[e]);
-            order[p2] = j;
-            rank_of[j] = p2;
-            cnt[p2] = (uint32_t)(o_hi[e] - o_lo[e]);
-            ostart[p2] = o_lo[e];
+            for (int e = 0; e < kE; ++e)
+#pragma unroll
+              for (int i = 0; i < kK; ++i) kk[e][i] = keys[min(beg[e] + i, end[e] - 1)];  // the element is in it
+#pragma unroll
+            for (int e = 0; e < kE; ++e) {
+#pragma unroll
+              for (int i = 0; i < kK; ++i) r[e] += (beg[e] + i < end[e] && kk[e][i] < key[e]) ? 1u : 0u;
+              for (uint32_t t = beg[e] + kK; t < end[e]; ++t) r[e] += keys[t] < key[e] ? 1u : 0u;
+            }
+          }
+#pragma unroll
+          for (int e = 0; e < kE; ++e) {
+            const int j = j0 + e * nt;
+            if (j < C) {
+              const int p2 = all_equal ? j : (int)(beg[e] + r[e]);
+              order[p2] = j;
+              rank_of[j] = p2;
+              cnt[p2] = (uint32_t)(o_hi[e] - o_lo[e]);
+            }
           }
         }
       }
-    }
-    __syncthreads();  // sizes and starts by rank are visible
-    // exclusive prefix of the sizes in rank order: 32 consecutive ranks per
-    // thread per pass, loaded together
-    {
-      constexpr int kS = 32;
-      uint32_t carry = 0;
-      for (int base = 0; base < C; base += kS * nt) {
-        const int r0 = base + tid * kS;
-        uint32_t v[kS];
+      __syncthreads();  // sizes and starts by rank are visible
+      // exclusive prefix of the sizes in rank order: 32 consecutive ranks per
+      // thread per pass, loaded together
+      {
+        constexpr int kS = 32;
+        uint32_t carry = 0;
+        for (int base = 0; base < C; base += kS * nt) {
+          const int r0 = base + tid * kS;
+          uint32_t v[kS];
 #pragma unroll
-        for (int e = 0; e < kS; ++e) v[e] = r0 + e < C ? cnt[r0 + e] : 0u;
-        uint32_t local = 0;
+          for (int e = 0; e < kS; ++e) v[e] = r0 + e < C ? cnt[r0 + e] : 0u;
+          uint32_t local = 0;
 #pragma unroll
-        for (int e = 0; e < kS; ++e) local += v[e];
-        const uint32_t incl = wave_incl_scan(local);  // DPP, no LDS
-        if ((tid & (kWave - 1)) == kWave - 1) s_wave_u[tid / kWave] = incl;
-        __syncthreads();
-        uint32_t run = carry + incl - local, tot = 0;
-        for (int w = 0; w < nt / kWave; ++w) {
-          const uint32_t t = s_wave_u[w];
-          if (w < tid / kWave) run += t;
-          tot += t;
+          for (int e = 0; e < kS; ++e) local += v[e];
+          const uint32_t incl = wave_incl_scan(local);  // DPP, no LDS
+          if ((tid & (kWave - 1)) == kWave - 1) s_wave_u[tid / kWave] = incl;
+          __syncthreads();
+          uint32_t run = carry + incl - local, tot = 0;
+          for (int w = 0; w < nt / kWave; ++w) {
+            const uint32_t t = s_wave_u[w];
+            if (w < tid / kWave) run += t;
+            tot += t;
+          }
+#pragma unroll
+          for (int e = 0; e < kS; ++e) {
+            if (r0 + e < C) cnt[r0 + e] = run;
+            run += v[e];
+          }
+          carry += tot;
+          __syncthreads();  // s_wave_u is reused; the prefix is visible
         }
-#pragma unroll
-        for (int e = 0; e < kS; ++e) {
-          if (r0 + e < C) cnt[r0 + e] = run;
-          run += v[e];
-        }
-        carry += tot;
-        __syncthreads();  // s_wave_u is reused; the prefix is visible
+        total = carry;
       }
-      total = carry;
-    }
-    int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
-    for (int r0 = tid; r0 <= C; r0 += kB * nt) {
-      uint32_t v[kB];
+      int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
+      for (int r0 = tid; r0 <= C; r0 += kB * nt) {
+        uint32_t v[kB];
 #pragma unroll
-      for (int e = 0; e < kB; ++e) v[e] = cnt[min(r0 + e * nt, C - 1)];
+        for (int e = 0; e < kB; ++e) v[e] = cnt[min(r0 + e * nt, C - 1)];
 #pragma unroll
-      for (int e = 0; e < kB; ++e) {
-        const int r = r0 + e * nt;
-        if (r <= C) rpre[r] = (int32_t)(r < C ? v[e] : total);
+        for (int e = 0; e < kB; ++e) {
+          const int r = r0 + e * nt;
+          if (r <= C) rpre[r] = (int32_t)(r < C ? v[e] : total);
+        }
       }
     }
   }
@@ -576,10 +776,13 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
   const int64_t W1 = geo.exact ? 0 : geo.t1 - geo.s1 + 1;
   auto prefix_at = [&](int r) -> uint32_t { return r < C ? cnt[r] : total; };  // r in [0, C]
   if constexpr (!kLds) {
-    // workspace path: every kStr-th prefix entry in LDS (the bucket arrays are
-    // dead), a binary search there, then the last kStr entries from memory
+    // workspace path: every kStr-th prefix entry in LDS (every entry up to
+    // kSortWsLdsBytes / 4 clusters; the bucket arrays are dead), a binary
+    // search there, then the last kStr entries from memory.  The row of
+    // position i in rank r's cluster is off[order[r]] + i - 1 - prefix[r].
     uint32_t* s_pre = reinterpret_cast<uint32_t*>(smem_raw);
-    const int kStr = (C + 2 * kSortLdsBuckets - 1) / (2 * kSortLdsBuckets);  // 16384 LDS entries at most
+    constexpr int kPreCap = (int)(kSortWsLdsBytes / 4);
+    const int kStr = (C + kPreCap - 1) / kPreCap;
     const int nsp = (C + kStr - 1) / kStr;
     for (int i0 = tid; i0 < nsp; i0 += 8 * nt) {
       uint32_t v[8];
@@ -624,12 +827,19 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
           lr[k] = (t < C && (int64_t)pv[k] < iv[k]) ? t : lr[k];
         }
       }
+      int first[kU];
+      uint32_t pr[kU];
+#pragma unroll
+      for (int k = 0; k < kU; ++k) {
+        const int r = min(lr[k], C - 1);
+        first[k] = off[order[r]];
+        pr[k] = kStr == 1 ? s_pre[r] : cnt[r];
+      }
 #pragma unroll
       for (int k = 0; k < kU; ++k) {
         const int64_t u = u0 + (int64_t)k * nt;
         if (u < S_main) {
-          const int r = min(lr[k], C - 1);
-          const int32_t row = ostart[r] + (int32_t)(iv[k] - 1 - (int64_t)prefix_at(r));
+          const int32_t row = first[k] + (int32_t)(iv[k] - 1 - (int64_t)pr[k]);
           rows[u] = min(max(row, 0), n - 1);
         }
       }
@@ -1304,8 +1514,7 @@ hipError_t launch_sort(const SortArgs& a, bool lds, int n_heads, hipStream_t st)
     const size_t bytes = (size_t)kSortLdsBuckets * 16;  // keys u64, cnt u32, start u32
     hipLaunchKernelGGL(sort_clusters_kernel<true>, dim3(n_heads), dim3(1024), bytes, st, a);
   } else {
-    const size_t bytes = (size_t)kSortLdsBuckets * 8;  // bucket cnt u32, start u32; then the sampled prefix
-    hipLaunchKernelGGL(sort_clusters_kernel<false>, dim3(n_heads), dim3(1024), bytes, st, a);
+    hipLaunchKernelGGL(sort_clusters_kernel<false>, dim3(n_heads), dim3(1024), kSortWsLdsBytes, st, a);
   }
   return hipGetLastError();
 }
