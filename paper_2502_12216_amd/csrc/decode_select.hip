@@ -208,8 +208,10 @@ __device__ __forceinline__ float key_score(uint32_t k) {
 
 // Workspace sort of 8192 < C <= kPieceMaxC clusters: the scores and sizes of
 // a thread's 32 clusters stay in registers; the bucket counts (kPieceBuckets)
-// sit in LDS, and the buckets are taken in pieces of consecutive buckets
-// holding at most kPieceCap clusters, whose keys are staged in LDS: every
+// sit in LDS, and counting them gives each cluster its place in its bucket,
+// so after the scan each cluster knows its position in bucket order.  The
+// buckets are then taken in pieces of consecutive buckets holding at most
+// kPieceCap clusters, whose keys are staged in LDS at those positions: every
 // access of the rank computation is an LDS access, and the global accesses
 // are coalesced.  A piece's ranks are consecutive, so its order, rank-prefix
 // and size entries leave in order.
@@ -404,40 +406,46 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     if (C <= kPieceMaxC) {  // uniform
       constexpr int nbk = kPieceBuckets, kE = kPieceMaxC / 1024;
       uint32_t* cnt_l = reinterpret_cast<uint32_t*>(smem_raw);  // bucket sizes
-      uint32_t* cur_l = cnt_l + nbk;                            // bucket starts, then scatter cursors
-      uint64_t* s_keys = reinterpret_cast<uint64_t*>(cur_l + nbk);  // the piece's keys by bucket position
+      uint32_t* st_l = cnt_l + nbk;                             // bucket starts
+      uint64_t* s_keys = reinterpret_cast<uint64_t*>(st_l + nbk);  // the piece's keys by bucket position
       uint32_t* s_aux = reinterpret_cast<uint32_t*>(s_keys + kPieceCap);  // size by position, then rank
       int32_t* s_ord = reinterpret_cast<int32_t*>(s_aux + kPieceCap);     // cluster by rank in the piece
       uint32_t* s_sz = reinterpret_cast<uint32_t*>(s_ord + kPieceCap);    // size, then prefix, by rank
-      float v[kE];          // the score; the bucket position while its piece is ranked; then the rank
-      uint32_t sz2[kE / 2];  // cluster sizes, two 16-bit halves (larger sizes take the general path)
+      float v[kE];     // the score, then the rank
+      uint32_t ps[kE];  // size (low 16 bits) | place in its bucket, then bucket position (high 16 bits)
       uint32_t size_or = 0;  // OR of the sizes: any bit above 15 sends the head to the general path
+      const int nv = C > tid ? (C - tid + 1023) / 1024 : 0;  // clusters of this thread: tid + 1024 e, e < nv
+      // the cluster id, rebuilt at each use rather than kept in 32 registers
+      auto cid = [&](int e) {
+        int t = tid;
+        asm volatile("" : "+v"(t));
+        return t + e * 1024;
+      };
 #pragma unroll
-      for (int e = 0; e < kE; ++e) v[e] = sc[min(tid + e * 1024, C - 1)];
+      for (int e = 0; e < kE; ++e) v[e] = sc[min(cid(e), C - 1)];
 #pragma unroll
-      for (int e0 = 0; e0 < kE; e0 += 8) {  // sizes: 16 loads in flight per batch
-        int o0[8], o1[8];
+      for (int e0 = 0; e0 < kE; e0 += kE / 2) {  // sizes: 32 offset loads in flight per batch
+        int o0[kE / 2], o1[kE / 2];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int jc = min(tid + (e0 + e) * 1024, C - 1);
+        for (int e = 0; e < kE / 2; ++e) {
+          const int jc = min(cid(e0 + e), C - 1);
           o0[e] = off[jc];
           o1[e] = off[jc + 1];
         }
 #pragma unroll
-        for (int e = 0; e < 8; e += 2) {
-          const uint32_t x = (uint32_t)(o1[e] - o0[e]), y = (uint32_t)(o1[e + 1] - o0[e + 1]);
-          size_or |= x | y;
-          uint32_t packed = x | (y << 16);
-          // packed (and OR-ed) now, so that the loaded offsets die here
-          asm volatile("" : "+v"(packed), "+v"(size_or));
-          sz2[(e0 + e) / 2] = packed;
+        for (int e = 0; e < kE / 2; ++e) {
+          uint32_t x = (uint32_t)(o1[e] - o0[e]);
+          size_or |= x;
+          // taken now, so that the loaded offsets die here
+          asm volatile("" : "+v"(x), "+v"(size_or));
+          ps[e0 + e] = x & 0xffffu;
         }
       }
       reinterpret_cast<uint4*>(cnt_l)[tid] = make_uint4(0, 0, 0, 0);
       float sm = 0.f, sq = 0.f, lo = INFINITY, hi = -INFINITY, nf = 0.f;
 #pragma unroll
       for (int e = 0; e < kE; ++e) {
-        if (tid + e * 1024 < C && v[e] == v[e]) {
+        if (e < nv && v[e] == v[e]) {
           sm += v[e];
           sq += v[e] * v[e];
           lo = fminf(lo, v[e]);
@@ -472,80 +480,97 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
       const float sd = sqrtf(var);
       const float inv_sd = sd > 0.f ? 1.f / sd : (hi > lo ? 1.f / (hi - lo) : 1.f);
       if (!all_equal) {
+        // counting: each cluster's place in its bucket (arrival order)
 #pragma unroll
-        for (int e = 0; e < kE; ++e)
-          if (tid + e * 1024 < C) atomicAdd(&cnt_l[squash_bucket(v[e], mu, inv_sd, nbk)], 1u);
+        for (int e0 = 0; e0 < kE; e0 += 8) {  // unconditional (adding 0 past C): 8 returns in flight
+#pragma unroll
+          for (int e = e0; e < e0 + 8; ++e)
+            ps[e] |= atomicAdd(&cnt_l[squash_bucket(v[e], mu, inv_sd, nbk)], e < nv ? 1u : 0u) << 16;
+#pragma unroll
+          for (int e = e0; e < e0 + 8; ++e) asm volatile("" : "+v"(ps[e]));  // done before the next 8
+        }
         __syncthreads();
         // the largest bucket must fit a piece
         const uint4 c4 = reinterpret_cast<const uint4*>(cnt_l)[tid];
-        reinterpret_cast<uint4*>(cur_l)[tid] = c4;
+        reinterpret_cast<uint4*>(st_l)[tid] = c4;
         float mb = (float)max(max(c4.x, c4.y), max(c4.z, c4.w));  // counts <= 2^15: exact
         mb = wave_allmax_f(size_or > 0xffffu ? INFINITY : mb);
         if ((tid & (kWave - 1)) == 0) s_wave_f[tid / kWave] = mb;
-        scan_lds<nbk / 1024>(cur_l, s_wave_u);  // bucket starts; its barriers publish s_wave_f
+        scan_lds<nbk / 1024>(st_l, s_wave_u);  // bucket starts; its barriers publish s_wave_f
         float maxb = 0.f;
         for (int w = 0; w < 1024 / kWave; ++w) maxb = fmaxf(maxb, s_wave_f[w]);
         pieces_done = maxb <= (float)kPieceCap;
+        // bucket position = bucket start + place (C <= 2^15: 16 bits)
+#pragma unroll
+        for (int e0 = 0; e0 < kE; e0 += 8) {  // 8 reads in flight
+#pragma unroll
+          for (int e = e0; e < e0 + 8; ++e) ps[e] += st_l[squash_bucket(v[e], mu, inv_sd, nbk)] << 16;
+#pragma unroll
+          for (int e = e0; e < e0 + 8; ++e) asm volatile("" : "+v"(ps[e]));
+        }
       }
       if (pieces_done) {
         int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
-        __shared__ int s_b1;
-        uint32_t carry = 0, ranked = 0;  // bit e: cluster e has its rank in v[e]
+        uint32_t carry = 0;
         for (int b0 = 0; b0 < nbk;) {
           // the piece: buckets [b0, b1), the last b1 whose start is within
-          // kPieceCap of the piece's start (buckets from b0 on still hold
-          // their start; the bucket b0 alone fits)
-          const uint32_t p0 = cur_l[b0];
-          if (tid == 0) {
-            int lo_b = b0 + 1, hi_b = nbk;
-            while (lo_b < hi_b) {
-              const int mid = (lo_b + hi_b + 1) >> 1;
-              const uint32_t st = mid < nbk ? cur_l[mid] : (uint32_t)C;
-              if (st - p0 <= (uint32_t)kPieceCap) lo_b = mid;
-              else hi_b = mid - 1;
-            }
-            s_b1 = lo_b;
+          // kPieceCap of the piece's start (the bucket b0 alone fits)
+          // (starts are non-decreasing: b1 counts the b in [1, nbk] with
+          // start(b) <= p0 + kPieceCap, start(nbk) = C)
+          const uint32_t p0 = st_l[b0];
+          {
+            const uint4 s4 = reinterpret_cast<const uint4*>(st_l)[tid];
+            const uint32_t lim = p0 + (uint32_t)kPieceCap;
+            uint32_t c = (tid > 0 && s4.x <= lim ? 1u : 0u) + (s4.y <= lim ? 1u : 0u) + (s4.z <= lim ? 1u : 0u) +
+                         (s4.w <= lim ? 1u : 0u) + (tid == 1023 && (uint32_t)C <= lim ? 1u : 0u);
+            c = (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(c), kWave - 1);  // DPP, no LDS
+            if ((tid & (kWave - 1)) == 0) s_wave_u[tid / kWave] = c;
           }
           __syncthreads();  // also: the previous piece's LDS reads are done
-          const int b1 = s_b1;
-          const uint32_t p1 = b1 < nbk ? cur_l[b1] : (uint32_t)C;
+          int b1 = 0;
+          for (int w = 0; w < 1024 / kWave; ++w) b1 += (int)s_wave_u[w];
+          const uint32_t len = (b1 < nbk ? st_l[b1] : (uint32_t)C) - p0;
 #pragma unroll
           for (int e = 0; e < kPiecePer; ++e) s_sz[tid * kPiecePer + e] = 0u;
           // the owners place the piece's keys and sizes at their bucket positions
-          uint32_t mine = 0;
 #pragma unroll
           for (int e = 0; e < kE; ++e) {
-            const int j = tid + e * 1024;
-            if (j < C && !((ranked >> e) & 1u)) {
-              const int bk = squash_bucket(v[e], mu, inv_sd, nbk);
-              if (bk >= b0 && bk < b1) {
-                const uint32_t pos = atomicAdd(&cur_l[bk], 1u) - p0;
-                s_keys[pos] = ((uint64_t)desc_key_bits(v[e]) << 32) | (uint32_t)j;
-                s_aux[pos] = (sz2[e / 2] >> (16 * (e & 1))) & 0xffffu;
-                v[e] = __uint_as_float(pos);
-                mine |= 1u << e;
-              }
+            const uint32_t pos = (ps[e] >> 16) - p0;
+            if (e < nv && pos < len) {
+              s_keys[pos] = ((uint64_t)desc_key_bits(v[e]) << 32) | (uint32_t)cid(e);
+              s_aux[pos] = ps[e] & 0xffffu;
             }
           }
-          __syncthreads();  // cur_l now holds the piece's bucket ends
+          __syncthreads();
           // by position: rank = bucket start + smaller keys of the bucket
-          for (int t = tid; t < (int)(p1 - p0); t += nt) {
+          for (int t = tid; t < (int)len; t += 1024) {
             const uint64_t key = s_keys[t];
             const int bk = squash_bucket(key_score((uint32_t)(key >> 32)), mu, inv_sd, nbk);
-            const uint32_t end = cur_l[bk] - p0, beg = end - cnt_l[bk];
-            uint32_t r = beg;
-            for (uint32_t i = beg; i < end; ++i) r += s_keys[i] < key ? 1u : 0u;
+            const uint32_t beg = st_l[bk] - p0, end = beg + cnt_l[bk];
+            uint32_t r = beg, i = beg;
+            for (; i + 4 <= end; i += 4) {  // four reads in flight
+              const uint64_t k0 = s_keys[i], k1 = s_keys[i + 1], k2 = s_keys[i + 2], k3 = s_keys[i + 3];
+              r += (k0 < key ? 1u : 0u) + (k1 < key ? 1u : 0u) + (k2 < key ? 1u : 0u) + (k3 < key ? 1u : 0u);
+            }
+            for (; i < end; ++i) r += s_keys[i] < key ? 1u : 0u;
             s_ord[r] = (int32_t)(uint32_t)key;
             s_sz[r] = s_aux[t];
             s_aux[t] = p0 + r;
           }
           __syncthreads();
 #pragma unroll
-          for (int e = 0; e < kE; ++e)
-            if ((mine >> e) & 1u) v[e] = __uint_as_float(s_aux[__float_as_uint(v[e])]);
-          ranked |= mine;
+          for (int e0 = 0; e0 < kE; e0 += 8) {  // reads at clamped positions, 8 in flight
+#pragma unroll
+            for (int e = e0; e < e0 + 8; ++e) {
+              const uint32_t pos = (ps[e] >> 16) - p0;
+              const uint32_t rk = s_aux[min(pos, (uint32_t)kPieceCap - 1)];
+              v[e] = (e < nv && pos < len) ? __uint_as_float(rk) : v[e];
+            }
+#pragma unroll
+            for (int e = e0; e < e0 + 8; ++e) asm volatile("" : "+v"(v[e]));
+          }
           const uint32_t tot = scan_lds<kPiecePer>(s_sz, s_wave_u);
-          for (int t = tid; t < (int)(p1 - p0); t += nt) {
+          for (int t = tid; t < (int)len; t += 1024) {
             const uint32_t pf = carry + s_sz[t];
             order[p0 + t] = s_ord[t];
             cnt[p0 + t] = pf;
@@ -556,7 +581,7 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
         }
 #pragma unroll
         for (int e = 0; e < kE; ++e)
-          if (tid + e * 1024 < C) rank_of[tid + e * 1024] = (int32_t)__float_as_uint(v[e]);
+          if (e < nv) rank_of[cid(e)] = (int32_t)__float_as_uint(v[e]);
         total = carry;
         if (tid == 0) rpre[C] = (int32_t)total;
       }
@@ -784,18 +809,18 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     constexpr int kPreCap = (int)(kSortWsLdsBytes / 4);
     const int kStr = (C + kPreCap - 1) / kPreCap;
     const int nsp = (C + kStr - 1) / kStr;
-    for (int i0 = tid; i0 < nsp; i0 += 8 * nt) {
-      uint32_t v[8];
+    for (int i0 = tid; i0 < nsp; i0 += 16 * nt) {
+      uint32_t v[16];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = cnt[min((i0 + e * nt) * kStr, C - 1)];
+      for (int e = 0; e < 16; ++e) v[e] = cnt[min((i0 + e * nt) * kStr, C - 1)];
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
+      for (int e = 0; e < 16; ++e)
         if (i0 + e * nt < nsp) s_pre[i0 + e * nt] = v[e];
     }
     __syncthreads();
     int top = 1;
     while (top * 2 <= nsp) top <<= 1;
-    constexpr int kU = 4;  // independent searches in flight per thread
+    constexpr int kU = 8;  // independent searches in flight per thread
     for (int64_t u0 = tid; u0 < S_main; u0 += (int64_t)kU * nt) {
       int64_t iv[kU];
       int li[kU];
@@ -805,12 +830,16 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
         iv[k] = u < N ? u + 1 : (u < N + W1 ? geo.s1 + (u - N) : geo.s2 + (u - N - W1));
         li[k] = 0;
       }
-      // largest i with s_pre[i] < position (s_pre[0] = prefix[0] = 0)
+      // largest i with s_pre[i] < position (s_pre[0] = prefix[0] = 0); the
+      // reads at clamped indices, so that the kU of a step are in flight together
       for (int step = top; step > 0; step >>= 1) {
+        uint32_t pv[kU];
+#pragma unroll
+        for (int k = 0; k < kU; ++k) pv[k] = s_pre[min(li[k] + step, nsp - 1)];
 #pragma unroll
         for (int k = 0; k < kU; ++k) {
           const int t = li[k] + step;
-          li[k] = (t < nsp && (int64_t)s_pre[t] < iv[k]) ? t : li[k];
+          li[k] = (t < nsp && (int64_t)pv[k] < iv[k]) ? t : li[k];
         }
       }
       // then the largest r in [li * kStr, li * kStr + kStr) with prefix[r] < position
