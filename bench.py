@@ -282,7 +282,7 @@ def config_record(T, wl, Ps, dev, flush, reps: int, stage_ev, ceiling, host_grou
             rec["union_per_kv_head"] = [int(x) for x in skv.cpu().numpy()[0]]
         points.append(rec)
         del dec
-    sort_path = "LDS" if max(ncl) <= 8192 else "workspace (out of LDS)"
+    sort_path = "LDS" if max(ncl) <= 8192 else ("LDS pieces" if max(ncl) <= 32768 else "workspace")
     out = {"batch": B, "seq_lens": (list(map(int, wl.seq_lens)) if B > 1 else int(wl.seq_lens[0])),
            "n_q_heads": Hq, "n_kv_heads": Hkv, "clusters_per_seq": (list(map(int, ncl)) if B > 1 else int(ncl[0])),
            "cluster_sort": sort_path, "kmeans_ms": round(km_ms, 2), "dense_us": round(us_dense, 2),
