@@ -175,8 +175,11 @@ void attn_splitk_kernel(AttnArgs a) {
   // wave scan and the four wave totals
   {
     const int per = (BG + 255) / 256, g0 = min(BG, tid * per), g1 = min(BG, g0 + per);
-    int64_t loc = 0;
-    for (int bg = g0; bg < g1; ++bg) loc += split_units(a, bg);
+    // the first group's units are kept (up to 256 groups it is the thread's
+    // only one), so the second pass does not load them again
+    const int64_t u_first = g0 < g1 ? split_units(a, g0) : 0;
+    int64_t loc = u_first;
+    for (int bg = g0 + 1; bg < g1; ++bg) loc += split_units(a, bg);
     int64_t incl = wave_incl_scan(loc);  // DPP, no LDS
     if (lane == kWave - 1) s_wsum[wave] = incl;
     __syncthreads();
@@ -184,7 +187,7 @@ void attn_splitk_kernel(AttnArgs a) {
     for (int w = 0; w < wave; ++w) run += s_wsum[w];
     for (int bg = g0; bg < g1; ++bg) {
       s_prefix[bg] = run;
-      run += split_units(a, bg);
+      run += bg == g0 ? u_first : split_units(a, bg);
     }
     if (tid == 255) s_prefix[BG] = run;
     __syncthreads();

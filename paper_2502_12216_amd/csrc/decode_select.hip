@@ -96,8 +96,11 @@ __global__ __launch_bounds__(256) void score_clusters_kernel(ScoreArgs a) {
     uint4 c[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
+      // unconditional loads at clamped rows (C > j0 >= 0), masked after, so
+      // that the four are in flight together
       const int j = j0 + wave * kPerWave + (it0 + k) * 4 + grp;
-      c[k] = j < C ? load_stream16(cbase + (int64_t)j * kHeadDim) : make_uint4(0, 0, 0, 0);
+      const uint4 x = load_stream16(cbase + (int64_t)min(j, C - 1) * kHeadDim);
+      c[k] = j < C ? x : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -1035,16 +1038,18 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
     const int64_t ro = rl >= 0 ? paged_row(a.pk, a.Hkv, a.total, kvb, b, g, rl, hm[0]) : -1;
     const uint16_t* Kl = a.K + sl * 8;
 #pragma unroll
-    for (int k = 0; k < kR; ++k) {
+    for (int k = 0; k < kR; ++k) {  // unconditional loads (row 0 for no sample), then masked
       const int64_t rk = __shfl(ro, k * 4 + grp, kWave);
-      kv[k] = rk >= 0 ? load_stream16(Kl + rk * kHeadDim) : make_uint4(0, 0, 0, 0);
+      const uint4 x = load_stream16(Kl + max(rk, (int64_t)0) * kHeadDim);
+      kv[k] = rk >= 0 ? x : make_uint4(0, 0, 0, 0);
     }
   } else {
     const uint16_t* Kg = a.K + ((int64_t)g * a.total + kvb) * kHeadDim + sl * 8;
 #pragma unroll
-    for (int k = 0; k < kR; ++k) {
+    for (int k = 0; k < kR; ++k) {  // unconditional loads (the sequence's row 0 for no sample), then masked
       const int rk = __shfl(rl, k * 4 + grp, kWave);
-      kv[k] = rk >= 0 ? load_stream16(Kg + (int64_t)rk * kHeadDim) : make_uint4(0, 0, 0, 0);
+      const uint4 x = load_stream16(Kg + (int64_t)max(rk, 0) * kHeadDim);
+      kv[k] = rk >= 0 ? x : make_uint4(0, 0, 0, 0);
     }
   }
 #pragma unroll
@@ -1142,12 +1147,14 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
 #pragma unroll
     for (int rg = 0; rg < kRg; ++rg)
       R[rg] = (lane < nch && pre[rg * 2] != -INFINITY) ? pre[rg * 2 + 1] * exp(pre[rg * 2] - m) : 0.0;
-    for (int c = lane + kWave; c < nch; c += kWave)
+    for (int c = lane + kWave; c < nch; c += kWave) {
+      double ms[2 * kRg];  // all 8 loads in flight before any is used
 #pragma unroll
-      for (int rg = 0; rg < kRg; ++rg) {
-        const double mc = lse[(c * kRg + rg) * 2];
-        if (mc != -INFINITY) R[rg] += lse[(c * kRg + rg) * 2 + 1] * exp(mc - m);
-      }
+      for (int i = 0; i < 2 * kRg; ++i) ms[i] = lse[c * 2 * kRg + i];
+#pragma unroll
+      for (int rg = 0; rg < kRg; ++rg)
+        if (ms[rg * 2] != -INFINITY) R[rg] += ms[rg * 2 + 1] * exp(ms[rg * 2] - m);
+    }
 #pragma unroll
     for (int rg = 0; rg < kRg; ++rg) R[rg] = wave_sum_d(R[rg]);
     EN = R[0];
@@ -1198,9 +1205,10 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
         double base = 0.0;
         int cstar = nhc - 1;
         for (int c0 = 0; c0 < nhc; c0 += kWave) {
-          const int c = c0 + lane;
-          const double mc = c < nhc ? (c0 == 0 ? pre[0] : lse[(c * kRg) * 2]) : -INFINITY;
-          const double sc = c0 == 0 ? pre[1] : (c < nhc ? lse[(c * kRg) * 2 + 1] : 0.0);
+          const int c = c0 + lane, cc = min(c, nhc - 1);  // loads at clamped chunks, in flight together
+          const double ml = c0 == 0 ? pre[0] : lse[(cc * kRg) * 2], sl_ = c0 == 0 ? pre[1] : lse[(cc * kRg) * 2 + 1];
+          const double mc = c < nhc ? ml : -INFINITY;
+          const double sc = c < nhc ? sl_ : 0.0;
           const double v = (c < nhc && mc != -INFINITY) ? sc * exp(mc - m) : 0.0;
           double incl = wave_incl_scan(v);  // DPP, no LDS
           // the running sum only grows, so the crossing is the first lane that reaches Tc
@@ -1223,8 +1231,8 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
 #pragma unroll
             for (int i = 0; i < kLg0; ++i)
               if (v0 == i * kWave) lu = lg0[i];
-          } else if (u < ue) {
-            lu = lg[u];
+          } else {
+            lu = lg[min(u, ue - 1)];  // unconditional (u >= ue is masked below)
           }
           const double e = u < ue ? exp(lu - m) : 0.0;
           double incl = wave_incl_scan(e);  // DPP, no LDS
