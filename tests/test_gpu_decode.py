@@ -479,6 +479,40 @@ def test_sparse_target_one_at_128k_matches_dense_and_paged():
     print(f"128k P=1: sparse-dense {float((out - d_tok).abs().max()):.2e}, oracle max-abs {err:.2e}")
 
 
+@pytest.mark.parametrize("case", ["c34000", "big_bucket", "big_cluster"])
+def test_sparse_sort_general_workspace_path(case):
+    """Heads that the LDS-piece sort of 8192 < C <= 32768 clusters hands to
+    the general workspace path: more than 32768 clusters (34000 clusters of
+    about two tokens), a bucket larger than a piece (7000 of 9000 clusters of
+    sequence 0 share one centroid, so 7000 equal scores), and a cluster of
+    more than 65535 tokens (cluster 0 of every KV head holds 70000 of 90000
+    tokens).  Staged parity on every group at P = 0.9."""
+    import dataclasses
+    P = 0.9
+    lens, C = {"c34000": ([70000], 34000), "big_bucket": ([20000, 12000], 9000),
+               "big_cluster": ([90000], 9000)}[case]
+    base = _small("ctx32k_llama8b", lens)
+    wl = dataclasses.replace(base, fixed_clusters=C, name=f"{base.name}_{case}")
+    inp = synth.make_layer(wl, 0)
+    lay = synth.label_layout(inp)
+    if case == "big_bucket":
+        cent = lay.centroids.clone()
+        c0 = int(lay.cl_indptr[0])
+        cent[:, c0:c0 + 7000] = cent[:, c0:c0 + 1]
+        lay.centroids = cent
+    if case == "big_cluster":
+        # a valid layout with other cluster boundaries: cluster 0 takes the
+        # first 70000 sorted rows, the other 8999 share the rest evenly
+        n = lens[0]
+        rest = np.round(np.linspace(70000, n, C)).astype(np.int32)
+        off = np.concatenate([[0], rest]).astype(np.int32)
+        assert off[1] == 70000 and off[-1] == n and np.all(np.diff(off) >= 0)
+        lay.offsets = torch.as_tensor(np.tile(off, (wl.n_kv_heads, 1)))
+    res = run_sparse(inp, lay, P)
+    st = check_layer(inp, lay, P, res, label=f"sort general path {case}")
+    print(f"sort general path {case}: k={[s['k'] for s in st][:2]} union={[s['union'] for s in st][:4]}")
+
+
 @pytest.mark.parametrize("P", [0.5, 0.9])
 def test_sparse_degenerate_scores_out_of_lds_sort(P):
     """The sort of more than 8192 clusters per head runs out of the
