@@ -406,7 +406,7 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     cnt = a.g_cnt + (int64_t)bh * (a.nb_max + 4);  // per rank: size, then prefix
     ostart = nullptr;                              // the sample rows start from off[order[r]]
     bool pieces_done = false;
-    if (C <= kPieceMaxC) {  // uniform
+    if (C > 0 && C <= kPieceMaxC) {  // uniform; its loads clamp indices to C - 1
       constexpr int nbk = kPieceBuckets, kE = kPieceMaxC / 1024;
       uint32_t* cnt_l = reinterpret_cast<uint32_t*>(smem_raw);  // bucket sizes
       uint32_t* st_l = cnt_l + nbk;                             // bucket starts
@@ -763,7 +763,7 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
       for (int r0 = tid; r0 <= C; r0 += kB * nt) {
         uint32_t v[kB];
 #pragma unroll
-        for (int e = 0; e < kB; ++e) v[e] = cnt[min(r0 + e * nt, C - 1)];
+        for (int e = 0; e < kB; ++e) v[e] = cnt[min(r0 + e * nt, max(C - 1, 0))];  // (entry 0 when C = 0: unused)
 #pragma unroll
         for (int e = 0; e < kB; ++e) {
           const int r = r0 + e * nt;

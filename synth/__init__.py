@@ -189,7 +189,7 @@ def make_layer(wl: Workload, layer: int = 0, device="cpu", seq_subset=None) -> L
         for g in range(wl.n_kv_heads):
             gen = _gen(sub_seed(wl.wid, b, layer, g), device)
             cen = torch.randn(M, d, generator=gen, device=device)
-            lab = torch.randint(0, M, (n,), generator=gen, device=device)
+            lab = torch.randint(0, max(M, 1), (n,), generator=gen, device=device)  # M = 0 only when n = 0
             k = cen[lab]
             k += wl.noise * torch.randn(n, d, generator=gen, device=device)
             u = torch.rand(n, generator=gen, device=device)

@@ -479,18 +479,20 @@ def test_sparse_target_one_at_128k_matches_dense_and_paged():
     print(f"128k P=1: sparse-dense {float((out - d_tok).abs().max()):.2e}, oracle max-abs {err:.2e}")
 
 
-@pytest.mark.parametrize("case", ["c34000", "big_bucket", "big_cluster"])
+@pytest.mark.parametrize("case", ["c34000", "big_bucket", "big_cluster", "empty_seq"])
 def test_sparse_sort_general_workspace_path(case):
     """Heads that the LDS-piece sort of 8192 < C <= 32768 clusters hands to
     the general workspace path: more than 32768 clusters (34000 clusters of
     about two tokens), a bucket larger than a piece (7000 of 9000 clusters of
     sequence 0 share one centroid, so 7000 equal scores), and a cluster of
     more than 65535 tokens (cluster 0 of every KV head holds 70000 of 90000
-    tokens).  Staged parity on every group at P = 0.9."""
+    tokens); and an empty sequence with no clusters between two of 9000
+    clusters (its heads take no piece and must return zeros).  Staged parity
+    on every group at P = 0.9."""
     import dataclasses
     P = 0.9
     lens, C = {"c34000": ([70000], 34000), "big_bucket": ([20000, 12000], 9000),
-               "big_cluster": ([90000], 9000)}[case]
+               "big_cluster": ([90000], 9000), "empty_seq": ([20000, 0, 12000], 9000)}[case]
     base = _small("ctx32k_llama8b", lens)
     wl = dataclasses.replace(base, fixed_clusters=C, name=f"{base.name}_{case}")
     inp = synth.make_layer(wl, 0)
