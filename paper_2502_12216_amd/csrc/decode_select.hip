@@ -391,17 +391,27 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     }
     __syncthreads();
     total = scan8k_lds(cnt, s_wave_u);  // cnt has no entry C when C == 8192
-    // global results after the last barrier (no barrier waits on these stores)
+    // global results after the last barrier (no barrier waits on these
+    // stores); the LDS reads first, unconditional (every index is inside the
+    // 8192-entry arrays), so that they are in flight together
+    int os[8];
+    uint32_t pv[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      os[e] = ord_s[tid + e * 1024];
+      pv[e] = cnt[tid + e * 1024];
+    }
+    int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int j = tid + e * 1024;
       if (j < C) {
         rank_of[j] = pos[e];
-        order[j] = ord_s[j];
+        order[j] = os[e];
       }
+      if (j <= C) rpre[j] = (int32_t)(j < C ? pv[e] : total);
     }
-    int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
-    for (int r = tid; r <= C; r += nt) rpre[r] = (int32_t)(r < C ? cnt[r] : total);
+    if (tid == 0 && C == kSortLdsBuckets) rpre[C] = (int32_t)total;  // the one entry past the 8192
   } else {
     cnt = a.g_cnt + (int64_t)bh * (a.nb_max + 4);  // per rank: size, then prefix
     ostart = nullptr;                              // the sample rows start from off[order[r]]
@@ -802,7 +812,6 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
   if (C <= 0) return;
   const int64_t N = geo.exact ? n_c : geo.N;
   const int64_t W1 = geo.exact ? 0 : geo.t1 - geo.s1 + 1;
-  auto prefix_at = [&](int r) -> uint32_t { return r < C ? cnt[r] : total; };  // r in [0, C]
   if constexpr (!kLds) {
     // workspace path: every kStr-th prefix entry in LDS (every entry up to
     // kSortWsLdsBytes / 4 clusters; the bucket arrays are dead), a binary
@@ -824,13 +833,15 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     int top = 1;
     while (top * 2 <= nsp) top <<= 1;
     constexpr int kU = 8;  // independent searches in flight per thread
-    for (int64_t u0 = tid; u0 < S_main; u0 += (int64_t)kU * nt) {
-      int64_t iv[kU];
+    // positions and prefixes in 32 bits (a sequence holds fewer than 2^31 tokens)
+    const int N32 = (int)N, NW = (int)(N + W1), s1 = (int)geo.s1, s2 = (int)geo.s2, Sm = (int)S_main;
+    for (int u0 = tid; u0 < Sm; u0 += kU * nt) {
+      uint32_t iv[kU];
       int li[kU];
 #pragma unroll
       for (int k = 0; k < kU; ++k) {
-        const int64_t u = u0 + (int64_t)k * nt;
-        iv[k] = u < N ? u + 1 : (u < N + W1 ? geo.s1 + (u - N) : geo.s2 + (u - N - W1));
+        const int u = u0 + k * nt;
+        iv[k] = (uint32_t)(u < N32 ? u + 1 : (u < NW ? s1 + (u - N32) : s2 + (u - NW)));
         li[k] = 0;
       }
       // largest i with s_pre[i] < position (s_pre[0] = prefix[0] = 0); the
@@ -842,7 +853,7 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
 #pragma unroll
         for (int k = 0; k < kU; ++k) {
           const int t = li[k] + step;
-          li[k] = (t < nsp && (int64_t)pv[k] < iv[k]) ? t : li[k];
+          li[k] = (t < nsp && pv[k] < iv[k]) ? t : li[k];
         }
       }
       // then the largest r in [li * kStr, li * kStr + kStr) with prefix[r] < position
@@ -856,7 +867,7 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
 #pragma unroll
         for (int k = 0; k < kU; ++k) {
           const int t = li[k] * kStr + d;
-          lr[k] = (t < C && (int64_t)pv[k] < iv[k]) ? t : lr[k];
+          lr[k] = (t < C && pv[k] < iv[k]) ? t : lr[k];
         }
       }
       int first[kU];
@@ -869,25 +880,26 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
       }
 #pragma unroll
       for (int k = 0; k < kU; ++k) {
-        const int64_t u = u0 + (int64_t)k * nt;
-        if (u < S_main) {
-          const int32_t row = first[k] + (int32_t)(iv[k] - 1 - (int64_t)pr[k]);
-          rows[u] = min(max(row, 0), n - 1);
-        }
+        const int u = u0 + k * nt;
+        if (u < Sm) rows[u] = min(max(first[k] + (int32_t)(iv[k] - 1 - pr[k]), 0), n - 1);
       }
     }
     return;
   }
   int top = 1;
   while (top * 2 <= C) top <<= 1;
-  constexpr int kU = 4;  // independent searches in flight per thread
-  for (int64_t u0 = tid; u0 < S_main; u0 += (int64_t)kU * nt) {
-    int64_t iv[kU];  // 1-based position in the unpacked list
+  // positions and prefixes in 32 bits (a sequence holds fewer than 2^31
+  // tokens); three searches per thread, which covers the timed shape's 2623
+  // samples in one round
+  constexpr int kU = 3;  // independent searches in flight per thread
+  const int N32 = (int)N, NW = (int)(N + W1), s1 = (int)geo.s1, s2 = (int)geo.s2, Sm = (int)S_main;
+  for (int u0 = tid; u0 < Sm; u0 += kU * nt) {
+    uint32_t iv[kU];  // 1-based position in the unpacked list
     int lr[kU];
 #pragma unroll
     for (int k = 0; k < kU; ++k) {
-      const int64_t u = u0 + (int64_t)k * nt;
-      iv[k] = u < N ? u + 1 : (u < N + W1 ? geo.s1 + (u - N) : geo.s2 + (u - N - W1));
+      const int u = u0 + k * nt;
+      iv[k] = (uint32_t)(u < N32 ? u + 1 : (u < NW ? s1 + (u - N32) : s2 + (u - NW)));
       lr[k] = 0;
     }
     // largest r in [0, C] with prefix[r] < i (prefix[0] = 0 < i); branch-free
@@ -899,18 +911,22 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
 #pragma unroll
       for (int k = 0; k < kU; ++k) {
         const int t = lr[k] + step;
-        const int64_t p = t < C ? (int64_t)pv[k] : (t == C ? (int64_t)total : INT64_MAX);
+        const uint32_t p = t < C ? pv[k] : (t == C ? total : 0xffffffffu);
         lr[k] = p < iv[k] ? t : lr[k];
       }
     }
+    int32_t first[kU];
+    uint32_t pr[kU];
+#pragma unroll
+    for (int k = 0; k < kU; ++k) {  // read together (r < C: C only with offsets that disagree with kv_indptr)
+      const int r = min(lr[k], C - 1);
+      first[k] = ostart[r];
+      pr[k] = cnt[r];
+    }
 #pragma unroll
     for (int k = 0; k < kU; ++k) {
-      const int64_t u = u0 + (int64_t)k * nt;
-      if (u < S_main) {
-        const int r = min(lr[k], C - 1);  // C only with offsets that disagree with kv_indptr
-        const int32_t row = ostart[r] + (int32_t)(iv[k] - 1 - (int64_t)prefix_at(r));
-        rows[u] = min(max(row, 0), n - 1);
-      }
+      const int u = u0 + k * nt;
+      if (u < Sm) rows[u] = min(max(first[k] + (int32_t)(iv[k] - 1 - pr[k]), 0), n - 1);
     }
   }
 }
