@@ -266,30 +266,19 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     constexpr int nb = kSortLdsBuckets;
     // every thread keeps its 8 elements in registers (C <= 8192 = 8 * 1024)
     float v[8];
-    int sz[8], o0[8], bk[8], pos[8];
+    int o0[8], o1[8], bk[8], pos[8];
     // the offsets too are loaded unconditionally, at indices clamped into the
     // (b, g) list, so that all of them are in flight together (a guarded load
-    // whose value is used inside its guard waits there)
-    {
-      int o1[8];
+    // whose value is used inside its guard waits there); they are first used
+    // after the ranking, so their latency hides behind the phases before it
 #pragma unroll
-      for (int e = 0; e < 8; ++e) o0[e] = o1[e] = 0;
-      if (C > 0) {  // uniform: the offsets hold C + 1 entries
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int jc = min(tid + e * 1024, C - 1);
-          o0[e] = off[jc];
-          o1[e] = off[jc + 1];
-        }
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const bool in = tid + e * 1024 < C;
-        v[e] = in ? raw[e] : NAN;
-        sz[e] = in ? o1[e] - o0[e] : 0;
-        o0[e] = in ? o0[e] : 0;
-      }
+    for (int e = 0; e < 8; ++e) {  // the (b, g) list holds C + 1 entries (one when C = 0)
+      const int jc = max(min(tid + e * 1024, C - 1), 0);
+      o0[e] = off[jc];
+      o1[e] = off[min(jc + 1, C)];
     }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = tid + e * 1024 < C ? raw[e] : NAN;
     {
       uint4* c4 = reinterpret_cast<uint4*>(cnt) + tid * 2;
       c4[0] = make_uint4(0, 0, 0, 0);
@@ -384,7 +373,7 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       if (tid + e * 1024 < C) {
-        cnt[pos[e]] = (uint32_t)sz[e];
+        cnt[pos[e]] = (uint32_t)(o1[e] - o0[e]);
         ostart[pos[e]] = o0[e];
         ord_s[pos[e]] = tid + e * 1024;
       }
