@@ -1482,7 +1482,12 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
   __syncthreads();
   const int32_t* off = a.offsets + (int64_t)kvh * (a.Ct + a.B) + cb + b;
   int32_t* ulen = a.union_len + (int64_t)jg * a.Ct + cb;
-  int32_t* Ls = a.Cm <= kUnionLdsMax ? reinterpret_cast<int32_t*>(smem_raw) : ulen;
+  // union lengths in LDS (else in their output array); in LDS one pad entry
+  // follows every 32, so that the threads' contiguous 32-entry segments of
+  // pass 2 start in different banks
+  const bool lds_L = a.Cm <= kUnionLdsMax;
+  int32_t* Ls = lds_L ? reinterpret_cast<int32_t*>(smem_raw) : ulen;
+  auto li = [&](int j) { return lds_L ? j + (j >> 5) : j; };
   // pass 1 (coalesced): selected prefix length of every cluster = max over heads
 #pragma unroll 4
   for (int j = tid; j < C; j += nt) {
@@ -1494,17 +1499,22 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
       const int len = r < s_cut[hh][0] ? size : (r == s_cut[hh][0] ? s_cut[hh][1] : 0);
       L = max(L, len);
     }
-    Ls[j] = L;
+    Ls[li(j)] = L;
     ulen[j] = L;
   }
   __syncthreads();
-  // pass 2: compact the non-empty clusters into ranges (contiguous segment per thread)
+  // pass 2: compact the non-empty clusters into ranges (contiguous segment per
+  // thread), 8 entries per step read together
   const int seg = (C + nt - 1) / nt;
   const int beg = min(C, tid * seg), end = min(C, beg + seg);
   uint64_t loc = 0;  // (ranges << 32) | tokens
-  for (int j = beg; j < end; ++j) {
-    const int L = Ls[j];
-    if (L > 0) loc += (1ull << 32) | (uint64_t)L;
+  for (int j0 = beg; j0 < end; j0 += 8) {
+    int Lv[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) Lv[e] = Ls[li(min(j0 + e, end - 1))];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (j0 + e < end && Lv[e] > 0) loc += (1ull << 32) | (uint64_t)Lv[e];
   }
   uint64_t incl = wave_incl_scan(loc);  // DPP, no LDS
   if (lane == kWave - 1) s_wave_u[wave] = incl;
@@ -1521,17 +1531,30 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
   __syncthreads();
   const uint64_t base = s_wave_u[wave] + incl - loc;
   const uint64_t tot = s_wave_u[16];
-  // position -> range index of the union, one entry per kCfrTokens positions
+  // position -> range index of the union, one entry per kCfrTokens positions;
+  // 8 lengths and cluster starts per step loaded together (union positions
+  // fit 32 bits: a sequence holds fewer than 2^31 tokens)
   int idx = (int)(base >> 32);
-  int64_t upos = (int64_t)(base & 0xffffffffu);
-  for (int j = beg; j < end; ++j) {
-    const int L = Ls[j];
-    if (L <= 0) continue;
-    rstart[idx] = off[j];
-    rupos[idx] = (int32_t)upos;
-    for (int64_t c = (upos + T - 1) / T; c * T < upos + L && c < a.max_chunks; ++c) cfr[c] = idx;
-    ++idx;
-    upos += L;
+  int upos = (int)(base & 0xffffffffu);
+  const int mc = (int)min((int64_t)a.max_chunks, (int64_t)INT32_MAX), Ti = (int)T;
+  for (int j0 = beg; j0 < end; j0 += 8) {
+    int Lv[8], ov[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int jj = min(j0 + e, end - 1);
+      Lv[e] = Ls[li(jj)];
+      ov[e] = off[jj];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      if (j0 + e < end && Lv[e] > 0) {
+        rstart[idx] = ov[e];
+        rupos[idx] = upos;
+        for (int c = (upos + Ti - 1) / Ti; c * Ti < upos + Lv[e] && c < mc; ++c) cfr[c] = idx;
+        ++idx;
+        upos += Lv[e];
+      }
+    }
   }
   if (tid == 0) union_close(a, bg, b, kvh, n_c, tail, tot, rstart, rupos, cfr);
 }
@@ -1570,7 +1593,7 @@ hipError_t launch_sample(const FitArgs& a, int split, int n_heads, bool paged, h
 hipError_t launch_fit_union(const FitArgs& a, int G, int n_groups, hipStream_t st) {
   const int64_t Cp = (a.Cm + kUnionSeg - 1) / kUnionSeg * kUnionSeg;
   const size_t lds = union_staged(G, a.Cm) ? (size_t)(G * Cp * 2 + (Cp + 4) * 4 + Cp * 4)
-                                           : (a.Cm <= kUnionLdsMax ? (size_t)a.Cm * 4 : 0);
+                                           : (a.Cm <= kUnionLdsMax ? (size_t)(a.Cm + a.Cm / 32 + 1) * 4 : 0);
   switch (G) {
     case 1: hipLaunchKernelGGL(fit_union_kernel<1>, dim3(n_groups), dim3(1024), lds, st, a); break;
     case 2: hipLaunchKernelGGL(fit_union_kernel<2>, dim3(n_groups), dim3(1024), lds, st, a); break;
