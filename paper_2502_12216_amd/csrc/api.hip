@@ -357,6 +357,7 @@ static tactic_status sparse_decode_impl(const uint16_t* q, const uint16_t* K_sor
   fa.sample_rows = so.sample_rows;
   fa.rprefix = so.rprefix;
   fa.rank_of = so.rank_of;
+  fa.order = so.order;
   fa.logits = reinterpret_cast<double*>(ws + p.off_logit);
   fa.fit = reinterpret_cast<double*>(ws + p.off_fit);
   fa.lse = reinterpret_cast<double*>(ws + p.off_lse);

@@ -863,9 +863,17 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
       uint32_t pr[kU];
 #pragma unroll
       for (int k = 0; k < kU; ++k) {
-        const int r = min(lr[k], C - 1);
-        first[k] = off[order[r]];
-        pr[k] = kStr == 1 ? s_pre[r] : cnt[r];
+        lr[k] = min(lr[k], C - 1);
+        first[k] = off[order[lr[k]]];
+      }
+      // the rank's prefix from LDS when every entry is there (kept apart from
+      // the memory read so that each compiles to its own instruction kind)
+      if (kStr == 1) {
+#pragma unroll
+        for (int k = 0; k < kU; ++k) pr[k] = s_pre[lr[k]];
+      } else {
+#pragma unroll
+        for (int k = 0; k < kU; ++k) pr[k] = cnt[lr[k]];
       }
 #pragma unroll
       for (int k = 0; k < kU; ++k) {
@@ -1478,81 +1486,294 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
     return;
   }
 
-  if (wave < G) fit_head_wave(a, h0 + wave, lane, s_cut[wave]);
-  __syncthreads();
   const int32_t* off = a.offsets + (int64_t)kvh * (a.Ct + a.B) + cb + b;
   int32_t* ulen = a.union_len + (int64_t)jg * a.Ct + cb;
-  // union lengths in LDS (else in their output array); in LDS one pad entry
-  // follows every 32, so that the threads' contiguous 32-entry segments of
-  // pass 2 start in different banks
-  const bool lds_L = a.Cm <= kUnionLdsMax;
-  int32_t* Ls = lds_L ? reinterpret_cast<int32_t*>(smem_raw) : ulen;
-  auto li = [&](int j) { return lds_L ? j + (j >> 5) : j; };
-  // pass 1 (coalesced): selected prefix length of every cluster = max over heads
-#pragma unroll 4
-  for (int j = tid; j < C; j += nt) {
-    const int size = off[j + 1] - off[j];
-    int L = 0;
-#pragma unroll
-    for (int hh = 0; hh < G; ++hh) {
-      const int r = a.rank_of[(int64_t)(h0 + hh) * a.Cm + j];
-      const int len = r < s_cut[hh][0] ? size : (r == s_cut[hh][0] ? s_cut[hh][1] : 0);
-      L = max(L, len);
-    }
-    Ls[li(j)] = L;
-    ulen[j] = L;
-  }
-  __syncthreads();
-  // pass 2: compact the non-empty clusters into ranges (contiguous segment per
-  // thread), 8 entries per step read together
-  const int seg = (C + nt - 1) / nt;
-  const int beg = min(C, tid * seg), end = min(C, beg + seg);
-  uint64_t loc = 0;  // (ranges << 32) | tokens
-  for (int j0 = beg; j0 < end; j0 += 8) {
-    int Lv[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) Lv[e] = Ls[li(min(j0 + e, end - 1))];
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      if (j0 + e < end && Lv[e] > 0) loc += (1ull << 32) | (uint64_t)Lv[e];
-  }
-  uint64_t incl = wave_incl_scan(loc);  // DPP, no LDS
-  if (lane == kWave - 1) s_wave_u[wave] = incl;
-  __syncthreads();
-  if (tid == 0) {
-    uint64_t run = 0;
-    for (int w = 0; w < nt / kWave; ++w) {
-      const uint64_t t = s_wave_u[w];
-      s_wave_u[w] = run;
-      run += t;
-    }
-    s_wave_u[16] = run;
-  }
-  __syncthreads();
-  const uint64_t base = s_wave_u[wave] + incl - loc;
-  const uint64_t tot = s_wave_u[16];
-  // position -> range index of the union, one entry per kCfrTokens positions;
-  // 8 lengths and cluster starts per step loaded together (union positions
-  // fit 32 bits: a sequence holds fewer than 2^31 tokens)
-  int idx = (int)(base >> 32);
-  int upos = (int)(base & 0xffffffffu);
   const int mc = (int)min((int64_t)a.max_chunks, (int64_t)INT32_MAX), Ti = (int)T;
-  for (int j0 = beg; j0 < end; j0 += 8) {
-    int Lv[8], ov[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int jj = min(j0 + e, end - 1);
-      Lv[e] = Ls[li(jj)];
-      ov[e] = off[jj];
+  uint64_t tot;  // (ranges << 32) | tokens of the clustered union
+  // exclusive block scan of (ranges << 32) | tokens: DPP within the wave,
+  // then the wave totals; returns the thread's base and sets tot
+  auto block_scan = [&](uint64_t loc) {
+    const uint64_t incl = wave_incl_scan(loc);
+    if (lane == kWave - 1) s_wave_u[wave] = incl;
+    __syncthreads();
+    if (tid == 0) {
+      uint64_t run = 0;
+      for (int w = 0; w < nt / kWave; ++w) {
+        const uint64_t t = s_wave_u[w];
+        s_wave_u[w] = run;
+        run += t;
+      }
+      s_wave_u[16] = run;
     }
+    __syncthreads();
+    tot = s_wave_u[16];
+    return s_wave_u[wave] + incl - loc;
+  };
+
+  if (a.Cm <= kUnionLdsMax) {
+    // One workgroup per group runs every pass here, so the passes are kept
+    // short in instructions per cluster. LDS holds the cluster offsets (one
+    // pad entry after every 32, so that the threads' 32-entry segments start
+    // in different banks), their top bit set for clusters some head takes
+    // whole; later each cluster's union length or position. With many
+    // ranges: per 32 clusters a bit per non-empty cluster and the count of
+    // non-empty clusters before them.
+    static_assert(kUnionLdsMax <= 32 * 1024, "one 32-cluster segment per thread");
+    const int Cp = (a.Cm + 31) / 32 * 32;                      // whole segments
+    int32_t* const Lo = reinterpret_cast<int32_t*>(smem_raw);  // [Cp + Cp / 32 + 1]
+    auto li = [](int j) { return j + (j >> 5); };
+    uint32_t* s_nz = reinterpret_cast<uint32_t*>(Lo + Cp + Cp / 32 + 1);  // [Cp / 32]
+    int32_t* s_wb = reinterpret_cast<int32_t*>(s_nz + Cp / 32);           // [Cp / 32]
+    __shared__ int s_cutj[G];                                                  // cut cluster, -1: none
+    if (wave < G) {
+      fit_head_wave(a, h0 + wave, lane, s_cut[wave]);
+      if (lane == 0) s_cutj[wave] = -1;
+    } else {
+      // offsets 0 .. C into LDS while the fit runs (8 per thread and step loaded together)
+      constexpr int nw = 1024 - G * kWave;
+      const int w = tid - G * kWave;
+      for (int k0 = 0; k0 * nw <= C; k0 += 8) {
+        int o[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      if (j0 + e < end && Lv[e] > 0) {
-        rstart[idx] = ov[e];
-        rupos[idx] = upos;
-        for (int c = (upos + Ti - 1) / Ti; c * Ti < upos + Lv[e] && c < mc; ++c) cfr[c] = idx;
-        ++idx;
-        upos += Lv[e];
+        for (int e = 0; e < 8; ++e) o[e] = off[min((k0 + e) * nw + w, C)];
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if ((k0 + e) * nw + w <= C) Lo[li((k0 + e) * nw + w)] = o[e];
+      }
+    }
+    __syncthreads();
+    {
+      // marks: every head's clusters ranked before its cut (its first
+      // cut-rank entries of the sort order) get the top bit, and the cut
+      // cluster is noted; the heads' entries taken as one list, 8 per thread
+      // and step loaded together
+      int pre[G + 1];
+      pre[0] = 0;
+#pragma unroll
+      for (int hh = 0; hh < G; ++hh) {
+        const int c0 = s_cut[hh][0];
+        pre[hh + 1] = pre[hh] + (c0 < C ? c0 + 1 : C);  // c0 = -1: no cluster
+      }
+      const int NR = pre[G];
+      auto head_of = [&](int t) {
+        int hh = 0;
+#pragma unroll
+        for (int k = 1; k < G; ++k) hh += t >= pre[k] ? 1 : 0;
+        return hh;
+      };
+      for (int t0 = 0; t0 < NR; t0 += 8 * nt) {
+        int jv[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int t = min(t0 + e * nt + tid, NR - 1);
+          const int hh = head_of(t);
+          jv[e] = a.order[(int64_t)(h0 + hh) * a.Cm + (t - pre[hh])];
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int t = t0 + e * nt + tid;
+          if (t < NR) {
+            const int hh = head_of(t);
+            if (t - pre[hh] == s_cut[hh][0]) s_cutj[hh] = jv[e];
+            else atomicOr(reinterpret_cast<unsigned int*>(Lo) + li(jv[e]), 0x80000000u);
+          }
+        }
+      }
+    }
+    __syncthreads();
+    // segments of 32 clusters (C <= 32 * 1024): union length = the size for
+    // a marked cluster, at least the cut length at a head's cut cluster
+    constexpr int kSeg = 32;
+    const int beg = tid * kSeg;
+    int L[kSeg];
+    uint64_t loc = 0;  // (ranges << 32) | tokens
+    if (beg < C) {
+      int o[kSeg + 1];
+#pragma unroll
+      for (int e = 0; e <= kSeg; ++e) o[e] = Lo[li(min(beg + e, C))];
+#pragma unroll
+      for (int e = 0; e < kSeg; ++e) {
+        L[e] = (o[e] < 0 && beg + e < C) ? (o[e + 1] & 0x7fffffff) - (o[e] & 0x7fffffff) : 0;
+        loc += L[e];
+      }
+      bool has_cut = false;
+#pragma unroll
+      for (int hh = 0; hh < G; ++hh) has_cut |= (unsigned)(s_cutj[hh] - beg) < (unsigned)kSeg;
+      if (has_cut) {
+        loc = 0;
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) {
+          const int cj = s_cutj[hh], cl = s_cut[hh][1];
+#pragma unroll
+          for (int e = 0; e < kSeg; ++e)
+            if (beg + e == cj) L[e] = max(L[e], cl);
+        }
+#pragma unroll
+        for (int e = 0; e < kSeg; ++e) loc += L[e];
+      }
+      int nr = 0;
+#pragma unroll
+      for (int e = 0; e < kSeg; ++e) nr += L[e] > 0 ? 1 : 0;
+      loc |= (uint64_t)nr << 32;
+    }
+    const uint64_t base = block_scan(loc);
+    // few ranges (the common case with this many clusters): each thread
+    // writes its segment's ranges, scattered across the lanes but rare;
+    // else a coalesced pass writes them, neighbouring lanes writing
+    // neighbouring ranges
+    const bool few = (tot >> 32) * 8 <= (uint64_t)C;
+    if (beg < C) {
+      int idx = (int)(base >> 32), upos = (int)(base & 0xffffffffu);
+      if (few) {
+        // each cluster's union length replaces its offset (the last segment
+        // also writes entries past C, which nothing reads); a non-empty
+        // cluster's range and the position -> range index, one entry per
+        // kCfrTokens positions
+#pragma unroll
+        for (int e0 = 0; e0 < kSeg; e0 += 8) {
+          int o[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = Lo[li(beg + e0 + e)];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int Le = L[e0 + e];
+            Lo[li(beg + e0 + e)] = Le;
+            if (Le > 0) {
+              rstart[idx] = o[e] & 0x7fffffff;
+              rupos[idx] = upos;
+              for (int c = (upos + Ti - 1) / Ti; c * Ti < upos + Le && c < mc; ++c) cfr[c] = idx;
+              ++idx;
+            }
+            upos += Le;
+          }
+        }
+      } else {
+        // each cluster's union position replaces its offset (the last
+        // segment writes C's entry, the total, and entries past it, which
+        // nothing reads); the segment's non-empty bits and the range count
+        // before it
+        uint32_t nzb = 0;
+#pragma unroll
+        for (int e = 0; e < kSeg; ++e) {
+          Lo[li(beg + e)] = upos;
+          upos += L[e];
+          nzb |= (L[e] > 0 ? 1u : 0u) << e;
+        }
+        s_nz[tid] = nzb;
+        s_wb[tid] = idx;
+      }
+    }
+    if (!few && tid == 0 && (C & 31) == 0) Lo[li(C)] = (int)(tot & 0xffffffffu);  // no segment holds C
+    __syncthreads();
+    if (few) {
+      // union lengths out (coalesced)
+      for (int k0 = 0; k0 * nt < C; k0 += 8) {
+        int v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = Lo[li(min((k0 + e) * nt + tid, C - 1))];
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if ((k0 + e) * nt + tid < C) ulen[(k0 + e) * nt + tid] = v[e];
+      }
+    } else {
+      // coalesced: union lengths out, and per non-empty cluster its range
+      // (index = non-empty clusters before it) and the position -> range
+      // index; the cluster starts are loaded with the step's LDS reads, so
+      // that no load waits behind the stores
+      for (int k0 = 0; k0 * nt < C; k0 += 4) {
+        int u0[4], u1[4], wb[4], ov[4];
+        uint32_t m[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int jj = min((k0 + e) * nt + tid, C - 1);
+          ov[e] = off[jj];
+          u0[e] = Lo[li(jj)];
+          u1[e] = Lo[li(jj + 1)];
+          m[e] = s_nz[jj >> 5];
+          wb[e] = s_wb[jj >> 5];
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int j = (k0 + e) * nt + tid;
+          const int Lj = u1[e] - u0[e];
+          if (j < C) {
+            ulen[j] = Lj;
+            if (Lj > 0) {
+              const int r = wb[e] + __popc(m[e] & ((1u << (j & 31)) - 1u));
+              rstart[r] = ov[e];
+              rupos[r] = u0[e];
+              for (int c = (u0[e] + Ti - 1) / Ti; c * Ti < u0[e] + Lj && c < mc; ++c) cfr[c] = r;
+            }
+          }
+        }
+      }
+    }
+  } else {
+    if (wave < G) fit_head_wave(a, h0 + wave, lane, s_cut[wave]);
+    __syncthreads();
+    // pass 1 (coalesced, kB clusters per thread and step loaded together at
+    // clamped indices): selected prefix length of every cluster = max over
+    // heads, into the union-length output
+    constexpr int kB = G >= 8 ? 4 : 8;
+    for (int k0 = 0; k0 * nt < C; k0 += kB) {
+      int o0[kB], o1[kB], rk[kB][G];
+#pragma unroll
+      for (int e = 0; e < kB; ++e) {
+        const int jj = min((k0 + e) * nt + tid, C - 1);
+        o0[e] = off[jj];
+        o1[e] = off[jj + 1];
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) rk[e][hh] = a.rank_of[(int64_t)(h0 + hh) * a.Cm + jj];
+      }
+#pragma unroll
+      for (int e = 0; e < kB; ++e) {
+        const int j = (k0 + e) * nt + tid;
+        const int size = o1[e] - o0[e];
+        int L = 0;
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) {
+          const int r = rk[e][hh];
+          L = max(L, r < s_cut[hh][0] ? size : (r == s_cut[hh][0] ? s_cut[hh][1] : 0));
+        }
+        if (j < C) ulen[j] = L;
+      }
+    }
+    __syncthreads();
+    // pass 2: compact the non-empty clusters into ranges (contiguous segment
+    // per thread), 8 entries per step read together
+    const int seg = (C + nt - 1) / nt;
+    const int beg = min(C, tid * seg), end = min(C, beg + seg);
+    uint64_t loc = 0;  // (ranges << 32) | tokens
+    for (int j0 = beg; j0 < end; j0 += 8) {
+      int Lv[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) Lv[e] = ulen[min(j0 + e, end - 1)];
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (j0 + e < end && Lv[e] > 0) loc += (1ull << 32) | (uint64_t)Lv[e];
+    }
+    const uint64_t base = block_scan(loc);
+    // the thread writes its own segment's ranges, 8 lengths and cluster
+    // starts per step loaded together (union positions fit 32 bits: a
+    // sequence holds fewer than 2^31 tokens)
+    int idx = (int)(base >> 32), upos = (int)(base & 0xffffffffu);
+    for (int j0 = beg; j0 < end; j0 += 8) {
+      int Lv[8], ov[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int jj = min(j0 + e, end - 1);
+        Lv[e] = ulen[jj];
+        ov[e] = off[jj];
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        if (j0 + e < end && Lv[e] > 0) {
+          rstart[idx] = ov[e];
+          rupos[idx] = upos;
+          for (int c = (upos + Ti - 1) / Ti; c * Ti < upos + Lv[e] && c < mc; ++c) cfr[c] = idx;
+          ++idx;
+          upos += Lv[e];
+        }
       }
     }
   }
@@ -1592,8 +1813,9 @@ hipError_t launch_sample(const FitArgs& a, int split, int n_heads, bool paged, h
 
 hipError_t launch_fit_union(const FitArgs& a, int G, int n_groups, hipStream_t st) {
   const int64_t Cp = (a.Cm + kUnionSeg - 1) / kUnionSeg * kUnionSeg;
+  const int64_t C32 = (a.Cm + 31) / 32 * 32;
   const size_t lds = union_staged(G, a.Cm) ? (size_t)(G * Cp * 2 + (Cp + 4) * 4 + Cp * 4)
-                                           : (a.Cm <= kUnionLdsMax ? (size_t)(a.Cm + a.Cm / 32 + 1) * 4 : 0);
+                                           : (a.Cm <= kUnionLdsMax ? (size_t)(C32 + 3 * (C32 / 32) + 1) * 4 : 0);
   switch (G) {
     case 1: hipLaunchKernelGGL(fit_union_kernel<1>, dim3(n_groups), dim3(1024), lds, st, a); break;
     case 2: hipLaunchKernelGGL(fit_union_kernel<2>, dim3(n_groups), dim3(1024), lds, st, a); break;

@@ -109,6 +109,7 @@ struct FitArgs {
   const int32_t* sample_rows;
   const int32_t* rprefix;
   const int32_t* rank_of;
+  const int32_t* order;       // [B*Hq][Cm]: cluster at each rank
   double* logits;             // [B*Hq][S_cap]
   double* lse;                // [B*Hq][split][4 regions][max, sum exp(l - max)]
   double* fit;                // [B*Hq][16]
