@@ -131,19 +131,18 @@ __global__ __launch_bounds__(256) void km_init_kernel(KmArgs a) {
 // (two 32-token MFMA B operands held in registers for the whole pass);
 // centroids stream through LDS 64 at a time as the A operand, each tile
 // loaded into registers while the one before it is contracted.  The nearest
-// centroid maximises s = k.c - ||c||^2 / 2; the -||c||^2 / 2 term enters the
-// contraction as one more K step (the A operand holds it split into two bf16
-// parts, hi + lo, within about 2^-17 of the fp32 value; the B operand holds
-// ones there), so the epilogue reads finished scores: a 3-input max over each
-// lane's 16 scores of a block, and the search for the row that holds it only
-// when some lane of the wave improved on its best (strict, so the smaller
-// centroid id wins a tie).
+// centroid maximises s = k.c - ||c||^2 / 2; the accumulators of a block start
+// at the fp32 -||c||^2 / 2 of their centroid row, so the contraction ends on
+// finished scores and the epilogue is a 3-input max over each lane's 16
+// scores of a block, and the search for the row that holds it only when some
+// lane of the wave improved on its best (strict, so the smaller centroid id
+// wins a tie).
 // ---------------------------------------------------------------------------
 // three waves per SIMD: the accumulators then live in VGPRs next to the
 // prefetched tile, without spills
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void km_assign_kernel(KmArgs a) {
   __shared__ __align__(16) uint16_t s_c[kAsgCen * kLdsRow];
-  __shared__ uint32_t s_hl[kAsgCen];  // bf16 pair (hi, lo) of -||c||^2 / 2
+  __shared__ __align__(16) float s_nh[kAsgCen];  // -||c||^2 / 2 (-inf past the last centroid)
   const int p = blockIdx.y;
   if (a.done[p]) return;
   const Problem q = problem(a, p);
@@ -164,9 +163,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
       bt[bb][s] = __builtin_bit_cast(bf16x8, v);
     }
   }
-  // the extra K step: ones against (hi, lo) in the first two K slots of the
-  // lanes of half 0, zeros elsewhere
-  const bf16x8 ones = __builtin_bit_cast(bf16x8, half == 0 ? make_uint4(0x3F803F80u, 0, 0, 0) : make_uint4(0, 0, 0, 0));
   float best_v[2] = {-INFINITY, -INFINITY};
   int best_j[2] = {0x7fffffff, 0x7fffffff};
   const uint16_t* cbase = a.centroids + q.cl_base * kHeadDim;
@@ -191,32 +187,27 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
       const int idx = tid + 256 * k, row = idx >> 4, pc = idx & 15;
       *reinterpret_cast<uint4*>(s_c + row * kLdsRow + pc * 8) = pf[k];
     }
-    if (tid < kAsgCen) {
-      uint32_t hl = 0xFF80u;  // rows past the last centroid score -inf (hi = -inf, zero data)
-      if (c0 + tid < q.C) {
-        const float x = -0.5f * pfn;
-        const uint16_t hi = f32_to_bf16_rne(x);
-        hl = (uint32_t)hi | ((uint32_t)f32_to_bf16_rne(x - bf16lo(hi)) << 16);
-      }
-      s_hl[tid] = hl;
-    }
+    if (tid < kAsgCen) s_nh[tid] = c0 + tid < q.C ? -0.5f * pfn : -INFINITY;  // rows past C hold zero data
     __syncthreads();
     if (c0 + kAsgCen < q.C) fetch(c0 + kAsgCen);
     const int nblk = min(kAsgCen / 32, (q.C - c0 + 31) / 32);
     for (int cb = 0; cb < nblk; ++cb) {
-      f32x16 acc[2] = {{}, {}};
+      // accumulator i of a lane is row 8 (i / 4) + 4 half + i % 4 of the block
+      f32x16 acc[2];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float4 x = *reinterpret_cast<const float4*>(s_nh + cb * 32 + 8 * k + 4 * half);
+        acc[0][4 * k] = acc[1][4 * k] = x.x;
+        acc[0][4 * k + 1] = acc[1][4 * k + 1] = x.y;
+        acc[0][4 * k + 2] = acc[1][4 * k + 2] = x.z;
+        acc[0][4 * k + 3] = acc[1][4 * k + 3] = x.w;
+      }
       const uint16_t* arow = s_c + (cb * 32 + col) * kLdsRow + 64 * half;
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
         const bf16x8 av = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(arow + 8 * s));
         acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bt[0][s], acc[0], 0, 0, 0);
         acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bt[1][s], acc[1], 0, 0, 0);
-      }
-      {
-        const uint32_t hl = half == 0 ? s_hl[cb * 32 + col] : 0u;
-        const bf16x8 av = __builtin_bit_cast(bf16x8, make_uint4(hl, 0, 0, 0));
-        acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, ones, acc[0], 0, 0, 0);
-        acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, ones, acc[1], 0, 0, 0);
       }
 #pragma unroll
       for (int bb = 0; bb < 2; ++bb) {
