@@ -883,8 +883,12 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     }
     return;
   }
+  // the prefix array holds the total at every rank from C to 8191 (those
+  // ranks have size 0), so steps from 4096 down never leave it and need no
+  // clamp or end case: every entry there is >= any position searched
   int top = 1;
   while (top * 2 <= C) top <<= 1;
+  top = min(top, kSortLdsBuckets / 2);
   // positions and prefixes in 32 bits (a sequence holds fewer than 2^31
   // tokens); three searches per thread, which covers the timed shape's 2623
   // samples in one round
@@ -899,18 +903,14 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
       iv[k] = (uint32_t)(u < N32 ? u + 1 : (u < NW ? s1 + (u - N32) : s2 + (u - NW)));
       lr[k] = 0;
     }
-    // largest r in [0, C] with prefix[r] < i (prefix[0] = 0 < i); branch-free
+    // largest r in [0, C) with prefix[r] < i (prefix[0] = 0 < i); branch-free
     // so that the kU lookups of a step are in flight together
     for (int step = top; step > 0; step >>= 1) {
       uint32_t pv[kU];
 #pragma unroll
-      for (int k = 0; k < kU; ++k) pv[k] = cnt[min(lr[k] + step, C - 1)];
+      for (int k = 0; k < kU; ++k) pv[k] = cnt[lr[k] + step];
 #pragma unroll
-      for (int k = 0; k < kU; ++k) {
-        const int t = lr[k] + step;
-        const uint32_t p = t < C ? pv[k] : (t == C ? total : 0xffffffffu);
-        lr[k] = p < iv[k] ? t : lr[k];
-      }
+      for (int k = 0; k < kU; ++k) lr[k] = pv[k] < iv[k] ? lr[k] + step : lr[k];
     }
     int32_t first[kU];
     uint32_t pr[kU];
