@@ -521,25 +521,28 @@ def test_sparse_union_range_writers(Hq, Hkv):
     one of two ways: from each thread's 32-cluster segment when at most an
     eighth of the clusters are non-empty, else in a coalesced pass over the
     clusters. 9000 clusters of about two tokens at a low and a high target
-    cover both (asserted from the union lengths), with staged parity on every
-    group."""
+    cover both (asserted from the union lengths), in union and per-head modes
+    and with 300 recent tokens after the clusters of sequence 0 (their range
+    follows the clusters' ranges), with staged parity on every group."""
     import dataclasses
+    T = _tactic()
     base = _small("ctx32k_llama8b", [20000, 12000])
     wl = dataclasses.replace(base, n_q_heads=Hq, n_kv_heads=Hkv, fixed_clusters=9000,
                              name=f"{base.name}_c9000_h{Hq}x{Hkv}")
     inp = synth.make_layer(wl, 0)
-    lay = synth.label_layout(inp)
-    seen = set()
-    for P in (0.3, 0.99):
-        res = run_sparse(inp, lay, P)
-        check_layer(inp, lay, P, res, label=f"range writers G={Hq // Hkv} P={P}")
-        ulen = res["view"]["union_len"]
-        for b in range(len(wl.seq_lens)):
-            c0, c1 = int(lay.cl_indptr[b]), int(lay.cl_indptr[b + 1])
-            for g in range(Hkv):
-                nz = int((ulen[g, c0:c1] > 0).sum())
-                seen.add("segment" if nz * 8 <= c1 - c0 else "coalesced")
-    assert seen == {"segment", "coalesced"}, seen
+    lay = synth.label_layout(inp, tail=[300, 0])
+    for union in (1, 0):
+        seen = set()
+        for P in (0.3, 0.99):
+            res = run_sparse(inp, lay, P, T.decode_params(P, use_union=union, max_tail=512))
+            check_layer(inp, lay, P, res, label=f"range writers G={Hq // Hkv} union={union} P={P}")
+            ulen = res["view"]["union_len"]
+            for b in range(len(wl.seq_lens)):
+                c0, c1 = int(lay.cl_indptr[b]), int(lay.cl_indptr[b + 1])
+                for row in range(Hkv if union else Hq):  # one row per selection group
+                    nz = int((ulen[row, c0:c1] > 0).sum())
+                    seen.add("segment" if nz * 8 <= c1 - c0 else "coalesced")
+        assert seen == {"segment", "coalesced"}, (union, seen)
 
 
 @pytest.mark.parametrize("P", [0.5, 0.9])
