@@ -545,6 +545,27 @@ def test_sparse_union_range_writers(Hq, Hkv):
         assert seen == {"segment", "coalesced"}, (union, seen)
 
 
+@pytest.mark.parametrize("case", ["pieces", "workspace"])
+def test_sparse_large_sort_paths_with_recent_tail(case):
+    """Recent tokens after the clusters on the sorts of more than 8192
+    clusters: 12000 clusters (LDS pieces) and 34000 clusters (workspace
+    path), with a tail of 200 and 150 tokens on the first sequence (its
+    sampled rows follow the windows', its range follows the union's), in
+    union and per-head modes, staged parity on every group at P = 0.9."""
+    import dataclasses
+    T = _tactic()
+    P = 0.9
+    lens, C, tail = {"pieces": ([30000, 12000], 12000, [200, 0]), "workspace": ([70000], 34000, [150])}[case]
+    base = _small("ctx32k_llama8b", lens)
+    wl = dataclasses.replace(base, fixed_clusters=C, name=f"{base.name}_{case}_tail")
+    inp = synth.make_layer(wl, 0)
+    lay = synth.label_layout(inp, tail=tail)
+    for union in (1, 0):
+        res = run_sparse(inp, lay, P, T.decode_params(P, use_union=union, max_tail=256))
+        st = check_layer(inp, lay, P, res, label=f"{case} tail union={union}")
+        print(f"{case} tail union={union}: k={[s['k'] for s in st][:2]}")
+
+
 @pytest.mark.parametrize("P", [0.5, 0.9])
 def test_sparse_degenerate_scores_out_of_lds_sort(P):
     """The sort of more than 8192 clusters per head runs out of the
