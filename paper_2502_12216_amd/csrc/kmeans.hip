@@ -32,8 +32,7 @@ constexpr int kKmTile = 2048;       // tokens per counting tile
 constexpr int kKmChunk = 16384;     // table entries per scan chunk
 constexpr int kKmMaxIters = 1000;
 constexpr int kAsgTok = 256;        // tokens per assignment workgroup (4 waves x 64)
-constexpr int kAsgCen = 64;         // centroids staged in LDS per step
-constexpr int kLdsRow = kHeadDim + 8;  // padded LDS row (bf16): 272 bytes, 2-way bank conflicts
+constexpr int kAsgCen = 96;         // centroids staged in LDS per step
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -129,8 +128,9 @@ __global__ __launch_bounds__(256) void km_init_kernel(KmArgs a) {
 // ---------------------------------------------------------------------------
 // assignment: grid (ceil(nmax/256), BG), 256 threads.  A wave owns 64 tokens
 // (two 32-token MFMA B operands held in registers for the whole pass);
-// centroids stream through LDS 64 at a time as the A operand, each tile
-// loaded into registers while the one before it is contracted.  The nearest
+// centroids stream through LDS 96 at a time as the A operand, each tile
+// loaded from memory straight into the other of two LDS buffers while the
+// one before it is contracted (one barrier per tile).  The nearest
 // centroid maximises s = k.c - ||c||^2 / 2; the accumulators of a block start
 // at the fp32 -||c||^2 / 2 of their centroid row, so the contraction ends on
 // finished scores and the epilogue is a 3-input max over each lane's 16
@@ -138,11 +138,16 @@ __global__ __launch_bounds__(256) void km_init_kernel(KmArgs a) {
 // lane of the wave improved on its best (strict, so the smaller centroid id
 // wins a tie).
 // ---------------------------------------------------------------------------
-// three waves per SIMD: the accumulators then live in VGPRs next to the
-// prefetched tile, without spills
+// three waves per SIMD: the B operands and accumulators live in VGPRs (a
+// few registers of the unrolled tile staging spill; rolling that loop to
+// avoid it was slower)
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void km_assign_kernel(KmArgs a) {
-  __shared__ __align__(16) uint16_t s_c[kAsgCen * kLdsRow];
-  __shared__ __align__(16) float s_nh[kAsgCen];  // -||c||^2 / 2 (-inf past the last centroid)
+  // two centroid tiles (the next one loads while this one is contracted):
+  // rows of 16 chunks of 16 bytes, logical chunk c of row r stored at chunk
+  // c ^ (r & 15), so that the 32 rows an A-operand read touches at one
+  // logical chunk fall in distinct LDS bank groups
+  __shared__ __align__(16) uint16_t s_c[2][kAsgCen * kHeadDim];
+  __shared__ __align__(16) float s_nh[2][kAsgCen];  // -||c||^2 / 2 (-inf past the last centroid)
   const int p = blockIdx.y;
   if (a.done[p]) return;
   const Problem q = problem(a, p);
@@ -166,46 +171,47 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
   float best_v[2] = {-INFINITY, -INFINITY};
   int best_j[2] = {0x7fffffff, 0x7fffffff};
   const uint16_t* cbase = a.centroids + q.cl_base * kHeadDim;
-  // the next tile's centroids and norms load during this tile's contraction
-  constexpr int kPieces = kAsgCen * 16 / 256;  // 16-byte pieces per thread
-  uint4 pf[kPieces];
-  float pfn = 0.f;
-  auto fetch = [&](int c0) {
+  // a tile goes from memory straight to LDS (no registers): each wave moves
+  // four blocks of 64 chunks; lane L of block blk fills stored chunk
+  // blk * 64 + L, i.e. row (blk * 64 + L) / 16, with the row's logical chunk
+  // that the swizzle puts there; rows past C load a valid row (their scores
+  // are -inf through the norm term)
+  auto stage = [&](int c0, int buf) {
 #pragma unroll
-    for (int k = 0; k < kPieces; ++k) {
-      const int idx = tid + 256 * k, row = idx >> 4, pc = idx & 15;
-      pf[k] = c0 + row < q.C ? *reinterpret_cast<const uint4*>(cbase + (int64_t)(c0 + row) * kHeadDim + pc * 8)
-                             : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < kAsgCen * 16 / 256; ++i) {
+      const int blk = wave * (kAsgCen * 16 / 256) + i, qq = blk * 64 + lane, row = qq >> 4;
+      const int grow = min(c0 + row, q.C - 1);
+      __builtin_amdgcn_global_load_lds(cbase + (int64_t)grow * kHeadDim + ((qq & 15) ^ (row & 15)) * 8,
+                                       (__attribute__((address_space(3))) void*)(s_c[buf] + blk * 512), 16, 0, 0);
     }
-    if (tid < kAsgCen && c0 + tid < q.C) pfn = a.cnorm[q.cl_base + c0 + tid];
   };
-  fetch(0);
-  for (int c0 = 0; c0 < q.C; c0 += kAsgCen) {
-    __syncthreads();
-#pragma unroll
-    for (int k = 0; k < kPieces; ++k) {
-      const int idx = tid + 256 * k, row = idx >> 4, pc = idx & 15;
-      *reinterpret_cast<uint4*>(s_c + row * kLdsRow + pc * 8) = pf[k];
+  float pfn = (tid < kAsgCen && tid < q.C) ? a.cnorm[q.cl_base + tid] : 0.f;
+  if (q.C > 0) stage(0, 0);
+  int buf = 0;
+  for (int c0 = 0; c0 < q.C; c0 += kAsgCen, buf ^= 1) {
+    if (tid < kAsgCen) s_nh[buf][tid] = c0 + tid < q.C ? -0.5f * pfn : -INFINITY;
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's tile loads have reached LDS
+    __syncthreads();  // every wave's part of the tile and the norms in place; the other buffer free
+    if (c0 + kAsgCen < q.C) {
+      stage(c0 + kAsgCen, buf ^ 1);
+      if (tid < kAsgCen && c0 + kAsgCen + tid < q.C) pfn = a.cnorm[q.cl_base + c0 + kAsgCen + tid];
     }
-    if (tid < kAsgCen) s_nh[tid] = c0 + tid < q.C ? -0.5f * pfn : -INFINITY;  // rows past C hold zero data
-    __syncthreads();
-    if (c0 + kAsgCen < q.C) fetch(c0 + kAsgCen);
     const int nblk = min(kAsgCen / 32, (q.C - c0 + 31) / 32);
     for (int cb = 0; cb < nblk; ++cb) {
       // accumulator i of a lane is row 8 (i / 4) + 4 half + i % 4 of the block
       f32x16 acc[2];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        const float4 x = *reinterpret_cast<const float4*>(s_nh + cb * 32 + 8 * k + 4 * half);
+        const float4 x = *reinterpret_cast<const float4*>(s_nh[buf] + cb * 32 + 8 * k + 4 * half);
         acc[0][4 * k] = acc[1][4 * k] = x.x;
         acc[0][4 * k + 1] = acc[1][4 * k + 1] = x.y;
         acc[0][4 * k + 2] = acc[1][4 * k + 2] = x.z;
         acc[0][4 * k + 3] = acc[1][4 * k + 3] = x.w;
       }
-      const uint16_t* arow = s_c + (cb * 32 + col) * kLdsRow + 64 * half;
+      const uint16_t* arow = s_c[buf] + (cb * 32 + col) * kHeadDim;  // row cb * 32 + col: swizzle col & 15
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
-        const bf16x8 av = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(arow + 8 * s));
+        const bf16x8 av = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(arow + (((8 * half + s) ^ (col & 15)) * 8)));
         acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bt[0][s], acc[0], 0, 0, 0);
         acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bt[1][s], acc[1], 0, 0, 0);
       }
