@@ -1325,8 +1325,11 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
 //     while the first G waves fit, the other waves copy the heads' cluster
 //     ranks (u16) and the cluster offsets to LDS; then every thread takes 8
 //     consecutive clusters and keeps their union lengths and offsets in
-//     registers through the scan and the range list.  Otherwise the union
-//     lengths are staged in LDS (or the output array) between the passes.
+//     registers through the scan and the range list.  Otherwise, up to
+//     32768 clusters: offsets to LDS while the fit runs, the heads' first
+//     cut-rank clusters marked there from the sort order, 32-cluster segments
+//     per thread through the scan; beyond that the union lengths go through
+//     the output array between the passes.
 constexpr int kUnionSeg = 8;              // clusters per thread in the staged union
 constexpr int kUnionStagedMax = 8 * 1024;  // clusters of the staged union (kUnionSeg per thread)
 __host__ __device__ inline bool union_staged(int G, int64_t Cm) { return G <= 4 && Cm <= kUnionStagedMax; }
