@@ -61,7 +61,7 @@ def _slices(inp, res, lens, ncl, b, g):
                 perm=res.perm[g, s0:s1].cpu().numpy().astype(np.int64))
 
 
-@pytest.mark.parametrize("lens", [[4096], [3000, 1500, 700]])
+@pytest.mark.parametrize("lens", [[4096], [3000, 1500, 700], [1, 3, 97, 5000]])
 def test_kmeans_one_step_parity(lens):
     wl = synth.small_workload(synth.WORKLOADS["ctx4k_gqa4"], lens)
     inp = synth.make_layer(wl, 0)
