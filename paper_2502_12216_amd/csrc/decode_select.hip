@@ -1078,9 +1078,9 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
   }
   __syncthreads();
   if (tid < kSampleChunk && u0 + tid < S) lg[u0 + tid] = s_lg[tid];  // contiguous stores
-  // per-region (max, sum exp(l - max)) of this chunk by the first wave, kRW
-  // samples per lane; regions: exact head, window 1, window 2, recent tokens
-  if (wave != 0) return;
+  // per-region (max, sum exp(l - max)) of this chunk, wave r taking region r
+  // (4 waves, 4 regions: exact head, window 1, window 2, recent tokens), kRW
+  // samples per lane
   const int64_t S_main = hm[12];
   const int64_t N = hm[8] ? S_main : hm[1];
   const int64_t N1 = N + hm[2];
@@ -1096,22 +1096,21 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
     reg[i] = region(u0 + i * kWave + lane);
   }
   double* out = a.lse + ((int64_t)bh * a.split + blockIdx.x) * 8;
-  for (int rg = 0; rg < 4; ++rg) {
-    double mx = -INFINITY, sm = 0.0;
-    if (rg >= rg_lo && rg <= rg_hi) {
-      double m0 = -INFINITY;
+  const int rg = wave;
+  double mx = -INFINITY, sm = 0.0;
+  if (rg >= rg_lo && rg <= rg_hi) {
+    double m0 = -INFINITY;
 #pragma unroll
-      for (int i = 0; i < kRW; ++i) m0 = fmax(m0, reg[i] == rg ? l[i] : -INFINITY);
-      mx = wave_max_d(m0);
-      double e = 0.0;
+    for (int i = 0; i < kRW; ++i) m0 = fmax(m0, reg[i] == rg ? l[i] : -INFINITY);
+    mx = wave_max_d(m0);
+    double e = 0.0;
 #pragma unroll
-      for (int i = 0; i < kRW; ++i) e += reg[i] == rg ? exp(l[i] - mx) : 0.0;
-      sm = wave_sum_d(e);
-    }
-    if (lane == 0) {
-      out[rg * 2] = mx;
-      out[rg * 2 + 1] = mx == -INFINITY ? 0.0 : sm;
-    }
+    for (int i = 0; i < kRW; ++i) e += reg[i] == rg ? exp(l[i] - mx) : 0.0;
+    sm = wave_sum_d(e);
+  }
+  if (lane == 0) {
+    out[rg * 2] = mx;
+    out[rg * 2 + 1] = mx == -INFINITY ? 0.0 : sm;
   }
 }
 
