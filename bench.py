@@ -16,8 +16,9 @@ same-GPU dense decode time and speedup, the HBM rate on the bytes the
 kernels must read, a roofline record of the dominant kernel and the CPU
 oracle's time on a bounded sample.  The same line carries one record per
 other workload (4K, 32K at three target fractions, the ragged batch of 16,
-1M tokens): single-layer timings with the caches flushed before every rep,
-and the device's measured streaming-read ceiling.
+1M tokens) and for one layer of the timed shape at five target fractions:
+single-layer timings with the caches flushed before every rep, and the
+device's measured streaming-read ceiling.
 
 Bytes "touched" per layer: every centroid row and cluster offset, every K and
 V row of each group's union, and the distinct sampled key rows of a group
@@ -708,14 +709,16 @@ def main():
         log(f"streaming-read ceiling {ceiling:.0f} GB/s (by workgroups: "
             f"{ {k: round(v) for k, v in probe['gbps_by_workgroups'].items()} })")
 
-    # ---------------------------------------------------------------- the other workloads, one layer each
+    # ---------------------------------------------------------------- the other workloads (and the timed shape over P), one layer each
     configs, hosts = None, {}
     if not args.no_configs:
         configs = {}
         for name, Ps, hg in (("ctx4k_gqa4", (0.9,), [(0, 0), (0, 1)]),
                              ("ctx32k_llama8b", (0.8, 0.9, 0.95), [(0, 0), (0, 5)]),
                              ("ragged16_16k_128k", (0.9,), None),
-                             ("ctx1m", (0.9,), None)):
+                             ("ctx1m", (0.9,), None),
+                             # the timed shape, one layer, over the target fraction
+                             ("ctx128k_b4_32layer", (0.5, 0.8, 0.9, 0.95, 0.99), None)):
             rec, host = config_record(T, synth.WORKLOADS[name], Ps, dev, flush, args.config_reps, stage_ev, ceiling,
                                       host_groups=None if args.no_cpu else hg)
             configs[name] = rec
