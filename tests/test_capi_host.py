@@ -187,3 +187,84 @@ def test_status_strings():
     L = C.lib()
     for s in range(5):
         assert len(L.tactic_status_string(s)) > 0
+
+
+@pytest.mark.parametrize("field,value", [("exact_bp", -1), ("exact_bp", 10001), ("win_bp", 10001), ("win_min", 0),
+                                         ("p1_bp", -5), ("p2_bp", 20000), ("max_tail", -1)])
+def test_plan_rejects_fit_parameters_out_of_range(field, value):
+    """Basis-point fractions outside [0, 10000], a window below one token and a
+    negative recent-token capacity are rejected at plan time."""
+    p = _params()
+    setattr(p, field, value)
+    st, _, _ = _plan(_shape(), C.ClusterMeta(256, 256, FAKE, FAKE, FAKE), p)
+    assert st == 1, (field, value)
+
+
+def test_plan_shape_and_cluster_limits():
+    """A sequence of 2^31 tokens, more (sequence, KV head) groups than the
+    attention's work list holds (4096), and more than 2^24 clusters per
+    sequence are unsupported (status 2), before any device work."""
+    L = C.lib()
+    meta = C.ClusterMeta(256, 256, FAKE, FAKE, FAKE)
+    st, _, _ = _plan(_shape(total=1 << 31, nmax=1 << 31), meta, _params())
+    assert st == 2 and b"2^31" in L.tactic_last_error()
+    B = 1000
+    st, _, _ = _plan(_shape(B=B, Hq=64, Hkv=8, total=B * 64, nmax=64), C.ClusterMeta(B * 4, 4, FAKE, FAKE, FAKE),
+                     _params())
+    assert st == 2 and b"n_kv_heads" in L.tactic_last_error()
+    big = (1 << 24) + 1
+    st, _, _ = _plan(_shape(total=1 << 25, nmax=1 << 25), C.ClusterMeta(big, big, FAKE, FAKE, FAKE), _params())
+    assert st == 2 and b"2^24" in L.tactic_last_error()
+
+
+@pytest.mark.parametrize("case,code", [("null_table", 1), ("page_size", 1), ("few_pages", 1), ("huge_pages", 2),
+                                       ("too_many_rows", 2)])
+def test_paged_decode_validates_its_page_table(case, code):
+    """The paged calls check the page table before any device work: null
+    pointers, a zero page size, fewer pages per sequence than its longest
+    sequence needs, and page counts whose rows overflow 32-bit indices."""
+    L = C.lib()
+    shape = _shape()  # longest sequence 4096 tokens, 2 KV heads
+    kv = C.PagedKV(FAKE, FAKE, FAKE, None, 16, 256, 512)  # 16 x 256 = 4096 tokens per sequence
+    if case == "null_table":
+        kv.page_table = None
+    elif case == "page_size":
+        kv.page_size = 0
+    elif case == "few_pages":
+        kv.max_pages = 100
+    elif case == "huge_pages":
+        kv.max_pages = 1 << 27  # 2^27 pages x 16 tokens = 2^31 positions
+    else:
+        kv.num_pages = 1 << 26  # 2^26 pages x 2 heads x 16 rows = 2^31 rows
+    n = L.tactic_dense_decode_workspace_size(ctypes.byref(shape))
+    st = L.tactic_dense_decode_paged(FAKE, ctypes.byref(kv), ctypes.byref(shape), FAKE, FAKE, n, None)
+    assert st == code, (case, L.tactic_last_error())
+
+
+def test_build_clusters_rejects_bad_requests():
+    """K-means build: V_sorted without V, max_iters outside [1, 1000], 2^21 or
+    more clusters per sequence (status 2) and a workspace one byte short
+    (status 3) are rejected before any device work."""
+    L = C.lib()
+    shape = _shape()
+    m = L.tactic_build_clusters_workspace_size(ctypes.byref(shape), 256, 256)
+    kp = C.KMeansParams(10)
+
+    def build(V=FAKE, total=256, cmax=256, params=kp, V_sorted=FAKE, nbytes=m):
+        return L.tactic_build_clusters(FAKE, V, ctypes.byref(shape), FAKE, total, cmax, FAKE, ctypes.byref(params),
+                                       FAKE, FAKE, FAKE, FAKE, FAKE, V_sorted, FAKE, nbytes, None)
+
+    assert build(V=None) == 1 and b"without V" in L.tactic_last_error()
+    assert build(params=C.KMeansParams(1001)) == 1
+    big = 1 << 21
+    assert build(total=big, cmax=big) == 2 and b"2^21" in L.tactic_last_error()
+    assert build(nbytes=m - 1) == 3
+
+
+def test_stream_read_probe_validation():
+    """The read-ceiling probe rejects a null buffer, a size that is not a
+    multiple of 16 bytes and a negative workgroup count."""
+    L = C.lib()
+    assert L.tactic_probe_stream_read(None, 1 << 20, 0, FAKE, None) == 1
+    assert L.tactic_probe_stream_read(FAKE, (1 << 20) + 8, 0, FAKE, None) == 1
+    assert L.tactic_probe_stream_read(FAKE, 1 << 20, -1, FAKE, None) == 1
