@@ -65,6 +65,14 @@ MUTATIONS = [
      "assignment to the farthest centroid"),
     ("kmeans", "C[m:] = K[init_idx[m:]]", "C[m:] = K[init_idx[m:] - 1]", "initial centroids off by one token"),
     ("kmeans", "perm[fill[c]] = t", "perm[fill[c]] = len(assign) - 1 - t", "layout not in ascending token order"),
+    ("tactic", "union = np.unique(np.concatenate(sels))", "union = np.unique(sels[0])",
+     "union of the first head's selection only"),
+    ("tactic", "sels.append(np.concatenate([rows[:k], tail]))", "sels.append(rows[:k])",
+     "recent tokens left out of the selection"),
+    ("tactic", "T = P * S[-1]", "T = P * (S[-1] - E_t)", "target taken on the listed tokens' mass only"),
+    ("tactic", "k = 0 if (has_tail and E_t >= T) else int(np.argmax(S >= T)) + 1", "k = int(np.argmax(S >= T)) + 1",
+     "recent tokens that alone meet the target still take a listed token"),
+    ("kmeans", "C = C_prev.copy()", "C = np.zeros_like(C_prev)", "an empty cluster's centroid reset to zero"),
 ]
 
 # which module object of tests/test_oracle.py each oracle module replaces
