@@ -73,6 +73,13 @@ MUTATIONS = [
     ("tactic", "k = 0 if (has_tail and E_t >= T) else int(np.argmax(S >= T)) + 1", "k = int(np.argmax(S >= T)) + 1",
      "recent tokens that alone meet the target still take a listed token"),
     ("kmeans", "C = C_prev.copy()", "C = np.zeros_like(C_prev)", "an empty cluster's centroid reset to zero"),
+    ("tactic", "t1 = min(s1 + W - 1, n)", "t1 = min(s1 + W, n)", "window 1 one position too long"),
+    ("tactic", "W = max(prm.win_min, _ceil_div(n * prm.win_bp, 10000))", "W = _ceil_div(n * prm.win_bp, 10000)",
+     "window width without its minimum"),
+    ("tactic", "c2 = (n * prm.p2_bp + 5000) // 10000", "c2 = (n * prm.p2_bp) // 10000",
+     "window 2 centre truncated instead of rounded"),
+    ("tactic", "exact = (N == n) or (s1 > t1) or (s2 > t2) or (t1 >= s2)", "exact = (N == n) or (s1 > t1) or (s2 > t2)",
+     "overlapping windows not sent to exact mode"),
 ]
 
 # which module object of tests/test_oracle.py each oracle module replaces
