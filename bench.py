@@ -205,12 +205,14 @@ STAGE_KERNEL = {n: n for n in STAGE_NAMES}
 SEL, ATT, COMB = STAGE_NAMES.index("sample_logits"), STAGE_NAMES.index("attn_splitk"), STAGE_NAMES.index("combine")
 
 
-def config_record(T, wl, Ps, dev, flush, reps: int, stage_ev, ceiling, host_groups=None):
+def config_record(T, wl, Ps, dev, flush, reps: int, stage_ev, ceiling, host_groups=None, union_ab=None):
     """One layer of workload `wl` on the library's K-means clusters: sparse and
     dense decode times (medians of `reps` calls, caches flushed before each),
     per-kernel times (library events, flushed), touched bytes and rates,
     selected fractions.  host_groups: (sequence, KV head) groups whose fp64
-    inputs are returned for the CPU oracle legs."""
+    inputs are returned for the CPU oracle legs.  union_ab: a target fraction
+    (one of Ps) at which every query head also attends over its own selection
+    (the GQA-union ablation, Sec. 4.5)."""
     import ctypes
     from paper_2502_12216_amd import _capi as C
     B, Hq, Hkv = wl.batch, wl.n_q_heads, wl.n_kv_heads
@@ -243,9 +245,8 @@ def config_record(T, wl, Ps, dev, flush, reps: int, stage_ev, ceiling, host_grou
         den(q, Ks, Vs)
     us_dense = float(np.median(timed_reps(lambda: den(q, Ks, Vs), reps, flush))) * 1000
     dense_bytes = float(lens.sum()) * Hkv * 512
-    points = []
-    for P in Ps:
-        dec = T.SparseDecoder(batch, ncl, T.decode_params(P))
+    def timed_and_staged(dec):
+        """Flushed median time of one call (us) and per-kernel event times (us)."""
         for _ in range(3):
             dec(q, Ks, Vs, cl)
         us = float(np.median(timed_reps(lambda: dec(q, Ks, Vs, cl), reps, flush))) * 1000
@@ -258,7 +259,13 @@ def config_record(T, wl, Ps, dev, flush, reps: int, stage_ev, ceiling, host_grou
             torch.cuda.synchronize()
             acc += [stage_ev.elapsed(i, i + 1) for i in range(len(STAGE_NAMES))]
         C.check(C.lib().tactic_sparse_decode_plan_set_events(ctypes.byref(dec.plan), None), "set_events")
-        stage_us = acc / n_ev * 1000
+        return us, acc / n_ev * 1000
+
+    points = []
+    ab_union = None
+    for P in Ps:
+        dec = T.SparseDecoder(batch, ncl, T.decode_params(P))
+        us, stage_us = timed_and_staged(dec)
         _, sq, skv = dec(q, Ks, Vs, cl)
         torch.cuda.synchronize()
         tb = touched_bytes(dec.view(), cl, skv, G)
@@ -282,12 +289,27 @@ def config_record(T, wl, Ps, dev, flush, reps: int, stage_ev, ceiling, host_grou
             rec["k_per_query_head"] = [int(x) for x in sq.cpu().numpy()[0]]
             rec["union_per_kv_head"] = [int(x) for x in skv.cpu().numpy()[0]]
         points.append(rec)
+        if union_ab is not None and P == union_ab:
+            ab_union = (us, float(stage_us[ATT] + stage_us[COMB]), int(skv.sum()))
         del dec
+    ablation = None
+    if ab_union is not None:
+        dph = T.SparseDecoder(batch, ncl, T.decode_params(union_ab, use_union=0))
+        us_ph, st_ph = timed_and_staged(dph)
+        _, _, skv_ph = dph(q, Ks, Vs, cl)
+        att_ph = float(st_ph[ATT] + st_ph[COMB])
+        ablation = {"target_frac": union_ab, "per_head_us": round(us_ph, 2), "union_us": round(ab_union[0], 2),
+                    "per_head_attn_us": round(att_ph, 2), "union_attn_us": round(ab_union[1], 2),
+                    "attn_speedup_from_union": round(att_ph / ab_union[1], 3),
+                    "kv_rows_per_head_over_union": round(int(skv_ph.sum()) / max(1, ab_union[2]), 3)}
+        del dph
     sort_path = "LDS" if max(ncl) <= 8192 else ("LDS pieces" if max(ncl) <= 32768 else "workspace")
     out = {"batch": B, "seq_lens": (list(map(int, wl.seq_lens)) if B > 1 else int(wl.seq_lens[0])),
            "n_q_heads": Hq, "n_kv_heads": Hkv, "clusters_per_seq": (list(map(int, ncl)) if B > 1 else int(ncl[0])),
            "cluster_sort": sort_path, "kmeans_ms": round(km_ms, 2), "dense_us": round(us_dense, 2),
            "dense_gbps": round(dense_bytes / (us_dense * 1e3), 1), "points": points}
+    if ablation is not None:
+        out["union_ablation"] = ablation
     del den, q, Ks, Vs, cl, cb
     torch.cuda.empty_cache()
     return out, host
@@ -713,14 +735,14 @@ def main():
     configs, hosts = None, {}
     if not args.no_configs:
         configs = {}
-        for name, Ps, hg in (("ctx4k_gqa4", (0.9,), [(0, 0), (0, 1)]),
-                             ("ctx32k_llama8b", (0.8, 0.9, 0.95), [(0, 0), (0, 5)]),
-                             ("ragged16_16k_128k", (0.9,), None),
-                             ("ctx1m", (0.9,), None),
-                             # the timed shape, one layer, over the target fraction
-                             ("ctx128k_b4_32layer", (0.5, 0.8, 0.9, 0.95, 0.99), None)):
+        for name, Ps, hg, ab in (("ctx4k_gqa4", (0.9,), [(0, 0), (0, 1)], None),
+                                 ("ctx32k_llama8b", (0.8, 0.9, 0.95), [(0, 0), (0, 5)], 0.9),
+                                 ("ragged16_16k_128k", (0.9,), None, None),
+                                 ("ctx1m", (0.9,), None, None),
+                                 # the timed shape, one layer, over the target fraction
+                                 ("ctx128k_b4_32layer", (0.5, 0.8, 0.9, 0.95, 0.99), None, None)):
             rec, host = config_record(T, synth.WORKLOADS[name], Ps, dev, flush, args.config_reps, stage_ev, ceiling,
-                                      host_groups=None if args.no_cpu else hg)
+                                      host_groups=None if args.no_cpu else hg, union_ab=ab)
             configs[name] = rec
             if host is not None:
                 hosts[name] = host
