@@ -18,7 +18,7 @@ constexpr int kMaxGroups = 4096;       // B * Hkv limit of the attention work li
 constexpr int kFitFields = 16;
 constexpr int kStageEvents = 7;        // start + after each of the six decode kernels
 constexpr int kUnionLdsMax = 32768;     // clusters whose union lengths are staged in LDS
-constexpr int kScoreRows = 128;        // centroids per scoring workgroup
+constexpr int kScoreRows = 64;         // centroids per scoring workgroup (4096 workgroups at 8192 x 32)
 #ifndef TACTIC_SAMPLE_CHUNK
 #define TACTIC_SAMPLE_CHUNK 128
 #endif
