@@ -131,7 +131,8 @@ __global__ __launch_bounds__(256) void score_clusters_kernel(ScoreArgs a) {
 //    linear map over [min, max] would crowd the bulk into a few buckets.  Then
 //    the tokens ahead of every rank (exclusive prefix of cluster sizes in rank
 //    order) and the rows of the sampled positions: exact head 1..N and the
-//    two windows (Alg. 1).  One workgroup (1024 threads) per query head.
+//    two windows (Alg. 1).  One workgroup (1024 threads) per query head (up
+//    to eight per head beyond 8192 clusters, see the workspace sort below).
 // ============================================================================
 __device__ __forceinline__ uint32_t desc_key_bits(float s) {
   const uint32_t u = __float_as_uint(s + 0.0f);  // -0 -> +0
@@ -217,7 +218,12 @@ __device__ __forceinline__ float key_score(uint32_t k) {
 // kPieceCap clusters, whose keys are staged in LDS at those positions: every
 // access of the rank computation is an LDS access, and the global accesses
 // are coalesced.  A piece's ranks are consecutive, so its order, rank-prefix
-// and size entries leave in order.
+// and size entries leave in order.  A head's buckets are shared by the
+// workgroups of its grid column (blockIdx.y): each counts every cluster (the
+// bucket starts must be known everywhere), then ranks only the pieces of its
+// own run of whole buckets, its prefix starting at the tokens of the
+// clusters before them, and finds the sampled rows that fall in its ranks.
+// The workgroups exchange nothing; the first one also writes the head record.
 constexpr int kPieceBuckets = 4096;
 constexpr int kPiecePer = 6;                    // entries per thread in the piece scan
 constexpr int kPieceCap = kPiecePer * 1024;     // clusters per piece
@@ -255,6 +261,10 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
   uint32_t* cnt;      // per rank: cluster size, then the exclusive prefix
   int32_t* ostart;    // per rank: first row of the cluster
   uint32_t total = 0; // tokens of the sequence (prefix at rank C)
+  // ranks [rk_lo, rk_hi) of this workgroup, holding token positions
+  // (tok_lo, tok_hi]; the whole order except when a head's pieces are shared
+  int rk_lo = 0, rk_hi = -1;
+  uint32_t tok_lo = 0, tok_hi = 0;
   if constexpr (kLds) {
     // LDS: keys u64[8192] (after ranking: ostart i32[8192], ord_s i32[8192]),
     // cnt u32[8192], start u32[8192]
@@ -513,8 +523,72 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
       }
       if (pieces_done) {
         int32_t* rpre = a.rprefix + (int64_t)bh * (a.Cm + 1);
+        // the head's rank order is shared by the gridDim.y workgroups of the
+        // head: workgroup kw takes the buckets [b_lo, b_hi), b_lo the largest
+        // bucket whose start is at most kw C / nw (counted as b1 below), so
+        // the ranges are whole buckets, disjoint and cover every cluster; its
+        // first rank carries the tokens of the clusters before b_lo
+        const int nw = (int)gridDim.y, kw = (int)blockIdx.y;
+        const uint32_t t_lo = (uint32_t)((int64_t)kw * C / nw), t_hi = (uint32_t)((int64_t)(kw + 1) * C / nw);
+        uint32_t* s_cnt2 = reinterpret_cast<uint32_t*>(&s_red[0][0]);  // 64 words: three wave-total slots of 16
+        int b_lo, b_hi;
+        {
+          const uint4 s4 = reinterpret_cast<const uint4*>(st_l)[tid];
+          auto count_le = [&](uint32_t lim) {
+            return (tid > 0 && s4.x <= lim ? 1u : 0u) + (s4.y <= lim ? 1u : 0u) + (s4.z <= lim ? 1u : 0u) +
+                   (s4.w <= lim ? 1u : 0u) + (tid == 1023 && (uint32_t)C <= lim ? 1u : 0u);
+          };
+          const uint32_t clo = (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(count_le(t_lo)), kWave - 1);
+          const uint32_t chi = (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(count_le(t_hi)), kWave - 1);
+          if ((tid & (kWave - 1)) == 0) {
+            s_wave_u[tid / kWave] = clo;
+            s_cnt2[tid / kWave] = chi;
+          }
+        }
+        __syncthreads();
+        b_lo = 0;
+        b_hi = 0;
+        for (int w = 0; w < 1024 / kWave; ++w) {
+          b_lo += (int)s_wave_u[w];
+          b_hi += (int)s_cnt2[w];
+        }
+        if (kw == 0) b_lo = 0;        // (the buckets before are empty)
+        if (kw == nw - 1) b_hi = nbk;  // (every bucket start is at most C)
+        // uniform over the workgroup: kept in scalar registers (the thread's
+        // 32 scores and sizes fill its vector registers)
+        b_lo = __builtin_amdgcn_readfirstlane(b_lo);
+        b_hi = __builtin_amdgcn_readfirstlane(b_hi);
+        const uint32_t r_lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(b_lo < nbk ? st_l[b_lo] : (uint32_t)C));
+        const uint32_t r_hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(b_hi < nbk ? st_l[b_hi] : (uint32_t)C));
+        {
+          // tokens of the clusters ranked before r_lo, and of all clusters
+          uint32_t before = 0, all = 0;
+#pragma unroll
+          for (int e = 0; e < kE; ++e) {
+            const uint32_t sz = e < nv ? (ps[e] & 0xffffu) : 0u;
+            all += sz;
+            before += (ps[e] >> 16) < r_lo ? sz : 0u;
+          }
+          before = (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(before), kWave - 1);
+          all = (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(all), kWave - 1);
+          if ((tid & (kWave - 1)) == 0) {
+            s_cnt2[16 + tid / kWave] = before;
+            s_cnt2[32 + tid / kWave] = all;
+          }
+        }
+        __syncthreads();  // (s_wave_u was read before it: the piece loop may write it)
         uint32_t carry = 0;
-        for (int b0 = 0; b0 < nbk;) {
+        total = 0;
+        for (int w = 0; w < 1024 / kWave; ++w) {
+          carry += s_cnt2[16 + w];
+          total += s_cnt2[32 + w];
+        }
+        carry = (uint32_t)__builtin_amdgcn_readfirstlane((int)carry);
+        total = (uint32_t)__builtin_amdgcn_readfirstlane((int)total);
+        rk_lo = (int)r_lo;
+        rk_hi = (int)r_hi;
+        tok_lo = carry;
+        for (int b0 = b_lo; b0 < b_hi;) {
           // the piece: buckets [b0, b1), the last b1 whose start is within
           // kPieceCap of the piece's start (the bucket b0 alone fits)
           // (starts are non-decreasing: b1 counts the b in [1, nbk] with
@@ -531,6 +605,7 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
           __syncthreads();  // also: the previous piece's LDS reads are done
           int b1 = 0;
           for (int w = 0; w < 1024 / kWave; ++w) b1 += (int)s_wave_u[w];
+          b1 = min(b1, b_hi);
           const uint32_t len = (b1 < nbk ? st_l[b1] : (uint32_t)C) - p0;
 #pragma unroll
           for (int e = 0; e < kPiecePer; ++e) s_sz[tid * kPiecePer + e] = 0u;
@@ -582,13 +657,18 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
           b0 = b1;
         }
 #pragma unroll
-        for (int e = 0; e < kE; ++e)
-          if (e < nv) rank_of[cid(e)] = (int32_t)__float_as_uint(v[e]);
-        total = carry;
-        if (tid == 0) rpre[C] = (int32_t)total;
+        for (int e = 0; e < kE; ++e) {
+          const uint32_t pos = ps[e] >> 16;
+          if (e < nv && pos >= r_lo && pos < r_hi) rank_of[cid(e)] = (int32_t)__float_as_uint(v[e]);
+        }
+        if (tid == 0 && kw == 0) rpre[C] = (int32_t)total;
+        tok_hi = carry;
       }
       __syncthreads();  // the general path below reuses the LDS and s_red
     }
+    // the general path runs in the head's first workgroup; after the pieces
+    // every workgroup finds the sampled rows of its own ranks
+    if (!pieces_done && blockIdx.y != 0) return;
     if (!pieces_done) {
       // C > 8192: the bucket counts (8192 buckets) in LDS, the keys and the
       // per-rank sizes / starts in the workspace.  Every loop over the elements
@@ -779,7 +859,8 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
   const Geometry geo = make_geometry(n_c, a.prm);
   const int64_t S_main = min(geo.samples, a.S_cap);
   const int64_t S = min(S_main + tail, a.S_cap);
-  if (tid == 0) {
+  const bool first_wg = blockIdx.y == 0;  // (more than one only when the pieces are shared)
+  if (tid == 0 && first_wg) {
     int32_t* hm = a.head_meta + (int64_t)bh * 16;
     hm[0] = n_c;
     hm[1] = (int32_t)geo.N;
@@ -797,23 +878,31 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     if (a.per_head && h % a.G == 0) a.sel_count_kv[b * a.Hkv + g] = 0;  // summed by fit_union
   }
   int32_t* rows = a.sample_rows + (int64_t)bh * a.S_cap;
-  for (int64_t u = S_main + tid; u < S; u += nt) rows[u] = n_c + (int32_t)(u - S_main);
+  if (first_wg)
+    for (int64_t u = S_main + tid; u < S; u += nt) rows[u] = n_c + (int32_t)(u - S_main);
   if (C <= 0) return;
   const int64_t N = geo.exact ? n_c : geo.N;
   const int64_t W1 = geo.exact ? 0 : geo.t1 - geo.s1 + 1;
   if constexpr (!kLds) {
-    // workspace path: every kStr-th prefix entry in LDS (every entry up to
-    // kSortWsLdsBytes / 4 clusters; the bucket arrays are dead), a binary
-    // search there, then the last kStr entries from memory.  The row of
-    // position i in rank r's cluster is off[order[r]] + i - 1 - prefix[r].
+    // workspace path: ranks [r0, r0 + R) of the order (the whole order, or
+    // this workgroup's share of it), every kStr-th of their prefix entries in
+    // LDS (every entry up to kSortWsLdsBytes / 4 clusters; the bucket arrays
+    // are dead), a binary search there, then the last kStr entries from
+    // memory, for the sampled positions in (p_lo, p_hi], the tokens of those
+    // ranks.  The row of position i in rank r's cluster is
+    // off[order[r]] + i - 1 - prefix[r].
+    const bool whole = rk_hi < 0;
+    const int r0 = whole ? 0 : rk_lo, R = whole ? C : rk_hi - rk_lo;
+    const int64_t p_lo = whole ? 0 : tok_lo, p_hi = whole ? (int64_t)total : tok_hi;
+    if (R <= 0) return;
     uint32_t* s_pre = reinterpret_cast<uint32_t*>(smem_raw);
     constexpr int kPreCap = (int)(kSortWsLdsBytes / 4);
-    const int kStr = (C + kPreCap - 1) / kPreCap;
-    const int nsp = (C + kStr - 1) / kStr;
+    const int kStr = (R + kPreCap - 1) / kPreCap;
+    const int nsp = (R + kStr - 1) / kStr;
     for (int i0 = tid; i0 < nsp; i0 += 16 * nt) {
       uint32_t v[16];
 #pragma unroll
-      for (int e = 0; e < 16; ++e) v[e] = cnt[min((i0 + e * nt) * kStr, C - 1)];
+      for (int e = 0; e < 16; ++e) v[e] = cnt[r0 + min((i0 + e * nt) * kStr, R - 1)];
 #pragma unroll
       for (int e = 0; e < 16; ++e)
         if (i0 + e * nt < nsp) s_pre[i0 + e * nt] = v[e];
@@ -822,63 +911,74 @@ __global__ __launch_bounds__(1024) void sort_clusters_kernel(SortArgs a) {
     int top = 1;
     while (top * 2 <= nsp) top <<= 1;
     constexpr int kU = 8;  // independent searches in flight per thread
-    // positions and prefixes in 32 bits (a sequence holds fewer than 2^31 tokens)
+    // positions and prefixes in 32 bits (a sequence holds fewer than 2^31
+    // tokens).  The sampled positions of each region (exact head 1..N, the
+    // two windows) that fall in (p_lo, p_hi] are a run of sample indices.
     const int N32 = (int)N, NW = (int)(N + W1), s1 = (int)geo.s1, s2 = (int)geo.s2, Sm = (int)S_main;
-    for (int u0 = tid; u0 < Sm; u0 += kU * nt) {
-      uint32_t iv[kU];
-      int li[kU];
-#pragma unroll
-      for (int k = 0; k < kU; ++k) {
-        const int u = u0 + k * nt;
-        iv[k] = (uint32_t)(u < N32 ? u + 1 : (u < NW ? s1 + (u - N32) : s2 + (u - NW)));
-        li[k] = 0;
-      }
-      // largest i with s_pre[i] < position (s_pre[0] = prefix[0] = 0); the
-      // reads at clamped indices, so that the kU of a step are in flight together
-      for (int step = top; step > 0; step >>= 1) {
-        uint32_t pv[kU];
-#pragma unroll
-        for (int k = 0; k < kU; ++k) pv[k] = s_pre[min(li[k] + step, nsp - 1)];
+    for (int rg = 0; rg < 3; ++rg) {
+      const int u_beg = rg == 0 ? 0 : (rg == 1 ? min(N32, Sm) : min(NW, Sm));
+      const int u_end = rg == 0 ? min(N32, Sm) : (rg == 1 ? min(NW, Sm) : Sm);
+      const int64_t pos0 = rg == 0 ? 1 : (rg == 1 ? s1 : s2);  // position of sample u_beg
+      // the samples u in [u_beg, u_end) whose position pos0 + (u - u_beg) is in (p_lo, p_hi]
+      const int ua = (int)max((int64_t)u_beg, u_beg + (p_lo + 1 - pos0));
+      const int ub = (int)min((int64_t)u_end, u_beg + (p_hi + 1 - pos0));
+      for (int u0 = ua + tid; u0 < ub; u0 += kU * nt) {
+        uint32_t iv[kU];
+        int li[kU];
 #pragma unroll
         for (int k = 0; k < kU; ++k) {
-          const int t = li[k] + step;
-          li[k] = (t < nsp && pv[k] < iv[k]) ? t : li[k];
+          const int u = min(u0 + k * nt, ub - 1);  // (past ub: the last sample again, not stored)
+          iv[k] = (uint32_t)(pos0 + (u - u_beg));
+          li[k] = 0;
         }
-      }
-      // then the largest r in [li * kStr, li * kStr + kStr) with prefix[r] < position
-      int lr[kU];
+        // largest i with s_pre[i] < position (s_pre[0] = prefix[r0] = p_lo <
+        // position); the reads at clamped indices, so that the kU of a step
+        // are in flight together
+        for (int step = top; step > 0; step >>= 1) {
+          uint32_t pv[kU];
 #pragma unroll
-      for (int k = 0; k < kU; ++k) lr[k] = li[k] * kStr;
-      for (int d = 1; d < kStr; ++d) {
-        uint32_t pv[kU];
+          for (int k = 0; k < kU; ++k) pv[k] = s_pre[min(li[k] + step, nsp - 1)];
 #pragma unroll
-        for (int k = 0; k < kU; ++k) pv[k] = cnt[min(li[k] * kStr + d, C - 1)];
+          for (int k = 0; k < kU; ++k) {
+            const int t = li[k] + step;
+            li[k] = (t < nsp && pv[k] < iv[k]) ? t : li[k];
+          }
+        }
+        // then the largest r in [li * kStr, li * kStr + kStr) with prefix[r] < position
+        int lr[kU];
+#pragma unroll
+        for (int k = 0; k < kU; ++k) lr[k] = li[k] * kStr;
+        for (int d = 1; d < kStr; ++d) {
+          uint32_t pv[kU];
+#pragma unroll
+          for (int k = 0; k < kU; ++k) pv[k] = cnt[r0 + min(li[k] * kStr + d, R - 1)];
+#pragma unroll
+          for (int k = 0; k < kU; ++k) {
+            const int t = li[k] * kStr + d;
+            lr[k] = (t < R && pv[k] < iv[k]) ? t : lr[k];
+          }
+        }
+        int first[kU];
+        uint32_t pr[kU];
 #pragma unroll
         for (int k = 0; k < kU; ++k) {
-          const int t = li[k] * kStr + d;
-          lr[k] = (t < C && pv[k] < iv[k]) ? t : lr[k];
+          lr[k] = min(lr[k], R - 1);
+          first[k] = off[order[r0 + lr[k]]];
         }
-      }
-      int first[kU];
-      uint32_t pr[kU];
+        // the rank's prefix from LDS when every entry is there (kept apart from
+        // the memory read so that each compiles to its own instruction kind)
+        if (kStr == 1) {
 #pragma unroll
-      for (int k = 0; k < kU; ++k) {
-        lr[k] = min(lr[k], C - 1);
-        first[k] = off[order[lr[k]]];
-      }
-      // the rank's prefix from LDS when every entry is there (kept apart from
-      // the memory read so that each compiles to its own instruction kind)
-      if (kStr == 1) {
+          for (int k = 0; k < kU; ++k) pr[k] = s_pre[lr[k]];
+        } else {
 #pragma unroll
-        for (int k = 0; k < kU; ++k) pr[k] = s_pre[lr[k]];
-      } else {
+          for (int k = 0; k < kU; ++k) pr[k] = cnt[r0 + lr[k]];
+        }
 #pragma unroll
-        for (int k = 0; k < kU; ++k) pr[k] = cnt[lr[k]];
-      }
-#pragma unroll
-      for (int k = 0; k < kU; ++k) {
-        const int u = u0 + k * nt;
-        if (u < Sm) rows[u] = min(max(first[k] + (int32_t)(iv[k] - 1 - pr[k]), 0), n - 1);
+        for (int k = 0; k < kU; ++k) {
+          const int u = u0 + k * nt;
+          if (u < ub) rows[u] = min(max(first[k] + (int32_t)(iv[k] - 1 - pr[k]), 0), n - 1);
+        }
       }
     }
     return;
@@ -1802,7 +1902,10 @@ hipError_t launch_sort(const SortArgs& a, bool lds, int n_heads, hipStream_t st)
     const size_t bytes = (size_t)kSortLdsBuckets * 16;  // keys u64, cnt u32, start u32
     hipLaunchKernelGGL(sort_clusters_kernel<true>, dim3(n_heads), dim3(1024), bytes, st, a);
   } else {
-    hipLaunchKernelGGL(sort_clusters_kernel<false>, dim3(n_heads), dim3(1024), kSortWsLdsBytes, st, a);
+    // beyond 8192 clusters a head's pieces are shared by up to 8 workgroups,
+    // so that few heads still occupy the device's 256 compute units
+    const int nw = max(1, min(8, 256 / max(n_heads, 1)));
+    hipLaunchKernelGGL(sort_clusters_kernel<false>, dim3(n_heads, nw), dim3(1024), kSortWsLdsBytes, st, a);
   }
   return hipGetLastError();
 }
