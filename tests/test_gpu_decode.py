@@ -545,17 +545,21 @@ def test_sparse_union_range_writers(Hq, Hkv):
         assert seen == {"segment", "coalesced"}, (union, seen)
 
 
-@pytest.mark.parametrize("case", ["pieces", "workspace"])
+@pytest.mark.parametrize("case", ["pieces", "workspace", "mixed"])
 def test_sparse_large_sort_paths_with_recent_tail(case):
     """Recent tokens after the clusters on the sorts of more than 8192
     clusters: 12000 clusters (LDS pieces) and 34000 clusters (workspace
     path), with a tail of 200 and 150 tokens on the first sequence (its
-    sampled rows follow the windows', its range follows the union's), in
-    union and per-head modes, staged parity on every group at P = 0.9."""
+    sampled rows follow the windows', its range follows the union's), and a
+    batch that mixes 12000 clusters with 3000 (the smaller sequence's heads
+    then take the pieces, shared by the same number of workgroups, with a
+    tail of 100), in union and per-head modes, staged parity on every group
+    at P = 0.9."""
     import dataclasses
     T = _tactic()
     P = 0.9
-    lens, C, tail = {"pieces": ([30000, 12000], 12000, [200, 0]), "workspace": ([70000], 34000, [150])}[case]
+    lens, C, tail = {"pieces": ([30000, 12000], 12000, [200, 0]), "workspace": ([70000], 34000, [150]),
+                     "mixed": ([30000, 3000], 12000, [0, 100])}[case]
     base = _small("ctx32k_llama8b", lens)
     wl = dataclasses.replace(base, fixed_clusters=C, name=f"{base.name}_{case}_tail")
     inp = synth.make_layer(wl, 0)
