@@ -227,6 +227,7 @@ tactic_status tactic_sparse_decode_plan(const tactic_kv_shape* shape, const tact
   p.off_rstart = L.take(BG * (p.Cm + 2) * 4);  // ranges: clusters, then the recent tokens
   p.off_rupos = L.take(BG * (p.Cm + 2) * 4);
   p.off_cfr = L.take(BG * p.max_chunks * 4);
+  p.off_slice_tot = L.take(BG * tactic::kMaxUnionSlices * 8);
   p.off_partials = L.take((BG + p.attn_grid) * p.GV * (tactic::kHeadDim + 2) * 4);
   p.off_ameta = L.take((BG + 2) * 8);
   if (!p.sort_lds) {
@@ -369,6 +370,7 @@ static tactic_status sparse_decode_impl(const uint16_t* q, const uint16_t* K_sor
   fa.rstart = reinterpret_cast<int32_t*>(ws + p.off_rstart);
   fa.rupos = reinterpret_cast<int32_t*>(ws + p.off_rupos);
   fa.cfr = reinterpret_cast<int32_t*>(ws + p.off_cfr);
+  fa.slice_tot = reinterpret_cast<uint64_t*>(ws + p.off_slice_tot);
   if (pk) fa.pk = *pk;
   e = tactic::launch_sample(fa, (int)p.split, BH, pk != nullptr, stream);
   if (e == hipSuccess) e = record(3);

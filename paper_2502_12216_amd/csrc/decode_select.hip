@@ -7,6 +7,8 @@
 //   fit_union          per GQA group: fit y = a/x + b and the budget k of
 //                      every head, then the union of the group's selections
 //                      and the attention work list                         Sec. 4.4, 4.5, Alg. 1
+//   union_ranges       (8192 to 65536 clusters per group, up to 4 heads: the
+//                      union in slices) the slices' ranges end to end      Sec. 4.5, 4.6
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -1219,7 +1221,9 @@ __global__ __launch_bounds__(256) void sample_logits_kernel(FitArgs a) {
 // Region sums come from the per-chunk (max, sum) partials of the sampling
 // kernel: with M the maximum over the exact head (the shift m), a region's sum
 // of exp(l - m) is sum_c exp(M_c - m) S_c.
-__device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
+// (store: write the head's budget and fit record; false where another
+// workgroup fitting the same head writes them)
+__device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut, bool store) {
   constexpr int kRg = 4;  // regions: exact head, window 1, window 2, recent tokens
   const int32_t* hm = a.head_meta + (int64_t)bh * 16;
   const double* lg = a.logits + (int64_t)bh * a.S_cap;
@@ -1409,6 +1413,8 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
   if (lane == 0) {
     cut[0] = cut_r;
     cut[1] = cut_len;
+  }
+  if (lane == 0 && store) {
     a.sel_count_q[bh] = k + tail;  // tokens the head attends to
     double* fit = a.fit + (int64_t)bh * kFitFields;
     fit[0] = m; fit[1] = mu1; fit[2] = mu2; fit[3] = fa; fit[4] = fb; fit[5] = Sn; fit[6] = T;
@@ -1424,14 +1430,19 @@ __device__ void fit_head_wave(const FitArgs& a, int bh, int lane, int* cut) {
 //     while the first G waves fit, the other waves copy the heads' cluster
 //     ranks (u16) and the cluster offsets to LDS; then every thread takes 8
 //     consecutive clusters and keeps their union lengths and offsets in
-//     registers through the scan and the range list.  Otherwise, up to
+//     registers through the scan and the range list.  Up to 65536 clusters
+//     the staged form runs in slices (grid B*Hkv x slices) and
+//     union_ranges_kernel writes the ranges.  Otherwise (G = 8), up to
 //     32768 clusters: offsets to LDS while the fit runs, the heads' first
 //     cut-rank clusters marked there from the sort order, 32-cluster segments
 //     per thread through the scan; beyond that the union lengths go through
 //     the output array between the passes.
 constexpr int kUnionSeg = 8;              // clusters per thread in the staged union
-constexpr int kUnionStagedMax = 8 * 1024;  // clusters of the staged union (kUnionSeg per thread)
-__host__ __device__ inline bool union_staged(int G, int64_t Cm) { return G <= 4 && Cm <= kUnionStagedMax; }
+constexpr int kUnionStagedMax = 8 * 1024;  // clusters of one workgroup of the staged union (kUnionSeg per thread)
+__host__ __device__ inline bool union_staged(int G, int64_t Cm) {
+  return G <= 4 && Cm <= (int64_t)kUnionStagedMax * kMaxUnionSlices;
+}
+__host__ __device__ inline bool union_sliced(int G, int64_t Cm) { return union_staged(G, Cm) && Cm > kUnionStagedMax; }
 
 // The group's range list ends with the recent tokens (rows n_c .. n_c + tail
 // - 1, the same for every head of the group) as one more range; then the
@@ -1480,52 +1491,61 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
   const int n_c = a.head_meta[(int64_t)h0 * 16 + 0], tail = a.head_meta[(int64_t)h0 * 16 + 11];
 
   if (union_staged(G, a.Cm)) {
-    const int Cp = (a.Cm + kUnionSeg - 1) / kUnionSeg * kUnionSeg;
+    // up to kUnionStagedMax clusters one workgroup measures and lays out the
+    // whole union; beyond that (sliced) the clusters come in slices of
+    // a.union_slice, one per workgroup of the grid column (blockIdx.y): every
+    // workgroup fits the group's heads, stages and measures its own slice,
+    // and leaves the slice's union lengths and (ranges, tokens) total, and
+    // union_ranges_kernel lays the slices' ranges end to end
+    const bool sliced = a.Cm > kUnionStagedMax;
+    const int kw = sliced ? (int)blockIdx.y : 0;
+    const int Cp = sliced ? a.union_slice : (a.Cm + kUnionSeg - 1) / kUnionSeg * kUnionSeg;
+    const int jb = kw * Cp, ns = sliced ? max(0, min(C - jb, Cp)) : C;  // clusters jb .. jb + ns - 1
     uint16_t* s_rk = reinterpret_cast<uint16_t*>(smem_raw);        // [G][Cp]
     int32_t* s_off = reinterpret_cast<int32_t*>(s_rk + G * Cp);  // [Cp + 1]
     int32_t* s_L = s_off + Cp + 4;                                // [Cp]: union lengths (16-byte aligned)
     if (wave < G) {
-      fit_head_wave(a, h0 + wave, lane, s_cut[wave]);
+      fit_head_wave(a, h0 + wave, lane, s_cut[wave], kw == 0);
     } else {
-      const int32_t* off = a.offsets + (int64_t)kvh * (a.Ct + a.B) + cb + b;
+      const int32_t* off = a.offsets + (int64_t)kvh * (a.Ct + a.B) + cb + b + jb;
       // all loads of a thread are issued before its LDS stores
       constexpr int nw = 1024 - G * kWave;
-      constexpr int kW = (kUnionStagedMax + nw) / nw;  // covers j in [0, C] for C <= kUnionStagedMax
+      constexpr int kW = (kUnionStagedMax + nw) / nw;  // covers j in [0, ns] for ns <= kUnionStagedMax
       const int w = tid - G * kWave;
       int32_t ov[kW];
 #pragma unroll
-      for (int i = 0; i < kW; ++i) ov[i] = w + i * nw <= C ? off[w + i * nw] : 0;
+      for (int i = 0; i < kW; ++i) ov[i] = w + i * nw <= ns ? off[w + i * nw] : 0;
       int32_t rv[G][kW];
 #pragma unroll
       for (int hh = 0; hh < G; ++hh)
 #pragma unroll
         for (int i = 0; i < kW; ++i)
-          rv[hh][i] = w + i * nw < C ? a.rank_of[(int64_t)(h0 + hh) * a.Cm + w + i * nw] : 0;
+          rv[hh][i] = w + i * nw < ns ? a.rank_of[(int64_t)(h0 + hh) * a.Cm + jb + w + i * nw] : 0;
 #pragma unroll
       for (int i = 0; i < kW; ++i)
-        if (w + i * nw <= C) s_off[w + i * nw] = ov[i];
+        if (w + i * nw <= ns) s_off[w + i * nw] = ov[i];
 #pragma unroll
       for (int hh = 0; hh < G; ++hh)
 #pragma unroll
         for (int i = 0; i < kW; ++i)
-          if (w + i * nw < C) s_rk[hh * Cp + w + i * nw] = (uint16_t)rv[hh][i];
+          if (w + i * nw < ns) s_rk[hh * Cp + w + i * nw] = (uint16_t)rv[hh][i];
     }
     __syncthreads();
-    int32_t* ulen = a.union_len + (int64_t)jg * a.Ct + cb;
-    // union length of the thread's clusters j0 .. j0 + 7: the whole cluster
+    int32_t* ulen = a.union_len + (int64_t)jg * a.Ct + cb + jb;
+    // union length of the thread's clusters jb + j0 .. jb + j0 + 7: the whole cluster
     // when some head ranks it before its cut (rank - cut < 0), the largest
     // cut length among the heads whose cut cluster it is (rank - cut = 0)
     const int j0 = tid * kUnionSeg;
     int32_t o[kUnionSeg + 1], L[kUnionSeg];
     uint64_t loc = 0;  // (ranges << 32) | tokens
-    if (j0 < C) {
+    if (j0 < ns) {
       {  // two 16-byte LDS reads (j0 is a multiple of 8) and the next thread's first entry
         const int4 x = *reinterpret_cast<const int4*>(s_off + j0);
         const int4 y = *reinterpret_cast<const int4*>(s_off + j0 + 4);
         o[0] = x.x; o[1] = x.y; o[2] = x.z; o[3] = x.w;
         o[4] = y.x; o[5] = y.y; o[6] = y.z; o[7] = y.w;
       }
-      o[kUnionSeg] = j0 + kUnionSeg <= C ? s_off[j0 + kUnionSeg] : 0;
+      o[kUnionSeg] = j0 + kUnionSeg <= ns ? s_off[j0 + kUnionSeg] : 0;
       int dmin[kUnionSeg];
 #pragma unroll
       for (int e = 0; e < kUnionSeg; ++e) dmin[e] = 0x7fffffff;
@@ -1548,7 +1568,7 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
       }
 #pragma unroll
       for (int e = 0; e < kUnionSeg; ++e) {
-        if (j0 + e < C) {
+        if (j0 + e < ns) {
           if (L[e] > 0) loc += (1ull << 32) | (uint64_t)L[e];
         } else {
           L[e] = 0;
@@ -1569,8 +1589,12 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
     }
 #pragma unroll
     for (int i = 0; i < kUnionSeg; ++i)
-      if (tid + i * 1024 < C) ulen[tid + i * 1024] = s_L[tid + i * 1024];
-    if (j0 < C) {
+      if (tid + i * 1024 < ns) ulen[tid + i * 1024] = s_L[tid + i * 1024];
+    if (sliced) {
+      if (tid == 0) a.slice_tot[(int64_t)bg * kMaxUnionSlices + kw] = tot;
+      return;
+    }
+    if (j0 < ns) {
       int idx = (int)(base >> 32);
       int64_t upos = (int64_t)(base & 0xffffffffu);
 #pragma unroll
@@ -1628,7 +1652,7 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
     int32_t* s_wb = reinterpret_cast<int32_t*>(s_nz + Cp / 32);           // [Cp / 32]
     __shared__ int s_cutj[G];                                                  // cut cluster, -1: none
     if (wave < G) {
-      fit_head_wave(a, h0 + wave, lane, s_cut[wave]);
+      fit_head_wave(a, h0 + wave, lane, s_cut[wave], true);
       if (lane == 0) s_cutj[wave] = -1;
     } else {
       // offsets 0 .. C into LDS while the fit runs (8 per thread and step loaded together)
@@ -1811,7 +1835,7 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
       }
     }
   } else {
-    if (wave < G) fit_head_wave(a, h0 + wave, lane, s_cut[wave]);
+    if (wave < G) fit_head_wave(a, h0 + wave, lane, s_cut[wave], true);
     __syncthreads();
     // pass 1 (coalesced, kB clusters per thread and step loaded together at
     // clamped indices): selected prefix length of every cluster = max over
@@ -1882,6 +1906,67 @@ __global__ __launch_bounds__(1024) void fit_union_kernel(FitArgs a) {
   if (tid == 0) union_close(a, bg, b, kvh, n_c, tail, tot, rstart, rupos, cfr);
 }
 
+// Ranges of the sliced staged union: workgroup kw of group bg takes its
+// slice of clusters, starts from the (ranges, tokens) of the slices before
+// it, and writes the slice's (row, position) ranges and the chunk-index
+// entries whose first position falls in them; the last slice's workgroup
+// closes the group's list.
+__global__ __launch_bounds__(1024) void union_ranges_kernel(FitArgs a) {
+  __shared__ uint64_t s_wave_u[16];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int bg = blockIdx.x, kw = blockIdx.y, nwu = gridDim.y;
+  const int b = bg / a.NV, jg = bg % a.NV, kvh = jg / a.kv_div;
+  const int h0 = b * a.Hq + jg * (a.Hq / a.NV);  // first query head of the group
+  const int64_t T = kCfrTokens;
+  int32_t* rstart = a.rstart + (int64_t)bg * (a.Cm + 2);
+  int32_t* rupos = a.rupos + (int64_t)bg * (a.Cm + 2);
+  int32_t* cfr = a.cfr + (int64_t)bg * a.max_chunks;
+  const int64_t cb = a.cl_indptr[b];
+  const int C = min((int)(a.cl_indptr[b + 1] - cb), a.Cm);
+  const int Cs = a.union_slice, jb = kw * Cs, ns = max(0, min(C - jb, Cs));
+  const int32_t* off = a.offsets + (int64_t)kvh * (a.Ct + a.B) + cb + b + jb;
+  const int32_t* ulen = a.union_len + (int64_t)jg * a.Ct + cb + jb;
+  uint64_t base = 0, all = 0;  // the slices before this one; all of them
+  for (int w = 0; w < nwu; ++w) {
+    const uint64_t t = a.slice_tot[(int64_t)bg * kMaxUnionSlices + w];
+    base += w < kw ? t : 0ull;
+    all += t;
+  }
+  const int j0 = tid * kUnionSeg;  // the thread's clusters jb + j0 .. jb + j0 + 7
+  int32_t o[kUnionSeg], L[kUnionSeg];
+  uint64_t loc = 0;
+#pragma unroll
+  for (int e = 0; e < kUnionSeg; ++e) {
+    const bool in = j0 + e < ns;
+    o[e] = in ? off[j0 + e] : 0;
+    L[e] = in ? ulen[j0 + e] : 0;
+  }
+#pragma unroll
+  for (int e = 0; e < kUnionSeg; ++e)
+    if (L[e] > 0) loc += (1ull << 32) | (uint64_t)L[e];
+  const uint64_t incl = wave_incl_scan(loc);  // DPP, no LDS
+  if (lane == kWave - 1) s_wave_u[wave] = incl;
+  __syncthreads();
+  uint64_t mine = base + incl - loc;
+  for (int w = 0; w < wave; ++w) mine += s_wave_u[w];
+  int idx = (int)(mine >> 32);
+  int64_t upos = (int64_t)(mine & 0xffffffffu);
+#pragma unroll
+  for (int e = 0; e < kUnionSeg; ++e) {
+    if (L[e] > 0) {
+      rstart[idx] = o[e];
+      rupos[idx] = (int32_t)upos;
+      for (int64_t c = (upos + T - 1) / T; c * T < upos + L[e] && c < a.max_chunks; ++c) cfr[c] = idx;
+      ++idx;
+      upos += L[e];
+    }
+  }
+  if (kw == nwu - 1 && tid == 0) {
+    const int n_c = a.head_meta[(int64_t)h0 * 16 + 0], tail = a.head_meta[(int64_t)h0 * 16 + 11];
+    union_close(a, bg, b, kvh, n_c, tail, all, rstart, rupos, cfr);
+  }
+}
+
 // ============================================================================
 // Launchers
 // ============================================================================
@@ -1916,17 +2001,37 @@ hipError_t launch_sample(const FitArgs& a, int split, int n_heads, bool paged, h
   return hipGetLastError();
 }
 
-hipError_t launch_fit_union(const FitArgs& a, int G, int n_groups, hipStream_t st) {
-  const int64_t Cp = (a.Cm + kUnionSeg - 1) / kUnionSeg * kUnionSeg;
+hipError_t launch_fit_union(const FitArgs& args, int G, int n_groups, hipStream_t st) {
+  FitArgs a = args;
+  const bool sliced = union_sliced(G, a.Cm);
+  // beyond kUnionStagedMax clusters the staged union runs in slices of at
+  // most that many, up to kMaxUnionSlices workgroups per group (as many as
+  // fill the device's 256 compute units), then a second kernel lays out the
+  // ranges
+  int nwu = 1;
+  a.union_slice = 0;
+  if (sliced) {
+    nwu = (int)max((a.Cm + kUnionStagedMax - 1) / kUnionStagedMax, (int64_t)min(kMaxUnionSlices, 256 / max(n_groups, 1)));
+    nwu = min(nwu, kMaxUnionSlices);
+    a.union_slice = (int)(((a.Cm + nwu - 1) / nwu + kUnionSeg - 1) / kUnionSeg * kUnionSeg);
+    nwu = (int)((a.Cm + a.union_slice - 1) / a.union_slice);
+  }
+  const int64_t Cp = sliced ? a.union_slice : (a.Cm + kUnionSeg - 1) / kUnionSeg * kUnionSeg;
   const int64_t C32 = (a.Cm + 31) / 32 * 32;
   const size_t lds = union_staged(G, a.Cm) ? (size_t)(G * Cp * 2 + (Cp + 4) * 4 + Cp * 4)
                                            : (a.Cm <= kUnionLdsMax ? (size_t)(C32 + 3 * (C32 / 32) + 1) * 4 : 0);
+  const dim3 grid(n_groups, nwu);
   switch (G) {
-    case 1: hipLaunchKernelGGL(fit_union_kernel<1>, dim3(n_groups), dim3(1024), lds, st, a); break;
-    case 2: hipLaunchKernelGGL(fit_union_kernel<2>, dim3(n_groups), dim3(1024), lds, st, a); break;
-    case 4: hipLaunchKernelGGL(fit_union_kernel<4>, dim3(n_groups), dim3(1024), lds, st, a); break;
-    case 8: hipLaunchKernelGGL(fit_union_kernel<8>, dim3(n_groups), dim3(1024), lds, st, a); break;
+    case 1: hipLaunchKernelGGL(fit_union_kernel<1>, grid, dim3(1024), lds, st, a); break;
+    case 2: hipLaunchKernelGGL(fit_union_kernel<2>, grid, dim3(1024), lds, st, a); break;
+    case 4: hipLaunchKernelGGL(fit_union_kernel<4>, grid, dim3(1024), lds, st, a); break;
+    case 8: hipLaunchKernelGGL(fit_union_kernel<8>, grid, dim3(1024), lds, st, a); break;
     default: return hipErrorInvalidValue;
+  }
+  if (sliced) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(union_ranges_kernel, grid, dim3(1024), 0, st, a);
   }
   return hipGetLastError();
 }

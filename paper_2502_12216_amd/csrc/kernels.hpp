@@ -121,6 +121,8 @@ struct FitArgs {
   int32_t* rstart;            // [B*NV][Cm+2]: first row of each selected range
   int32_t* rupos;             // [B*NV][Cm+2]: its first position in the group's token list
   int32_t* cfr;               // [B*NV][max_chunks]
+  uint64_t* slice_tot;        // [B*NV][kMaxUnionSlices]: (ranges << 32) | tokens of each union slice
+  int union_slice;            // clusters per union slice (set by the launcher; 0: not sliced)
   PagedKV pk;                 // used by the paged launches (K then points at the pages)
 };
 

@@ -18,6 +18,7 @@ constexpr int kMaxGroups = 4096;       // B * Hkv limit of the attention work li
 constexpr int kFitFields = 16;
 constexpr int kStageEvents = 7;        // start + after each of the six decode kernels
 constexpr int kUnionLdsMax = 32768;     // clusters whose union lengths are staged in LDS
+constexpr int kMaxUnionSlices = 8;    // workgroups per selection group of the sliced union
 constexpr int kScoreRows = 64;         // centroids per scoring workgroup (4096 workgroups at 8192 x 32)
 #ifndef TACTIC_SAMPLE_CHUNK
 #define TACTIC_SAMPLE_CHUNK 128
@@ -37,7 +38,7 @@ struct DecodePlan {
   // workspace byte offsets
   int64_t off_scores, off_order, off_rank, off_rprefix, off_headmeta, off_rows, off_logit;
   int64_t off_fit, off_cut, off_union_len, off_gmeta, off_rstart, off_rupos, off_cfr, off_lse;
-  int64_t off_partials, off_sort_keys, off_sort_cnt, off_sort_start, off_ameta;
+  int64_t off_partials, off_sort_keys, off_sort_cnt, off_sort_start, off_ameta, off_slice_tot;
   int64_t ws_bytes;
   int64_t exact_bp, win_bp, win_min, p1_bp, p2_bp;
   int64_t events[kStageEvents];  // optional hipEvent_t recorded between the kernels
@@ -46,7 +47,7 @@ struct DecodePlan {
   int64_t max_tail;      // capacity for recent (unclustered) tokens per sequence
   int64_t attn_dev;      // device the resident attention grids below were measured on (-1: none)
   int64_t attn_res[2];   // attention workgroups resident at once on it: contiguous, paged
-  int64_t pad[64 - 56];
+  int64_t pad[64 - 57];
 };
 static_assert(sizeof(DecodePlan) == 64 * sizeof(int64_t), "plan must fill tactic_decode_plan");
 

@@ -517,13 +517,16 @@ def test_sparse_sort_general_workspace_path(case):
 
 @pytest.mark.parametrize("Hq,Hkv", [(32, 8), (16, 2)])
 def test_sparse_union_range_writers(Hq, Hkv):
-    """The union of more than 8192 clusters (or of 8 heads) writes its ranges
-    one of two ways: from each thread's 32-cluster segment when at most an
-    eighth of the clusters are non-empty, else in a coalesced pass over the
-    clusters. 9000 clusters of about two tokens at a low and a high target
-    cover both (asserted from the union lengths), in union and per-head modes
-    and with 300 recent tokens after the clusters of sequence 0 (their range
-    follows the clusters' ranges), with staged parity on every group."""
+    """Unions of more than 8192 clusters. With 8 heads per group (16 / 2) the
+    group's one workgroup writes the ranges one of two ways: from each
+    thread's 32-cluster segment when at most an eighth of the clusters are
+    non-empty, else in a coalesced pass over the clusters; with 4 heads (32 /
+    8) and in per-head mode the union runs in slices with a second kernel for
+    the ranges. 9000 clusters of about two tokens at a low and a high target
+    give both densities (asserted from the union lengths), in union and
+    per-head modes and with 300 recent tokens after the clusters of sequence
+    0 (their range follows the clusters' ranges), with staged parity on
+    every group."""
     import dataclasses
     T = _tactic()
     base = _small("ctx32k_llama8b", [20000, 12000])
