@@ -548,7 +548,7 @@ def test_sparse_union_range_writers(Hq, Hkv):
         assert seen == {"segment", "coalesced"}, (union, seen)
 
 
-@pytest.mark.parametrize("case", ["pieces", "workspace", "mixed"])
+@pytest.mark.parametrize("case", ["pieces", "workspace", "mixed", "odd_split"])
 def test_sparse_large_sort_paths_with_recent_tail(case):
     """Recent tokens after the clusters on the sorts of more than 8192
     clusters: 12000 clusters (LDS pieces) and 34000 clusters (workspace
@@ -556,15 +556,19 @@ def test_sparse_large_sort_paths_with_recent_tail(case):
     sampled rows follow the windows', its range follows the union's), and a
     batch that mixes 12000 clusters with 3000 (the smaller sequence's heads
     then take the pieces, shared by the same number of workgroups, with a
-    tail of 100), in union and per-head modes, staged parity on every group
-    at P = 0.9."""
+    tail of 100), and three sequences of 16 / 4 heads at 9000 clusters (48
+    heads: five workgroups share each head's sort, five slices of 1800
+    clusters each per-head union), in union and per-head modes, staged parity
+    on every group at P = 0.9."""
     import dataclasses
     T = _tactic()
     P = 0.9
     lens, C, tail = {"pieces": ([30000, 12000], 12000, [200, 0]), "workspace": ([70000], 34000, [150]),
-                     "mixed": ([30000, 3000], 12000, [0, 100])}[case]
+                     "mixed": ([30000, 3000], 12000, [0, 100]),
+                     "odd_split": ([20000, 15000, 12000], 9000, [0, 50, 0])}[case]
     base = _small("ctx32k_llama8b", lens)
-    wl = dataclasses.replace(base, fixed_clusters=C, name=f"{base.name}_{case}_tail")
+    heads = {"n_q_heads": 16, "n_kv_heads": 4} if case == "odd_split" else {}
+    wl = dataclasses.replace(base, fixed_clusters=C, name=f"{base.name}_{case}_tail", **heads)
     inp = synth.make_layer(wl, 0)
     lay = synth.label_layout(inp, tail=tail)
     for union in (1, 0):
