@@ -200,8 +200,19 @@ def test_sparse_single_cluster_and_target_one_is_dense():
     check_layer(inp1, lay1, 0.9, res1, label="one cluster")
 
 
-def test_sparse_is_deterministic():
-    inp = synth.make_layer(_small("ctx32k_llama8b", [5000, 2500]), 0)
+@pytest.mark.parametrize("case", ["lds", "shared"])
+def test_sparse_is_deterministic(case):
+    """Two calls give bit-identical outputs and counts: the in-LDS sort, and
+    12000 clusters per sequence, where workgroups share each head's sort (a
+    cluster's place inside its bucket follows the order of atomic arrivals,
+    which may differ between calls) and each group's union runs in slices."""
+    import dataclasses
+    if case == "lds":
+        wl = _small("ctx32k_llama8b", [5000, 2500])
+    else:
+        base = _small("ctx32k_llama8b", [30000, 12000])
+        wl = dataclasses.replace(base, fixed_clusters=12000, name=f"{base.name}_c12000_det")
+    inp = synth.make_layer(wl, 0)
     lay = synth.label_layout(inp)
     a = run_sparse(inp, lay, 0.9)
     b = run_sparse(inp, lay, 0.9)
