@@ -21,7 +21,7 @@ constexpr int kUnionLdsMax = 32768;     // clusters whose union lengths are stag
 constexpr int kMaxUnionSlices = 8;    // workgroups per selection group of the sliced union
 constexpr int kScoreRows = 64;         // centroids per scoring workgroup (4096 workgroups at 8192 x 32)
 #ifndef TACTIC_SAMPLE_CHUNK
-#define TACTIC_SAMPLE_CHUNK 128
+#define TACTIC_SAMPLE_CHUNK 64
 #endif
 constexpr int kSampleChunk = TACTIC_SAMPLE_CHUNK;  // sampled rows per sampling workgroup
 
